@@ -1,0 +1,174 @@
+#!/usr/bin/env python3
+"""One decode step of graph-segment attention on one MI355X, timed.
+
+A step is the whole hot path over one batch of synthetic rollout-graph inputs already resident
+in HBM: the GPU segment scheduler (group the branches sharing each segment, rank, chunk, build
+the work list), the grouped segment attention kernel, and the log-sum-exp merge.  The default
+workload is the merged-DAG rollout (64 prompts, 1024 branches, 7B attention shape).
+
+Prints one JSON line: branch-tokens/s (one decode token per branch per step), the attention
+kernel's achieved fraction of the HBM roofline counting unique K/V bytes, and the CPU oracle
+timed on a bounded sample of the same workload.
+"""
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+HBM_PEAK_GBS = 8000.0
+METRIC = "branch-tokens/s per decode step; % of HBM roofline on unique KV bytes"
+COUNTERS_MD = os.path.join(ROOT, "profiles", "seg_attn_merged_dag_counters.md")
+KERNEL_SRC = os.path.join(ROOT, "paper_2606_18954_amd", "csrc", "seg_attn.hip")
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_hash():
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_counters(config):
+    """HBM traffic and MFMA busy fraction from the committed rocprofv3 counter summary, only
+    if it was taken on this exact attention kernel source and workload."""
+    if not os.path.exists(COUNTERS_MD):
+        return None
+    txt = open(COUNTERS_MD).read()
+    kv = dict(re.findall(r"^- (\w+): (\S+)", txt, flags=re.M))
+    if kv.get("kernel_source_sha256_16") != kernel_hash() or kv.get("workload") != config:
+        return None
+    return kv
+
+
+def cpu_baseline(wl, n_sample):
+    sys.path.insert(0, ROOT)
+    from oracle import graphattn_oracle as O
+    from paper_2606_18954_amd import workloads as W
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = 1
+    g = wl.graph
+    br = W.sample_branches(g, n_sample, seed=11)
+    qb, pb = wl.q_bits(), wl.pool_bits()
+    t0 = time.perf_counter()
+    O.decode(qb, pb, g.seg_len, g.seg_page_offsets, g.seg_pages, g.path_offsets, g.path_segs,
+             wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.dtype, branches=br)
+    dt = time.perf_counter() - t0
+    toks = sum(g.path_tokens(int(b)) for b in br)
+    return {"value": len(br) / dt, "unit": "branch-tokens/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{len(br)} seeded branches of the same workload ({toks} attended tokens), "
+                      f"fp64 NumPy, {dt:.1f} s wall",
+            "attended_tokens_per_s": toks / dt}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="c3",
+                    choices=["c1", "c2", "c3", "c4", "c5chain", "c5graph"])
+    ap.add_argument("--cpu-sample", type=int, default=128,
+                    help="branches the CPU oracle is timed on (0 skips it)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (the design notes "
+              "describe how prompts would be sharded across GPUs). Run with --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    sys.path.insert(0, ROOT)
+    import torch
+    from paper_2606_18954_amd import graphattn as G
+    from paper_2606_18954_amd import workloads as W
+
+    t0 = time.time()
+    wl = W.CONFIGS[args.config]()
+    g = wl.graph
+    log(f"workload {wl.name}: B={g.num_branches} S={g.num_segments} pages={g.num_pages} "
+        f"generated in {time.time() - t0:.1f}s")
+    dev = torch.device("cuda:0")
+    q, pool = wl.q.to(dev), wl.pool.to(dev)
+    B, Hq, D = g.num_branches, wl.num_q_heads, wl.head_dim
+    out = torch.empty((B, Hq, D), dtype=q.dtype, device=dev)
+    lse = torch.empty((B, Hq), dtype=torch.float32, device=dev)
+    hg = G.HostGraph.from_graph(g)
+    params = G.make_params(Hq, wl.num_kv_heads, D, g.num_pages, wl.dtype)
+    plan = G.Plan(hg, params)
+    info = plan.info()
+
+    def step():
+        plan.schedule()
+        plan.run(q, pool, out, lse)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"warmup done ({args.warmup} steps)")
+    plan.profile(args.steps)
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record()
+    for _ in range(args.steps):
+        step()
+    ev1.record()
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / args.steps
+    prof = plan.profile_read()
+    attn_ms = prof.attn_ms / max(1, prof.runs)
+    merge_ms = prof.merge_ms / max(1, prof.runs)
+    sched_ms = prof.sched_ms / max(1, prof.schedules)
+    log(f"timed {args.steps} steps: {ms:.4f} ms/step (attention {attn_ms:.4f} ms, merge "
+        f"{merge_ms:.4f} ms, scheduler {sched_ms:.4f} ms)")
+
+    ukv = wl.unique_kv_bytes()
+    achieved = ukv / (attn_ms * 1e-3) / 1e9
+    cnt = measured_counters(args.config)
+    traffic = None
+    mfma = None
+    if cnt:
+        traffic = float(cnt["fetch_bytes_per_launch"]) + float(cnt["write_bytes_per_launch"])
+        mfma = float(cnt.get("mfma_busy_fraction", "nan"))
+    res = {
+        "metric": METRIC,
+        "value": B / (ms * 1e-3),
+        "unit": "branch-tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic (seeded N(0,1) K/V/Q, seeded rollout graph)",
+        "config": {"workload": wl.name, "branches": B, "segments": g.num_segments,
+                   "unique_tokens": g.unique_tokens(), "attended_tokens": g.attended_tokens(),
+                   "q_heads": Hq, "kv_heads": wl.num_kv_heads, "head_dim": D, "page_tokens": 16,
+                   "chunk_pages": info.chunk_pages},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic},
+        "kernel_ms": {"scheduler": sched_ms, "attention": attn_ms, "merge": merge_ms},
+        "unique_kv_bytes": ukv,
+        "step_unique_kv_frac": ukv / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+        "attended_tokens_per_s": g.attended_tokens() / (ms * 1e-3),
+        "mfma_busy_fraction": mfma,
+    }
+    plan.close()
+    del q, pool, out, lse
+    torch.cuda.empty_cache()
+    if args.cpu_sample > 0:
+        log(f"timing the CPU oracle on {args.cpu_sample} branches")
+        res["cpu_baseline"] = cpu_baseline(wl, args.cpu_sample)
+        log("CPU oracle done")
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,170 @@
+/*
+ * graphattn.h -- C ABI of graph-segment decode attention on MI355X (gfx950).
+ *
+ * Problem (GraphPO, Sec. 3.2 "Graph Construction" and Alg. S.1 Stage 1): a rollout graph has
+ * reasoning steps as edges and the prompt as its root; the generation context of a state is the
+ * ordered concatenation of the edge tokens on its path from the root.  Each edge's tokens form
+ * a *segment* whose K/V live in fixed-size pages of a shared pool.  Every active *branch* (a
+ * state being extended) is a list of segment ids, and at each decode step it issues one query
+ * per q-head that attends, with ordinary scaled-dot-product softmax attention, over all tokens
+ * of all segments on its path.  Siblings share their parent's prefix segments (Sec. 1) and
+ * virtually merged states share the representative's successors (Sec. 3.2, graph suffix C_g),
+ * so one segment is usually read by many branches.
+ *
+ * The library groups the branches that share each segment (a GPU segment scheduler), computes
+ * every segment's contribution for all of its branches at once (a grouped dense contraction on
+ * bf16 MFMA with a wave-level online softmax), and folds the per-segment partial results of
+ * each branch with a log-sum-exp merge.  The result equals the textbook attention over the
+ * branch's concatenated context up to floating-point rounding.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Device buffers (q, kv_page_pool, out, lse) are caller-owned device pointers; the library never
+ * frees or reallocates them.  Index arrays (segment table, branch paths) are caller-owned HOST
+ * arrays, read only during the call that receives them.
+ *
+ *   q             [B][Hq][D]                 dtype; one decode query per branch and q-head
+ *   kv_page_pool  [num_pages][Hkv][2][16][D] dtype; index 0 of the third axis is K, 1 is V
+ *   out           [B][Hq][D]                 dtype (same as q)
+ *   lse           [B][Hq]                    float32, natural log of sum_j exp(scale * q.k_j)
+ *
+ * Token t of segment s sits in page seg_pages[seg_page_offsets[s] + t / 16], slot t % 16.  Each
+ * segment starts at slot 0 of its first page.  The contents of slots >= seg_len in a segment's
+ * last page, and of pages no segment references, are unspecified (they may hold NaN) and are
+ * never used.  Grouped-query attention: q-head h reads kv-head h / (Hq / Hkv).
+ *
+ * Errors: all inputs are validated on the host before any device work is enqueued.  On error
+ * the call returns a negative ga_status, writes nothing to any caller buffer, and
+ * graphattn_last_error() describes the failure (thread-local).  Device work is asynchronous on
+ * the given HIP stream (NULL = the default stream).
+ */
+#ifndef GRAPHATTN_H
+#define GRAPHATTN_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  GA_OK = 0,
+  GA_EINVAL = -1,        /* malformed argument: null pointer, bad CSR, empty or repeating path */
+  GA_ERANGE = -2,        /* segment id or page id out of range */
+  GA_ENOMEM = -3,        /* device or pinned-host allocation failed */
+  GA_EHIP = -4,          /* a HIP runtime call or kernel launch failed */
+  GA_EUNSUPPORTED = -5   /* head_dim, page_size or dtype outside what the kernels implement */
+} ga_status;
+
+typedef enum { GA_F32 = 0, GA_BF16 = 1 } ga_dtype;
+
+/* The rollout graph's segments: one segment per generated step (edge) plus the prompt (root).
+ * seg_len[s] >= 1 tokens; seg_page_offsets is CSR into seg_pages with seg_page_offsets[0] = 0,
+ * non-decreasing, and at least ceil(seg_len[s] / 16) pages per segment.  Page ids lie in
+ * [0, num_pages).  Host memory. */
+typedef struct {
+  int32_t num_segments;
+  const int32_t* seg_len;           /* [S] */
+  const int64_t* seg_page_offsets;  /* [S + 1] */
+  const int32_t* seg_pages;         /* [seg_page_offsets[S]] */
+} ga_segment_table;
+
+/* The active branches: branch b's context is segments path_segs[path_offsets[b] ..
+ * path_offsets[b+1]), root first.  Paths are non-empty and visit a segment at most once (paths
+ * in a DAG are simple, Sec. 3.2); the order of segments does not change the result.  Host
+ * memory. */
+typedef struct {
+  int32_t num_branches;
+  const int64_t* path_offsets;      /* [B + 1], path_offsets[0] = 0, non-decreasing */
+  const int32_t* path_segs;         /* [path_offsets[B]] */
+} ga_branch_paths;
+
+typedef struct {
+  int32_t num_q_heads;     /* Hq, a positive multiple of num_kv_heads */
+  int32_t num_kv_heads;    /* Hkv > 0 */
+  int32_t head_dim;        /* D: 64 or 128 */
+  int32_t page_size;       /* tokens per page: 16 */
+  int64_t num_pages;       /* extent of kv_page_pool, for range checks */
+  int32_t dtype;           /* ga_dtype of q, kv_page_pool and out */
+  float softmax_scale;     /* 0 selects 1/sqrt(head_dim) */
+} ga_params;
+
+/* A validated rollout graph uploaded to the device, plus its schedule and workspace. */
+typedef struct ga_plan ga_plan;
+
+/* One decode step of graph-segment attention, end to end: validate, upload the graph, group
+ * the branches of every segment, run the grouped segment attention and merge each branch's
+ * partials.  Equivalent to plan_create + schedule + run + destroy, but reuses a cached device
+ * workspace between calls (calls on different streams are ordered through an event).  q,
+ * kv_page_pool, out, lse: device pointers as described above; with num_branches = 0 nothing is
+ * launched.  Returns GA_OK or a negative ga_status. */
+ga_status graphattn_decode(const void* q, const void* kv_page_pool,
+                           const ga_segment_table* segment_table,
+                           const ga_branch_paths* branch_paths, void* out, float* lse,
+                           const ga_params* params, void* hip_stream);
+
+/* Validate the graph and parameters, allocate the plan's device workspace (sized for this
+ * graph) and enqueue the upload of the index arrays on hip_stream.  The host arrays may be
+ * released when the call returns.  *plan receives a new plan (NULL on error). */
+ga_status graphattn_plan_create(const ga_segment_table* segment_table,
+                                const ga_branch_paths* branch_paths, const ga_params* params,
+                                void* hip_stream, ga_plan** plan);
+
+/* Segment scheduler, on the GPU: transpose branch->segments into segment->branches (B(s) in
+ * ascending branch order), give each path entry the branch's position inside B(s), split long
+ * segments into page chunks and emit the work list of (segment, chunk, row block) items.
+ * Enqueued on hip_stream; must precede graphattn_run.  Deterministic: the same graph always
+ * yields the same schedule. */
+ga_status graphattn_schedule(ga_plan* plan, void* hip_stream);
+
+/* Grouped segment attention and log-sum-exp merge for one layer's q and K/V pool, using the
+ * plan's schedule (the rollout graph is shared by every layer of a decode step, so a schedule
+ * serves any number of runs).  Device pointers as described above.  Enqueued on hip_stream;
+ * runs on one plan must not overlap (they share the partial-result workspace). */
+ga_status graphattn_run(ga_plan* plan, const void* q, const void* kv_page_pool, void* out,
+                        float* lse, void* hip_stream);
+
+/* Sizes of the schedule, available after plan_create: */
+typedef struct {
+  int32_t num_segments, num_branches, num_entries;  /* S, B, E = path_offsets[B] */
+  int32_t chunk_pages;        /* maximum pages per work item */
+  int32_t rows_per_block;     /* maximum query rows (branch x q-head-in-group) per work item */
+  int64_t num_items;          /* work items per kv-head */
+  int64_t num_partial_rows;   /* partial results per q-head: sum over entries of chunks */
+} ga_plan_info;
+ga_status graphattn_plan_info(const ga_plan* plan, ga_plan_info* info);
+
+/* Copy the device schedule back to host arrays for inspection (synchronises hip_stream).  Any
+ * pointer may be NULL to skip that array.  Sizes: group_offsets [S+1] and group_branches [E]
+ * (B(s) as CSR, ascending ids), entry_ranks [E] (position of each path entry's branch inside
+ * its segment's group), items [3 * num_items] as (segment, chunk, row block) triples, and
+ * segment_chunks [S]. */
+ga_status graphattn_plan_debug_dump(const ga_plan* plan, void* hip_stream,
+                                    int64_t* group_offsets, int32_t* group_branches,
+                                    int32_t* entry_ranks, int32_t* items,
+                                    int32_t* segment_chunks);
+
+/* Kernel timing with HIP events recorded on the launch stream around each scheduler pass, each
+ * attention launch and each merge launch.  graphattn_plan_profile(plan, n) arms recording for the
+ * next n schedule and n run calls (n = 0 disarms and clears); graphattn_plan_profile_read
+ * synchronises on the last recorded event and returns the accumulated times in milliseconds
+ * and the number of calls recorded. */
+typedef struct {
+  int32_t schedules, runs;     /* calls recorded */
+  double sched_ms;             /* sum over recorded schedule calls */
+  double attn_ms;              /* sum over recorded runs: grouped segment attention kernel */
+  double merge_ms;             /* sum over recorded runs: log-sum-exp merge kernel */
+} ga_profile;
+ga_status graphattn_plan_profile(ga_plan* plan, int32_t max_calls);
+ga_status graphattn_plan_profile_read(ga_plan* plan, ga_profile* out);
+
+/* Release the plan and its device workspace (waits for work still using it). */
+void graphattn_plan_destroy(ga_plan* plan);
+
+/* Thread-local description of the last failure in this thread ("" if none). */
+const char* graphattn_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* GRAPHATTN_H */

@@ -1,0 +1,641 @@
+// Host runtime of the graph-segment decode attention library: validation, plans, workspace,
+// launches and the C entry points declared in include/graphattn.h.
+#include "../../include/graphattn.h"
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "ga_internal.hpp"
+
+namespace {
+
+thread_local std::string g_err;
+
+ga_status fail(ga_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+ga_status hip_fail(hipError_t e, const char* what) {
+  return fail(GA_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define GA_HIP(call, what)                       \
+  do {                                           \
+    hipError_t e_ = (call);                      \
+    if (e_ != hipSuccess) return hip_fail(e_, what); \
+  } while (0)
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Attention workgroups kept resident per device (persistent grid).
+int device_cus() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 256;
+  int n = 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+    return 256;
+  return n;
+}
+
+struct Sizes {
+  int32_t S = 0, B = 0, E = 0;
+  int64_t P = 0;               // entries of seg_pages
+  int32_t chunk_pages = 0;
+  int64_t max_items = 0;       // upper bound on work items per kv-head
+  int64_t prows = 0;           // partial rows per q-head
+};
+
+}  // namespace
+
+struct ga_plan {
+  ga_params p{};
+  Sizes z;
+  // One device allocation carved into the graph copy, the schedule and the partial buffers.
+  void* dev = nullptr;
+  size_t dev_bytes = 0;
+  void* pin = nullptr;         // pinned host staging of the graph upload
+  size_t pin_bytes = 0;
+  bool owns_memory = true;
+  bool scheduled = false;
+  int num_cus = 256;
+  ga::DevGraph g{};
+  ga::DevSchedule sc{};
+  float* po = nullptr;
+  float* plse = nullptr;
+  // Kernel timing (graphattn_plan_profile): events for up to prof_cap schedule / run calls.
+  int32_t prof_cap = 0, prof_sched = 0, prof_runs = 0;
+  std::vector<hipEvent_t> ev_sched;   // 2 per recorded schedule call
+  std::vector<hipEvent_t> ev_run;     // 3 per recorded run: attention start, attention end, merge end
+  hipEvent_t ev_last = nullptr;
+};
+
+namespace {
+
+// ----------------------------------------------------------------------------------------------
+// Validation (host, before any device work)
+// ----------------------------------------------------------------------------------------------
+
+ga_status validate_params(const ga_params* p) {
+  if (!p) return fail(GA_EINVAL, "params is NULL");
+  if (p->num_q_heads <= 0 || p->num_kv_heads <= 0)
+    return fail(GA_EINVAL, "head counts must be positive (Hq=%d, Hkv=%d)", p->num_q_heads,
+                p->num_kv_heads);
+  if (p->num_q_heads % p->num_kv_heads)
+    return fail(GA_EINVAL, "num_q_heads (%d) is not a multiple of num_kv_heads (%d)",
+                p->num_q_heads, p->num_kv_heads);
+  if (p->head_dim != 64 && p->head_dim != 128)
+    return fail(GA_EUNSUPPORTED, "head_dim %d unsupported (64 or 128)", p->head_dim);
+  if (p->page_size != ga::kPageTokens)
+    return fail(GA_EUNSUPPORTED, "page_size %d unsupported (16)", p->page_size);
+  if (p->dtype != GA_F32 && p->dtype != GA_BF16)
+    return fail(GA_EUNSUPPORTED, "dtype %d unsupported", p->dtype);
+  if (p->num_pages < 0) return fail(GA_EINVAL, "num_pages is negative");
+  if (!std::isfinite(p->softmax_scale) || p->softmax_scale < 0.f)
+    return fail(GA_EINVAL, "softmax_scale must be finite and >= 0");
+  return GA_OK;
+}
+
+ga_status validate_graph(const ga_segment_table* st, const ga_branch_paths* bp,
+                         const ga_params* p, Sizes* z, std::vector<int32_t>* seg_npages) {
+  if (!st) return fail(GA_EINVAL, "segment_table is NULL");
+  if (!bp) return fail(GA_EINVAL, "branch_paths is NULL");
+  const int32_t S = st->num_segments, B = bp->num_branches;
+  if (S < 0) return fail(GA_EINVAL, "num_segments is negative");
+  if (B < 0) return fail(GA_EINVAL, "num_branches is negative");
+  if (!st->seg_page_offsets) return fail(GA_EINVAL, "seg_page_offsets is NULL");
+  if (S > 0 && !st->seg_len) return fail(GA_EINVAL, "seg_len is NULL");
+  if (st->seg_page_offsets[0] != 0) return fail(GA_EINVAL, "seg_page_offsets[0] must be 0");
+  seg_npages->assign(S, 0);
+  for (int32_t s = 0; s < S; ++s) {
+    const int32_t len = st->seg_len[s];
+    if (len < 1) return fail(GA_EINVAL, "segment %d has length %d (< 1)", s, len);
+    const int64_t a = st->seg_page_offsets[s], b = st->seg_page_offsets[s + 1];
+    if (b < a) return fail(GA_EINVAL, "seg_page_offsets decreases at segment %d", s);
+    const int64_t need = (len + ga::kPageTokens - 1) / ga::kPageTokens;
+    if (b - a < need)
+      return fail(GA_EINVAL, "segment %d has %lld tokens but only %lld pages", s, (long long)len,
+                  (long long)(b - a));
+    (*seg_npages)[s] = (int32_t)need;
+  }
+  const int64_t P = st->seg_page_offsets[S];
+  if (P > 0 && !st->seg_pages) return fail(GA_EINVAL, "seg_pages is NULL");
+  for (int64_t i = 0; i < P; ++i) {
+    const int32_t pg = st->seg_pages[i];
+    if (pg < 0 || pg >= p->num_pages)
+      return fail(GA_ERANGE, "seg_pages[%lld] = %d outside [0, %lld)", (long long)i, pg,
+                  (long long)p->num_pages);
+  }
+  if (!bp->path_offsets) return fail(GA_EINVAL, "path_offsets is NULL");
+  if (bp->path_offsets[0] != 0) return fail(GA_EINVAL, "path_offsets[0] must be 0");
+  const int64_t E = bp->path_offsets[B];
+  if (E > 0x7fffffffLL) return fail(GA_EINVAL, "too many path entries (%lld)", (long long)E);
+  if (E > 0 && !bp->path_segs) return fail(GA_EINVAL, "path_segs is NULL");
+  std::vector<int32_t> stamp(S, -1);
+  for (int32_t b = 0; b < B; ++b) {
+    const int64_t a = bp->path_offsets[b], e1 = bp->path_offsets[b + 1];
+    if (e1 < a) return fail(GA_EINVAL, "path_offsets decreases at branch %d", b);
+    if (e1 == a) return fail(GA_EINVAL, "branch %d has an empty path", b);
+    for (int64_t e = a; e < e1; ++e) {
+      const int32_t s = bp->path_segs[e];
+      if (s < 0 || s >= S)
+        return fail(GA_ERANGE, "branch %d names segment %d outside [0, %d)", b, s, S);
+      if (stamp[s] == b) return fail(GA_EINVAL, "branch %d visits segment %d twice", b, s);
+      stamp[s] = b;
+    }
+  }
+  z->S = S;
+  z->B = B;
+  z->E = (int32_t)E;
+  z->P = P;
+  return GA_OK;
+}
+
+// Chunking policy: split a segment only when the whole step would otherwise leave the
+// persistent grid short of work; every extra chunk costs one more partial per branch row.
+void size_schedule(const ga_segment_table* st, const ga_branch_paths* bp, const ga_params* p,
+                   const std::vector<int32_t>& npg, int num_cus, Sizes* z) {
+  std::vector<char> used(z->S, 0);
+  for (int64_t e = 0; e < z->E; ++e) used[bp->path_segs[e]] = 1;
+  int64_t ref_pages = 0;
+  for (int32_t s = 0; s < z->S; ++s) ref_pages += used[s] ? npg[s] : 0;
+  const int64_t target_items = 4LL * num_cus * 2;   // ~4 work items per resident workgroup
+  int64_t cap = (ref_pages * p->num_kv_heads + target_items - 1) / target_items;
+  if (cap < 16) cap = 16;
+  if (cap > ga::kMaxChunkPages) cap = ga::kMaxChunkPages;
+  z->chunk_pages = (int32_t)cap;
+  const int32_t group = p->num_q_heads / p->num_kv_heads;
+  int64_t chunks_ref = 0, prows = 0;
+  for (int32_t s = 0; s < z->S; ++s)
+    if (used[s]) chunks_ref += (npg[s] + cap - 1) / cap;
+  for (int64_t e = 0; e < z->E; ++e) {
+    const int32_t s = bp->path_segs[e];
+    prows += (npg[s] + cap - 1) / cap;
+  }
+  z->prows = prows;
+  // items(s) = chunks(s) * ceil(|B(s)| g / 128) <= chunks(s) * (|B(s)| g / 128 + 1)
+  z->max_items = chunks_ref + (prows * group + ga::kRowsPerBlock - 1) / ga::kRowsPerBlock;
+  (void)st;
+}
+
+struct Layout {
+  size_t off[32];
+  size_t total;
+};
+
+// Device workspace layout (byte offsets of every array in the single allocation).
+enum {
+  L_SEG_LEN, L_SEG_PAGE_OFF, L_SEG_PAGES, L_PATH_OFF, L_PATH_SEGS,  // uploaded graph (contiguous)
+  L_GRP_CNT, L_GRP_FILL, L_GRP_OFF, L_GRP_TMP, L_GRP_BR, L_ENTRY_BR, L_ENTRY_RANK, L_SEG_NCH,
+  L_SEG_ITEM_OFF, L_SEG_PROW_OFF, L_ITEMS, L_COUNTERS, L_PO, L_PLSE, L_COUNT
+};
+
+Layout layout(const Sizes& z, const ga_params& p) {
+  size_t sz[L_COUNT];
+  sz[L_SEG_LEN] = sizeof(int32_t) * z.S;
+  sz[L_SEG_PAGE_OFF] = sizeof(int64_t) * (z.S + 1);
+  sz[L_SEG_PAGES] = sizeof(int32_t) * z.P;
+  sz[L_PATH_OFF] = sizeof(int64_t) * (z.B + 1);
+  sz[L_PATH_SEGS] = sizeof(int32_t) * z.E;
+  sz[L_GRP_CNT] = sizeof(int32_t) * z.S;
+  sz[L_GRP_FILL] = sizeof(int32_t) * z.S;
+  sz[L_GRP_OFF] = sizeof(int64_t) * (z.S + 1);
+  sz[L_GRP_TMP] = sizeof(int32_t) * z.E;
+  sz[L_GRP_BR] = sizeof(int32_t) * z.E;
+  sz[L_ENTRY_BR] = sizeof(int32_t) * z.E;
+  sz[L_ENTRY_RANK] = sizeof(int32_t) * z.E;
+  sz[L_SEG_NCH] = sizeof(int32_t) * z.S;
+  sz[L_SEG_ITEM_OFF] = sizeof(int64_t) * (z.S + 1);
+  sz[L_SEG_PROW_OFF] = sizeof(int64_t) * (z.S + 1);
+  sz[L_ITEMS] = sizeof(int4) * (z.max_items > 0 ? z.max_items : 1);
+  sz[L_COUNTERS] = sizeof(int64_t) * 4;
+  sz[L_PO] = sizeof(float) * (size_t)z.prows * p.num_q_heads * p.head_dim;
+  sz[L_PLSE] = sizeof(float) * (size_t)z.prows * p.num_q_heads;
+  Layout L{};
+  size_t o = 0;
+  for (int i = 0; i < L_COUNT; ++i) {
+    // The uploaded graph arrays are packed back to back (8-byte aligned) so one copy moves them.
+    o = align_up(o, i <= L_PATH_SEGS ? 8 : 256);
+    L.off[i] = o;
+    o += sz[i];
+  }
+  L.total = align_up(o, 256);
+  return L;
+}
+
+size_t upload_bytes(const Layout& L) { return L.off[L_GRP_CNT]; }
+
+void bind(ga_plan* pl, const Layout& L) {
+  char* d = static_cast<char*>(pl->dev);
+  const Sizes& z = pl->z;
+  pl->g.S = z.S;
+  pl->g.B = z.B;
+  pl->g.E = z.E;
+  pl->g.seg_len = reinterpret_cast<const int32_t*>(d + L.off[L_SEG_LEN]);
+  pl->g.seg_page_off = reinterpret_cast<const int64_t*>(d + L.off[L_SEG_PAGE_OFF]);
+  pl->g.seg_pages = reinterpret_cast<const int32_t*>(d + L.off[L_SEG_PAGES]);
+  pl->g.path_off = reinterpret_cast<const int64_t*>(d + L.off[L_PATH_OFF]);
+  pl->g.path_segs = reinterpret_cast<const int32_t*>(d + L.off[L_PATH_SEGS]);
+  pl->sc.grp_cnt = reinterpret_cast<int32_t*>(d + L.off[L_GRP_CNT]);
+  pl->sc.grp_fill = reinterpret_cast<int32_t*>(d + L.off[L_GRP_FILL]);
+  pl->sc.grp_off = reinterpret_cast<int64_t*>(d + L.off[L_GRP_OFF]);
+  pl->sc.grp_tmp = reinterpret_cast<int32_t*>(d + L.off[L_GRP_TMP]);
+  pl->sc.grp_br = reinterpret_cast<int32_t*>(d + L.off[L_GRP_BR]);
+  pl->sc.entry_branch = reinterpret_cast<int32_t*>(d + L.off[L_ENTRY_BR]);
+  pl->sc.entry_rank = reinterpret_cast<int32_t*>(d + L.off[L_ENTRY_RANK]);
+  pl->sc.seg_nchunk = reinterpret_cast<int32_t*>(d + L.off[L_SEG_NCH]);
+  pl->sc.seg_item_off = reinterpret_cast<int64_t*>(d + L.off[L_SEG_ITEM_OFF]);
+  pl->sc.seg_prow_off = reinterpret_cast<int64_t*>(d + L.off[L_SEG_PROW_OFF]);
+  pl->sc.items = reinterpret_cast<int4*>(d + L.off[L_ITEMS]);
+  pl->sc.counters = reinterpret_cast<int64_t*>(d + L.off[L_COUNTERS]);
+  pl->po = reinterpret_cast<float*>(d + L.off[L_PO]);
+  pl->plse = reinterpret_cast<float*>(d + L.off[L_PLSE]);
+}
+
+void pack_upload(const ga_segment_table* st, const ga_branch_paths* bp, const Layout& L,
+                 const Sizes& z, char* h) {
+  if (z.S) std::memcpy(h + L.off[L_SEG_LEN], st->seg_len, sizeof(int32_t) * z.S);
+  std::memcpy(h + L.off[L_SEG_PAGE_OFF], st->seg_page_offsets, sizeof(int64_t) * (z.S + 1));
+  if (z.P) std::memcpy(h + L.off[L_SEG_PAGES], st->seg_pages, sizeof(int32_t) * z.P);
+  std::memcpy(h + L.off[L_PATH_OFF], bp->path_offsets, sizeof(int64_t) * (z.B + 1));
+  if (z.E) std::memcpy(h + L.off[L_PATH_SEGS], bp->path_segs, sizeof(int32_t) * z.E);
+}
+
+// Process-wide workspace reused by graphattn_decode.
+struct DecodeCache {
+  std::mutex mu;
+  void* dev = nullptr;
+  size_t dev_bytes = 0;
+  void* pin = nullptr;
+  size_t pin_bytes = 0;
+  int device = -1;
+  hipEvent_t done = nullptr;      // recorded after the last decode's kernels
+  hipEvent_t uploaded = nullptr;  // recorded after the last decode's upload
+};
+DecodeCache g_cache;
+
+ga_status plan_init(const ga_segment_table* st, const ga_branch_paths* bp, const ga_params* p,
+                    ga_plan* pl, Layout* L) {
+  ga_status rc = validate_params(p);
+  if (rc) return rc;
+  std::vector<int32_t> npg;
+  rc = validate_graph(st, bp, p, &pl->z, &npg);
+  if (rc) return rc;
+  pl->p = *p;
+  if (pl->p.softmax_scale == 0.f) pl->p.softmax_scale = 1.f / std::sqrt((float)p->head_dim);
+  pl->num_cus = device_cus();
+  size_schedule(st, bp, p, npg, pl->num_cus, &pl->z);
+  *L = layout(pl->z, pl->p);
+  return GA_OK;
+}
+
+ga_status upload(ga_plan* pl, const ga_segment_table* st, const ga_branch_paths* bp,
+                 const Layout& L, hipStream_t stream) {
+  pack_upload(st, bp, L, pl->z, static_cast<char*>(pl->pin));
+  GA_HIP(hipMemcpyAsync(pl->dev, pl->pin, upload_bytes(L), hipMemcpyHostToDevice, stream),
+         "graph upload");
+  return GA_OK;
+}
+
+ga_status check_run_ptrs(const ga_plan* pl, const void* q, const void* pool, const void* out,
+                         const float* lse) {
+  if (pl->z.B == 0) return GA_OK;
+  if (!q || !pool || !out || !lse) return fail(GA_EINVAL, "q, kv_page_pool, out and lse must be non-NULL");
+  if ((reinterpret_cast<uintptr_t>(q) | reinterpret_cast<uintptr_t>(pool) |
+       reinterpret_cast<uintptr_t>(out)) & 15)
+    return fail(GA_EINVAL, "q, kv_page_pool and out must be 16-byte aligned");
+  if (reinterpret_cast<uintptr_t>(lse) & 3) return fail(GA_EINVAL, "lse must be 4-byte aligned");
+  return GA_OK;
+}
+
+ga_status do_schedule(ga_plan* pl, hipStream_t stream) {
+  const bool rec = pl->prof_sched < pl->prof_cap;
+  if (rec) GA_HIP(hipEventRecord(pl->ev_sched[2 * pl->prof_sched], stream), "profile event");
+  if (pl->z.B > 0 || pl->z.S > 0) {
+    GA_HIP(ga::launch_schedule(pl->g, pl->sc, pl->p.num_q_heads / pl->p.num_kv_heads,
+                               pl->z.chunk_pages, stream),
+           "scheduler launch");
+  }
+  if (rec) {
+    hipEvent_t e = pl->ev_sched[2 * pl->prof_sched + 1];
+    GA_HIP(hipEventRecord(e, stream), "profile event");
+    pl->ev_last = e;
+    ++pl->prof_sched;
+  }
+  pl->scheduled = true;
+  return GA_OK;
+}
+
+ga_status do_run(ga_plan* pl, const void* q, const void* pool, void* out, float* lse,
+                 hipStream_t stream) {
+  if (!pl->scheduled) return fail(GA_EINVAL, "plan has no schedule (call graphattn_schedule)");
+  ga_status rc = check_run_ptrs(pl, q, pool, out, lse);
+  if (rc) return rc;
+  if (pl->z.B == 0) return GA_OK;
+  const bool bf16 = pl->p.dtype == GA_BF16;
+  ga::AttnArgs a{};
+  a.q = q;
+  a.pool = pool;
+  a.seg_len = pl->g.seg_len;
+  a.seg_page_off = pl->g.seg_page_off;
+  a.seg_pages = pl->g.seg_pages;
+  a.grp_off = pl->sc.grp_off;
+  a.grp_br = pl->sc.grp_br;
+  a.grp_cnt = pl->sc.grp_cnt;
+  a.seg_prow_off = pl->sc.seg_prow_off;
+  a.items = pl->sc.items;
+  a.counters = pl->sc.counters;
+  a.po = pl->po;
+  a.plse = pl->plse;
+  a.Hq = pl->p.num_q_heads;
+  a.Hkv = pl->p.num_kv_heads;
+  a.group = a.Hq / a.Hkv;
+  a.chunk_pages = pl->z.chunk_pages;
+  a.scale_log2 = pl->p.softmax_scale * 1.4426950408889634f;
+  int64_t grid = (int64_t)ga::seg_attn_grid(pl->p.head_dim, bf16, pl->num_cus);
+  const int64_t work = pl->z.max_items * pl->p.num_kv_heads;
+  if (work < grid) grid = work;
+  const bool rec = pl->prof_runs < pl->prof_cap;
+  hipEvent_t* ev = rec ? &pl->ev_run[3 * pl->prof_runs] : nullptr;
+  if (rec) GA_HIP(hipEventRecord(ev[0], stream), "profile event");
+  if (grid > 0)
+    GA_HIP(ga::launch_seg_attn(a, pl->p.head_dim, bf16, (int)grid, stream), "attention launch");
+  if (rec) GA_HIP(hipEventRecord(ev[1], stream), "profile event");
+  ga::MergeArgs m{};
+  m.path_off = pl->g.path_off;
+  m.path_segs = pl->g.path_segs;
+  m.entry_rank = pl->sc.entry_rank;
+  m.grp_cnt = pl->sc.grp_cnt;
+  m.seg_nchunk = pl->sc.seg_nchunk;
+  m.seg_prow_off = pl->sc.seg_prow_off;
+  m.po = pl->po;
+  m.plse = pl->plse;
+  m.out = out;
+  m.lse = lse;
+  m.counters = pl->sc.counters;
+  m.B = pl->z.B;
+  m.Hq = pl->p.num_q_heads;
+  GA_HIP(ga::launch_merge(m, pl->p.head_dim, bf16, stream), "merge launch");
+  if (rec) {
+    GA_HIP(hipEventRecord(ev[2], stream), "profile event");
+    pl->ev_last = ev[2];
+    ++pl->prof_runs;
+  }
+  return GA_OK;
+}
+
+void profile_clear(ga_plan* pl) {
+  for (hipEvent_t e : pl->ev_sched) (void)hipEventDestroy(e);
+  for (hipEvent_t e : pl->ev_run) (void)hipEventDestroy(e);
+  pl->ev_sched.clear();
+  pl->ev_run.clear();
+  pl->prof_cap = pl->prof_sched = pl->prof_runs = 0;
+  pl->ev_last = nullptr;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* graphattn_last_error(void) { return g_err.c_str(); }
+
+ga_status graphattn_plan_create(const ga_segment_table* segment_table,
+                                const ga_branch_paths* branch_paths, const ga_params* params,
+                                void* hip_stream, ga_plan** plan) {
+  g_err.clear();
+  if (!plan) return fail(GA_EINVAL, "plan out-pointer is NULL");
+  *plan = nullptr;
+  ga_plan* pl = new ga_plan();
+  Layout L;
+  ga_status rc = plan_init(segment_table, branch_paths, params, pl, &L);
+  if (rc) {
+    delete pl;
+    return rc;
+  }
+  pl->dev_bytes = L.total;
+  pl->pin_bytes = upload_bytes(L);
+  if (hipMalloc(&pl->dev, pl->dev_bytes) != hipSuccess) {
+    delete pl;
+    (void)hipGetLastError();
+    return fail(GA_ENOMEM, "device workspace of %zu bytes", L.total);
+  }
+  if (hipHostMalloc(&pl->pin, pl->pin_bytes > 0 ? pl->pin_bytes : 1) != hipSuccess) {
+    (void)hipFree(pl->dev);
+    delete pl;
+    (void)hipGetLastError();
+    return fail(GA_ENOMEM, "pinned staging of %zu bytes", pl->pin_bytes);
+  }
+  bind(pl, L);
+  rc = upload(pl, segment_table, branch_paths, L, static_cast<hipStream_t>(hip_stream));
+  if (rc) {
+    graphattn_plan_destroy(pl);
+    return rc;
+  }
+  *plan = pl;
+  return GA_OK;
+}
+
+ga_status graphattn_schedule(ga_plan* plan, void* hip_stream) {
+  g_err.clear();
+  if (!plan) return fail(GA_EINVAL, "plan is NULL");
+  return do_schedule(plan, static_cast<hipStream_t>(hip_stream));
+}
+
+ga_status graphattn_run(ga_plan* plan, const void* q, const void* kv_page_pool, void* out,
+                        float* lse, void* hip_stream) {
+  g_err.clear();
+  if (!plan) return fail(GA_EINVAL, "plan is NULL");
+  return do_run(plan, q, kv_page_pool, out, lse, static_cast<hipStream_t>(hip_stream));
+}
+
+ga_status graphattn_plan_info(const ga_plan* plan, ga_plan_info* info) {
+  g_err.clear();
+  if (!plan || !info) return fail(GA_EINVAL, "plan or info is NULL");
+  info->num_segments = plan->z.S;
+  info->num_branches = plan->z.B;
+  info->num_entries = plan->z.E;
+  info->chunk_pages = plan->z.chunk_pages;
+  info->rows_per_block = ga::kRowsPerBlock;
+  info->num_items = -1;
+  info->num_partial_rows = plan->z.prows;
+  if (plan->scheduled) {
+    int64_t n = 0;
+    if (hipMemcpy(&n, plan->sc.counters, sizeof n, hipMemcpyDeviceToHost) == hipSuccess)
+      info->num_items = n;
+  }
+  return GA_OK;
+}
+
+ga_status graphattn_plan_debug_dump(const ga_plan* plan, void* hip_stream,
+                                    int64_t* group_offsets, int32_t* group_branches,
+                                    int32_t* entry_ranks, int32_t* items,
+                                    int32_t* segment_chunks) {
+  g_err.clear();
+  if (!plan) return fail(GA_EINVAL, "plan is NULL");
+  if (!plan->scheduled) return fail(GA_EINVAL, "plan has no schedule");
+  hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  GA_HIP(hipStreamSynchronize(s), "synchronise");
+  const Sizes& z = plan->z;
+  if (group_offsets)
+    GA_HIP(hipMemcpy(group_offsets, plan->sc.grp_off, sizeof(int64_t) * (z.S + 1),
+                     hipMemcpyDeviceToHost), "dump group offsets");
+  if (group_branches && z.E)
+    GA_HIP(hipMemcpy(group_branches, plan->sc.grp_br, sizeof(int32_t) * z.E,
+                     hipMemcpyDeviceToHost), "dump groups");
+  if (entry_ranks && z.E)
+    GA_HIP(hipMemcpy(entry_ranks, plan->sc.entry_rank, sizeof(int32_t) * z.E,
+                     hipMemcpyDeviceToHost), "dump ranks");
+  if (segment_chunks && z.S)
+    GA_HIP(hipMemcpy(segment_chunks, plan->sc.seg_nchunk, sizeof(int32_t) * z.S,
+                     hipMemcpyDeviceToHost), "dump chunks");
+  if (items) {
+    int64_t n = 0;
+    GA_HIP(hipMemcpy(&n, plan->sc.counters, sizeof n, hipMemcpyDeviceToHost), "dump count");
+    if (n > z.max_items) return fail(GA_EINVAL, "schedule overflow (%lld items)", (long long)n);
+    std::vector<int4> tmp(n);
+    if (n)
+      GA_HIP(hipMemcpy(tmp.data(), plan->sc.items, sizeof(int4) * n, hipMemcpyDeviceToHost),
+             "dump items");
+    for (int64_t i = 0; i < n; ++i) {
+      items[3 * i] = tmp[i].x;
+      items[3 * i + 1] = tmp[i].y;
+      items[3 * i + 2] = tmp[i].z;
+    }
+  }
+  return GA_OK;
+}
+
+ga_status graphattn_plan_profile(ga_plan* plan, int32_t max_calls) {
+  g_err.clear();
+  if (!plan) return fail(GA_EINVAL, "plan is NULL");
+  if (max_calls < 0) return fail(GA_EINVAL, "max_calls is negative");
+  if (plan->ev_last) GA_HIP(hipEventSynchronize(plan->ev_last), "profile sync");
+  profile_clear(plan);
+  plan->ev_sched.resize(2 * (size_t)max_calls);
+  plan->ev_run.resize(3 * (size_t)max_calls);
+  for (auto* v : {&plan->ev_sched, &plan->ev_run})
+    for (hipEvent_t& e : *v)
+      if (hipEventCreate(&e) != hipSuccess) {
+        e = nullptr;
+        profile_clear(plan);
+        return fail(GA_EHIP, "profile event creation failed");
+      }
+  plan->prof_cap = max_calls;
+  return GA_OK;
+}
+
+ga_status graphattn_plan_profile_read(ga_plan* plan, ga_profile* out) {
+  g_err.clear();
+  if (!plan || !out) return fail(GA_EINVAL, "plan or out is NULL");
+  *out = ga_profile{};
+  if (plan->ev_last) GA_HIP(hipEventSynchronize(plan->ev_last), "profile sync");
+  for (int32_t i = 0; i < plan->prof_sched; ++i) {
+    float ms = 0.f;
+    GA_HIP(hipEventElapsedTime(&ms, plan->ev_sched[2 * i], plan->ev_sched[2 * i + 1]), "elapsed");
+    out->sched_ms += ms;
+  }
+  for (int32_t i = 0; i < plan->prof_runs; ++i) {
+    float a = 0.f, m = 0.f;
+    GA_HIP(hipEventElapsedTime(&a, plan->ev_run[3 * i], plan->ev_run[3 * i + 1]), "elapsed");
+    GA_HIP(hipEventElapsedTime(&m, plan->ev_run[3 * i + 1], plan->ev_run[3 * i + 2]), "elapsed");
+    out->attn_ms += a;
+    out->merge_ms += m;
+  }
+  out->schedules = plan->prof_sched;
+  out->runs = plan->prof_runs;
+  return GA_OK;
+}
+
+void graphattn_plan_destroy(ga_plan* plan) {
+  if (!plan) return;
+  profile_clear(plan);
+  if (plan->owns_memory) {
+    if (plan->dev) {
+      (void)hipDeviceSynchronize();
+      (void)hipFree(plan->dev);
+    }
+    if (plan->pin) (void)hipHostFree(plan->pin);
+  }
+  delete plan;
+}
+
+ga_status graphattn_decode(const void* q, const void* kv_page_pool,
+                           const ga_segment_table* segment_table,
+                           const ga_branch_paths* branch_paths, void* out, float* lse,
+                           const ga_params* params, void* hip_stream) {
+  g_err.clear();
+  hipStream_t stream = static_cast<hipStream_t>(hip_stream);
+  ga_plan pl;
+  Layout L;
+  ga_status rc = plan_init(segment_table, branch_paths, params, &pl, &L);
+  if (rc) return rc;
+  rc = check_run_ptrs(&pl, q, kv_page_pool, out, lse);
+  if (rc) return rc;
+  pl.scheduled = false;
+  pl.owns_memory = false;
+  std::lock_guard<std::mutex> lock(g_cache.mu);
+  int dev = 0;
+  GA_HIP(hipGetDevice(&dev), "current device");
+  if (g_cache.device != dev) {
+    // A new device: drop the old cache (its buffers belong to the previous device).
+    g_cache.dev = nullptr;
+    g_cache.pin = nullptr;
+    g_cache.dev_bytes = g_cache.pin_bytes = 0;
+    g_cache.done = g_cache.uploaded = nullptr;
+    g_cache.device = dev;
+  }
+  if (!g_cache.done) {
+    GA_HIP(hipEventCreateWithFlags(&g_cache.done, hipEventDisableTiming), "event");
+    GA_HIP(hipEventCreateWithFlags(&g_cache.uploaded, hipEventDisableTiming), "event");
+  }
+  // The previous call's upload must have left the staging buffer before it is refilled, and its
+  // kernels must be done with the device workspace before this stream reuses it.
+  GA_HIP(hipEventSynchronize(g_cache.uploaded), "wait for previous upload");
+  if (g_cache.dev_bytes < L.total) {
+    GA_HIP(hipEventSynchronize(g_cache.done), "wait for previous decode");
+    if (g_cache.dev) (void)hipFree(g_cache.dev);
+    g_cache.dev = nullptr;
+    g_cache.dev_bytes = 0;
+    if (hipMalloc(&g_cache.dev, L.total) != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(GA_ENOMEM, "device workspace of %zu bytes", L.total);
+    }
+    g_cache.dev_bytes = L.total;
+  }
+  const size_t ub = upload_bytes(L);
+  if (g_cache.pin_bytes < ub || !g_cache.pin) {
+    if (g_cache.pin) (void)hipHostFree(g_cache.pin);
+    g_cache.pin = nullptr;
+    g_cache.pin_bytes = 0;
+    if (hipHostMalloc(&g_cache.pin, ub > 0 ? ub : 1) != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(GA_ENOMEM, "pinned staging of %zu bytes", ub);
+    }
+    g_cache.pin_bytes = ub;
+  }
+  pl.dev = g_cache.dev;
+  pl.pin = g_cache.pin;
+  bind(&pl, L);
+  GA_HIP(hipStreamWaitEvent(stream, g_cache.done, 0), "order after previous decode");
+  rc = upload(&pl, segment_table, branch_paths, L, stream);
+  if (rc) return rc;
+  GA_HIP(hipEventRecord(g_cache.uploaded, stream), "record upload");
+  rc = do_schedule(&pl, stream);
+  if (rc) return rc;
+  rc = do_run(&pl, q, kv_page_pool, out, lse, stream);
+  if (rc) return rc;
+  GA_HIP(hipEventRecord(g_cache.done, stream), "record decode");
+  return GA_OK;
+}
+
+}  // extern "C"

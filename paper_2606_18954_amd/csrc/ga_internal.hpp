@@ -1,0 +1,84 @@
+// Internal declarations shared by the host runtime (api.cpp) and the HIP kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <cstdint>
+
+namespace ga {
+
+constexpr int kPageTokens = 16;
+// Query rows (branch x q-head-in-group) handled by one work item: 8 MFMA row tiles of 16.
+constexpr int kRowsPerBlock = 128;
+// Upper bound on pages per work item (the chunk's page ids are staged in LDS).
+constexpr int kMaxChunkPages = 1024;
+constexpr int kAttnThreads = 256;        // 4 wave64 per workgroup
+
+// Device copy of the rollout graph (written once by plan_create's upload).
+struct DevGraph {
+  int32_t S, B, E;
+  const int32_t* seg_len;        // [S]
+  const int64_t* seg_page_off;   // [S+1]
+  const int32_t* seg_pages;      // [P]
+  const int64_t* path_off;       // [B+1]
+  const int32_t* path_segs;      // [E]
+};
+
+// Scheduler outputs (device memory owned by the plan).
+struct DevSchedule {
+  int32_t* grp_cnt;        // [S]   |B(s)|
+  int32_t* grp_fill;       // [S]   scatter cursors
+  int64_t* grp_off;        // [S+1] CSR offsets of B(s)
+  int32_t* grp_tmp;        // [E]   B(s) in arrival order
+  int32_t* grp_br;         // [E]   B(s), ascending branch ids
+  int32_t* entry_branch;   // [E]   branch of each path entry
+  int32_t* entry_rank;     // [E]   position of the entry's branch inside B(s)
+  int32_t* seg_nchunk;     // [S]   page chunks of each segment
+  int64_t* seg_item_off;   // [S+1] first work item of each segment
+  int64_t* seg_prow_off;   // [S+1] first partial row (per q-head) of each segment
+  int4* items;             // [max_items] (segment, chunk, row block, unused)
+  int64_t* counters;       // [4]: items, partial rows, work-queue head, spare
+};
+
+struct AttnArgs {
+  const void* q;
+  const void* pool;
+  const int32_t* seg_len;
+  const int64_t* seg_page_off;
+  const int32_t* seg_pages;
+  const int64_t* grp_off;
+  const int32_t* grp_br;
+  const int32_t* grp_cnt;
+  const int64_t* seg_prow_off;
+  const int4* items;
+  int64_t* counters;
+  float* po;               // [partial rows][Hq][D] normalised partial outputs
+  float* plse;             // [partial rows][Hq] log2-domain log-sum-exp of each partial
+  int32_t Hq, Hkv, group, chunk_pages;
+  float scale_log2;        // softmax scale * log2(e)
+};
+
+struct MergeArgs {
+  const int64_t* path_off;
+  const int32_t* path_segs;
+  const int32_t* entry_rank;
+  const int32_t* grp_cnt;
+  const int32_t* seg_nchunk;
+  const int64_t* seg_prow_off;
+  const float* po;
+  const float* plse;
+  void* out;
+  float* lse;
+  int64_t* counters;       // the attention work-queue head (counters[2]) is re-armed here
+  int32_t B, Hq;
+};
+
+// Launchers (each returns the launch status).
+hipError_t launch_schedule(const DevGraph& g, const DevSchedule& sc, int32_t group,
+                           int32_t chunk_pages, hipStream_t stream);
+hipError_t launch_seg_attn(const AttnArgs& a, int head_dim, bool bf16, int grid,
+                           hipStream_t stream);
+hipError_t launch_merge(const MergeArgs& a, int head_dim, bool bf16, hipStream_t stream);
+// Number of co-resident attention workgroups the persistent grid uses on this device.
+int seg_attn_grid(int head_dim, bool bf16, int num_cus);
+
+}  // namespace ga

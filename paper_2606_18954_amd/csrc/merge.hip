@@ -1,0 +1,85 @@
+// Log-sum-exp merge of per-segment partials along each branch's path.
+//
+// A branch's context is the disjoint union of its segments' tokens (and of each segment's page
+// chunks), so with lambda_i = log2 sum_{j in piece i} 2^(s_j) and o_i the piece's normalised
+// output, the exact result over the whole context is
+//   Lambda = log2 sum_i 2^(lambda_i),  out = sum_i 2^(lambda_i - Lambda) o_i.
+// Pieces are folded in path order, then chunk order, with a running maximum, so the result is
+// deterministic.  The natural-log lse is Lambda * ln 2.
+#include "ga_internal.hpp"
+
+namespace ga {
+namespace {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+template <int D, bool BF16>
+__global__ __launch_bounds__(256) void k_merge(MergeArgs a) {
+  constexpr int LPR = D / 4;               // lanes per (branch, q-head) row, 4 columns each
+  constexpr int RPB = 256 / LPR;           // rows per workgroup
+  const int tid = threadIdx.x;
+  // The attention kernel has drained its work queue (stream order): re-arm it for the next run.
+  if (blockIdx.x == 0 && tid == 0) a.counters[2] = 0;
+  const int64_t row = (int64_t)blockIdx.x * RPB + tid / LPR;
+  const int sub = tid % LPR;
+  if (row >= (int64_t)a.B * a.Hq) return;
+  const int b = (int)(row / a.Hq);
+  const int h = (int)(row % a.Hq);
+  const float NEG_INF = -__builtin_huge_valf();
+  float M = NEG_INF, W = 0.f;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  for (int64_t e = a.path_off[b]; e < a.path_off[b + 1]; ++e) {
+    const int s = a.path_segs[e];
+    const int j = a.entry_rank[e];
+    const int cnt = a.grp_cnt[s];
+    const int nch = a.seg_nchunk[s];
+    const int64_t base = a.seg_prow_off[s];
+    for (int c = 0; c < nch; ++c) {
+      const int64_t idx = (base + (int64_t)c * cnt + j) * a.Hq + h;
+      const float lam = a.plse[idx];
+      const f32x4 o = *reinterpret_cast<const f32x4*>(a.po + idx * D + 4 * sub);
+      const float Mn = fmaxf(M, lam);
+      const float sc = __builtin_amdgcn_exp2f(M - Mn);
+      const float wl = __builtin_amdgcn_exp2f(lam - Mn);
+      acc = acc * sc + o * wl;
+      W = W * sc + wl;
+      M = Mn;
+    }
+  }
+  const f32x4 r = acc * (1.f / W);
+  if constexpr (BF16) {
+    unsigned short u[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) u[i] = __builtin_bit_cast(unsigned short, (__bf16)r[i]);
+    uint2 pk = make_uint2(u[0] | ((unsigned)u[1] << 16), u[2] | ((unsigned)u[3] << 16));
+    *reinterpret_cast<uint2*>(static_cast<unsigned short*>(a.out) + row * D + 4 * sub) = pk;
+  } else {
+    *reinterpret_cast<f32x4*>(static_cast<float*>(a.out) + row * D + 4 * sub) = r;
+  }
+  if (sub == 0) a.lse[row] = (M + __builtin_amdgcn_logf(W)) * 0.69314718055994531f;
+}
+
+template <int D, bool BF16>
+hipError_t launch_t(const MergeArgs& a, hipStream_t stream) {
+  constexpr int RPB = 256 / (D / 4);
+  const int64_t rows = (int64_t)a.B * a.Hq;
+  const int grid = (int)((rows + RPB - 1) / RPB);
+  if (grid == 0) return hipSuccess;
+  hipLaunchKernelGGL((k_merge<D, BF16>), dim3(grid), dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_merge(const MergeArgs& a, int head_dim, bool bf16, hipStream_t stream) {
+  if (bf16) {
+    if (head_dim == 64) return launch_t<64, true>(a, stream);
+    if (head_dim == 128) return launch_t<128, true>(a, stream);
+  } else {
+    if (head_dim == 64) return launch_t<64, false>(a, stream);
+    if (head_dim == 128) return launch_t<128, false>(a, stream);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace ga

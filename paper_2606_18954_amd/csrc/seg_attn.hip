@@ -1,0 +1,375 @@
+// Grouped segment attention (gfx950): one work item = (segment, page chunk, row block, kv-head).
+//
+// All branches that share a segment (B(s), from the scheduler) attend over its tokens together:
+// their queries for the kv-head's q-head group form a tile of R = |B(s)| * (Hq/Hkv) rows, so the
+// segment's K/V are read from HBM once per kv-head and used by every row.  That turns the
+// memory-bound decode step into a dense contraction per segment:
+//
+//   S^T = K Q^T   (16 tokens x 16 rows per MFMA tile, contraction over head_dim)
+//   O^T += V^T P^T (contraction over tokens)
+//
+// Computing the transposed products keeps every row's state in one lane column: lane l owns row
+// l % 16 of a tile, holds scores of tokens 4*(l/16)..+3, and holds output columns
+// 16n + 4*(l/16)..+3.  The softmax scores come out of the first MFMA in exactly the register
+// layout the second MFMA takes as its B operand, so no shuffles are needed between them.
+//
+// Data movement: K/V pages of one kv-head are 16 x D contiguous blocks in HBM; 256 threads copy
+// a stage of pages with 16-byte loads (fully coalesced) into LDS, XOR-swizzled by token so the
+// MFMA operand reads are conflict-free.  The next stage is prefetched into registers while the
+// current one is consumed (double-buffered LDS).  K operands are 16-byte LDS reads; V operands
+// use the gfx950 transposing LDS read (ds_read_b64_tr_b16), which hands each lane 4 tokens of
+// one column.
+//
+// Online softmax (per row, in the log2 domain): m <- max(m, max_j s_j); alpha = 2^(m_old - m);
+// l <- alpha * l + sum_j 2^(s_j - m); O <- alpha * O + P V.  The row maximum is reduced across
+// the four lane groups of the wave; l is kept as per-lane partial sums and reduced once at the
+// end.  Each work item writes normalised partials o = O / l and lambda = m + log2(l) for every
+// row; the merge kernel folds them along each branch's path.
+#include "ga_internal.hpp"
+
+#include <type_traits>
+
+namespace ga {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+
+template <int D, bool BF16>
+struct Cfg {
+  static constexpr int ELT = BF16 ? 2 : 4;
+  static constexpr int ROW = D * ELT;               // bytes of one token row of K or V
+  static constexpr int CPR = ROW / 16;              // 16-byte chunks per token row
+  static constexpr int KVB = 16 * ROW;              // bytes of a page's K (or V) block
+  static constexpr int PB = 2 * KVB;                // bytes of one page of one kv-head
+  static constexpr int SP = PB <= 8192 ? 4 : 2;     // pages per pipeline stage
+  static constexpr int STAGE = SP * PB;
+  static constexpr int LOADS = STAGE / (kAttnThreads * 16);   // 16-B loads per thread per stage
+  static constexpr int NB = D / 16;                 // 16-wide output column blocks
+  static constexpr int QR = BF16 ? D / 32 : D / 4;  // Q operand registers per tile
+  static_assert(STAGE % (kAttnThreads * 16) == 0, "stage must split evenly over the threads");
+};
+
+// Byte offset of 16-byte chunk `ch` of token `tok` inside a K or V block in LDS.
+template <int D, bool BF16>
+__device__ __forceinline__ int swz(int tok, int ch) {
+  using C = Cfg<D, BF16>;
+  return tok * C::ROW + ((ch ^ (tok & (C::CPR - 1))) << 4);
+}
+
+__device__ __forceinline__ float xmax(float v) {
+  v = fmaxf(v, __shfl_xor(v, 16));
+  return fmaxf(v, __shfl_xor(v, 32));
+}
+__device__ __forceinline__ float xsum(float v) {
+  v += __shfl_xor(v, 16);
+  return v + __shfl_xor(v, 32);
+}
+__device__ __forceinline__ float exp2_(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ float log2_(float x) { return __builtin_amdgcn_logf(x); }
+
+template <bool BF16> struct QOp;
+template <> struct QOp<true> { bf16x8 v; };
+template <> struct QOp<false> { float v; };
+
+template <int D, bool BF16>
+__global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
+  using C = Cfg<D, BF16>;
+  using T = typename std::conditional<BF16, __bf16, float>::type;
+  __shared__ __align__(16) unsigned char smem[2 * C::STAGE];
+  __shared__ int s_pages[kMaxChunkPages];
+  __shared__ int64_t s_work;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int r16 = lane & 15, kg = lane >> 4;
+  const int64_t n_work = a.counters[0] * a.Hkv;
+  const float NEG_INF = -__builtin_huge_valf();
+  const unsigned char* pool = static_cast<const unsigned char*>(a.pool);
+  const T* qbase = static_cast<const T*>(a.q);
+
+  for (;;) {
+    if (tid == 0) s_work = (int64_t)atomicAdd((unsigned long long*)&a.counters[2], 1ull);
+    __syncthreads();
+    const int64_t w = s_work;
+    if (w >= n_work) break;
+    const int4 it = a.items[w / a.Hkv];
+    const int kvh = (int)(w % a.Hkv);
+    const int s = it.x, chunk = it.y, rb = it.z;
+
+    const int len = a.seg_len[s];
+    const int npg_seg = (len + kPageTokens - 1) / kPageTokens;
+    const int p0 = chunk * a.chunk_pages;
+    const int np = min(npg_seg, p0 + a.chunk_pages) - p0;
+    const int last_pg = npg_seg - 1 - p0;          // index (in chunk) of the segment's last page
+    const int last_valid = len - (npg_seg - 1) * kPageTokens;
+    const int64_t page_off = a.seg_page_off[s];
+    const int cnt = a.grp_cnt[s];
+    const int64_t goff = a.grp_off[s];
+    const int row0 = rb * kRowsPerBlock;
+    const int R = min(kRowsPerBlock, cnt * a.group - row0);
+    const int nrt = (R + 15) >> 4;
+
+    for (int i = tid; i < np; i += kAttnThreads) s_pages[i] = a.seg_pages[page_off + p0 + i];
+
+    // Wave roles: with >= 3 row tiles the waves split the tiles (tiles wave and wave + 4); with
+    // fewer, waves sharing a tile split the stage's pages and are combined at the end.
+    int ks, split, t0, ntile;
+    if (nrt >= 4) { ks = 1; split = 0; t0 = wave; ntile = (wave + 4 < nrt) ? 2 : 1; }
+    else if (nrt == 3) { ks = 1; split = 0; t0 = wave; ntile = wave < 3 ? 1 : 0; }
+    else if (nrt == 2) { ks = 2; split = wave >> 1; t0 = wave & 1; ntile = 1; }
+    else { ks = 4; split = wave; t0 = 0; ntile = 1; }
+
+    // Q operand (B of S^T = K Q^T): lane holds row r16 of the tile, head_dim slice by kg.
+    QOp<BF16> qop[2][C::QR];
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const int r = (t0 + 4 * k) * 16 + r16;
+      const bool live = k < ntile && r < R;
+      const T* qp = qbase;
+      if (live) {
+        const int gr = row0 + r;
+        const int j = gr / a.group;
+        const int h = kvh * a.group + (gr - j * a.group);
+        const int b = a.grp_br[goff + j];
+        qp = qbase + ((int64_t)b * a.Hq + h) * D;
+      }
+#pragma unroll
+      for (int jj = 0; jj < C::QR; ++jj) {
+        if constexpr (BF16) {
+          bf16x8 v = {};
+          if (live) v = *reinterpret_cast<const bf16x8*>(qp + 32 * jj + 8 * kg);
+          qop[k][jj].v = v;
+        } else {
+          qop[k][jj].v = live ? qp[4 * jj + kg] : 0.f;
+        }
+      }
+    }
+
+    float m[2] = {NEG_INF, NEG_INF}, l[2] = {0.f, 0.f};
+    f32x4 O[2][C::NB];
+#pragma unroll
+    for (int k = 0; k < 2; ++k)
+#pragma unroll
+      for (int n = 0; n < C::NB; ++n) O[k][n] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    uint4 pre[C::LOADS];
+    auto issue = [&](int st) {
+#pragma unroll
+      for (int i = 0; i < C::LOADS; ++i) {
+        const int idx = i * kAttnThreads + tid;
+        const int pis = idx / (C::PB / 16);
+        const int rem = idx % (C::PB / 16);
+        const int kv = rem / (C::KVB / 16);
+        const int tok = (rem % (C::KVB / 16)) / C::CPR;
+        const int ch = rem % C::CPR;
+        const int pg = st * C::SP + pis;
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (pg < np && tok < (pg == last_pg ? last_valid : kPageTokens)) {
+          const int64_t blk = ((int64_t)s_pages[pg] * a.Hkv + kvh) * 2 + kv;
+          v = *reinterpret_cast<const uint4*>(pool + blk * C::KVB + tok * C::ROW + ch * 16);
+        }
+        pre[i] = v;
+      }
+    };
+    auto commit = [&](int st, int buf) {
+#pragma unroll
+      for (int i = 0; i < C::LOADS; ++i) {
+        const int idx = i * kAttnThreads + tid;
+        const int pis = idx / (C::PB / 16);
+        const int rem = idx % (C::PB / 16);
+        const int kv = rem / (C::KVB / 16);
+        const int tok = (rem % (C::KVB / 16)) / C::CPR;
+        const int ch = rem % C::CPR;
+        if (st * C::SP + pis < np)
+          *reinterpret_cast<uint4*>(smem + buf * C::STAGE + pis * C::PB + kv * C::KVB +
+                                    swz<D, BF16>(tok, ch)) = pre[i];
+      }
+    };
+
+    __syncthreads();                       // s_pages visible
+    const int nst = (np + C::SP - 1) / C::SP;
+    issue(0);
+    commit(0, 0);
+    __syncthreads();
+    for (int st = 0; st < nst; ++st) {
+      if (st + 1 < nst) issue(st + 1);
+      const int buf = st & 1;
+      const int npst = min(C::SP, np - st * C::SP);
+      if (ntile > 0) {
+        for (int pis = split; pis < npst; pis += ks) {
+          const unsigned char* kb = smem + buf * C::STAGE + pis * C::PB;
+          const unsigned char* vb = kb + C::KVB;
+          const int valid = (st * C::SP + pis == last_pg) ? last_valid : kPageTokens;
+          f32x4 S[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+#pragma unroll
+          for (int jj = 0; jj < C::QR; ++jj) {
+            if constexpr (BF16) {
+              const bf16x8 ka = *reinterpret_cast<const bf16x8*>(kb + swz<D, BF16>(r16, 4 * jj + kg));
+              S[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qop[0][jj].v, S[0], 0, 0, 0);
+              if (ntile > 1)
+                S[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qop[1][jj].v, S[1], 0, 0, 0);
+            } else {
+              const float ka = *reinterpret_cast<const float*>(kb + swz<D, BF16>(r16, jj) + kg * 4);
+              S[0] = __builtin_amdgcn_mfma_f32_16x16x4f32(ka, qop[0][jj].v, S[0], 0, 0, 0);
+              if (ntile > 1)
+                S[1] = __builtin_amdgcn_mfma_f32_16x16x4f32(ka, qop[1][jj].v, S[1], 0, 0, 0);
+            }
+          }
+          // Online softmax over this page's 16 tokens for each of the wave's tiles.
+          float p[2][4];
+#pragma unroll
+          for (int k = 0; k < 2; ++k) {
+            if (k >= ntile) break;
+            float sv[4];
+            float mx = NEG_INF;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              sv[i] = (4 * kg + i < valid) ? S[k][i] * a.scale_log2 : NEG_INF;
+              mx = fmaxf(mx, sv[i]);
+            }
+            mx = xmax(mx);
+            const float mn = fmaxf(m[k], mx);
+            const float alpha = exp2_(m[k] - mn);
+            m[k] = mn;
+            float ps = 0.f;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              p[k][i] = exp2_(sv[i] - mn);
+              ps += p[k][i];
+            }
+            l[k] = l[k] * alpha + ps;
+#pragma unroll
+            for (int n = 0; n < C::NB; ++n) O[k][n] *= alpha;
+          }
+          if constexpr (BF16) {
+            s16x4 pb[2];
+#pragma unroll
+            for (int k = 0; k < 2; ++k)
+#pragma unroll
+              for (int i = 0; i < 4; ++i)
+                pb[k][i] = __builtin_bit_cast(short, (__bf16)(k < ntile ? p[k][i] : 0.f));
+            const int tv = 4 * kg + (r16 >> 2);
+#pragma unroll
+            for (int n = 0; n < C::NB; ++n) {
+              const int off = tv * C::ROW +
+                              (((2 * n + ((r16 & 3) >> 1)) ^ (tv & (C::CPR - 1))) << 4) +
+                              (r16 & 1) * 8;
+              const s16x4 va = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                  (lds_s16x4*)(vb + off));
+              O[0][n] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pb[0], O[0][n], 0, 0, 0);
+              if (ntile > 1)
+                O[1][n] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pb[1], O[1][n], 0, 0, 0);
+            }
+          } else {
+#pragma unroll
+            for (int n = 0; n < C::NB; ++n) {
+#pragma unroll
+              for (int i = 0; i < 4; ++i) {
+                const int tv = 4 * kg + i;
+                const float va = *reinterpret_cast<const float*>(
+                    vb + swz<D, BF16>(tv, 4 * n + (r16 >> 2)) + (r16 & 3) * 4);
+                O[0][n] = __builtin_amdgcn_mfma_f32_16x16x4f32(va, p[0][i], O[0][n], 0, 0, 0);
+                if (ntile > 1)
+                  O[1][n] = __builtin_amdgcn_mfma_f32_16x16x4f32(va, p[1][i], O[1][n], 0, 0, 0);
+              }
+            }
+          }
+        }
+      }
+      if (st + 1 < nst) commit(st + 1, buf ^ 1);
+      __syncthreads();
+    }
+
+    // Row sums: reduce the per-lane partials across the four lane groups.
+    float L[2];
+#pragma unroll
+    for (int k = 0; k < 2; ++k) L[k] = xsum(l[k]);
+
+    if (ks > 1) {
+      // Waves that split one tile's pages combine through LDS (the stage buffers are free).
+      constexpr int NV = C::NB * 4 + 2;
+      float* cb = reinterpret_cast<float*>(smem);
+      float* mine = cb + wave * NV * 64;
+      mine[0 * 64 + lane] = m[0];
+      mine[1 * 64 + lane] = L[0];
+#pragma unroll
+      for (int n = 0; n < C::NB; ++n)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) mine[(2 + 4 * n + i) * 64 + lane] = O[0][n][i];
+      __syncthreads();
+      if (split == 0) {
+        float M = NEG_INF;
+        for (int sp = 0; sp < ks; ++sp) M = fmaxf(M, cb[(t0 + nrt * sp) * NV * 64 + lane]);
+        float Lc = 0.f;
+        f32x4 Oc[C::NB];
+#pragma unroll
+        for (int n = 0; n < C::NB; ++n) Oc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int sp = 0; sp < ks; ++sp) {
+          const float* o = cb + (t0 + nrt * sp) * NV * 64;
+          const float wgt = exp2_(o[lane] - M);
+          Lc += wgt * o[64 + lane];
+#pragma unroll
+          for (int n = 0; n < C::NB; ++n)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) Oc[n][i] += wgt * o[(2 + 4 * n + i) * 64 + lane];
+        }
+        m[0] = M;
+        L[0] = Lc;
+#pragma unroll
+        for (int n = 0; n < C::NB; ++n) O[0][n] = Oc[n];
+      }
+    }
+
+    if (split == 0) {
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        if (k >= ntile) break;
+        const int r = (t0 + 4 * k) * 16 + r16;
+        if (r < R) {
+          const int gr = row0 + r;
+          const int j = gr / a.group;
+          const int h = kvh * a.group + (gr - j * a.group);
+          const int64_t row = (a.seg_prow_off[s] + (int64_t)chunk * cnt + j) * a.Hq + h;
+          const float inv = 1.f / L[k];
+          float* dst = a.po + row * D + 4 * kg;
+#pragma unroll
+          for (int n = 0; n < C::NB; ++n)
+            *reinterpret_cast<f32x4*>(dst + 16 * n) = O[k][n] * inv;
+          if (kg == 0) a.plse[row] = m[k] + log2_(L[k]);
+        }
+      }
+    }
+    __syncthreads();                       // smem and s_work are reused by the next item
+  }
+}
+
+template <int D, bool BF16>
+hipError_t launch_t(const AttnArgs& a, int grid, hipStream_t stream) {
+  hipLaunchKernelGGL((k_seg_attn<D, BF16>), dim3(grid), dim3(kAttnThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+int seg_attn_grid(int head_dim, bool bf16, int num_cus) {
+  (void)head_dim;
+  (void)bf16;
+  return num_cus * 2;                      // two 256-thread workgroups fit per CU (LDS-bound)
+}
+
+hipError_t launch_seg_attn(const AttnArgs& a, int head_dim, bool bf16, int grid,
+                           hipStream_t stream) {
+  if (bf16) {
+    if (head_dim == 64) return launch_t<64, true>(a, grid, stream);
+    if (head_dim == 128) return launch_t<128, true>(a, grid, stream);
+  } else {
+    if (head_dim == 64) return launch_t<64, false>(a, grid, stream);
+    if (head_dim == 128) return launch_t<128, false>(a, grid, stream);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace ga

@@ -1,0 +1,259 @@
+"""ctypes binding of libgraphattn.so (argument marshalling only).
+
+Every step of the computation runs in the HIP library; this module only turns numpy index arrays
+and torch device tensors into the C ABI's structs and pointers.  If the library is not built, or
+the process has no GPU, the compute entry points raise instead of falling back to anything.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from typing import Optional
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libgraphattn.so")
+
+GA_OK, GA_EINVAL, GA_ERANGE, GA_ENOMEM, GA_EHIP, GA_EUNSUPPORTED = 0, -1, -2, -3, -4, -5
+GA_F32, GA_BF16 = 0, 1
+STATUS_NAMES = {0: "GA_OK", -1: "GA_EINVAL", -2: "GA_ERANGE", -3: "GA_ENOMEM", -4: "GA_EHIP",
+                -5: "GA_EUNSUPPORTED"}
+
+
+class GraphAttnError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {message}")
+        self.status = status
+        self.message = message
+
+
+class SegmentTable(ctypes.Structure):
+    _fields_ = [("num_segments", ctypes.c_int32),
+                ("seg_len", ctypes.POINTER(ctypes.c_int32)),
+                ("seg_page_offsets", ctypes.POINTER(ctypes.c_int64)),
+                ("seg_pages", ctypes.POINTER(ctypes.c_int32))]
+
+
+class BranchPaths(ctypes.Structure):
+    _fields_ = [("num_branches", ctypes.c_int32),
+                ("path_offsets", ctypes.POINTER(ctypes.c_int64)),
+                ("path_segs", ctypes.POINTER(ctypes.c_int32))]
+
+
+class Params(ctypes.Structure):
+    _fields_ = [("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("page_size", ctypes.c_int32),
+                ("num_pages", ctypes.c_int64), ("dtype", ctypes.c_int32),
+                ("softmax_scale", ctypes.c_float)]
+
+
+class PlanInfo(ctypes.Structure):
+    _fields_ = [("num_segments", ctypes.c_int32), ("num_branches", ctypes.c_int32),
+                ("num_entries", ctypes.c_int32), ("chunk_pages", ctypes.c_int32),
+                ("rows_per_block", ctypes.c_int32), ("num_items", ctypes.c_int64),
+                ("num_partial_rows", ctypes.c_int64)]
+
+
+class Profile(ctypes.Structure):
+    _fields_ = [("schedules", ctypes.c_int32), ("runs", ctypes.c_int32),
+                ("sched_ms", ctypes.c_double), ("attn_ms", ctypes.c_double),
+                ("merge_ms", ctypes.c_double)]
+
+
+_lib = None
+
+
+def load_library() -> ctypes.CDLL:
+    """Load the HIP library; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                           f"`python -m paper_2606_18954_amd.build_lib` (there is no fallback)")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    P = ctypes.POINTER
+    lib.graphattn_decode.argtypes = [vp, vp, P(SegmentTable), P(BranchPaths), vp, vp, P(Params), vp]
+    lib.graphattn_decode.restype = ctypes.c_int
+    lib.graphattn_plan_create.argtypes = [P(SegmentTable), P(BranchPaths), P(Params), vp, P(vp)]
+    lib.graphattn_plan_create.restype = ctypes.c_int
+    lib.graphattn_schedule.argtypes = [vp, vp]
+    lib.graphattn_schedule.restype = ctypes.c_int
+    lib.graphattn_run.argtypes = [vp, vp, vp, vp, vp, vp]
+    lib.graphattn_run.restype = ctypes.c_int
+    lib.graphattn_plan_info.argtypes = [vp, P(PlanInfo)]
+    lib.graphattn_plan_info.restype = ctypes.c_int
+    lib.graphattn_plan_debug_dump.argtypes = [vp, vp, P(i64), P(i32), P(i32), P(i32), P(i32)]
+    lib.graphattn_plan_debug_dump.restype = ctypes.c_int
+    lib.graphattn_plan_profile.argtypes = [vp, i32]
+    lib.graphattn_plan_profile.restype = ctypes.c_int
+    lib.graphattn_plan_profile_read.argtypes = [vp, P(Profile)]
+    lib.graphattn_plan_profile_read.restype = ctypes.c_int
+    lib.graphattn_plan_destroy.argtypes = [vp]
+    lib.graphattn_plan_destroy.restype = None
+    lib.graphattn_last_error.argtypes = []
+    lib.graphattn_last_error.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def _check(status: int):
+    if status != GA_OK:
+        msg = load_library().graphattn_last_error().decode(errors="replace")
+        raise GraphAttnError(status, msg)
+
+
+def _ptr(a: np.ndarray, ctype):
+    return a.ctypes.data_as(ctypes.POINTER(ctype))
+
+
+class HostGraph:
+    """The rollout graph's index arrays as the C structs (keeps the numpy arrays alive)."""
+
+    def __init__(self, seg_len, seg_page_offsets, seg_pages, path_offsets, path_segs):
+        self.seg_len = np.ascontiguousarray(seg_len, dtype=np.int32)
+        self.seg_page_offsets = np.ascontiguousarray(seg_page_offsets, dtype=np.int64)
+        self.seg_pages = np.ascontiguousarray(seg_pages, dtype=np.int32)
+        self.path_offsets = np.ascontiguousarray(path_offsets, dtype=np.int64)
+        self.path_segs = np.ascontiguousarray(path_segs, dtype=np.int32)
+        self.st = SegmentTable(len(self.seg_len), _ptr(self.seg_len, ctypes.c_int32),
+                               _ptr(self.seg_page_offsets, ctypes.c_int64),
+                               _ptr(self.seg_pages, ctypes.c_int32))
+        self.bp = BranchPaths(len(self.path_offsets) - 1, _ptr(self.path_offsets, ctypes.c_int64),
+                              _ptr(self.path_segs, ctypes.c_int32))
+
+    @classmethod
+    def from_graph(cls, g) -> "HostGraph":
+        return cls(g.seg_len, g.seg_page_offsets, g.seg_pages, g.path_offsets, g.path_segs)
+
+
+def make_params(num_q_heads: int, num_kv_heads: int, head_dim: int, num_pages: int, dtype: str,
+                softmax_scale: float = 0.0) -> Params:
+    return Params(num_q_heads, num_kv_heads, head_dim, 16, num_pages,
+                  GA_BF16 if dtype == "bf16" else GA_F32, softmax_scale)
+
+
+def _stream_handle(stream) -> int:
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return int(stream.cuda_stream)
+
+
+def _dev_ptr(t) -> int:
+    if t is None:
+        return 0
+    if not t.is_cuda:
+        raise ValueError("tensors passed to the library must live on the GPU")
+    if not t.is_contiguous():
+        raise ValueError("tensors passed to the library must be contiguous")
+    return int(t.data_ptr())
+
+
+def decode(q, pool, graph: HostGraph, params: Params, out=None, lse=None, stream=None):
+    """graphattn_decode on torch tensors: returns (out [B, Hq, D], lse [B, Hq] float32)."""
+    import torch
+    lib = load_library()
+    B = graph.bp.num_branches
+    if out is None:
+        out = torch.empty((B, params.num_q_heads, params.head_dim), dtype=q.dtype, device=q.device)
+    if lse is None:
+        lse = torch.empty((B, params.num_q_heads), dtype=torch.float32, device=q.device)
+    _check(lib.graphattn_decode(_dev_ptr(q), _dev_ptr(pool), ctypes.byref(graph.st),
+                                ctypes.byref(graph.bp), _dev_ptr(out), _dev_ptr(lse),
+                                ctypes.byref(params), _stream_handle(stream)))
+    return out, lse
+
+
+class Plan:
+    """graphattn_plan_create / schedule / run / destroy."""
+
+    def __init__(self, graph: HostGraph, params: Params, stream=None):
+        self.lib = load_library()
+        self.graph = graph
+        self.params = params
+        h = ctypes.c_void_p()
+        _check(self.lib.graphattn_plan_create(ctypes.byref(graph.st), ctypes.byref(graph.bp),
+                                              ctypes.byref(params), _stream_handle(stream),
+                                              ctypes.byref(h)))
+        self.handle = h
+
+    def schedule(self, stream=None):
+        _check(self.lib.graphattn_schedule(self.handle, _stream_handle(stream)))
+
+    def run(self, q, pool, out, lse, stream=None):
+        _check(self.lib.graphattn_run(self.handle, _dev_ptr(q), _dev_ptr(pool), _dev_ptr(out),
+                                      _dev_ptr(lse), _stream_handle(stream)))
+
+    def info(self) -> PlanInfo:
+        inf = PlanInfo()
+        _check(self.lib.graphattn_plan_info(self.handle, ctypes.byref(inf)))
+        return inf
+
+    def debug_dump(self, stream=None):
+        """Device schedule as numpy arrays: group offsets/branches, entry ranks, items, chunks."""
+        inf = self.info()
+        S, E = inf.num_segments, inf.num_entries
+        goff = np.zeros(S + 1, dtype=np.int64)
+        gbr = np.zeros(max(E, 1), dtype=np.int32)
+        rk = np.zeros(max(E, 1), dtype=np.int32)
+        nit = max(int(inf.num_items), 0)
+        items = np.zeros(max(3 * nit, 3), dtype=np.int32)
+        nch = np.zeros(max(S, 1), dtype=np.int32)
+        _check(self.lib.graphattn_plan_debug_dump(
+            self.handle, _stream_handle(stream), _ptr(goff, ctypes.c_int64),
+            _ptr(gbr, ctypes.c_int32), _ptr(rk, ctypes.c_int32), _ptr(items, ctypes.c_int32),
+            _ptr(nch, ctypes.c_int32)))
+        return {"group_offsets": goff, "group_branches": gbr[:E], "entry_ranks": rk[:E],
+                "items": items[:3 * nit].reshape(nit, 3), "segment_chunks": nch[:S]}
+
+    def profile(self, max_calls: int):
+        """Record HIP-event kernel times for the next ``max_calls`` schedule/run calls."""
+        _check(self.lib.graphattn_plan_profile(self.handle, int(max_calls)))
+
+    def profile_read(self) -> Profile:
+        pr = Profile()
+        _check(self.lib.graphattn_plan_profile_read(self.handle, ctypes.byref(pr)))
+        return pr
+
+    def close(self):
+        if self.handle:
+            self.lib.graphattn_plan_destroy(self.handle)
+            self.handle = None
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def validate_only(graph: HostGraph, params: Params) -> int:
+    """Run the library's host-side validation through graphattn_decode with NULL device
+    buffers and no branches to compute; used by CPU tests of the error paths.  Returns the
+    status (only meaningful for invalid inputs, which are rejected before any HIP call)."""
+    lib = load_library()
+    return lib.graphattn_decode(None, None, ctypes.byref(graph.st), ctypes.byref(graph.bp), None,
+                                None, ctypes.byref(params), None)
+
+
+def last_error() -> str:
+    return load_library().graphattn_last_error().decode(errors="replace")
+
+
+def header_symbols() -> list:
+    """Function names declared in include/graphattn.h."""
+    import re
+    hdr = os.path.join(os.path.dirname(_PKG), "include", "graphattn.h")
+    text = open(hdr).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(graphattn_\w+)\s*\(", text)))

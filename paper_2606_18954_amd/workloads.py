@@ -26,6 +26,7 @@ from __future__ import annotations
 
 import dataclasses
 import math
+import os
 from typing import Dict, List, Optional, Sequence
 
 import numpy as np
@@ -136,26 +137,48 @@ def _bf16_rne(x: torch.Tensor) -> torch.Tensor:
     return x.to(torch.bfloat16)
 
 
+def _chunk_seed(seed: int, stream: int) -> int:
+    """Independent 63-bit seed for one chunk of the data stream."""
+    st = np.random.SeedSequence([int(seed), int(stream) + 1]).generate_state(1, np.uint64)[0]
+    return int(st) & ((1 << 63) - 1)
+
+
+def _randn(seed: int, stream: int, shape) -> torch.Tensor:
+    gen = torch.Generator(device="cpu")
+    gen.manual_seed(_chunk_seed(seed, stream))
+    return torch.randn(shape, generator=gen, dtype=torch.float32)
+
+
 def draw_data(graph: RolloutGraph, Hq: int, Hkv: int, D: int, dtype: str, seed: int,
               poison: bool = False, kzero_tags: bool = False):
     """Draw pool then q, i.i.d. N(0,1) in fp32, then round to ``dtype``.
+
+    The pool is drawn in chunks of pages, chunk c from its own generator seeded by (seed, c), so
+    chunks can be drawn in parallel and the values do not depend on the thread count; q comes
+    from the stream after the last pool chunk.
 
     ``poison`` writes NaN into every free page and into the unused slots of each segment's last
     page (the contract says those contents are unspecified). ``kzero_tags`` sets K = 0 and
     writes a per-segment tag vector into V (token values of segment s are
     ``(1 + s // D) * e_{s mod D}``), which gives every branch a closed-form answer.
     """
-    gen = torch.Generator(device="cpu")
-    gen.manual_seed(seed)
+    import concurrent.futures
     tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
     Np = graph.num_pages
     pool = torch.empty((Np, Hkv, 2, PAGE, D), dtype=tdt)
-    for p0 in range(0, Np, _DRAW_CHUNK_PAGES):
+    starts = list(range(0, Np, _DRAW_CHUNK_PAGES))
+
+    def one(ci):
+        p0 = starts[ci]
         p1 = min(Np, p0 + _DRAW_CHUNK_PAGES)
-        blk = torch.randn((p1 - p0, Hkv, 2, PAGE, D), generator=gen, dtype=torch.float32)
+        blk = _randn(seed, ci, (p1 - p0, Hkv, 2, PAGE, D))
         pool[p0:p1] = _bf16_rne(blk) if dtype == "bf16" else blk
+
+    workers = max(1, min(16, os.cpu_count() or 1, len(starts)))
+    with concurrent.futures.ThreadPoolExecutor(max_workers=workers) as ex:
+        list(ex.map(one, range(len(starts))))
     B = graph.num_branches
-    q = torch.randn((B, Hq, D), generator=gen, dtype=torch.float32)
+    q = _randn(seed, len(starts), (B, Hq, D))
     q = _bf16_rne(q) if dtype == "bf16" else q
     S = graph.num_segments
     if kzero_tags:

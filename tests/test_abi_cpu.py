@@ -1,0 +1,119 @@
+"""C-ABI checks that need no GPU: the library loads, exports every declared entry point, and
+rejects malformed inputs during host validation (before any device work) with the documented
+status codes."""
+import ctypes
+
+import numpy as np
+import pytest
+
+from paper_2606_18954_amd import graphattn as G
+
+
+def test_library_exports_every_declared_symbol():
+    lib = G.load_library()
+    syms = G.header_symbols()
+    assert set(syms) == {"graphattn_decode", "graphattn_plan_create", "graphattn_schedule",
+                         "graphattn_run", "graphattn_plan_info", "graphattn_plan_debug_dump",
+                         "graphattn_plan_destroy", "graphattn_last_error",
+                         "graphattn_plan_profile", "graphattn_plan_profile_read"}
+    for s in syms:
+        assert hasattr(lib, s), s
+
+
+def _graph(lens=(20, 7, 33), pages=None, paths=((0, 1), (0, 2)), num_pages=None):
+    lens = list(lens)
+    npg = [(l + 15) // 16 for l in lens]
+    offs = np.concatenate([[0], np.cumsum(npg)]).astype(np.int64)
+    if pages is None:
+        pages = np.arange(offs[-1], dtype=np.int32)
+    po = np.concatenate([[0], np.cumsum([len(p) for p in paths])]).astype(np.int64)
+    ps = np.array([s for p in paths for s in p], dtype=np.int32)
+    g = G.HostGraph(lens, offs, pages, po, ps)
+    return g, int(offs[-1]) if num_pages is None else num_pages
+
+
+def _status(g, np_, Hq=8, Hkv=2, D=64, dtype="f32", page=16, scale=0.0):
+    p = G.make_params(Hq, Hkv, D, np_, dtype, scale)
+    p.page_size = page
+    return G.validate_only(g, p)
+
+
+def test_null_structs_rejected():
+    lib = G.load_library()
+    p = G.make_params(8, 2, 64, 4, "f32")
+    g, _ = _graph()
+    assert lib.graphattn_decode(None, None, None, ctypes.byref(g.bp), None, None,
+                                ctypes.byref(p), None) == G.GA_EINVAL
+    assert lib.graphattn_decode(None, None, ctypes.byref(g.st), None, None, None,
+                                ctypes.byref(p), None) == G.GA_EINVAL
+    assert lib.graphattn_decode(None, None, ctypes.byref(g.st), ctypes.byref(g.bp), None, None,
+                                None, None) == G.GA_EINVAL
+    assert "NULL" in G.last_error()
+    h = ctypes.c_void_p(1)
+    assert lib.graphattn_plan_create(ctypes.byref(g.st), ctypes.byref(g.bp), None, None,
+                                     ctypes.byref(h)) == G.GA_EINVAL
+    assert h.value is None                       # *plan is cleared on error
+    assert lib.graphattn_plan_create(ctypes.byref(g.st), ctypes.byref(g.bp), ctypes.byref(p),
+                                     None, None) == G.GA_EINVAL
+    assert lib.graphattn_schedule(None, None) == G.GA_EINVAL
+    assert lib.graphattn_run(None, None, None, None, None, None) == G.GA_EINVAL
+    lib.graphattn_plan_destroy(None)              # no-op
+
+
+@pytest.mark.parametrize("Hq,Hkv,D,dtype,page,scale,code", [
+    (8, 3, 64, "f32", 16, 0.0, G.GA_EINVAL),          # Hq % Hkv
+    (0, 2, 64, "f32", 16, 0.0, G.GA_EINVAL),
+    (8, 0, 64, "f32", 16, 0.0, G.GA_EINVAL),
+    (8, 2, 96, "f32", 16, 0.0, G.GA_EUNSUPPORTED),    # head_dim
+    (8, 2, 64, "f32", 32, 0.0, G.GA_EUNSUPPORTED),    # page size
+    (8, 2, 64, "f32", 16, float("nan"), G.GA_EINVAL),
+    (8, 2, 64, "f32", 16, -1.0, G.GA_EINVAL),
+])
+def test_param_errors(Hq, Hkv, D, dtype, page, scale, code):
+    g, n = _graph()
+    assert _status(g, n, Hq, Hkv, D, dtype, page, scale) == code
+    assert G.last_error()
+
+
+def test_bad_dtype():
+    g, n = _graph()
+    p = G.make_params(8, 2, 64, n, "f32")
+    p.dtype = 7
+    assert G.validate_only(g, p) == G.GA_EUNSUPPORTED
+
+
+def test_graph_errors():
+    # empty path
+    g, n = _graph(paths=((0,), ()))
+    assert _status(g, n) == G.GA_EINVAL and "empty path" in G.last_error()
+    # duplicate segment in a path
+    g, n = _graph(paths=((0, 1, 0),))
+    assert _status(g, n) == G.GA_EINVAL and "twice" in G.last_error()
+    # segment id out of range
+    g, n = _graph(paths=((0, 3),))
+    assert _status(g, n) == G.GA_ERANGE
+    g, n = _graph(paths=((-1,),))
+    assert _status(g, n) == G.GA_ERANGE
+    # page id out of range
+    g, n = _graph(pages=np.array([0, 1, 2, 3, 9], dtype=np.int32), num_pages=5)
+    assert _status(g, n) == G.GA_ERANGE and "seg_pages" in G.last_error()
+    g, n = _graph(pages=np.array([0, 1, 2, -4, 3], dtype=np.int32), num_pages=5)
+    assert _status(g, n) == G.GA_ERANGE
+    # zero-length segment
+    g = G.HostGraph([0, 5], [0, 0, 1], [0], [0, 1], [1])
+    assert _status(g, 1) == G.GA_EINVAL and "length" in G.last_error()
+    # too few pages for the segment length
+    g = G.HostGraph([40], [0, 2], [0, 1], [0, 1], [0])
+    assert _status(g, 2) == G.GA_EINVAL and "pages" in G.last_error()
+    # CSR offsets that do not start at 0 / decrease
+    g = G.HostGraph([5], [1, 2], [0, 0], [0, 1], [0])
+    assert _status(g, 2) == G.GA_EINVAL
+    g = G.HostGraph([5, 5], [0, 1, 2], [0, 1], [0, 2, 1], [0, 1])
+    assert _status(g, 2) == G.GA_EINVAL
+
+
+def test_null_device_buffers_with_branches():
+    g, n = _graph()
+    p = G.make_params(8, 2, 64, n, "f32")
+    assert G.validate_only(g, p) == G.GA_EINVAL
+    assert "non-NULL" in G.last_error()

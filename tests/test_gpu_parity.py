@@ -1,0 +1,210 @@
+"""Parity of the HIP path (through the C ABI) with the fp64 CPU oracle on seeded inputs.
+
+Bar: max |out - oracle| <= 1e-2 and max |lse - oracle| <= 1e-3 (bf16 inputs, fp32 accumulation);
+the fp32 tiny graph must also stay within 1e-4 (a quality gate, not the binding bar).
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import graphattn_oracle as O
+from paper_2606_18954_amd import graphattn as G
+from paper_2606_18954_amd import workloads as W
+
+from gpu_util import (TOL_LSE, TOL_OUT, check_workload, compare, gpu_decode, oracle_decode,
+                      params_of, say, to_device)
+
+pytestmark = pytest.mark.gpu
+
+
+# ---------------------------------------------------------------------------------------------
+# The configurations: full size where the oracle finishes in seconds, otherwise fewer prompts
+# (same shapes) compared in full plus the full size compared on sampled branches.
+# ---------------------------------------------------------------------------------------------
+
+def test_config1_tiny_fp32():
+    wl = W.config1_tiny(slack_pages=6, poison=True)
+    dout, dlse = check_workload(wl)
+    assert dout <= 1e-4 and dlse <= 1e-4
+
+
+def test_config2_tree_full():
+    check_workload(W.config2_tree(slack_pages=17, poison=True))
+
+
+def test_config3_merged_dag_reduced():
+    check_workload(W.config3_merged_dag(prompts=6, slack_pages=9, poison=True))
+
+
+def test_config4_long_reduced():
+    check_workload(W.config4_long(prompts=2, slack_pages=5, poison=True))
+
+
+def test_config5_chain_reduced():
+    check_workload(W.config5_chain(paths_n=12, slack_pages=3, poison=True))
+
+
+def test_config5_graph_reduced():
+    check_workload(W.config5_graph(prompts=2, slack_pages=3, poison=True))
+
+
+def _full_size_plan_path(wl, n_sample, seed):
+    """The launch configuration the benchmark times: plan, GPU schedule, run."""
+    q, pool = to_device(wl)
+    hg = G.HostGraph.from_graph(wl.graph)
+    B, Hq, D = wl.graph.num_branches, wl.num_q_heads, wl.head_dim
+    out = torch.empty((B, Hq, D), dtype=q.dtype, device="cuda")
+    lse = torch.empty((B, Hq), dtype=torch.float32, device="cuda")
+    with G.Plan(hg, params_of(wl)) as plan:
+        plan.schedule()
+        plan.run(q, pool, out, lse)
+        torch.cuda.synchronize()
+    go, gl = out.double().cpu().numpy(), lse.double().cpu().numpy()
+    assert np.isfinite(go).all() and np.isfinite(gl).all()
+    br = W.sample_branches(wl.graph, n_sample, seed)
+    oo, ol = oracle_decode(wl, br)
+    compare(wl.name + " (sampled)", go[br], gl[br], oo, ol)
+    return go, gl
+
+
+@pytest.mark.parametrize("name", ["c3", "c4", "c5chain", "c5graph"])
+def test_full_size_sampled(name):
+    wl = W.CONFIGS[name]()
+    say(f"[case] full-size {name}: B={wl.graph.num_branches} pages={wl.graph.num_pages}")
+    _full_size_plan_path(wl, 24, seed=7)
+
+
+# ---------------------------------------------------------------------------------------------
+# Structure: closed forms, poisoned slack, determinism, multi-run plans, permutations
+# ---------------------------------------------------------------------------------------------
+
+def test_tag_closed_form_on_gpu():
+    """K = 0: lse = ln L_b, out = sum_s (len_s / L_b) tag_s; NaN in all slack must not leak."""
+    wl = W.config3_merged_dag(prompts=3, kzero_tags=True, slack_pages=11, poison=True)
+    go, gl = gpu_decode(wl)
+    g = wl.graph
+    D = wl.head_dim
+    for b in range(g.num_branches):
+        Lb = g.path_tokens(b)
+        exp = np.zeros(D)
+        for s in g.path(b):
+            exp[s % D] += (1 + s // D) * g.seg_len[s] / Lb
+        assert np.abs(gl[b] - math.log(Lb)).max() < 1e-5, b
+        assert np.abs(go[b] - exp[None, :]).max() < 8e-3, b
+
+
+def test_determinism_bitwise():
+    wl = W.config2_tree(prompts=3, slack_pages=4, poison=True)
+    q, pool = to_device(wl)
+    hg = G.HostGraph.from_graph(wl.graph)
+    o1, l1 = G.decode(q, pool, hg, params_of(wl))
+    o2, l2 = G.decode(q, pool, hg, params_of(wl))
+    torch.cuda.synchronize()
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
+    assert torch.equal(l1, l2)
+
+
+def test_plan_serves_several_layers():
+    """One schedule, several runs with different q / pools (layers of one decode step)."""
+    wl = W.config3_merged_dag(prompts=2)
+    hg = G.HostGraph.from_graph(wl.graph)
+    B, Hq, D = wl.graph.num_branches, wl.num_q_heads, wl.head_dim
+    with G.Plan(hg, params_of(wl)) as plan:
+        plan.schedule()
+        for layer in range(3):
+            q2, pool2 = W.draw_data(wl.graph, Hq, wl.num_kv_heads, D, "bf16", wl.seed + 17 * layer)
+            wl_l = W.Workload(wl.name + f" layer {layer}", wl.graph, Hq, wl.num_kv_heads, D,
+                              "bf16", q2, pool2, wl.seed)
+            out = torch.empty((B, Hq, D), dtype=torch.bfloat16, device="cuda")
+            lse = torch.empty((B, Hq), dtype=torch.float32, device="cuda")
+            plan.run(q2.cuda(), pool2.cuda(), out, lse)
+            torch.cuda.synchronize()
+            oo, ol = oracle_decode(wl_l)
+            compare(wl_l.name, out.double().cpu().numpy(), lse.double().cpu().numpy(), oo, ol)
+
+
+def test_path_order_does_not_matter():
+    wl = W.config2_tree(prompts=2, slack_pages=2)
+    go, gl = gpu_decode(wl)
+    g = wl.graph
+    segs = g.path_segs.copy()
+    for b in range(g.num_branches):
+        a, e = g.path_offsets[b], g.path_offsets[b + 1]
+        segs[a:e] = segs[a:e][::-1]
+    g2 = W.RolloutGraph(g.seg_len, g.seg_page_offsets, g.seg_pages, g.path_offsets, segs,
+                        g.num_pages)
+    go2, gl2 = gpu_decode(wl, graph=g2)
+    assert np.abs(go - go2).max() <= 8e-3 and np.abs(gl - gl2).max() <= 1e-5
+
+
+def test_empty_step():
+    wl = W.config1_tiny()
+    g = W.assemble_graph([5, 9], [], 3)
+    q = torch.zeros((0, 8, 64), dtype=torch.float32, device="cuda")
+    pool = wl.pool[:1].cuda()
+    out = torch.full((1,), 7.0, device="cuda")
+    hg = G.HostGraph.from_graph(g)
+    p = G.make_params(8, 2, 64, g.num_pages, "f32")
+    o, l = G.decode(q, pool, hg, p)
+    torch.cuda.synchronize()
+    assert o.shape == (0, 8, 64) and l.shape == (0, 8)
+
+
+# ---------------------------------------------------------------------------------------------
+# Edge cases: tiny and huge groups, one-token segments, heavy chunking, every head shape
+# ---------------------------------------------------------------------------------------------
+
+def _mk(lens, paths, Hq, Hkv, D, dtype, seed, slack=3):
+    g = W.assemble_graph(lens, paths, seed, slack)
+    return W.make_workload(f"custom {Hq}/{Hkv}/{D} {dtype} S={len(lens)} B={len(paths)}", g,
+                           Hq, Hkv, D, dtype, seed, poison=True)
+
+
+@pytest.mark.parametrize("Hq,Hkv", [(4, 4), (16, 4), (20, 4), (28, 4), (64, 8), (40, 8)])
+@pytest.mark.parametrize("D", [64, 128])
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_head_shapes(Hq, Hkv, D, dtype):
+    rng = np.random.default_rng(Hq * 1000 + D + (dtype == "f32"))
+    g = W.random_graph(rng, 7, 9, 80, 4, slack_pages=4, seed=Hq + D)
+    wl = W.make_workload(f"random DAG {Hq}/{Hkv}/{D} {dtype}", g, Hq, Hkv, D, dtype, Hq + D,
+                         poison=True)
+    check_workload(wl)
+
+
+def test_one_token_segments():
+    lens = [1, 2, 1, 3, 1, 17, 16, 15]
+    paths = [[0], [0, 1], [2, 3, 4], [5, 6, 7, 0], [6], [7, 1, 2]]
+    check_workload(_mk(lens, paths, 28, 4, 128, "bf16", 5))
+    check_workload(_mk(lens, paths, 8, 2, 64, "f32", 6))
+
+
+def test_large_group_row_blocks():
+    """A root shared by 45 branches: 315 rows -> three row blocks (128, 128, 59)."""
+    lens = [700] + [33 + 5 * i for i in range(45)]
+    paths = [[0, 1 + i] for i in range(45)]
+    check_workload(_mk(lens, paths, 28, 4, 128, "bf16", 8))
+
+
+def test_long_segment_chunking():
+    """A 40k-token segment is split into many page chunks, all folded by the merge."""
+    lens = [40000, 100, 260, 1]
+    paths = [[0, 1], [0, 2], [0, 3], [1]]
+    wl = _mk(lens, paths, 28, 4, 128, "bf16", 9)
+    hg = G.HostGraph.from_graph(wl.graph)
+    with G.Plan(hg, params_of(wl)) as plan:
+        assert plan.info().chunk_pages < (40000 + 15) // 16
+    check_workload(wl)
+
+
+def test_scale_override():
+    wl = W.config2_tree(prompts=1)
+    q, pool = to_device(wl)
+    hg = G.HostGraph.from_graph(wl.graph)
+    out, lse = G.decode(q, pool, hg, params_of(wl, scale=0.05))
+    torch.cuda.synchronize()
+    g = wl.graph
+    oo, ol = O.decode(wl.q_bits(), wl.pool_bits(), g.seg_len, g.seg_page_offsets, g.seg_pages,
+                      g.path_offsets, g.path_segs, 28, 4, 128, "bf16", scale=0.05)
+    compare("scale 0.05", out.double().cpu().numpy(), lse.double().cpu().numpy(), oo, ol)

@@ -1,0 +1,97 @@
+"""The GPU segment scheduler against plain-loop CPU grouping: bit-exact groups, ranks, chunking
+and work list, and identical schedules on repeated runs."""
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import graphattn_oracle as O
+from paper_2606_18954_amd import graphattn as G
+from paper_2606_18954_amd import workloads as W
+
+from gpu_util import params_of, say
+
+pytestmark = pytest.mark.gpu
+
+ROWS_PER_BLOCK = 128
+
+
+def expected_items(g, group, chunk_pages, cnt):
+    items = []
+    for s in range(g.num_segments):
+        if cnt[s] == 0:
+            continue
+        npg = (int(g.seg_len[s]) + 15) // 16
+        nch = (npg + chunk_pages - 1) // chunk_pages
+        nrb = (cnt[s] * group + ROWS_PER_BLOCK - 1) // ROWS_PER_BLOCK
+        for c in range(nch):
+            for rb in range(nrb):
+                items.append((s, c, rb))
+    return np.array(items, dtype=np.int32).reshape(-1, 3)
+
+
+def check_schedule(wl):
+    g = wl.graph
+    say(f"[case] schedule of {wl.name}")
+    hg = G.HostGraph.from_graph(g)
+    with G.Plan(hg, params_of(wl)) as plan:
+        plan.schedule()
+        d = plan.debug_dump()
+        info = plan.info()
+        plan.schedule()                       # rescheduling gives the same bits
+        d2 = plan.debug_dump()
+    offs, ids = O.segment_groups(g.path_offsets, g.path_segs, g.num_segments)
+    ranks = O.branch_slot_ranks(g.path_offsets, g.path_segs, g.num_segments)
+    assert np.array_equal(d["group_offsets"], offs)
+    assert np.array_equal(d["group_branches"], ids)
+    assert np.array_equal(d["entry_ranks"], ranks)
+    cnt = np.diff(offs)
+    group = wl.num_q_heads // wl.num_kv_heads
+    exp_items = expected_items(g, group, info.chunk_pages, cnt)
+    assert np.array_equal(d["items"], exp_items)
+    chunks = np.array([((int(g.seg_len[s]) + 15) // 16 + info.chunk_pages - 1) // info.chunk_pages
+                       if cnt[s] else 0 for s in range(g.num_segments)], dtype=np.int32)
+    assert np.array_equal(d["segment_chunks"], chunks)
+    assert info.num_partial_rows == int(sum(chunks[s] for s in g.path_segs))
+    for k in d:
+        assert np.array_equal(d[k], d2[k]), k
+
+
+def test_golden_small_dag():
+    with open(os.path.join(os.path.dirname(__file__), "golden", "groups_small_dag.json")) as f:
+        fx = json.load(f)
+    lens = [40, 17, 5, 90, 16, 1]
+    paths = [fx["path_segs"][a:b] for a, b in zip(fx["path_offsets"][:-1], fx["path_offsets"][1:])]
+    g = W.assemble_graph(lens, paths, 1, 2)
+    wl = W.make_workload("golden small DAG", g, 8, 2, 64, "f32", 1)
+    hg = G.HostGraph.from_graph(g)
+    with G.Plan(hg, params_of(wl)) as plan:
+        plan.schedule()
+        d = plan.debug_dump()
+    assert d["group_offsets"].tolist() == fx["group_offsets"]
+    assert d["group_branches"].tolist() == fx["group_branches"]
+    assert d["entry_ranks"].tolist() == fx["entry_ranks"]
+
+
+@pytest.mark.parametrize("name,kw", [("c1", {}), ("c2", {}), ("c3", {"prompts": 12}),
+                                     ("c4", {"prompts": 3}), ("c5graph", {"prompts": 3})])
+def test_config_schedules(name, kw):
+    check_schedule(W.CONFIGS[name](**kw))
+
+
+def test_random_graphs():
+    rng = np.random.default_rng(42)
+    for t in range(6):
+        g = W.random_graph(rng, int(rng.integers(1, 60)), int(rng.integers(1, 200)), 300, 12,
+                           seed=t)
+        check_schedule(W.make_workload(f"random {t}", g, 28, 4, 64, "bf16", t))
+
+
+def test_segment_shared_by_many_branches():
+    n = 600
+    lens = [64] + [5] * n
+    paths = [[0, 1 + i] for i in range(n)]
+    g = W.assemble_graph(lens, paths, 3)
+    check_schedule(W.make_workload("600-way shared root", g, 28, 4, 64, "bf16", 3))

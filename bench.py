@@ -77,8 +77,11 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="c3",
                     choices=["c1", "c2", "c3", "c4", "c5chain", "c5graph"])
-    ap.add_argument("--cpu-sample", type=int, default=128,
+    ap.add_argument("--cpu-sample", type=int, default=1024,
                     help="branches the CPU oracle is timed on (0 skips it)")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="also run a plain 1 GiB device copy (torch elementwise kernel) so HBM "
+                         "counters can be scaled against a kernel of known traffic")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (the design notes "
@@ -163,6 +166,16 @@ def main():
     plan.close()
     del q, pool, out, lse
     torch.cuda.empty_cache()
+    if args.calibrate_copy:
+        n = 1 << 29                                   # 1 GiB of bf16 read, 1 GiB written
+        a = torch.ones(n, dtype=torch.bfloat16, device=dev)
+        b = torch.empty_like(a)
+        for _ in range(3):
+            torch.mul(a, 1.0, out=b)
+        torch.cuda.synchronize()
+        log("copy calibration: 3 launches of a 1 GiB elementwise copy")
+        del a, b
+        torch.cuda.empty_cache()
     if args.cpu_sample > 0:
         log(f"timing the CPU oracle on {args.cpu_sample} branches")
         res["cpu_baseline"] = cpu_baseline(wl, args.cpu_sample)

@@ -25,7 +25,7 @@
  *
  *   q             [B][Hq][D]                 dtype; one decode query per branch and q-head
  *   kv_page_pool  [num_pages][Hkv][2][16][D] dtype; index 0 of the third axis is K, 1 is V
- *   out           [B][Hq][D]                 dtype (same as q)
+ *   out           [B][Hq][D]                 dtype (same as q), or float32 if params->out_f32
  *   lse           [B][Hq]                    float32, natural log of sum_j exp(scale * q.k_j)
  *
  * Token t of segment s sits in page seg_pages[seg_page_offsets[s] + t / 16], slot t % 16.  Each
@@ -85,8 +85,9 @@ typedef struct {
   int32_t head_dim;        /* D: 64 or 128 */
   int32_t page_size;       /* tokens per page: 16 */
   int64_t num_pages;       /* extent of kv_page_pool, for range checks */
-  int32_t dtype;           /* ga_dtype of q, kv_page_pool and out */
+  int32_t dtype;           /* ga_dtype of q and kv_page_pool (and of out unless out_f32) */
   float softmax_scale;     /* 0 selects 1/sqrt(head_dim) */
+  int32_t out_f32;         /* 0: out has dtype; 1: out is float32 (no final rounding) */
 } ga_params;
 
 /* A validated rollout graph uploaded to the device, plus its schedule and workspace. */

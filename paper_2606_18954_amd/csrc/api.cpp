@@ -103,6 +103,7 @@ ga_status validate_params(const ga_params* p) {
   if (p->num_pages < 0) return fail(GA_EINVAL, "num_pages is negative");
   if (!std::isfinite(p->softmax_scale) || p->softmax_scale < 0.f)
     return fail(GA_EINVAL, "softmax_scale must be finite and >= 0");
+  if (p->out_f32 != 0 && p->out_f32 != 1) return fail(GA_EINVAL, "out_f32 must be 0 or 1");
   return GA_OK;
 }
 
@@ -385,7 +386,7 @@ ga_status do_run(ga_plan* pl, const void* q, const void* pool, void* out, float*
   m.counters = pl->sc.counters;
   m.B = pl->z.B;
   m.Hq = pl->p.num_q_heads;
-  GA_HIP(ga::launch_merge(m, pl->p.head_dim, bf16, stream), "merge launch");
+  GA_HIP(ga::launch_merge(m, pl->p.head_dim, bf16 && !pl->p.out_f32, stream), "merge launch");
   if (rec) {
     GA_HIP(hipEventRecord(ev[2], stream), "profile event");
     pl->ev_last = ev[2];

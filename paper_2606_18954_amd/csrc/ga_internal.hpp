@@ -77,7 +77,7 @@ hipError_t launch_schedule(const DevGraph& g, const DevSchedule& sc, int32_t gro
                            int32_t chunk_pages, hipStream_t stream);
 hipError_t launch_seg_attn(const AttnArgs& a, int head_dim, bool bf16, int grid,
                            hipStream_t stream);
-hipError_t launch_merge(const MergeArgs& a, int head_dim, bool bf16, hipStream_t stream);
+hipError_t launch_merge(const MergeArgs& a, int head_dim, bool out_bf16, hipStream_t stream);
 // Number of co-resident attention workgroups the persistent grid uses on this device.
 int seg_attn_grid(int head_dim, bool bf16, int num_cus);
 

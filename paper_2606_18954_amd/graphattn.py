@@ -46,7 +46,7 @@ class Params(ctypes.Structure):
     _fields_ = [("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("page_size", ctypes.c_int32),
                 ("num_pages", ctypes.c_int64), ("dtype", ctypes.c_int32),
-                ("softmax_scale", ctypes.c_float)]
+                ("softmax_scale", ctypes.c_float), ("out_f32", ctypes.c_int32)]
 
 
 class PlanInfo(ctypes.Structure):
@@ -131,9 +131,9 @@ class HostGraph:
 
 
 def make_params(num_q_heads: int, num_kv_heads: int, head_dim: int, num_pages: int, dtype: str,
-                softmax_scale: float = 0.0) -> Params:
+                softmax_scale: float = 0.0, out_f32: bool = False) -> Params:
     return Params(num_q_heads, num_kv_heads, head_dim, 16, num_pages,
-                  GA_BF16 if dtype == "bf16" else GA_F32, softmax_scale)
+                  GA_BF16 if dtype == "bf16" else GA_F32, softmax_scale, int(bool(out_f32)))
 
 
 def _stream_handle(stream) -> int:
@@ -159,7 +159,8 @@ def decode(q, pool, graph: HostGraph, params: Params, out=None, lse=None, stream
     lib = load_library()
     B = graph.bp.num_branches
     if out is None:
-        out = torch.empty((B, params.num_q_heads, params.head_dim), dtype=q.dtype, device=q.device)
+        odt = torch.float32 if params.out_f32 else q.dtype
+        out = torch.empty((B, params.num_q_heads, params.head_dim), dtype=odt, device=q.device)
     if lse is None:
         lse = torch.empty((B, params.num_q_heads), dtype=torch.float32, device=q.device)
     _check(lib.graphattn_decode(_dev_ptr(q), _dev_ptr(pool), ctypes.byref(graph.st),

@@ -23,21 +23,21 @@ def require_gpu():
     G.load_library()
 
 
-def params_of(wl, scale=0.0):
+def params_of(wl, scale=0.0, out_f32=False):
     return G.make_params(wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.graph.num_pages,
-                         wl.dtype, scale)
+                         wl.dtype, scale, out_f32)
 
 
 def to_device(wl):
     return wl.q.cuda(), wl.pool.cuda()
 
 
-def gpu_decode(wl, q=None, pool=None, graph=None):
+def gpu_decode(wl, q=None, pool=None, graph=None, out_f32=False):
     require_gpu()
     if q is None:
         q, pool = to_device(wl)
     hg = G.HostGraph.from_graph(wl.graph if graph is None else graph)
-    out, lse = G.decode(q, pool, hg, params_of(wl))
+    out, lse = G.decode(q, pool, hg, params_of(wl, out_f32=out_f32))
     torch.cuda.synchronize()
     return out.double().cpu().numpy(), lse.double().cpu().numpy()
 
@@ -61,11 +61,11 @@ def compare(tag, got_out, got_lse, ref_out, ref_lse, tol_out=TOL_OUT, tol_lse=TO
     return dout, dlse
 
 
-def check_workload(wl, branches=None, tol_out=TOL_OUT, tol_lse=TOL_LSE):
+def check_workload(wl, branches=None, tol_out=TOL_OUT, tol_lse=TOL_LSE, out_f32=False):
     g = wl.graph
     say(f"[case] {wl.name}: B={g.num_branches} S={g.num_segments} pages={g.num_pages} "
-        f"sampled={'all' if branches is None else len(branches)}")
-    go, gl = gpu_decode(wl)
+        f"sampled={'all' if branches is None else len(branches)} out_f32={out_f32}")
+    go, gl = gpu_decode(wl, out_f32=out_f32)
     oo, ol = oracle_decode(wl, branches)
     if branches is not None:
         go, gl = go[branches], gl[branches]

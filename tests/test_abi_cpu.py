@@ -80,6 +80,9 @@ def test_bad_dtype():
     p = G.make_params(8, 2, 64, n, "f32")
     p.dtype = 7
     assert G.validate_only(g, p) == G.GA_EUNSUPPORTED
+    p = G.make_params(8, 2, 64, n, "bf16")
+    p.out_f32 = 2
+    assert G.validate_only(g, p) == G.GA_EINVAL
 
 
 def test_graph_errors():

@@ -141,7 +141,7 @@ def main():
     mfma = None
     if cnt:
         traffic = float(cnt["fetch_bytes_per_launch"]) + float(cnt["write_bytes_per_launch"])
-        mfma = float(cnt.get("mfma_busy_fraction", "nan"))
+        mfma = float(cnt["mfma_busy_fraction"]) if "mfma_busy_fraction" in cnt else None
     res = {
         "metric": METRIC,
         "value": B / (ms * 1e-3),

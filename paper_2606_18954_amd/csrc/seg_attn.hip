@@ -13,12 +13,16 @@
 // 16n + 4*(l/16)..+3.  The softmax scores come out of the first MFMA in exactly the register
 // layout the second MFMA takes as its B operand, so no shuffles are needed between them.
 //
-// Data movement: K/V pages of one kv-head are 16 x D contiguous blocks in HBM; 256 threads copy
-// a stage of pages with 16-byte loads (fully coalesced) into LDS, XOR-swizzled by token so the
-// MFMA operand reads are conflict-free.  The next stage is prefetched into registers while the
-// current one is consumed (double-buffered LDS).  K operands are 16-byte LDS reads; V operands
-// use the gfx950 transposing LDS read (ds_read_b64_tr_b16), which hands each lane 4 tokens of
-// one column.
+// Data movement: K/V pages of one kv-head are 16 x D contiguous blocks in HBM.  They are copied
+// straight into LDS with the gfx950 direct-to-LDS load (global_load_lds_dwordx4: every lane moves
+// 16 bytes, a wave instruction fills 1 KiB of LDS), so no VGPRs stage the data and several stages
+// stay in flight: a ring of NBUF 16 KiB stages, NBUF-1 of them loading while one is consumed.
+// The global side of each wave instruction is a contiguous 1 KiB run of the page block, with the
+// 16-byte chunks of every token row permuted (XOR with the token index) so that the MFMA
+// operand reads from LDS are free of bank conflicts.  K operands are 16-byte LDS reads; V
+// operands use the gfx950 transposing LDS read (ds_read_b64_tr_b16), which hands each lane 4
+// tokens of one column.  Slots past the end of a segment are filled from its last valid token
+// (finite data whose scores are masked to -inf), so NaN in unused slots never reaches an MFMA.
 //
 // Online softmax (per row, in the log2 domain): m <- max(m, max_j s_j); alpha = 2^(m_old - m);
 // l <- alpha * l + sum_j 2^(s_j - m); O <- alpha * O + P V.  The row maximum is reduced across
@@ -44,13 +48,46 @@ struct Cfg {
   static constexpr int CPR = ROW / 16;              // 16-byte chunks per token row
   static constexpr int KVB = 16 * ROW;              // bytes of a page's K (or V) block
   static constexpr int PB = 2 * KVB;                // bytes of one page of one kv-head
-  static constexpr int SP = PB <= 8192 ? 4 : 2;     // pages per pipeline stage
-  static constexpr int STAGE = SP * PB;
-  static constexpr int LOADS = STAGE / (kAttnThreads * 16);   // 16-B loads per thread per stage
+  static constexpr int STAGE = 16384;               // bytes per pipeline stage
+  static constexpr int SP = STAGE / PB;             // pages per stage
+  static constexpr int NBUF = 4;                    // stages in the LDS ring
+  static constexpr int IPP = PB / 1024;             // 1 KiB DMA wave instructions per page
+  static constexpr int IPW = IPP / (kAttnThreads / 64);   // ... issued by each wave per page
   static constexpr int NB = D / 16;                 // 16-wide output column blocks
   static constexpr int QR = BF16 ? D / 32 : D / 4;  // Q operand registers per tile
-  static_assert(STAGE % (kAttnThreads * 16) == 0, "stage must split evenly over the threads");
+  static_assert(SP >= 1 && IPW >= 1 && STAGE % PB == 0, "stage must hold whole pages");
+  static_assert((NBUF - 2) * SP * IPW <= 15, "pending DMA count must fit the wait helper");
 };
+
+// Direct-to-LDS copy of 16 bytes per lane: LDS[lds_base + 16 * lane] <- global[src].  Issued as
+// inline assembly so that the compiler's wait-count pass does not treat every later LDS read as
+// a possible alias of the copy (it would drain the whole pipeline before each stage); ordering
+// is explicit instead: wait_vmcnt() before the barrier that publishes a stage.  M0 holds the
+// wave-uniform LDS base; the kernel keeps no other value in M0.
+__device__ __forceinline__ void dma16(const void* src, unsigned lds_base) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+               :: "v"(src), "s"(lds_base) : "memory", "m0");
+}
+
+// s_waitcnt vmcnt(n) for a runtime n in [0, 15] (expcnt and lgkmcnt left alone).
+__device__ __forceinline__ void wait_vmcnt(int n) {
+#define GA_VMW(k) case k: __builtin_amdgcn_s_waitcnt((k) | (7 << 4) | (15 << 8)); break;
+  switch (n) {
+    GA_VMW(0) GA_VMW(1) GA_VMW(2) GA_VMW(3) GA_VMW(4) GA_VMW(5) GA_VMW(6) GA_VMW(7)
+    GA_VMW(8) GA_VMW(9) GA_VMW(10) GA_VMW(11) GA_VMW(12) GA_VMW(13) GA_VMW(14) GA_VMW(15)
+    default: __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8)); break;
+  }
+#undef GA_VMW
+}
+
+// Workgroup barrier without a memory fence: LDS-DMA completion is ordered by the explicit
+// vmcnt wait before it; the empty asm statements keep the compiler from moving LDS accesses
+// across it.
+__device__ __forceinline__ void wg_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
 
 // Byte offset of 16-byte chunk `ch` of token `tok` inside a K or V block in LDS.
 template <int D, bool BF16>
@@ -78,7 +115,7 @@ template <int D, bool BF16>
 __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
   using C = Cfg<D, BF16>;
   using T = typename std::conditional<BF16, __bf16, float>::type;
-  __shared__ __align__(16) unsigned char smem[2 * C::STAGE];
+  __shared__ __align__(1024) unsigned char smem[C::NBUF * C::STAGE];
   __shared__ int s_pages[kMaxChunkPages];
   __shared__ int64_t s_work;
 
@@ -89,6 +126,8 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
   const float NEG_INF = -__builtin_huge_valf();
   const unsigned char* pool = static_cast<const unsigned char*>(a.pool);
   const T* qbase = static_cast<const T*>(a.q);
+  const unsigned lds_ring =
+      (unsigned)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)smem;
 
   for (;;) {
     if (tid == 0) s_work = (int64_t)atomicAdd((unsigned long long*)&a.counters[2], 1ull);
@@ -119,8 +158,11 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
     int ks, split, t0, ntile;
     if (nrt >= 4) { ks = 1; split = 0; t0 = wave; ntile = (wave + 4 < nrt) ? 2 : 1; }
     else if (nrt == 3) { ks = 1; split = 0; t0 = wave; ntile = wave < 3 ? 1 : 0; }
-    else if (nrt == 2) { ks = 2; split = wave >> 1; t0 = wave & 1; ntile = 1; }
-    else { ks = 4; split = wave; t0 = 0; ntile = 1; }
+    else if (nrt == 2) {
+      ks = C::SP < 2 ? C::SP : 2; split = wave >> 1; t0 = wave & 1; ntile = split < ks;
+    } else {
+      ks = C::SP < 4 ? C::SP : 4; split = wave; t0 = 0; ntile = split < ks;
+    }
 
     // Q operand (B of S^T = K Q^T): lane holds row r16 of the tile, head_dim slice by kg.
     QOp<BF16> qop[2][C::QR];
@@ -155,49 +197,50 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
 #pragma unroll
       for (int n = 0; n < C::NB; ++n) O[k][n] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    uint4 pre[C::LOADS];
+    auto stage_pages = [&](int st) { return min(C::SP, np - st * C::SP); };
+    // Direct-to-LDS copy of stage st: wave instruction j covers bytes [1024 j, 1024 j + 1024) of
+    // the stage; this wave issues j = wave, wave + 4, ... (IPW instructions per page).
     auto issue = [&](int st) {
+      const unsigned dst = lds_ring + (st % C::NBUF) * C::STAGE;
+      const int npst = stage_pages(st);
 #pragma unroll
-      for (int i = 0; i < C::LOADS; ++i) {
-        const int idx = i * kAttnThreads + tid;
-        const int pis = idx / (C::PB / 16);
-        const int rem = idx % (C::PB / 16);
-        const int kv = rem / (C::KVB / 16);
-        const int tok = (rem % (C::KVB / 16)) / C::CPR;
-        const int ch = rem % C::CPR;
-        const int pg = st * C::SP + pis;
-        uint4 v = make_uint4(0, 0, 0, 0);
-        if (pg < np && tok < (pg == last_pg ? last_valid : kPageTokens)) {
+      for (int i = 0; i < C::SP * C::IPW; ++i) {
+        const int j = wave + 4 * i;
+        const int pis = j / C::IPP;
+        if (pis < npst) {
+          const int o = j * 1024 + lane * 16;
+          const int rem = o % C::PB;
+          const int kv = rem / C::KVB;
+          const int tok = (rem % C::KVB) / C::ROW;
+          const int pc = (rem % C::ROW) >> 4;
+          const int pg = st * C::SP + pis;
+          const int ts = min(tok, (pg == last_pg ? last_valid : kPageTokens) - 1);
           const int64_t blk = ((int64_t)s_pages[pg] * a.Hkv + kvh) * 2 + kv;
-          v = *reinterpret_cast<const uint4*>(pool + blk * C::KVB + tok * C::ROW + ch * 16);
+          const unsigned char* src =
+              pool + blk * C::KVB + ts * C::ROW + ((pc ^ (tok & (C::CPR - 1))) << 4);
+          dma16(src, __builtin_amdgcn_readfirstlane(dst + j * 1024));
         }
-        pre[i] = v;
-      }
-    };
-    auto commit = [&](int st, int buf) {
-#pragma unroll
-      for (int i = 0; i < C::LOADS; ++i) {
-        const int idx = i * kAttnThreads + tid;
-        const int pis = idx / (C::PB / 16);
-        const int rem = idx % (C::PB / 16);
-        const int kv = rem / (C::KVB / 16);
-        const int tok = (rem % (C::KVB / 16)) / C::CPR;
-        const int ch = rem % C::CPR;
-        if (st * C::SP + pis < np)
-          *reinterpret_cast<uint4*>(smem + buf * C::STAGE + pis * C::PB + kv * C::KVB +
-                                    swz<D, BF16>(tok, ch)) = pre[i];
       }
     };
 
-    __syncthreads();                       // s_pages visible
+    // The queries (and page ids) must have arrived before the first copy is issued: the
+    // compiler cannot see the copies, so any wait it places for its own loads inside the stage
+    // loop would also drain the copy pipeline.
+    wait_vmcnt(0);
+    __syncthreads();                       // s_pages visible; nothing of the last item in flight
     const int nst = (np + C::SP - 1) / C::SP;
-    issue(0);
-    commit(0, 0);
-    __syncthreads();
+    for (int st = 0; st < C::NBUF - 1 && st < nst; ++st) issue(st);
     for (int st = 0; st < nst; ++st) {
-      if (st + 1 < nst) issue(st + 1);
-      const int buf = st & 1;
-      const int npst = min(C::SP, np - st * C::SP);
+      // Wait until this wave's copies of stage st have landed (copies of later stages may stay
+      // in flight), then make every wave's copies visible.
+      int pend = 0;
+      for (int k = st + 1; k < nst && k < st + C::NBUF - 1; ++k) pend += C::IPW * stage_pages(k);
+      wait_vmcnt(pend);
+      wg_barrier();
+      // All waves are done with stage st - 1, so its buffer can be refilled.
+      if (st + C::NBUF - 1 < nst) issue(st + C::NBUF - 1);
+      const int buf = st % C::NBUF;
+      const int npst = stage_pages(st);
       if (ntile > 0) {
         for (int pis = split; pis < npst; pis += ks) {
           const unsigned char* kb = smem + buf * C::STAGE + pis * C::PB;
@@ -279,9 +322,8 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
           }
         }
       }
-      if (st + 1 < nst) commit(st + 1, buf ^ 1);
-      __syncthreads();
     }
+    __syncthreads();                       // every wave done with the ring
 
     // Row sums: reduce the per-lane partials across the four lane groups.
     float L[2];

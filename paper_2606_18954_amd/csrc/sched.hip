@@ -6,7 +6,8 @@
 //   B(s)          branches whose path contains s, ascending (CSR grp_off / grp_br)
 //   entry_rank    for each path entry (b, s): the position of b inside B(s)
 //   seg_nchunk    page chunks of each referenced segment (chunk_pages pages per chunk)
-//   items         (segment, chunk, row block) work items, segment-major
+//   items         (segment, chunk, row block) work items, grouped by segment; segments in
+//                 descending order of per-item cost (pages x (2 + row tiles)), ties by id
 //   seg_prow_off  first partial row of each segment; partial row of (s, chunk c, rank j) is
 //                 seg_prow_off[s] + c * |B(s)| + j
 // Every output is a pure function of the graph: group order comes from ranking, not from the
@@ -40,54 +41,121 @@ __global__ void k_count(DevGraph g, DevSchedule sc) {
   atomicAdd(&sc.grp_cnt[g.path_segs[e]], 1);
 }
 
-// Exclusive scans over segments (one workgroup; each thread owns a contiguous range).
+// Cost of one work item of segment s (pages of a chunk x per-page work), used to order the
+// work list longest first so the persistent grid does not end on a long item.
+__device__ __forceinline__ uint32_t item_cost(int npg, int cnt, int group, int chunk_pages) {
+  const int rows = min(cnt * group, kRowsPerBlock);
+  const int tiles = (rows + 15) / 16;
+  return (uint32_t)(min(npg, chunk_pages) * (2 + tiles));
+}
+
+constexpr int kSortCap = 8192;   // segments sorted in LDS; larger graphs keep segment order
+
+// Exclusive scans over segments (one workgroup; each thread owns a contiguous range):
+// group offsets and partial-row offsets in segment order, item offsets in work-list order.
 __global__ __launch_bounds__(1024) void k_scan(DevGraph g, DevSchedule sc, int32_t group,
                                                int32_t chunk_pages) {
   __shared__ int64_t sh[3][1024];
+  __shared__ uint64_t keys[kSortCap];
   const int t = threadIdx.x;
   const int S = g.S;
   const int per = (S + 1023) / 1024;
   const int s0 = min(S, t * per), s1 = min(S, s0 + per);
-  int64_t a = 0, b = 0, c = 0;
+  auto seg_info = [&](int s, int& cnt, int& nch, int& nrb, int& npg) {
+    cnt = sc.grp_cnt[s];
+    npg = (g.seg_len[s] + kPageTokens - 1) / kPageTokens;
+    nch = cnt > 0 ? (npg + chunk_pages - 1) / chunk_pages : 0;
+    nrb = (int)(((int64_t)cnt * group + kRowsPerBlock - 1) / kRowsPerBlock);
+  };
+  auto block_scan = [&](int64_t a, int64_t b, int64_t c) {
+    sh[0][t] = a; sh[1][t] = b; sh[2][t] = c;
+    __syncthreads();
+    for (int off = 1; off < 1024; off <<= 1) {   // Hillis-Steele inclusive scan
+      int64_t x0 = 0, x1 = 0, x2 = 0;
+      if (t >= off) { x0 = sh[0][t - off]; x1 = sh[1][t - off]; x2 = sh[2][t - off]; }
+      __syncthreads();
+      sh[0][t] += x0; sh[1][t] += x1; sh[2][t] += x2;
+      __syncthreads();
+    }
+  };
+
+  // 1. Group and partial-row offsets in segment order.
+  int64_t a = 0, c = 0;
   for (int s = s0; s < s1; ++s) {
-    const int cnt = sc.grp_cnt[s];
-    const int npg = (g.seg_len[s] + kPageTokens - 1) / kPageTokens;
-    const int nch = cnt > 0 ? (npg + chunk_pages - 1) / chunk_pages : 0;
-    const int nrb = (int)(((int64_t)cnt * group + kRowsPerBlock - 1) / kRowsPerBlock);
+    int cnt, nch, nrb, npg;
+    seg_info(s, cnt, nch, nrb, npg);
     a += cnt;
-    b += (int64_t)nch * nrb;
     c += (int64_t)nch * cnt;
   }
-  sh[0][t] = a; sh[1][t] = b; sh[2][t] = c;
-  __syncthreads();
-  // Hillis-Steele inclusive scan of the 1024 per-thread sums.
-  for (int off = 1; off < 1024; off <<= 1) {
-    int64_t x0 = 0, x1 = 0, x2 = 0;
-    if (t >= off) { x0 = sh[0][t - off]; x1 = sh[1][t - off]; x2 = sh[2][t - off]; }
-    __syncthreads();
-    sh[0][t] += x0; sh[1][t] += x1; sh[2][t] += x2;
-    __syncthreads();
-  }
-  int64_t ra = t ? sh[0][t - 1] : 0, rb = t ? sh[1][t - 1] : 0, rc = t ? sh[2][t - 1] : 0;
+  block_scan(a, 0, c);
+  int64_t ra = t ? sh[0][t - 1] : 0, rc = t ? sh[2][t - 1] : 0;
   for (int s = s0; s < s1; ++s) {
-    const int cnt = sc.grp_cnt[s];
-    const int npg = (g.seg_len[s] + kPageTokens - 1) / kPageTokens;
-    const int nch = cnt > 0 ? (npg + chunk_pages - 1) / chunk_pages : 0;
-    const int nrb = (int)(((int64_t)cnt * group + kRowsPerBlock - 1) / kRowsPerBlock);
+    int cnt, nch, nrb, npg;
+    seg_info(s, cnt, nch, nrb, npg);
     sc.grp_off[s] = ra;
-    sc.seg_item_off[s] = rb;
     sc.seg_prow_off[s] = rc;
     sc.seg_nchunk[s] = nch;
     ra += cnt;
-    rb += (int64_t)nch * nrb;
     rc += (int64_t)nch * cnt;
   }
   if (t == 1023) {
     sc.grp_off[S] = sh[0][1023];
-    sc.seg_item_off[S] = sh[1][1023];
     sc.seg_prow_off[S] = sh[2][1023];
-    sc.counters[0] = sh[1][1023];
     sc.counters[1] = sh[2][1023];
+  }
+  __syncthreads();
+
+  // 2. Work-list order: segments by descending item cost, ties by segment id (bitonic sort of
+  //    unique 64-bit keys, so the order is a pure function of the graph).
+  const bool sorted = S <= kSortCap;
+  int n = 1;
+  if (sorted) {
+    while (n < S) n <<= 1;
+    for (int i = t; i < n; i += 1024) {
+      uint64_t key = ~0ull;
+      if (i < S) {
+        int cnt, nch, nrb, npg;
+        seg_info(i, cnt, nch, nrb, npg);
+        const uint32_t cost = cnt > 0 ? item_cost(npg, cnt, group, chunk_pages) : 0u;
+        key = ((uint64_t)(0xffffffffu - cost) << 32) | (uint32_t)i;
+      }
+      keys[i] = key;
+    }
+    __syncthreads();
+    for (int k = 2; k <= n; k <<= 1) {
+      for (int j = k >> 1; j > 0; j >>= 1) {
+        for (int i = t; i < n; i += 1024) {
+          const int l = i ^ j;
+          if (l > i) {
+            const uint64_t x = keys[i], y = keys[l];
+            const bool up = (i & k) == 0;
+            if ((x > y) == up) { keys[i] = y; keys[l] = x; }
+          }
+        }
+        __syncthreads();
+      }
+    }
+  }
+  // 3. Item offsets in work-list order.
+  int64_t b = 0;
+  for (int i = s0; i < s1; ++i) {
+    const int s = sorted ? (int)(uint32_t)keys[i] : i;
+    int cnt, nch, nrb, npg;
+    seg_info(s, cnt, nch, nrb, npg);
+    b += (int64_t)nch * nrb;
+  }
+  block_scan(0, b, 0);
+  int64_t rb = t ? sh[1][t - 1] : 0;
+  for (int i = s0; i < s1; ++i) {
+    const int s = sorted ? (int)(uint32_t)keys[i] : i;
+    int cnt, nch, nrb, npg;
+    seg_info(s, cnt, nch, nrb, npg);
+    sc.seg_item_off[s] = rb;
+    rb += (int64_t)nch * nrb;
+  }
+  if (t == 1023) {
+    sc.seg_item_off[S] = sh[1][1023];
+    sc.counters[0] = sh[1][1023];
   }
 }
 

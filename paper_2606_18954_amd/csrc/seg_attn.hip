@@ -33,6 +33,13 @@
 
 #include <type_traits>
 
+#ifndef GA_STAGE_BYTES
+#define GA_STAGE_BYTES 16384
+#endif
+#ifndef GA_RING_STAGES
+#define GA_RING_STAGES 4
+#endif
+
 namespace ga {
 namespace {
 
@@ -48,37 +55,49 @@ struct Cfg {
   static constexpr int CPR = ROW / 16;              // 16-byte chunks per token row
   static constexpr int KVB = 16 * ROW;              // bytes of a page's K (or V) block
   static constexpr int PB = 2 * KVB;                // bytes of one page of one kv-head
-  static constexpr int STAGE = 16384;               // bytes per pipeline stage
+  static constexpr int STAGE = GA_STAGE_BYTES >= PB ? GA_STAGE_BYTES : PB;   // bytes per stage
   static constexpr int SP = STAGE / PB;             // pages per stage
-  static constexpr int NBUF = 4;                    // stages in the LDS ring
+  static constexpr int NBUF = GA_RING_STAGES;       // stages in the LDS ring
   static constexpr int IPP = PB / 1024;             // 1 KiB DMA wave instructions per page
   static constexpr int IPW = IPP / (kAttnThreads / 64);   // ... issued by each wave per page
   static constexpr int NB = D / 16;                 // 16-wide output column blocks
   static constexpr int QR = BF16 ? D / 32 : D / 4;  // Q operand registers per tile
   static_assert(SP >= 1 && IPW >= 1 && STAGE % PB == 0, "stage must hold whole pages");
-  static_assert((NBUF - 2) * SP * IPW <= 15, "pending DMA count must fit the wait helper");
+  static_assert((NBUF - 2) * SP * IPW <= 63, "pending DMA count must fit the wait helper");
 };
 
-// Direct-to-LDS copy of 16 bytes per lane: LDS[lds_base + 16 * lane] <- global[src].  Issued as
-// inline assembly so that the compiler's wait-count pass does not treat every later LDS read as
-// a possible alias of the copy (it would drain the whole pipeline before each stage); ordering
-// is explicit instead: wait_vmcnt() before the barrier that publishes a stage.  M0 holds the
-// wave-uniform LDS base; the kernel keeps no other value in M0.
-__device__ __forceinline__ void dma16(const void* src, unsigned lds_base) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
-               :: "v"(src), "s"(lds_base) : "memory", "m0");
+// Direct-to-LDS copy of 16 bytes per lane: LDS[lds_base + 16 * lane] <- global[base + off].
+// base (the page block) and lds_base are wave-uniform SGPR values, off a per-lane VGPR.  Issued
+// as inline assembly so that the compiler's wait-count pass does not treat every later LDS read
+// as a possible alias of the copy (it would drain the whole pipeline before each stage);
+// ordering is explicit instead: wait_vmcnt() before the barrier that publishes a stage.  M0
+// holds the LDS base; the kernel keeps no other value in M0.
+// (tests/test_isa_invariants.py checks in the built assembly that every M0 write is one of these.)
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void dma16(unsigned off, const void* base, unsigned lds_base) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+               :: "v"(off), "s"(base), "s"(lds_base) : "memory", "m0");
 }
+#pragma clang diagnostic pop
 
-// s_waitcnt vmcnt(n) for a runtime n in [0, 15] (expcnt and lgkmcnt left alone).
+// s_waitcnt vmcnt(n) for a runtime n in [0, 63] (expcnt and lgkmcnt left alone).  The gfx9
+// encoding splits vmcnt into bits [3:0] and [15:14].
+#define GA_VMCNT(k) (((k) & 15) | (7 << 4) | (15 << 8) | (((k) >> 4) << 14))
 __device__ __forceinline__ void wait_vmcnt(int n) {
-#define GA_VMW(k) case k: __builtin_amdgcn_s_waitcnt((k) | (7 << 4) | (15 << 8)); break;
+#define GA_VMW(k) case k: __builtin_amdgcn_s_waitcnt(GA_VMCNT(k)); break;
+#define GA_VMW8(b) GA_VMW(b) GA_VMW(b + 1) GA_VMW(b + 2) GA_VMW(b + 3) GA_VMW(b + 4) \
+                   GA_VMW(b + 5) GA_VMW(b + 6) GA_VMW(b + 7)
   switch (n) {
-    GA_VMW(0) GA_VMW(1) GA_VMW(2) GA_VMW(3) GA_VMW(4) GA_VMW(5) GA_VMW(6) GA_VMW(7)
-    GA_VMW(8) GA_VMW(9) GA_VMW(10) GA_VMW(11) GA_VMW(12) GA_VMW(13) GA_VMW(14) GA_VMW(15)
-    default: __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8)); break;
+    GA_VMW8(0) GA_VMW8(8) GA_VMW8(16) GA_VMW8(24) GA_VMW8(32) GA_VMW8(40) GA_VMW8(48) GA_VMW8(56)
+    default: __builtin_amdgcn_s_waitcnt(GA_VMCNT(0)); break;
   }
+#undef GA_VMW8
 #undef GA_VMW
 }
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt_const() { __builtin_amdgcn_s_waitcnt(GA_VMCNT(N)); }
 
 // Workgroup barrier without a memory fence: LDS-DMA completion is ordered by the explicit
 // vmcnt wait before it; the empty asm statements keep the compiler from moving LDS accesses
@@ -111,16 +130,28 @@ template <bool BF16> struct QOp;
 template <> struct QOp<true> { bf16x8 v; };
 template <> struct QOp<false> { float v; };
 
+__device__ __forceinline__ int64_t uniform64(int64_t v) {
+  const int lo = __builtin_amdgcn_readfirstlane((int)(uint32_t)(uint64_t)v);
+  const int hi = __builtin_amdgcn_readfirstlane((int)((uint64_t)v >> 32));
+  return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+}
+
+// Scores more than 2^kTau above a row's running reference trigger a reference update; below
+// that the stale reference is kept (probabilities up to 2^kTau are exact in fp32 and bf16).
+constexpr float kTau = 8.0f;
+
 template <int D, bool BF16>
 __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
   using C = Cfg<D, BF16>;
   using T = typename std::conditional<BF16, __bf16, float>::type;
+  constexpr int NI = C::SP * C::IPW;                // copies per wave per full stage
   __shared__ __align__(1024) unsigned char smem[C::NBUF * C::STAGE];
   __shared__ int s_pages[kMaxChunkPages];
   __shared__ int64_t s_work;
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int r16 = lane & 15, kg = lane >> 4;
   const int64_t n_work = a.counters[0] * a.Hkv;
   const float NEG_INF = -__builtin_huge_valf();
@@ -129,13 +160,28 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
   const unsigned lds_ring =
       (unsigned)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)smem;
 
+  // Per-lane source offsets inside a page block for this wave's copies: copy i of a stage covers
+  // bytes [1024 j, 1024 j + 1024) with j = wave + 4 i, i.e. page i / IPW of the stage, piece
+  // j % IPP of that page.  Chunks are XOR-permuted by token so the LDS layout is swizzled.
+  int c_tok[NI], c_rest[NI];
+#pragma unroll
+  for (int i = 0; i < NI; ++i) {
+    const int o = ((wave + 4 * i) % C::IPP) * 1024 + lane * 16;   // byte offset in the page
+    const int kv = o / C::KVB;
+    const int tok = (o % C::KVB) / C::ROW;
+    const int pc = (o % C::ROW) >> 4;
+    c_tok[i] = tok;
+    c_rest[i] = kv * C::KVB + ((pc ^ (tok & (C::CPR - 1))) << 4);
+  }
+
   for (;;) {
     if (tid == 0) s_work = (int64_t)atomicAdd((unsigned long long*)&a.counters[2], 1ull);
     __syncthreads();
-    const int64_t w = s_work;
+    const int64_t w = uniform64(s_work);
     if (w >= n_work) break;
-    const int4 it = a.items[w / a.Hkv];
-    const int kvh = (int)(w % a.Hkv);
+    const int64_t item = w / a.Hkv;
+    const int kvh = (int)(w - item * a.Hkv);
+    const int4 it = a.items[item];
     const int s = it.x, chunk = it.y, rb = it.z;
 
     const int len = a.seg_len[s];
@@ -144,14 +190,15 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
     const int np = min(npg_seg, p0 + a.chunk_pages) - p0;
     const int last_pg = npg_seg - 1 - p0;          // index (in chunk) of the segment's last page
     const int last_valid = len - (npg_seg - 1) * kPageTokens;
-    const int64_t page_off = a.seg_page_off[s];
+    // Page ids of the chunk go to LDS: read back with readfirstlane they give the copies their
+    // SGPR base without a vector load (whose wait would also drain the copies in flight).
+    const int* pages = a.seg_pages + a.seg_page_off[s] + p0;
+    for (int i = tid; i < np; i += kAttnThreads) s_pages[i] = pages[i];
     const int cnt = a.grp_cnt[s];
     const int64_t goff = a.grp_off[s];
     const int row0 = rb * kRowsPerBlock;
     const int R = min(kRowsPerBlock, cnt * a.group - row0);
     const int nrt = (R + 15) >> 4;
-
-    for (int i = tid; i < np; i += kAttnThreads) s_pages[i] = a.seg_pages[page_off + p0 + i];
 
     // Wave roles: with >= 3 row tiles the waves split the tiles (tiles wave and wave + 4); with
     // fewer, waves sharing a tile split the stage's pages and are combined at the end.
@@ -197,35 +244,36 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
 #pragma unroll
       for (int n = 0; n < C::NB; ++n) O[k][n] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    auto stage_pages = [&](int st) { return min(C::SP, np - st * C::SP); };
-    // Direct-to-LDS copy of stage st: wave instruction j covers bytes [1024 j, 1024 j + 1024) of
-    // the stage; this wave issues j = wave, wave + 4, ... (IPW instructions per page).
-    auto issue = [&](int st) {
-      const unsigned dst = lds_ring + (st % C::NBUF) * C::STAGE;
-      const int npst = stage_pages(st);
+    // Offsets for the segment's last page: slots past its end re-read its last valid token
+    // (finite data; their scores are masked).
+    unsigned off_full[NI], off_last[NI];
 #pragma unroll
-      for (int i = 0; i < C::SP * C::IPW; ++i) {
-        const int j = wave + 4 * i;
-        const int pis = j / C::IPP;
+    for (int i = 0; i < NI; ++i) {
+      off_full[i] = c_tok[i] * C::ROW + c_rest[i];
+      off_last[i] = min(c_tok[i], last_valid - 1) * C::ROW + c_rest[i];
+    }
+    const int64_t blk_stride = (int64_t)a.Hkv * 2 * C::KVB;
+    const unsigned char* pool_h = (const unsigned char*)uniform64(
+        (int64_t)(uintptr_t)(pool + (int64_t)kvh * 2 * C::KVB));
+
+    auto issue = [&](int st) {
+      const unsigned dst = lds_ring + (st % C::NBUF) * C::STAGE + wave * 1024;
+      const int npst = min(C::SP, np - st * C::SP);
+#pragma unroll
+      for (int i = 0; i < NI; ++i) {
+        const int pis = i / C::IPW;
         if (pis < npst) {
-          const int o = j * 1024 + lane * 16;
-          const int rem = o % C::PB;
-          const int kv = rem / C::KVB;
-          const int tok = (rem % C::KVB) / C::ROW;
-          const int pc = (rem % C::ROW) >> 4;
           const int pg = st * C::SP + pis;
-          const int ts = min(tok, (pg == last_pg ? last_valid : kPageTokens) - 1);
-          const int64_t blk = ((int64_t)s_pages[pg] * a.Hkv + kvh) * 2 + kv;
-          const unsigned char* src =
-              pool + blk * C::KVB + ts * C::ROW + ((pc ^ (tok & (C::CPR - 1))) << 4);
-          dma16(src, __builtin_amdgcn_readfirstlane(dst + j * 1024));
+          const int pid = __builtin_amdgcn_readfirstlane(s_pages[pg]);
+          const unsigned char* base = pool_h + (int64_t)pid * blk_stride;
+          dma16(pg == last_pg ? off_last[i] : off_full[i], base,
+                __builtin_amdgcn_readfirstlane(dst + i * 4096));
         }
       }
     };
 
-    // The queries (and page ids) must have arrived before the first copy is issued: the
-    // compiler cannot see the copies, so any wait it places for its own loads inside the stage
-    // loop would also drain the copy pipeline.
+    // The queries must have arrived before the first copy is issued: the compiler cannot see the
+    // copies, so a wait it placed for its own loads inside the stage loop would also drain them.
     wait_vmcnt(0);
     __syncthreads();                       // s_pages visible; nothing of the last item in flight
     const int nst = (np + C::SP - 1) / C::SP;
@@ -233,19 +281,20 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
     for (int st = 0; st < nst; ++st) {
       // Wait until this wave's copies of stage st have landed (copies of later stages may stay
       // in flight), then make every wave's copies visible.
-      int pend = 0;
-      for (int k = st + 1; k < nst && k < st + C::NBUF - 1; ++k) pend += C::IPW * stage_pages(k);
-      wait_vmcnt(pend);
+      const int ahead = min(nst - 1 - st, C::NBUF - 2);
+      const int pend = C::IPW * (min(np, (st + 1 + ahead) * C::SP) - (st + 1) * C::SP);
+      if (pend == (C::NBUF - 2) * NI) wait_vmcnt_const<(C::NBUF - 2) * NI>();
+      else wait_vmcnt(pend);
       wg_barrier();
       // All waves are done with stage st - 1, so its buffer can be refilled.
       if (st + C::NBUF - 1 < nst) issue(st + C::NBUF - 1);
       const int buf = st % C::NBUF;
-      const int npst = stage_pages(st);
+      const int npst = min(C::SP, np - st * C::SP);
       if (ntile > 0) {
         for (int pis = split; pis < npst; pis += ks) {
           const unsigned char* kb = smem + buf * C::STAGE + pis * C::PB;
           const unsigned char* vb = kb + C::KVB;
-          const int valid = (st * C::SP + pis == last_pg) ? last_valid : kPageTokens;
+          const bool last = st * C::SP + pis == last_pg;
           f32x4 S[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
           for (int jj = 0; jj < C::QR; ++jj) {
@@ -261,31 +310,32 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
                 S[1] = __builtin_amdgcn_mfma_f32_16x16x4f32(ka, qop[1][jj].v, S[1], 0, 0, 0);
             }
           }
-          // Online softmax over this page's 16 tokens for each of the wave's tiles.
+          // Online softmax (log2 domain) over this page's 16 tokens for each of the wave's tiles.
+          // The row reference m only moves when some score exceeds it by more than 2^kTau, so
+          // the common page needs no cross-lane reduction and no rescale of O.
           float p[2][4];
 #pragma unroll
           for (int k = 0; k < 2; ++k) {
             if (k >= ntile) break;
-            float sv[4];
-            float mx = NEG_INF;
+            if (last) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              sv[i] = (4 * kg + i < valid) ? S[k][i] * a.scale_log2 : NEG_INF;
-              mx = fmaxf(mx, sv[i]);
+              for (int i = 0; i < 4; ++i)
+                if (4 * kg + i >= last_valid) S[k][i] = NEG_INF;
             }
-            mx = xmax(mx);
-            const float mn = fmaxf(m[k], mx);
-            const float alpha = exp2_(m[k] - mn);
-            m[k] = mn;
-            float ps = 0.f;
+            const float lm =
+                fmaxf(fmaxf(S[k][0], S[k][1]), fmaxf(S[k][2], S[k][3])) * a.scale_log2;
+            if (__any(lm > m[k] + kTau)) {
+              const float mn = fmaxf(m[k], xmax(lm));
+              const float alpha = exp2_(m[k] - mn);
+              m[k] = mn;
+              l[k] *= alpha;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              p[k][i] = exp2_(sv[i] - mn);
-              ps += p[k][i];
+              for (int n = 0; n < C::NB; ++n) O[k][n] *= alpha;
             }
-            l[k] = l[k] * alpha + ps;
+            const float nm = -m[k];
 #pragma unroll
-            for (int n = 0; n < C::NB; ++n) O[k][n] *= alpha;
+            for (int i = 0; i < 4; ++i) p[k][i] = exp2_(fmaf(S[k][i], a.scale_log2, nm));
+            l[k] += (p[k][0] + p[k][1]) + (p[k][2] + p[k][3]);
           }
           if constexpr (BF16) {
             s16x4 pb[2];

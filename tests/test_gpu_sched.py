@@ -19,12 +19,19 @@ ROWS_PER_BLOCK = 128
 
 
 def expected_items(g, group, chunk_pages, cnt):
+    """Work list: items grouped by segment, segments by descending per-item cost
+    (chunk pages x (2 + row tiles)), ties by segment id; within a segment chunk-major."""
+    def npg(s):
+        return (int(g.seg_len[s]) + 15) // 16
+
+    def cost(s):
+        tiles = (min(cnt[s] * group, ROWS_PER_BLOCK) + 15) // 16
+        return min(npg(s), chunk_pages) * (2 + tiles)
+
+    order = sorted((s for s in range(g.num_segments) if cnt[s] > 0), key=lambda s: (-cost(s), s))
     items = []
-    for s in range(g.num_segments):
-        if cnt[s] == 0:
-            continue
-        npg = (int(g.seg_len[s]) + 15) // 16
-        nch = (npg + chunk_pages - 1) // chunk_pages
+    for s in order:
+        nch = (npg(s) + chunk_pages - 1) // chunk_pages
         nrb = (cnt[s] * group + ROWS_PER_BLOCK - 1) // ROWS_PER_BLOCK
         for c in range(nch):
             for rb in range(nrb):

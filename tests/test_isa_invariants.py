@@ -1,0 +1,61 @@
+"""Properties of the generated gfx950 assembly that the attention kernel relies on.
+
+The K/V copies are issued as inline assembly that loads M0 with the LDS destination and then
+issues global_load_lds_dwordx4.  That is only safe if the compiler keeps no value of its own in
+M0 across those statements, so every M0 write in the kernels must be one of these copies.
+"""
+import os
+import re
+import shutil
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "paper_2606_18954_amd", "csrc", "seg_attn.hip")
+HIPCC = "/opt/rocm/bin/hipcc"
+
+
+@pytest.fixture(scope="module")
+def asm(tmp_path_factory):
+    if not os.path.exists(HIPCC):
+        pytest.skip("hipcc not available")
+    out = tmp_path_factory.mktemp("isa") / "seg_attn.s"
+    cmd = [HIPCC, "--offload-arch=gfx950", "-O3", "-std=c++17", "-x", "hip", "-S",
+           "--cuda-device-only", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+           "-I", os.path.join(ROOT, "include"), SRC, "-o", str(out)]
+    subprocess.run(cmd, check=True, capture_output=True)
+    return out.read_text()
+
+
+def _kernels(text):
+    parts = re.split(r"^(_ZN2ga\w*k_seg_attn\w*):", text, flags=re.M)
+    return {parts[i]: parts[i + 1].split("s_endpgm")[0] for i in range(1, len(parts) - 1, 2)}
+
+
+def test_every_m0_write_feeds_a_direct_to_lds_copy(asm):
+    ks = _kernels(asm)
+    assert len(ks) == 4
+    for name, body in ks.items():
+        lines = [l.strip() for l in body.splitlines()
+                 if l.strip() and not l.strip().startswith(";") and not l.strip().startswith(".")]
+        copies = 0
+        for i, l in enumerate(lines):
+            if re.search(r"\bm0\b", l):
+                assert l.startswith("s_mov_b32 m0, s"), (name, l)
+                assert lines[i + 1].startswith("global_load_lds_dwordx4"), (name, lines[i + 1])
+                copies += 1
+        assert copies >= 1, name
+        assert sum(l.startswith("global_load_lds_dwordx4") for l in lines) == copies, name
+
+
+def test_bf16_kernels_do_not_spill(asm):
+    found = 0
+    parts = re.split(r"^(_ZN2ga\w*k_seg_attn\w*):", asm, flags=re.M)
+    for name, body in zip(parts[1::2], parts[2::2]):
+        if "ELb1E" in name:
+            m = re.search(r"ScratchSize:\s+(\d+)", body)
+            assert m, name
+            assert int(m.group(1)) == 0, name
+            found += 1
+    assert found == 2

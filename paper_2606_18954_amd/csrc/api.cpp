@@ -183,7 +183,7 @@ void size_schedule(const ga_segment_table* st, const ga_branch_paths* bp, const 
     const int32_t s = bp->path_segs[e];
     prows += (npg[s] + cap - 1) / cap;
   }
-  z->prows = prows;
+  z->prows = prows;   // partial rows are stored as int32 in the branch lists (checked by the caller)
   // items(s) = chunks(s) * ceil(|B(s)| g / 128) <= chunks(s) * (|B(s)| g / 128 + 1)
   z->max_items = chunks_ref + (prows * group + ga::kRowsPerBlock - 1) / ga::kRowsPerBlock;
   (void)st;
@@ -198,7 +198,8 @@ struct Layout {
 enum {
   L_SEG_LEN, L_SEG_PAGE_OFF, L_SEG_PAGES, L_PATH_OFF, L_PATH_SEGS,  // uploaded graph (contiguous)
   L_GRP_CNT, L_GRP_FILL, L_GRP_OFF, L_GRP_TMP, L_GRP_BR, L_ENTRY_BR, L_ENTRY_RANK, L_SEG_NCH,
-  L_SEG_ITEM_OFF, L_SEG_PROW_OFF, L_ITEMS, L_COUNTERS, L_PO, L_PLSE, L_COUNT
+  L_SEG_ITEM_OFF, L_SEG_PROW_OFF, L_ITEMS, L_RECS, L_COUNTERS, L_ENTRY_PART, L_BPART_OFF, L_BPART,
+  L_PO, L_PLSE, L_COUNT
 };
 
 Layout layout(const Sizes& z, const ga_params& p) {
@@ -219,7 +220,11 @@ Layout layout(const Sizes& z, const ga_params& p) {
   sz[L_SEG_ITEM_OFF] = sizeof(int64_t) * (z.S + 1);
   sz[L_SEG_PROW_OFF] = sizeof(int64_t) * (z.S + 1);
   sz[L_ITEMS] = sizeof(int4) * (z.max_items > 0 ? z.max_items : 1);
+  sz[L_RECS] = 2 * sizeof(int4) * (z.max_items > 0 ? z.max_items : 1);
   sz[L_COUNTERS] = sizeof(int64_t) * 4;
+  sz[L_ENTRY_PART] = sizeof(int64_t) * z.E;
+  sz[L_BPART_OFF] = sizeof(int64_t) * (z.B + 1);
+  sz[L_BPART] = sizeof(int32_t) * z.prows;
   sz[L_PO] = sizeof(float) * (size_t)z.prows * p.num_q_heads * p.head_dim;
   sz[L_PLSE] = sizeof(float) * (size_t)z.prows * p.num_q_heads;
   Layout L{};
@@ -258,7 +263,11 @@ void bind(ga_plan* pl, const Layout& L) {
   pl->sc.seg_item_off = reinterpret_cast<int64_t*>(d + L.off[L_SEG_ITEM_OFF]);
   pl->sc.seg_prow_off = reinterpret_cast<int64_t*>(d + L.off[L_SEG_PROW_OFF]);
   pl->sc.items = reinterpret_cast<int4*>(d + L.off[L_ITEMS]);
+  pl->sc.recs = reinterpret_cast<int4*>(d + L.off[L_RECS]);
   pl->sc.counters = reinterpret_cast<int64_t*>(d + L.off[L_COUNTERS]);
+  pl->sc.entry_part = reinterpret_cast<int64_t*>(d + L.off[L_ENTRY_PART]);
+  pl->sc.bpart_off = reinterpret_cast<int64_t*>(d + L.off[L_BPART_OFF]);
+  pl->sc.bpart = reinterpret_cast<int32_t*>(d + L.off[L_BPART]);
   pl->po = reinterpret_cast<float*>(d + L.off[L_PO]);
   pl->plse = reinterpret_cast<float*>(d + L.off[L_PLSE]);
 }
@@ -296,6 +305,10 @@ ga_status plan_init(const ga_segment_table* st, const ga_branch_paths* bp, const
   if (pl->p.softmax_scale == 0.f) pl->p.softmax_scale = 1.f / std::sqrt((float)p->head_dim);
   pl->num_cus = device_cus();
   size_schedule(st, bp, p, npg, pl->num_cus, &pl->z);
+  if (pl->z.prows > 0x7fffffffLL)
+    return fail(GA_EINVAL, "too many partial rows (%lld)", (long long)pl->z.prows);
+  if (pl->z.P > 0x7fffffffLL)
+    return fail(GA_EINVAL, "too many page-table entries (%lld)", (long long)pl->z.P);
   *L = layout(pl->z, pl->p);
   return GA_OK;
 }
@@ -347,14 +360,9 @@ ga_status do_run(ga_plan* pl, const void* q, const void* pool, void* out, float*
   ga::AttnArgs a{};
   a.q = q;
   a.pool = pool;
-  a.seg_len = pl->g.seg_len;
-  a.seg_page_off = pl->g.seg_page_off;
   a.seg_pages = pl->g.seg_pages;
-  a.grp_off = pl->sc.grp_off;
   a.grp_br = pl->sc.grp_br;
-  a.grp_cnt = pl->sc.grp_cnt;
-  a.seg_prow_off = pl->sc.seg_prow_off;
-  a.items = pl->sc.items;
+  a.recs = pl->sc.recs;
   a.counters = pl->sc.counters;
   a.po = pl->po;
   a.plse = pl->plse;
@@ -373,12 +381,8 @@ ga_status do_run(ga_plan* pl, const void* q, const void* pool, void* out, float*
     GA_HIP(ga::launch_seg_attn(a, pl->p.head_dim, bf16, (int)grid, stream), "attention launch");
   if (rec) GA_HIP(hipEventRecord(ev[1], stream), "profile event");
   ga::MergeArgs m{};
-  m.path_off = pl->g.path_off;
-  m.path_segs = pl->g.path_segs;
-  m.entry_rank = pl->sc.entry_rank;
-  m.grp_cnt = pl->sc.grp_cnt;
-  m.seg_nchunk = pl->sc.seg_nchunk;
-  m.seg_prow_off = pl->sc.seg_prow_off;
+  m.bpart_off = pl->sc.bpart_off;
+  m.bpart = pl->sc.bpart;
   m.po = pl->po;
   m.plse = pl->plse;
   m.out = out;

@@ -36,20 +36,21 @@ struct DevSchedule {
   int64_t* seg_item_off;   // [S+1] first work item of each segment
   int64_t* seg_prow_off;   // [S+1] first partial row (per q-head) of each segment
   int4* items;             // [max_items] (segment, chunk, row block, unused)
+  int4* recs;              // [2 * max_items] per-item record for the attention kernel:
+                           //   {pages, last page index, valid tokens of the last page, |B(s)|}
+                           //   {row block, group offset, page-table offset, first partial row}
   int64_t* counters;       // [4]: items, partial rows, work-queue head, spare
+  int64_t* entry_part;     // [E]   first slot of each path entry in the branch partial lists
+  int64_t* bpart_off;      // [B+1] CSR offsets of each branch's partial rows
+  int32_t* bpart;          // [partial rows] partial rows of each branch: path order, then chunk
 };
 
 struct AttnArgs {
   const void* q;
   const void* pool;
-  const int32_t* seg_len;
-  const int64_t* seg_page_off;
   const int32_t* seg_pages;
-  const int64_t* grp_off;
   const int32_t* grp_br;
-  const int32_t* grp_cnt;
-  const int64_t* seg_prow_off;
-  const int4* items;
+  const int4* recs;
   int64_t* counters;
   float* po;               // [partial rows][Hq][D] normalised partial outputs
   float* plse;             // [partial rows][Hq] log2-domain log-sum-exp of each partial
@@ -58,12 +59,8 @@ struct AttnArgs {
 };
 
 struct MergeArgs {
-  const int64_t* path_off;
-  const int32_t* path_segs;
-  const int32_t* entry_rank;
-  const int32_t* grp_cnt;
-  const int32_t* seg_nchunk;
-  const int64_t* seg_prow_off;
+  const int64_t* bpart_off;
+  const int32_t* bpart;
   const float* po;
   const float* plse;
   void* out;

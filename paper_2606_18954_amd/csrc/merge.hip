@@ -4,8 +4,9 @@
 // chunks), so with lambda_i = log2 sum_{j in piece i} 2^(s_j) and o_i the piece's normalised
 // output, the exact result over the whole context is
 //   Lambda = log2 sum_i 2^(lambda_i),  out = sum_i 2^(lambda_i - Lambda) o_i.
-// Pieces are folded in path order, then chunk order, with a running maximum, so the result is
-// deterministic.  The natural-log lse is Lambda * ln 2.
+// The scheduler lists each branch's partials in path order, then chunk order; the merge takes
+// their maximum first and then folds them in that order, so the result is deterministic.  The
+// natural-log lse is Lambda * ln 2.
 #include "ga_internal.hpp"
 
 namespace ga {
@@ -26,25 +27,21 @@ __global__ __launch_bounds__(256) void k_merge(MergeArgs a) {
   const int b = (int)(row / a.Hq);
   const int h = (int)(row % a.Hq);
   const float NEG_INF = -__builtin_huge_valf();
-  float M = NEG_INF, W = 0.f;
+  const int64_t k0 = a.bpart_off[b], k1 = a.bpart_off[b + 1];
+  // Pass 1: the largest partial log-sum-exp of the row.
+  float M = NEG_INF;
+#pragma unroll 4
+  for (int64_t k = k0; k < k1; ++k) M = fmaxf(M, a.plse[(int64_t)a.bpart[k] * a.Hq + h]);
+  // Pass 2: fold the partials in list order (path order, then chunk order).
+  float W = 0.f;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  for (int64_t e = a.path_off[b]; e < a.path_off[b + 1]; ++e) {
-    const int s = a.path_segs[e];
-    const int j = a.entry_rank[e];
-    const int cnt = a.grp_cnt[s];
-    const int nch = a.seg_nchunk[s];
-    const int64_t base = a.seg_prow_off[s];
-    for (int c = 0; c < nch; ++c) {
-      const int64_t idx = (base + (int64_t)c * cnt + j) * a.Hq + h;
-      const float lam = a.plse[idx];
-      const f32x4 o = *reinterpret_cast<const f32x4*>(a.po + idx * D + 4 * sub);
-      const float Mn = fmaxf(M, lam);
-      const float sc = __builtin_amdgcn_exp2f(M - Mn);
-      const float wl = __builtin_amdgcn_exp2f(lam - Mn);
-      acc = acc * sc + o * wl;
-      W = W * sc + wl;
-      M = Mn;
-    }
+#pragma unroll 4
+  for (int64_t k = k0; k < k1; ++k) {
+    const int64_t idx = (int64_t)a.bpart[k] * a.Hq + h;
+    const float wl = __builtin_amdgcn_exp2f(a.plse[idx] - M);
+    const f32x4 o = *reinterpret_cast<const f32x4*>(a.po + idx * D + 4 * sub);
+    acc += o * wl;
+    W += wl;
   }
   const f32x4 r = acc * (1.f / W);
   if constexpr (BF16) {

@@ -10,6 +10,8 @@
 //                 descending order of per-item cost (pages x (2 + row tiles)), ties by id
 //   seg_prow_off  first partial row of each segment; partial row of (s, chunk c, rank j) is
 //                 seg_prow_off[s] + c * |B(s)| + j
+//   bpart         each branch's partial rows as CSR (bpart_off), in path order then chunk
+//                 order: the merge folds them in exactly this order
 // Every output is a pure function of the graph: group order comes from ranking, not from the
 // order in which atomics land, so two schedules of one graph are bit-identical.
 #include "ga_internal.hpp"
@@ -18,6 +20,15 @@ namespace ga {
 namespace {
 
 constexpr int kT = 256;
+
+// Workgroup barrier for LDS data only: waits for this wave's LDS operations, not for its global
+// stores (no phase of the single-workgroup scheduler reads global data another thread wrote).
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);            // lgkmcnt(0); vmcnt and expcnt not waited on
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
 
 __global__ void k_init(DevGraph g, DevSchedule sc) {
   int s = blockIdx.x * kT + threadIdx.x;
@@ -49,25 +60,30 @@ __device__ __forceinline__ uint32_t item_cost(int npg, int cnt, int group, int c
   return (uint32_t)(min(npg, chunk_pages) * (2 + tiles));
 }
 
-constexpr int kSortCap = 8192;   // segments sorted in LDS; larger graphs keep segment order
+#ifndef GA_SORT_CAP
+#define GA_SORT_CAP 8192
+#endif
+constexpr int kSortCap = GA_SORT_CAP;   // segments sorted in LDS; larger graphs keep segment order
 
-// Exclusive scans over segments (one workgroup; each thread owns a contiguous range):
-// group offsets and partial-row offsets in segment order, item offsets in work-list order.
-__global__ __launch_bounds__(1024) void k_scan(DevGraph g, DevSchedule sc, int32_t group,
-                                               int32_t chunk_pages) {
-  __shared__ int64_t sh[3][1024];
-  __shared__ uint64_t keys[kSortCap];
+// Per-segment scans (run by one 1024-thread workgroup; each thread owns a contiguous range of
+// segments): group offsets and partial-row offsets in segment order, then item offsets in
+// work-list order.  cnt_of(s) returns |B(s)|; keys is LDS scratch of kSortCap entries.
+template <typename CntOf>
+__device__ void scan_segments(const DevGraph& g, const DevSchedule& sc, int32_t group,
+                              int32_t chunk_pages, CntOf cnt_of, int64_t (*sh)[1024],
+                              uint64_t* keys) {
   const int t = threadIdx.x;
   const int S = g.S;
   const int per = (S + 1023) / 1024;
   const int s0 = min(S, t * per), s1 = min(S, s0 + per);
   auto seg_info = [&](int s, int& cnt, int& nch, int& nrb, int& npg) {
-    cnt = sc.grp_cnt[s];
+    cnt = cnt_of(s);
     npg = (g.seg_len[s] + kPageTokens - 1) / kPageTokens;
     nch = cnt > 0 ? (npg + chunk_pages - 1) / chunk_pages : 0;
     nrb = (int)(((int64_t)cnt * group + kRowsPerBlock - 1) / kRowsPerBlock);
   };
   auto block_scan = [&](int64_t a, int64_t b, int64_t c) {
+    __syncthreads();
     sh[0][t] = a; sh[1][t] = b; sh[2][t] = c;
     __syncthreads();
     for (int off = 1; off < 1024; off <<= 1) {   // Hillis-Steele inclusive scan
@@ -103,13 +119,12 @@ __global__ __launch_bounds__(1024) void k_scan(DevGraph g, DevSchedule sc, int32
     sc.seg_prow_off[S] = sh[2][1023];
     sc.counters[1] = sh[2][1023];
   }
-  __syncthreads();
 
   // 2. Work-list order: segments by descending item cost, ties by segment id (bitonic sort of
   //    unique 64-bit keys, so the order is a pure function of the graph).
   const bool sorted = S <= kSortCap;
-  int n = 1;
   if (sorted) {
+    int n = 1;
     while (n < S) n <<= 1;
     for (int i = t; i < n; i += 1024) {
       uint64_t key = ~0ull;
@@ -159,6 +174,275 @@ __global__ __launch_bounds__(1024) void k_scan(DevGraph g, DevSchedule sc, int32
   }
 }
 
+__global__ __launch_bounds__(1024) void k_scan(DevGraph g, DevSchedule sc, int32_t group,
+                                               int32_t chunk_pages) {
+  __shared__ int64_t sh[3][1024];
+  __shared__ uint64_t keys[kSortCap];
+  scan_segments(g, sc, group, chunk_pages, [&](int s) { return sc.grp_cnt[s]; }, sh, keys);
+}
+
+// Exclusive scan over path entries of their chunk counts (one 1024-thread workgroup): the slot
+// of each entry's first partial in the flat per-branch lists, and the branch CSR offsets.
+__device__ void scan_entries(const DevGraph& g, const DevSchedule& sc, int64_t (*sh)[1024]) {
+  const int t = threadIdx.x;
+  const int E = g.E;
+  const int per = (E + 1023) / 1024;
+  const int e0 = min(E, t * per), e1 = min(E, e0 + per);
+  int64_t a = 0;
+  for (int e = e0; e < e1; ++e) a += sc.seg_nchunk[g.path_segs[e]];
+  __syncthreads();
+  sh[0][t] = a;
+  __syncthreads();
+  for (int off = 1; off < 1024; off <<= 1) {
+    const int64_t x = t >= off ? sh[0][t - off] : 0;
+    __syncthreads();
+    sh[0][t] += x;
+    __syncthreads();
+  }
+  int64_t r = t ? sh[0][t - 1] : 0;
+  for (int e = e0; e < e1; ++e) {
+    sc.entry_part[e] = r;
+    r += sc.seg_nchunk[g.path_segs[e]];
+  }
+  __syncthreads();
+  for (int b = t; b <= g.B; b += 1024)
+    sc.bpart_off[b] = b < g.B ? sc.entry_part[g.path_off[b]] : sh[0][1023];
+}
+
+// Partial rows of path entry e (its segment's chunks, in order) into the branch list.
+__device__ __forceinline__ void write_entry_parts(const DevGraph& g, const DevSchedule& sc,
+                                                  int e, int rank, int cnt) {
+  const int s = g.path_segs[e];
+  const int nch = sc.seg_nchunk[s];
+  const int64_t base = sc.seg_prow_off[s] + rank;
+  const int64_t slot = sc.entry_part[e];
+  for (int c = 0; c < nch; ++c) sc.bpart[slot + c] = (int32_t)(base + (int64_t)c * cnt);
+}
+
+__global__ __launch_bounds__(1024) void k_scan_entries(DevGraph g, DevSchedule sc) {
+  __shared__ int64_t sh[1][1024];
+  scan_entries(g, sc, sh);
+}
+
+// Emits the work items of segment s at work-list offset w (chunk-major, then row block): the
+// (segment, chunk, row block) triple and the record the attention kernel reads.
+__device__ __forceinline__ void emit_items(const DevGraph& g, const DevSchedule& sc, int s,
+                                           int cnt, int group, int chunk_pages, int64_t w,
+                                           int64_t goff, int64_t prow_off) {
+  const int len = g.seg_len[s];
+  const int npg = (len + kPageTokens - 1) / kPageTokens;
+  const int nch = cnt > 0 ? (npg + chunk_pages - 1) / chunk_pages : 0;
+  const int nrb = (int)(((int64_t)cnt * group + kRowsPerBlock - 1) / kRowsPerBlock);
+  const int64_t poff = g.seg_page_off[s];
+  const int last_valid = len - (npg - 1) * kPageTokens;
+  for (int c = 0; c < nch; ++c) {
+    const int p0 = c * chunk_pages;
+    const int np = min(npg, p0 + chunk_pages) - p0;
+    for (int rbk = 0; rbk < nrb; ++rbk, ++w) {
+      sc.items[w] = make_int4(s, c, rbk, 0);
+      sc.recs[2 * w] = make_int4(np, npg - 1 - p0, last_valid, cnt);
+      sc.recs[2 * w + 1] = make_int4(rbk, (int)goff, (int)(poff + p0),
+                                     (int)(prow_off + (int64_t)c * cnt));
+    }
+  }
+}
+
+// The whole scheduler in one workgroup for graphs that fit in LDS (<= kSmallSegs segments,
+// <= kSmallEntries path entries, < kSmallBranches branches): the graph is read once into LDS,
+// every phase works there between workgroup barriers, and the outputs are only written.
+constexpr int kSmallSegs = 4096;
+constexpr int kSmallEntries = 8192;
+constexpr int kSmallBranches = 4096;
+
+__global__ __launch_bounds__(1024) void k_sched_small(DevGraph g, DevSchedule sc, int32_t group,
+                                                      int32_t chunk_pages) {
+  constexpr int EP = kSmallEntries / 1024, BP = kSmallBranches / 1024, SPT = kSmallSegs / 1024;
+  __shared__ int l_segs[kSmallEntries];     // path_segs
+  __shared__ int l_tmp[kSmallEntries];      // work-list order, later B(s) in arrival order
+  __shared__ int l_poff[kSmallBranches];    // path_off
+  __shared__ int l_cnt[kSmallSegs];         // |B(s)|
+  __shared__ int l_goff[kSmallSegs];        // group offsets (scatter cursors in phase 5)
+  __shared__ int l_len[kSmallSegs];         // segment lengths
+  __shared__ uint32_t l_key[kSmallSegs];    // sort keys, later partial-row offsets
+  __shared__ int sh[3][1024];
+  const int t = threadIdx.x;
+  const int S = g.S, E = g.E, B = g.B;
+  auto block_scan = [&](int a, int b, int c) {   // inclusive over threads -> sh
+    lds_barrier();
+    sh[0][t] = a; sh[1][t] = b; sh[2][t] = c;
+    lds_barrier();
+    for (int off = 1; off < 1024; off <<= 1) {
+      int x0 = 0, x1 = 0, x2 = 0;
+      if (t >= off) { x0 = sh[0][t - off]; x1 = sh[1][t - off]; x2 = sh[2][t - off]; }
+      lds_barrier();
+      sh[0][t] += x0; sh[1][t] += x1; sh[2][t] += x2;
+      lds_barrier();
+    }
+  };
+  auto nch_of = [&](int s) {
+    const int npg = (l_len[s] + kPageTokens - 1) / kPageTokens;
+    return l_cnt[s] > 0 ? (npg + chunk_pages - 1) / chunk_pages : 0;
+  };
+  auto nrb_of = [&](int s) {
+    return (int)(((int64_t)l_cnt[s] * group + kRowsPerBlock - 1) / kRowsPerBlock);
+  };
+
+  // 0. Read the graph once (all loads issued before any is used).
+  {
+    int vs[EP], vp[BP + 1], vl[SPT];
+#pragma unroll
+    for (int u = 0; u < EP; ++u) vs[u] = t + 1024 * u < E ? g.path_segs[t + 1024 * u] : 0;
+#pragma unroll
+    for (int u = 0; u <= BP; ++u) vp[u] = t + 1024 * u <= B ? (int)g.path_off[t + 1024 * u] : 0;
+#pragma unroll
+    for (int u = 0; u < SPT; ++u) vl[u] = t + 1024 * u < S ? g.seg_len[t + 1024 * u] : 0;
+#pragma unroll
+    for (int u = 0; u < EP; ++u) if (t + 1024 * u < E) l_segs[t + 1024 * u] = vs[u];
+#pragma unroll
+    for (int u = 0; u <= BP; ++u) if (t + 1024 * u <= B && t + 1024 * u < kSmallBranches) l_poff[t + 1024 * u] = vp[u];
+#pragma unroll
+    for (int u = 0; u < SPT; ++u)
+      if (t + 1024 * u < S) { l_len[t + 1024 * u] = vl[u]; l_cnt[t + 1024 * u] = 0; }
+  }
+  if (t < 4) sc.counters[t] = 0;
+  lds_barrier();
+
+  // 1. |B(s)|.
+  for (int e = t; e < E; e += 1024) atomicAdd(&l_cnt[l_segs[e]], 1);
+  lds_barrier();
+
+  // 2. Group and partial-row offsets in segment order (each thread owns <= 4 segments), and
+  //    the sort keys.
+  const int per = (S + 1023) / 1024;
+  const int s0 = min(S, t * per), s1 = min(S, s0 + per);
+  int prow_r[SPT];
+  {
+    int a = 0, c = 0;
+    for (int s = s0; s < s1; ++s) {
+      a += l_cnt[s];
+      c += nch_of(s) * l_cnt[s];
+    }
+    block_scan(a, 0, c);
+    int ra = t ? sh[0][t - 1] : 0, rc = t ? sh[2][t - 1] : 0;
+#pragma unroll
+    for (int u = 0; u < SPT; ++u) {
+      const int s = s0 + u;
+      if (s < s1) {
+        const int cnt = l_cnt[s], nch = nch_of(s);
+        const int npg = (l_len[s] + kPageTokens - 1) / kPageTokens;
+        l_goff[s] = ra;
+        prow_r[u] = rc;
+        sc.grp_cnt[s] = cnt;
+        sc.grp_off[s] = ra;
+        sc.seg_prow_off[s] = rc;
+        sc.seg_nchunk[s] = nch;
+        const uint32_t cost = cnt > 0 ? item_cost(npg, cnt, group, chunk_pages) : 0u;
+        l_key[s] = ((0xffffu - min(cost, 0xffffu)) << 16) | (uint32_t)s;   // S <= 65536
+        ra += cnt;
+        rc += nch * cnt;
+      }
+    }
+    if (t == 1023) {
+      sc.grp_off[S] = sh[0][1023];
+      sc.seg_prow_off[S] = sh[2][1023];
+      sc.counters[1] = sh[2][1023];
+    }
+  }
+  lds_barrier();
+
+  // 3. Work-list order: descending cost, ties by id (bitonic sort of the unique keys, one
+  //    compare-exchange per thread per pass; the sorted keys carry the segment ids).
+  {
+    int n = 1;
+    while (n < S) n <<= 1;
+    for (int i = S + t; i < n; i += 1024) l_key[i] = 0xffffffffu;
+    lds_barrier();
+    for (int k = 2; k <= n; k <<= 1) {
+      for (int j = k >> 1; j > 0; j >>= 1) {
+        for (int pr = t; pr < (n >> 1); pr += 1024) {
+          const int i = ((pr / j) * 2 * j) + (pr % j);
+          const int l = i + j;
+          const uint32_t x = l_key[i], y = l_key[l];
+          if ((x > y) == ((i & k) == 0)) { l_key[i] = y; l_key[l] = x; }
+        }
+        lds_barrier();
+      }
+    }
+    for (int i = t; i < S; i += 1024) l_tmp[i] = (int)(l_key[i] & 0xffffu);
+  }
+  lds_barrier();
+#pragma unroll
+  for (int u = 0; u < SPT; ++u)
+    if (s0 + u < s1) l_key[s0 + u] = (uint32_t)prow_r[u];   // keys done: partial-row offsets
+  // 4. Item offsets in work-list order, and the items (each thread owns <= 4 positions).
+  {
+    int b = 0;
+    for (int i = s0; i < s1; ++i) b += nch_of(l_tmp[i]) * nrb_of(l_tmp[i]);
+    block_scan(0, b, 0);                         // (also publishes the partial-row offsets)
+    int64_t poff_r[SPT];
+#pragma unroll
+    for (int u = 0; u < SPT; ++u) poff_r[u] = s0 + u < s1 ? g.seg_page_off[l_tmp[s0 + u]] : 0;
+    int64_t w = t ? sh[1][t - 1] : 0;
+#pragma unroll
+    for (int u = 0; u < SPT; ++u) {
+      if (s0 + u >= s1) break;
+      const int s = l_tmp[s0 + u];
+      const int cnt = l_cnt[s], len = l_len[s];
+      const int npg = (len + kPageTokens - 1) / kPageTokens;
+      const int nch = nch_of(s), nrb = nrb_of(s);
+      const int last_valid = len - (npg - 1) * kPageTokens;
+      sc.seg_item_off[s] = w;
+      for (int c = 0; c < nch; ++c) {
+        const int p0 = c * chunk_pages;
+        const int np = min(npg, p0 + chunk_pages) - p0;
+        for (int rbk = 0; rbk < nrb; ++rbk, ++w) {
+          sc.items[w] = make_int4(s, c, rbk, 0);
+          sc.recs[2 * w] = make_int4(np, npg - 1 - p0, last_valid, cnt);
+          sc.recs[2 * w + 1] = make_int4(rbk, l_goff[s], (int)(poff_r[u] + p0),
+                                         (int)(l_key[s] + c * cnt));
+        }
+      }
+    }
+    if (t == 1023) {
+      sc.seg_item_off[S] = sh[1][1023];
+      sc.counters[0] = sh[1][1023];
+    }
+  }
+  lds_barrier();
+
+  // 5. Scatter branches into their groups (arrival order; the group offsets serve as cursors).
+  for (int bb = t; bb < B; bb += 1024)
+    for (int e = l_poff[bb]; e < l_poff[bb + 1]; ++e) {
+      const int s = l_segs[e];
+      l_tmp[atomicAdd(&l_goff[s], 1)] = bb;
+    }
+  // 6. Ranks inside each group, and each entry's slot in the branch partial lists (exclusive
+  //    scan of chunk counts over entries; each thread owns a contiguous run of branches).
+  const int pb = (B + 1023) / 1024;
+  const int b0 = min(B, t * pb), b1 = min(B, b0 + pb);
+  int ne = 0;
+  for (int e = l_poff[b0]; e < l_poff[b1]; ++e) ne += nch_of(l_segs[e]);
+  block_scan(ne, 0, 0);                          // (also orders the scatter before the ranks)
+  int slot = t ? sh[0][t - 1] : 0;
+  for (int bb = b0; bb < b1; ++bb) {
+    sc.bpart_off[bb] = slot;
+    for (int e = l_poff[bb]; e < l_poff[bb + 1]; ++e) {
+      const int s = l_segs[e];
+      const int cnt = l_cnt[s], off = l_goff[s] - cnt, nch = nch_of(s);
+      int r = 0;
+      for (int k = 0; k < cnt; ++k) r += l_tmp[off + k] < bb;
+      sc.grp_br[off + r] = bb;
+      sc.entry_rank[e] = r;
+      sc.entry_branch[e] = bb;
+      sc.entry_part[e] = slot;
+      const int base = (int)l_key[s] + r;       // the branch's partials: segment chunks in order
+      for (int c = 0; c < nch; ++c) sc.bpart[slot + c] = base + c * cnt;
+      slot += nch;
+    }
+  }
+  if (t == 1023) sc.bpart_off[B] = sh[0][1023];
+}
+
 __global__ void k_scatter(DevGraph g, DevSchedule sc) {
   int e = blockIdx.x * kT + threadIdx.x;
   if (e >= g.E) return;
@@ -169,7 +453,7 @@ __global__ void k_scatter(DevGraph g, DevSchedule sc) {
 
 // Rank of each entry's branch inside B(s) (branch ids within a group are distinct because a
 // path visits a segment at most once), placement into ascending order, and the work items.
-__global__ void k_rank_items(DevGraph g, DevSchedule sc, int32_t group) {
+__global__ void k_rank_items(DevGraph g, DevSchedule sc, int32_t group, int32_t chunk_pages) {
   int i = blockIdx.x * kT + threadIdx.x;
   if (i < g.E) {
     const int s = g.path_segs[i];
@@ -180,14 +464,11 @@ __global__ void k_rank_items(DevGraph g, DevSchedule sc, int32_t group) {
     for (int k = 0; k < cnt; ++k) r += sc.grp_tmp[off + k] < b;
     sc.grp_br[off + r] = b;
     sc.entry_rank[i] = r;
+    write_entry_parts(g, sc, i, r, cnt);
   }
-  if (i < g.S) {
-    const int nch = sc.seg_nchunk[i];
-    const int nrb = (int)(((int64_t)sc.grp_cnt[i] * group + kRowsPerBlock - 1) / kRowsPerBlock);
-    int64_t w = sc.seg_item_off[i];
-    for (int c = 0; c < nch; ++c)
-      for (int rbk = 0; rbk < nrb; ++rbk) sc.items[w++] = make_int4(i, c, rbk, 0);
-  }
+  if (i < g.S)
+    emit_items(g, sc, i, sc.grp_cnt[i], group, chunk_pages, sc.seg_item_off[i], sc.grp_off[i],
+               sc.seg_prow_off[i]);
 }
 
 inline int blocks(int64_t n) { return (int)((n + kT - 1) / kT); }
@@ -196,15 +477,21 @@ inline int blocks(int64_t n) { return (int)((n + kT - 1) / kT); }
 
 hipError_t launch_schedule(const DevGraph& g, const DevSchedule& sc, int32_t group,
                            int32_t chunk_pages, hipStream_t stream) {
+  if (g.S <= kSmallSegs && g.E <= kSmallEntries && g.B < kSmallBranches) {
+    hipLaunchKernelGGL(k_sched_small, dim3(1), dim3(1024), 0, stream, g, sc, group, chunk_pages);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(k_init, dim3(blocks(g.S > 4 ? g.S : 4)), dim3(kT), 0, stream, g, sc);
   if (g.E > 0)
     hipLaunchKernelGGL(k_count, dim3(blocks(g.E)), dim3(kT), 0, stream, g, sc);
   hipLaunchKernelGGL(k_scan, dim3(1), dim3(1024), 0, stream, g, sc, group, chunk_pages);
+  hipLaunchKernelGGL(k_scan_entries, dim3(1), dim3(1024), 0, stream, g, sc);
   if (g.E > 0)
     hipLaunchKernelGGL(k_scatter, dim3(blocks(g.E)), dim3(kT), 0, stream, g, sc);
   const int64_t n = g.E > g.S ? g.E : g.S;
   if (n > 0)
-    hipLaunchKernelGGL(k_rank_items, dim3(blocks(n)), dim3(kT), 0, stream, g, sc, group);
+    hipLaunchKernelGGL(k_rank_items, dim3(blocks(n)), dim3(kT), 0, stream, g, sc, group,
+                       chunk_pages);
   return hipGetLastError();
 }
 

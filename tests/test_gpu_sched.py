@@ -102,3 +102,19 @@ def test_segment_shared_by_many_branches():
     paths = [[0, 1 + i] for i in range(n)]
     g = W.assemble_graph(lens, paths, 3)
     check_schedule(W.make_workload("600-way shared root", g, 28, 4, 64, "bf16", 3))
+
+
+def test_large_graphs_use_the_multi_kernel_path():
+    """Graphs beyond the single-workgroup limits (4096 segments, 8192 path entries, 4095
+    branches) take the multi-kernel scheduler; its output must be the same function of the
+    graph."""
+    rng = np.random.default_rng(7)
+    # > 4096 segments and branches
+    g = W.random_graph(rng, 5000, 4500, 40, 3, seed=1)
+    check_schedule(W.make_workload("5000-segment graph", g, 28, 4, 64, "bf16", 1))
+    # > 8192 path entries with few segments
+    lens = [int(x) for x in rng.integers(1, 50, size=64)]
+    paths = [list(rng.choice(64, size=10, replace=False)) for _ in range(900)]
+    g2 = W.assemble_graph(lens, paths, 3)
+    assert g2.path_segs.shape[0] == 9000
+    check_schedule(W.make_workload("9000-entry graph", g2, 8, 2, 64, "f32", 3))

@@ -145,19 +145,15 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
   using C = Cfg<D, BF16>;
   using T = typename std::conditional<BF16, __bf16, float>::type;
   constexpr int NI = C::SP * C::IPW;                // copies per wave per full stage
-  constexpr int PW = C::SP;                         // pages a wave computes per stage (max)
   __shared__ __align__(1024) unsigned char smem[C::NBUF * C::STAGE];
-  __shared__ int s_pages[2][kMaxChunkPages];        // page ids of units k and k + 1
-  __shared__ int s_rowbr[2][kRowsPerBlock + 4];     // branch ids of their row blocks
-  __shared__ int4 s_rec[3][2];                      // records of units k .. k + 2
-  __shared__ int64_t s_idx[4];                      // work indices of units k .. k + 3
+  __shared__ int s_pages[kMaxChunkPages];
+  __shared__ int64_t s_work;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int r16 = lane & 15, kg = lane >> 4;
   const int64_t n_work = a.counters[0] * a.Hkv;
-  const int group = a.group;
   const float NEG_INF = -__builtin_huge_valf();
   const unsigned char* pool = static_cast<const unsigned char*>(a.pool);
   const T* qbase = static_cast<const T*>(a.q);
@@ -178,68 +174,24 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
     c_rest[i] = kv * C::KVB + ((pc ^ (tok & (C::CPR - 1))) << 4);
   }
 
-  // Work arrives through a metadata pipeline so that a unit's start costs one round trip: at
-  // the start of unit k the workgroup claims unit k + 3 (work queue), reads the record of unit
-  // k + 2, the page ids and row branches of unit k + 1, and the queries of unit k, all at once.
-  auto rows_of = [&](const int4& r0, const int4& r1, int& row0, int& R, int& j0, int& nbr) {
-    row0 = r1.x * kRowsPerBlock;
-    R = min(kRowsPerBlock, r0.w * group - row0);
-    j0 = row0 / group;
-    nbr = (row0 + R - 1) / group - j0 + 1;
-  };
-  if (tid == 0)
-    for (int k = 0; k < 3; ++k)
-      s_idx[k] = (int64_t)atomicAdd((unsigned long long*)&a.counters[2], 1ull);
-  __syncthreads();
-  for (int k = 0; k < 2; ++k) {
-    const int64_t w = s_idx[k];
-    if (tid < 2 && w < n_work) s_rec[k][tid] = a.recs[2 * (w / a.Hkv) + tid];
-  }
-  __syncthreads();
-  if (s_idx[0] < n_work) {
-    const int4 r0 = s_rec[0][0], r1 = s_rec[0][1];
-    int row0, R, j0, nbr;
-    rows_of(r0, r1, row0, R, j0, nbr);
-    for (int i = tid; i < r0.x; i += kAttnThreads) s_pages[0][i] = a.seg_pages[r1.z + i];
-    for (int i = tid; i < nbr; i += kAttnThreads) s_rowbr[0][i] = a.grp_br[r1.y + j0 + i];
-  }
-  __syncthreads();
-
-  for (int ku = 0;; ++ku) {
-    const int64_t w = uniform64(s_idx[ku & 3]);
+  for (;;) {
+    if (tid == 0) s_work = (int64_t)atomicAdd((unsigned long long*)&a.counters[2], 1ull);
+    __syncthreads();
+    const int64_t w = uniform64(s_work);
     if (w >= n_work) break;
-    const int kvh = (int)(w % a.Hkv);
-    const int4 rec0 = s_rec[ku % 3][0], rec1 = s_rec[ku % 3][1];
-    const int np = __builtin_amdgcn_readfirstlane(rec0.x);
-    const int last_pg = __builtin_amdgcn_readfirstlane(rec0.y);
-    const int last_valid = __builtin_amdgcn_readfirstlane(rec0.z);
-    const int cnt = __builtin_amdgcn_readfirstlane(rec0.w);
-    const int prow_base = __builtin_amdgcn_readfirstlane(rec1.w);
-    int row0, R, j0, nbr;
-    rows_of(make_int4(np, last_pg, last_valid, cnt),
-            make_int4(__builtin_amdgcn_readfirstlane(rec1.x), 0, 0, 0), row0, R, j0, nbr);
+    const int64_t item = w / a.Hkv;
+    const int kvh = (int)(w - item * a.Hkv);
+    // One record per item (written by the scheduler): pages, last page, its valid tokens,
+    // |B(s)|, row block, group offset, page-table offset, first partial row.
+    const int4 rec0 = a.recs[2 * item], rec1 = a.recs[2 * item + 1];
+    const int np = rec0.x, last_pg = rec0.y, last_valid = rec0.z, cnt = rec0.w;
+    const int rb = rec1.x, goff = rec1.y, prow_base = rec1.w;
+    const int* pages = a.seg_pages + rec1.z;
+    for (int i = tid; i < np; i += kAttnThreads) s_pages[i] = pages[i];
+    const int row0 = rb * kRowsPerBlock;
+    const int R = min(kRowsPerBlock, cnt * a.group - row0);
     const int nrt = (R + 15) >> 4;
-    const int* pages_k = s_pages[ku & 1];
-    const int* rowbr_k = s_rowbr[ku & 1];
 
-    // Metadata for the next units: loads first, LDS writes after, so the round trips overlap.
-    const int64_t w1 = s_idx[(ku + 1) & 3], w2 = s_idx[(ku + 2) & 3];
-    int4 nrec = make_int4(0, 0, 0, 0);
-    if (tid < 2 && w2 < n_work) nrec = a.recs[2 * (w2 / a.Hkv) + tid];
-    int npid[kMaxChunkPages / kAttnThreads];
-    int nbid = 0, np1 = 0, nbr1 = 0;
-    if (w1 < n_work) {
-      const int4 q0 = s_rec[(ku + 1) % 3][0], q1 = s_rec[(ku + 1) % 3][1];
-      int r0_1, R1, j01;
-      rows_of(q0, q1, r0_1, R1, j01, nbr1);
-      np1 = q0.x;
-#pragma unroll
-      for (int u = 0; u < kMaxChunkPages / kAttnThreads; ++u) {
-        const int i = tid + u * kAttnThreads;
-        npid[u] = i < np1 ? a.seg_pages[q1.z + i] : 0;
-      }
-      if (tid < nbr1) nbid = a.grp_br[q1.y + j01 + tid];
-    }
     // Wave roles: with >= 3 row tiles the waves split the tiles (tiles wave and wave + 4); with
     // fewer, waves sharing a tile split the stage's pages and are combined at the end.
     int ks, split, t0, ntile;
@@ -260,9 +212,9 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
       const T* qp = qbase;
       if (live) {
         const int gr = row0 + r;
-        const int j = gr / group;
-        const int h = kvh * group + (gr - j * group);
-        const int b = rowbr_k[j - j0];
+        const int j = gr / a.group;
+        const int h = kvh * a.group + (gr - j * a.group);
+        const int b = a.grp_br[goff + j];
         qp = qbase + ((int64_t)b * a.Hq + h) * D;
       }
 #pragma unroll
@@ -304,7 +256,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
         const int pis = i / C::IPW;
         if (pis < npst) {
           const int pg = st * C::SP + pis;
-          const int pid = __builtin_amdgcn_readfirstlane(pages_k[pg]);
+          const int pid = __builtin_amdgcn_readfirstlane(s_pages[pg]);
           const unsigned char* base = pool_h + (int64_t)pid * blk_stride;
           dma16(pg == last_pg ? off_last[i] : off_full[i], base,
                 __builtin_amdgcn_readfirstlane(dst + i * 4096));
@@ -312,24 +264,10 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
       }
     };
 
-    // Claim unit k + 3 last: the atomic's result is waited for right after it.
-    int64_t nidx = 0;
-    if (tid == 0) nidx = (int64_t)atomicAdd((unsigned long long*)&a.counters[2], 1ull);
-    // Publish the next units' metadata.
-    if (tid == 0) s_idx[(ku + 3) & 3] = nidx;
-    if (tid < 2 && w2 < n_work) s_rec[(ku + 2) % 3][tid] = nrec;
-    if (w1 < n_work) {
-#pragma unroll
-      for (int u = 0; u < kMaxChunkPages / kAttnThreads; ++u) {
-        const int i = tid + u * kAttnThreads;
-        if (i < np1) s_pages[(ku + 1) & 1][i] = npid[u];
-      }
-      if (tid < nbr1) s_rowbr[(ku + 1) & 1][tid] = nbid;
-    }
     // The queries must have arrived before the first copy is issued: the compiler cannot see the
     // copies, so a wait it placed for its own loads inside the stage loop would also drain them.
     wait_vmcnt(0);
-    __syncthreads();                       // metadata visible; nothing of the last unit in flight
+    __syncthreads();                       // s_pages visible; nothing of the last item in flight
     const int nst = (np + C::SP - 1) / C::SP;
     for (int st = 0; st < C::NBUF - 1 && st < nst; ++st) issue(st);
     for (int st = 0; st < nst; ++st) {
@@ -344,135 +282,73 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
       if (st + C::NBUF - 1 < nst) issue(st + C::NBUF - 1);
       const int buf = st % C::NBUF;
       const int npst = min(C::SP, np - st * C::SP);
-      // This wave's pages of the stage (split, split + ks, ...), at most PW of them; all of them
-      // are processed together so their MFMA chains interleave.
-      const int npw = ntile > 0 && split < npst ? (npst - split + ks - 1) / ks : 0;
-      if (npw > 0) {
-        const unsigned char* kbp[PW];
-        bool lastp[PW];
+      if (ntile > 0) {
+        for (int pis = split; pis < npst; pis += ks) {
+          const unsigned char* kb = smem + buf * C::STAGE + pis * C::PB;
+          const unsigned char* vb = kb + C::KVB;
+          const bool last = st * C::SP + pis == last_pg;
+          f32x4 S[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
-        for (int pp = 0; pp < PW; ++pp) {
-          const int pis = split + pp * ks;
-          kbp[pp] = smem + buf * C::STAGE + (pp < npw ? pis : split) * C::PB;
-          lastp[pp] = pp < npw && st * C::SP + pis == last_pg;
-        }
-        // S^T = K Q^T for every (page, tile) of the wave.
-        f32x4 S[PW][2];
-#pragma unroll
-        for (int pp = 0; pp < PW; ++pp) S[pp][0] = S[pp][1] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int jj = 0; jj < C::QR; ++jj) {
-#pragma unroll
-          for (int pp = 0; pp < PW; ++pp) {
-            if (pp >= npw) break;
+          for (int jj = 0; jj < C::QR; ++jj) {
             if constexpr (BF16) {
-              const bf16x8 ka =
-                  *reinterpret_cast<const bf16x8*>(kbp[pp] + swz<D, BF16>(r16, 4 * jj + kg));
-              S[pp][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qop[0][jj].v, S[pp][0], 0, 0, 0);
+              const bf16x8 ka = *reinterpret_cast<const bf16x8*>(kb + swz<D, BF16>(r16, 4 * jj + kg));
+              S[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qop[0][jj].v, S[0], 0, 0, 0);
               if (ntile > 1)
-                S[pp][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qop[1][jj].v, S[pp][1], 0, 0, 0);
+                S[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qop[1][jj].v, S[1], 0, 0, 0);
             } else {
-              const float ka =
-                  *reinterpret_cast<const float*>(kbp[pp] + swz<D, BF16>(r16, jj) + kg * 4);
-              S[pp][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(ka, qop[0][jj].v, S[pp][0], 0, 0, 0);
+              const float ka = *reinterpret_cast<const float*>(kb + swz<D, BF16>(r16, jj) + kg * 4);
+              S[0] = __builtin_amdgcn_mfma_f32_16x16x4f32(ka, qop[0][jj].v, S[0], 0, 0, 0);
               if (ntile > 1)
-                S[pp][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(ka, qop[1][jj].v, S[pp][1], 0, 0, 0);
+                S[1] = __builtin_amdgcn_mfma_f32_16x16x4f32(ka, qop[1][jj].v, S[1], 0, 0, 0);
             }
           }
-        }
-        // Online softmax (log2 domain) over the wave's pages of this stage.  The row reference m
-        // only moves when some score exceeds it by more than 2^kTau, so the common stage needs
-        // no cross-lane reduction and no rescale of O.
-        float pv[PW][2][4];
+          // Online softmax (log2 domain) over this page's 16 tokens for each of the wave's tiles.
+          // The row reference m only moves when some score exceeds it by more than 2^kTau, so
+          // the common page needs no cross-lane reduction and no rescale of O.
+          float p[2][4];
 #pragma unroll
-        for (int k = 0; k < 2; ++k) {
-          if (k >= ntile) break;
-          float lm = NEG_INF;
-#pragma unroll
-          for (int pp = 0; pp < PW; ++pp) {
-            if (pp >= npw) break;
-            if (lastp[pp]) {
+          for (int k = 0; k < 2; ++k) {
+            if (k >= ntile) break;
+            if (last) {
 #pragma unroll
               for (int i = 0; i < 4; ++i)
-                if (4 * kg + i >= last_valid) S[pp][k][i] = NEG_INF;
+                if (4 * kg + i >= last_valid) S[k][i] = NEG_INF;
             }
-            lm = fmaxf(lm, fmaxf(fmaxf(S[pp][k][0], S[pp][k][1]), fmaxf(S[pp][k][2], S[pp][k][3])));
-          }
-          lm *= a.scale_log2;
-          if (__any(lm > m[k] + kTau)) {
-            const float mn = fmaxf(m[k], xmax(lm));
-            const float alpha = exp2_(m[k] - mn);
-            m[k] = mn;
-            l[k] *= alpha;
+            const float lm =
+                fmaxf(fmaxf(S[k][0], S[k][1]), fmaxf(S[k][2], S[k][3])) * a.scale_log2;
+            if (__any(lm > m[k] + kTau)) {
+              const float mn = fmaxf(m[k], xmax(lm));
+              const float alpha = exp2_(m[k] - mn);
+              m[k] = mn;
+              l[k] *= alpha;
 #pragma unroll
-            for (int n = 0; n < C::NB; ++n) O[k][n] *= alpha;
-          }
-          const float nm = -m[k];
-#pragma unroll
-          for (int pp = 0; pp < PW; ++pp) {
-            if (pp >= npw) break;
-#pragma unroll
-            for (int i = 0; i < 4; ++i) pv[pp][k][i] = exp2_(fmaf(S[pp][k][i], a.scale_log2, nm));
-            l[k] += (pv[pp][k][0] + pv[pp][k][1]) + (pv[pp][k][2] + pv[pp][k][3]);
-          }
-        }
-        // O^T += V^T P^T.
-        if constexpr (BF16) {
-          const int tv = 4 * kg + (r16 >> 2);
-          auto vread = [&](const unsigned char* vb, int n) {
-            const int off = tv * C::ROW + (((2 * n + ((r16 & 3) >> 1)) ^ (tv & (C::CPR - 1))) << 4) +
-                            (r16 & 1) * 8;
-            return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vb + off));
-          };
-#pragma unroll
-          for (int pp = 0; pp < PW; pp += 2) {
-            if (pp >= npw) break;
-            if (pp + 1 < npw) {
-              // Two pages = 32 tokens: one 16x16x32 MFMA per column block and tile.  k-slots
-              // 0-3 hold tokens 4*kg..+3 of the first page, slots 4-7 those of the second.  The
-              // 8-element operands are assembled as two whole 4-element halves (a union), not
-              // element by element: element-wise packing of the transposing read's result gave
-              // wrong operands.
-              union Pair { s16x4 h[2]; bf16x8 v; };
-              Pair pb[2];
-#pragma unroll
-              for (int k = 0; k < 2; ++k)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                  pb[k].h[0][i] = __builtin_bit_cast(short, (__bf16)(k < ntile ? pv[pp][k][i] : 0.f));
-                  pb[k].h[1][i] = __builtin_bit_cast(
-                      short, (__bf16)(k < ntile ? pv[pp + 1 < PW ? pp + 1 : pp][k][i] : 0.f));
-                }
-#pragma unroll
-              for (int n = 0; n < C::NB; ++n) {
-                Pair va;
-                va.h[0] = vread(kbp[pp] + C::KVB, n);
-                va.h[1] = vread(kbp[pp + 1 < PW ? pp + 1 : pp] + C::KVB, n);
-                O[0][n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va.v, pb[0].v, O[0][n], 0, 0, 0);
-                if (ntile > 1)
-                  O[1][n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va.v, pb[1].v, O[1][n], 0, 0, 0);
-              }
-            } else {
-              s16x4 pb[2];
-#pragma unroll
-              for (int k = 0; k < 2; ++k)
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                  pb[k][i] = __builtin_bit_cast(short, (__bf16)(k < ntile ? pv[pp][k][i] : 0.f));
-#pragma unroll
-              for (int n = 0; n < C::NB; ++n) {
-                const s16x4 va = vread(kbp[pp] + C::KVB, n);
-                O[0][n] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pb[0], O[0][n], 0, 0, 0);
-                if (ntile > 1)
-                  O[1][n] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pb[1], O[1][n], 0, 0, 0);
-              }
+              for (int n = 0; n < C::NB; ++n) O[k][n] *= alpha;
             }
-          }
-        } else {
+            const float nm = -m[k];
 #pragma unroll
-          for (int pp = 0; pp < PW; ++pp) {
-            if (pp >= npw) break;
-            const unsigned char* vb = kbp[pp] + C::KVB;
+            for (int i = 0; i < 4; ++i) p[k][i] = exp2_(fmaf(S[k][i], a.scale_log2, nm));
+            l[k] += (p[k][0] + p[k][1]) + (p[k][2] + p[k][3]);
+          }
+          if constexpr (BF16) {
+            s16x4 pb[2];
+#pragma unroll
+            for (int k = 0; k < 2; ++k)
+#pragma unroll
+              for (int i = 0; i < 4; ++i)
+                pb[k][i] = __builtin_bit_cast(short, (__bf16)(k < ntile ? p[k][i] : 0.f));
+            const int tv = 4 * kg + (r16 >> 2);
+#pragma unroll
+            for (int n = 0; n < C::NB; ++n) {
+              const int off = tv * C::ROW +
+                              (((2 * n + ((r16 & 3) >> 1)) ^ (tv & (C::CPR - 1))) << 4) +
+                              (r16 & 1) * 8;
+              const s16x4 va = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                  (lds_s16x4*)(vb + off));
+              O[0][n] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pb[0], O[0][n], 0, 0, 0);
+              if (ntile > 1)
+                O[1][n] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pb[1], O[1][n], 0, 0, 0);
+            }
+          } else {
 #pragma unroll
             for (int n = 0; n < C::NB; ++n) {
 #pragma unroll
@@ -480,9 +356,9 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
                 const int tv = 4 * kg + i;
                 const float va = *reinterpret_cast<const float*>(
                     vb + swz<D, BF16>(tv, 4 * n + (r16 >> 2)) + (r16 & 3) * 4);
-                O[0][n] = __builtin_amdgcn_mfma_f32_16x16x4f32(va, pv[pp][0][i], O[0][n], 0, 0, 0);
+                O[0][n] = __builtin_amdgcn_mfma_f32_16x16x4f32(va, p[0][i], O[0][n], 0, 0, 0);
                 if (ntile > 1)
-                  O[1][n] = __builtin_amdgcn_mfma_f32_16x16x4f32(va, pv[pp][1][i], O[1][n], 0, 0, 0);
+                  O[1][n] = __builtin_amdgcn_mfma_f32_16x16x4f32(va, p[1][i], O[1][n], 0, 0, 0);
               }
             }
           }
@@ -538,8 +414,8 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
         const int r = (t0 + 4 * k) * 16 + r16;
         if (r < R) {
           const int gr = row0 + r;
-          const int j = gr / group;
-          const int h = kvh * group + (gr - j * group);
+          const int j = gr / a.group;
+          const int h = kvh * a.group + (gr - j * a.group);
           const int64_t row = ((int64_t)prow_base + j) * a.Hq + h;
           const float inv = 1.f / L[k];
           float* dst = a.po + row * D + 4 * kg;
@@ -550,7 +426,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
         }
       }
     }
-    __syncthreads();                       // ring and metadata slots are reused by the next unit
+    __syncthreads();                       // smem and s_work are reused by the next item
   }
 }
 

@@ -53,6 +53,7 @@ struct Sizes {
   int64_t P = 0;               // entries of seg_pages
   int32_t chunk_pages = 0;
   int64_t max_items = 0;       // upper bound on work items per kv-head
+  int32_t desc_words = 0;      // work-item descriptor stride (int32 words)
   int64_t prows = 0;           // partial rows per q-head
 };
 
@@ -186,6 +187,7 @@ void size_schedule(const ga_segment_table* st, const ga_branch_paths* bp, const 
   z->prows = prows;   // partial rows are stored as int32 in the branch lists (checked by the caller)
   // items(s) = chunks(s) * ceil(|B(s)| g / 128) <= chunks(s) * (|B(s)| g / 128 + 1)
   z->max_items = chunks_ref + (prows * group + ga::kRowsPerBlock - 1) / ga::kRowsPerBlock;
+  z->desc_words = ga::desc_words((int)cap, group);
   (void)st;
 }
 
@@ -198,7 +200,7 @@ struct Layout {
 enum {
   L_SEG_LEN, L_SEG_PAGE_OFF, L_SEG_PAGES, L_PATH_OFF, L_PATH_SEGS,  // uploaded graph (contiguous)
   L_GRP_CNT, L_GRP_FILL, L_GRP_OFF, L_GRP_TMP, L_GRP_BR, L_ENTRY_BR, L_ENTRY_RANK, L_SEG_NCH,
-  L_SEG_ITEM_OFF, L_SEG_PROW_OFF, L_ITEMS, L_RECS, L_COUNTERS, L_ENTRY_PART, L_BPART_OFF, L_BPART,
+  L_SEG_ITEM_OFF, L_SEG_PROW_OFF, L_ITEMS, L_DESC, L_COUNTERS, L_ENTRY_PART, L_BPART_OFF, L_BPART,
   L_PO, L_PLSE, L_COUNT
 };
 
@@ -220,7 +222,9 @@ Layout layout(const Sizes& z, const ga_params& p) {
   sz[L_SEG_ITEM_OFF] = sizeof(int64_t) * (z.S + 1);
   sz[L_SEG_PROW_OFF] = sizeof(int64_t) * (z.S + 1);
   sz[L_ITEMS] = sizeof(int4) * (z.max_items > 0 ? z.max_items : 1);
-  sz[L_RECS] = 2 * sizeof(int4) * (z.max_items > 0 ? z.max_items : 1);
+  // (padded so that whole-slot copies of the last descriptor stay inside the allocation)
+  sz[L_DESC] = sizeof(int32_t) * (size_t)z.desc_words * (z.max_items > 0 ? z.max_items : 1) +
+               ga::kDescMaxBytes;
   sz[L_COUNTERS] = sizeof(int64_t) * 4;
   sz[L_ENTRY_PART] = sizeof(int64_t) * z.E;
   sz[L_BPART_OFF] = sizeof(int64_t) * (z.B + 1);
@@ -263,7 +267,8 @@ void bind(ga_plan* pl, const Layout& L) {
   pl->sc.seg_item_off = reinterpret_cast<int64_t*>(d + L.off[L_SEG_ITEM_OFF]);
   pl->sc.seg_prow_off = reinterpret_cast<int64_t*>(d + L.off[L_SEG_PROW_OFF]);
   pl->sc.items = reinterpret_cast<int4*>(d + L.off[L_ITEMS]);
-  pl->sc.recs = reinterpret_cast<int4*>(d + L.off[L_RECS]);
+  pl->sc.desc = reinterpret_cast<int32_t*>(d + L.off[L_DESC]);
+  pl->sc.desc_words = z.desc_words;
   pl->sc.counters = reinterpret_cast<int64_t*>(d + L.off[L_COUNTERS]);
   pl->sc.entry_part = reinterpret_cast<int64_t*>(d + L.off[L_ENTRY_PART]);
   pl->sc.bpart_off = reinterpret_cast<int64_t*>(d + L.off[L_BPART_OFF]);
@@ -309,6 +314,11 @@ ga_status plan_init(const ga_segment_table* st, const ga_branch_paths* bp, const
     return fail(GA_EINVAL, "too many partial rows (%lld)", (long long)pl->z.prows);
   if (pl->z.P > 0x7fffffffLL)
     return fail(GA_EINVAL, "too many page-table entries (%lld)", (long long)pl->z.P);
+  // Work units (item x kv-head) are claimed through a 32-bit counter that may overshoot by a
+  // few claims per workgroup.
+  if (pl->z.max_items * p->num_kv_heads > (1LL << 30))
+    return fail(GA_EINVAL, "too many work units (%lld)",
+                (long long)(pl->z.max_items * p->num_kv_heads));
   *L = layout(pl->z, pl->p);
   return GA_OK;
 }
@@ -337,7 +347,7 @@ ga_status do_schedule(ga_plan* pl, hipStream_t stream) {
   if (rec) GA_HIP(hipEventRecord(pl->ev_sched[2 * pl->prof_sched], stream), "profile event");
   if (pl->z.B > 0 || pl->z.S > 0) {
     GA_HIP(ga::launch_schedule(pl->g, pl->sc, pl->p.num_q_heads / pl->p.num_kv_heads,
-                               pl->z.chunk_pages, stream),
+                               pl->z.chunk_pages, pl->z.max_items, stream),
            "scheduler launch");
   }
   if (rec) {
@@ -360,9 +370,7 @@ ga_status do_run(ga_plan* pl, const void* q, const void* pool, void* out, float*
   ga::AttnArgs a{};
   a.q = q;
   a.pool = pool;
-  a.seg_pages = pl->g.seg_pages;
-  a.grp_br = pl->sc.grp_br;
-  a.recs = pl->sc.recs;
+  a.desc = pl->sc.desc;
   a.counters = pl->sc.counters;
   a.po = pl->po;
   a.plse = pl->plse;
@@ -370,6 +378,7 @@ ga_status do_run(ga_plan* pl, const void* q, const void* pool, void* out, float*
   a.Hkv = pl->p.num_kv_heads;
   a.group = a.Hq / a.Hkv;
   a.chunk_pages = pl->z.chunk_pages;
+  a.desc_words = pl->z.desc_words;
   a.scale_log2 = pl->p.softmax_scale * 1.4426950408889634f;
   int64_t grid = (int64_t)ga::seg_attn_grid(pl->p.head_dim, bf16, pl->num_cus);
   const int64_t work = pl->z.max_items * pl->p.num_kv_heads;

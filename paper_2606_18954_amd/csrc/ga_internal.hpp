@@ -10,8 +10,27 @@ constexpr int kPageTokens = 16;
 // Query rows (branch x q-head-in-group) handled by one work item: 8 MFMA row tiles of 16.
 constexpr int kRowsPerBlock = 128;
 // Upper bound on pages per work item (the chunk's page ids are staged in LDS).
-constexpr int kMaxChunkPages = 1024;
+constexpr int kMaxChunkPages = 512;
 constexpr int kAttnThreads = 256;        // 4 wave64 per workgroup
+
+// Work-item descriptor (int32 words, one per item, fixed stride), written by the scheduler and
+// copied whole into LDS by the attention kernel:
+//   [0..3]  pages in the chunk, index of the segment's last page relative to the chunk start,
+//           valid tokens of that last page, |B(s)|
+//   [4..7]  row block, group offset of B(s), page-table offset of the chunk, first partial row
+//   [8 .. 8 + chunk_pages)            physical page ids of the chunk
+//   [8 + chunk_pages .. + branches)   branch ids of the row block's rows (B(s) from row0/group)
+constexpr int kDescHead = 8;
+constexpr int kDescMaxBytes = 3072;      // LDS slot per descriptor
+__host__ __device__ inline int desc_branch_max(int group) {
+  const int n = (kRowsPerBlock + group - 1) / group + 1;
+  return n < kRowsPerBlock ? n : kRowsPerBlock;
+}
+__host__ __device__ inline int desc_words(int chunk_pages, int group) {
+  return (kDescHead + chunk_pages + desc_branch_max(group) + 3) & ~3;
+}
+static_assert(4 * ((kDescHead + kMaxChunkPages + kRowsPerBlock + 3) & ~3) <= kDescMaxBytes,
+              "descriptor must fit its LDS slot");
 
 // Device copy of the rollout graph (written once by plan_create's upload).
 struct DevGraph {
@@ -36,9 +55,8 @@ struct DevSchedule {
   int64_t* seg_item_off;   // [S+1] first work item of each segment
   int64_t* seg_prow_off;   // [S+1] first partial row (per q-head) of each segment
   int4* items;             // [max_items] (segment, chunk, row block, unused)
-  int4* recs;              // [2 * max_items] per-item record for the attention kernel:
-                           //   {pages, last page index, valid tokens of the last page, |B(s)|}
-                           //   {row block, group offset, page-table offset, first partial row}
+  int32_t* desc;           // [max_items * desc_words (+ kDescMaxBytes of padding)] descriptors
+  int32_t desc_words;      // descriptor stride in int32 words (a multiple of 4)
   int64_t* counters;       // [4]: items, partial rows, work-queue head, spare
   int64_t* entry_part;     // [E]   first slot of each path entry in the branch partial lists
   int64_t* bpart_off;      // [B+1] CSR offsets of each branch's partial rows
@@ -48,13 +66,12 @@ struct DevSchedule {
 struct AttnArgs {
   const void* q;
   const void* pool;
-  const int32_t* seg_pages;
-  const int32_t* grp_br;
-  const int4* recs;
-  int64_t* counters;
+  const int32_t* desc;     // work-item descriptors (layout above)
+  int64_t* counters;       // [0] items, [2] work-queue head (units claimed so far, as int32)
   float* po;               // [partial rows][Hq][D] normalised partial outputs
   float* plse;             // [partial rows][Hq] log2-domain log-sum-exp of each partial
   int32_t Hq, Hkv, group, chunk_pages;
+  int32_t desc_words;      // descriptor stride (int32 words)
   float scale_log2;        // softmax scale * log2(e)
 };
 
@@ -71,7 +88,7 @@ struct MergeArgs {
 
 // Launchers (each returns the launch status).
 hipError_t launch_schedule(const DevGraph& g, const DevSchedule& sc, int32_t group,
-                           int32_t chunk_pages, hipStream_t stream);
+                           int32_t chunk_pages, int64_t max_items, hipStream_t stream);
 hipError_t launch_seg_attn(const AttnArgs& a, int head_dim, bool bf16, int grid,
                            hipStream_t stream);
 hipError_t launch_merge(const MergeArgs& a, int head_dim, bool out_bf16, hipStream_t stream);

@@ -225,7 +225,7 @@ __global__ __launch_bounds__(1024) void k_scan_entries(DevGraph g, DevSchedule s
 }
 
 // Emits the work items of segment s at work-list offset w (chunk-major, then row block): the
-// (segment, chunk, row block) triple and the record the attention kernel reads.
+// (segment, chunk, row block) triple and the head of the item's descriptor.
 __device__ __forceinline__ void emit_items(const DevGraph& g, const DevSchedule& sc, int s,
                                            int cnt, int group, int chunk_pages, int64_t w,
                                            int64_t goff, int64_t prow_off) {
@@ -240,9 +240,9 @@ __device__ __forceinline__ void emit_items(const DevGraph& g, const DevSchedule&
     const int np = min(npg, p0 + chunk_pages) - p0;
     for (int rbk = 0; rbk < nrb; ++rbk, ++w) {
       sc.items[w] = make_int4(s, c, rbk, 0);
-      sc.recs[2 * w] = make_int4(np, npg - 1 - p0, last_valid, cnt);
-      sc.recs[2 * w + 1] = make_int4(rbk, (int)goff, (int)(poff + p0),
-                                     (int)(prow_off + (int64_t)c * cnt));
+      int4* d = reinterpret_cast<int4*>(sc.desc + w * sc.desc_words);
+      d[0] = make_int4(np, npg - 1 - p0, last_valid, cnt);
+      d[1] = make_int4(rbk, (int)goff, (int)(poff + p0), (int)(prow_off + (int64_t)c * cnt));
     }
   }
 }
@@ -397,9 +397,9 @@ __global__ __launch_bounds__(1024) void k_sched_small(DevGraph g, DevSchedule sc
         const int np = min(npg, p0 + chunk_pages) - p0;
         for (int rbk = 0; rbk < nrb; ++rbk, ++w) {
           sc.items[w] = make_int4(s, c, rbk, 0);
-          sc.recs[2 * w] = make_int4(np, npg - 1 - p0, last_valid, cnt);
-          sc.recs[2 * w + 1] = make_int4(rbk, l_goff[s], (int)(poff_r[u] + p0),
-                                         (int)(l_key[s] + c * cnt));
+          int4* d = reinterpret_cast<int4*>(sc.desc + w * sc.desc_words);
+          d[0] = make_int4(np, npg - 1 - p0, last_valid, cnt);
+          d[1] = make_int4(rbk, l_goff[s], (int)(poff_r[u] + p0), (int)(l_key[s] + c * cnt));
         }
       }
     }
@@ -471,14 +471,35 @@ __global__ void k_rank_items(DevGraph g, DevSchedule sc, int32_t group, int32_t 
                sc.seg_prow_off[i]);
 }
 
+// Completes each item's descriptor after its head is written: the chunk's physical page ids and
+// the branch ids of its row block (one wave per item).
+__global__ void k_fill_desc(DevGraph g, DevSchedule sc, int32_t group, int32_t chunk_pages) {
+  const int64_t w = (int64_t)blockIdx.x * (kT / 64) + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (w >= sc.counters[0]) return;
+  int32_t* d = sc.desc + w * sc.desc_words;
+  const int4 h0 = reinterpret_cast<const int4*>(d)[0];
+  const int4 h1 = reinterpret_cast<const int4*>(d)[1];
+  const int np = h0.x, cnt = h0.w, rb = h1.x, goff = h1.y, poff = h1.z;
+  for (int i = lane; i < np; i += 64) d[kDescHead + i] = g.seg_pages[poff + i];
+  const int row0 = rb * kRowsPerBlock;
+  const int R = min(kRowsPerBlock, cnt * group - row0);
+  const int j0 = row0 / group, nbj = (row0 + R - 1) / group - j0 + 1;
+  for (int i = lane; i < nbj; i += 64) d[kDescHead + chunk_pages + i] = sc.grp_br[goff + j0 + i];
+}
+
 inline int blocks(int64_t n) { return (int)((n + kT - 1) / kT); }
 
 }  // namespace
 
 hipError_t launch_schedule(const DevGraph& g, const DevSchedule& sc, int32_t group,
-                           int32_t chunk_pages, hipStream_t stream) {
+                           int32_t chunk_pages, int64_t max_items, hipStream_t stream) {
+  const int fill_blocks = (int)((max_items + kT / 64 - 1) / (kT / 64));
   if (g.S <= kSmallSegs && g.E <= kSmallEntries && g.B < kSmallBranches) {
     hipLaunchKernelGGL(k_sched_small, dim3(1), dim3(1024), 0, stream, g, sc, group, chunk_pages);
+    if (fill_blocks > 0)
+      hipLaunchKernelGGL(k_fill_desc, dim3(fill_blocks), dim3(kT), 0, stream, g, sc, group,
+                         chunk_pages);
     return hipGetLastError();
   }
   hipLaunchKernelGGL(k_init, dim3(blocks(g.S > 4 ? g.S : 4)), dim3(kT), 0, stream, g, sc);
@@ -491,6 +512,9 @@ hipError_t launch_schedule(const DevGraph& g, const DevSchedule& sc, int32_t gro
   const int64_t n = g.E > g.S ? g.E : g.S;
   if (n > 0)
     hipLaunchKernelGGL(k_rank_items, dim3(blocks(n)), dim3(kT), 0, stream, g, sc, group,
+                       chunk_pages);
+  if (fill_blocks > 0)
+    hipLaunchKernelGGL(k_fill_desc, dim3(fill_blocks), dim3(kT), 0, stream, g, sc, group,
                        chunk_pages);
   return hipGetLastError();
 }

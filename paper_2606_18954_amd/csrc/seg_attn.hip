@@ -108,6 +108,15 @@ __device__ __forceinline__ void wg_barrier() {
   asm volatile("" ::: "memory");
 }
 
+// Barrier for data exchanged through LDS by ordinary LDS writes: waits for this wave's LDS
+// operations only (lgkmcnt(0)), not for its global stores.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 // Byte offset of 16-byte chunk `ch` of token `tok` inside a K or V block in LDS.
 template <int D, bool BF16>
 __device__ __forceinline__ int swz(int tok, int ch) {
@@ -140,25 +149,164 @@ __device__ __forceinline__ int64_t uniform64(int64_t v) {
 // that the stale reference is kept (probabilities up to 2^kTau are exact in fp32 and bf16).
 constexpr float kTau = 8.0f;
 
+// Online softmax (log2 domain) over one page's 16 tokens for each of the wave's NT tiles: masks
+// tokens past the segment end, and moves a row's reference m only when some score exceeds it by
+// more than 2^kTau, so the common page needs no cross-lane reduction and no rescale of O.
+template <int NT, int NBW, int NBT>
+__device__ __forceinline__ void softmax_page(f32x4 (&S)[NT], float (&p)[NT][4], float (&m)[2],
+                                             float (&l)[2], f32x4 (&O)[2][NBT], bool last,
+                                             int last_valid, int kg, float sl2) {
+  const float NEG_INF = -__builtin_huge_valf();
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    if (last) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (4 * kg + i >= last_valid) S[t][i] = NEG_INF;
+    }
+    const float lm = fmaxf(fmaxf(S[t][0], S[t][1]), fmaxf(S[t][2], S[t][3])) * sl2;
+    if (__any(lm > m[t] + kTau)) {
+      const float mn = fmaxf(m[t], xmax(lm));
+      const float alpha = exp2_(m[t] - mn);
+      m[t] = mn;
+      l[t] *= alpha;
+#pragma unroll
+      for (int i = 0; i < NBW; ++i) O[t][i] *= alpha;
+    }
+    const float nm = -m[t];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) p[t][i] = exp2_(fmaf(S[t][i], sl2, nm));
+    l[t] += (p[t][0] + p[t][1]) + (p[t][2] + p[t][3]);
+  }
+}
+
+// One K/V stage for one wave: NT row tiles (qop[0 .. NT-1]) against pages p0, p0 + pstep, ... of
+// the stage, producing
+// NBW output column blocks (O[t][i] holds column block n0 + i).  All LDS operand reads of a page
+// are issued before its first MFMA, so the V reads overlap S = K Q^T and the softmax.
+template <int D, bool BF16, int NT, int NBW>
+__device__ __forceinline__ void kv_stage(const unsigned char* sb, int pg0, int p0, int pstep,
+                                         int npst, int last_pg, int last_valid, float sl2,
+                                         int r16, int kg, int n0,
+                                         const QOp<BF16> (&qop)[2][Cfg<D, BF16>::QR],
+                                         float (&m)[2], float (&l)[2],
+                                         f32x4 (&O)[2][Cfg<D, BF16>::NB]) {
+  using C = Cfg<D, BF16>;
+  const float NEG_INF = -__builtin_huge_valf();
+  for (int pis = p0; pis < npst; pis += pstep) {
+    const unsigned char* kb = sb + pis * C::PB;
+    const unsigned char* vb = kb + C::KVB;
+    const bool last = pg0 + pis == last_pg;
+    f32x4 S[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) S[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float p[NT][4];
+    if constexpr (BF16) {
+      // V^T operand of column block n: lane reads 4 tokens (4 kg + r16 / 4 supplies the row) of
+      // 4 columns through the transposing read; the chunk index is permuted like the writes.
+      // With two row tiles the V operands are read in two batches (register budget).
+      constexpr int VB = NT == 2 ? NBW / 2 : NBW;
+      const int tv = 4 * kg + (r16 >> 2);
+      auto vread = [&](int n) {
+        const int off = tv * C::ROW + (((2 * n + ((r16 & 3) >> 1)) ^ (tv & (C::CPR - 1))) << 4) +
+                        (r16 & 1) * 8;
+        return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vb + off));
+      };
+      bf16x8 ka[C::QR];
+      s16x4 va[VB];
+#pragma unroll
+      for (int jj = 0; jj < C::QR; ++jj)
+        ka[jj] = *reinterpret_cast<const bf16x8*>(kb + swz<D, BF16>(r16, 4 * jj + kg));
+#pragma unroll
+      for (int i = 0; i < VB; ++i) va[i] = vread(n0 + i);
+#pragma unroll
+      for (int jj = 0; jj < C::QR; ++jj)
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+          S[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[jj], qop[t][jj].v, S[t], 0, 0, 0);
+      softmax_page<NT, NBW, Cfg<D, BF16>::NB>(S, p, m, l, O, last, last_valid, kg, sl2);
+      s16x4 pb[NT];
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) pb[t][i] = __builtin_bit_cast(short, (__bf16)p[t][i]);
+#pragma unroll
+      for (int i0 = 0; i0 < NBW; i0 += VB) {
+        if (i0 > 0) {
+#pragma unroll
+          for (int i = 0; i < VB; ++i) va[i] = vread(n0 + i0 + i);
+        }
+#pragma unroll
+        for (int i = 0; i < VB; ++i)
+#pragma unroll
+          for (int t = 0; t < NT; ++t)
+            O[t][i0 + i] =
+                __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va[i], pb[t], O[t][i0 + i], 0, 0, 0);
+      }
+    } else {
+#pragma unroll
+      for (int jj = 0; jj < C::QR; ++jj) {
+        const float ka = *reinterpret_cast<const float*>(kb + swz<D, BF16>(r16, jj) + kg * 4);
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+          S[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(ka, qop[t][jj].v, S[t], 0, 0, 0);
+      }
+      softmax_page<NT, NBW, Cfg<D, BF16>::NB>(S, p, m, l, O, last, last_valid, kg, sl2);
+#pragma unroll
+      for (int i = 0; i < NBW; ++i) {
+        const int n = n0 + i;
+#pragma unroll
+        for (int i4 = 0; i4 < 4; ++i4) {
+          const int tv = 4 * kg + i4;
+          const float va = *reinterpret_cast<const float*>(
+              vb + swz<D, BF16>(tv, 4 * n + (r16 >> 2)) + (r16 & 3) * 4);
+#pragma unroll
+          for (int t = 0; t < NT; ++t)
+            O[t][i] = __builtin_amdgcn_mfma_f32_16x16x4f32(va, p[t][i4], O[t][i], 0, 0, 0);
+        }
+      }
+    }
+    (void)NEG_INF;
+  }
+}
+
 template <int D, bool BF16>
 __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
   using C = Cfg<D, BF16>;
   using T = typename std::conditional<BF16, __bf16, float>::type;
   constexpr int NI = C::SP * C::IPW;                // copies per wave per full stage
   __shared__ __align__(1024) unsigned char smem[C::NBUF * C::STAGE];
-  __shared__ int s_pages[kMaxChunkPages];
-  __shared__ int64_t s_work;
+  // Descriptors of the current and the next work unit (double buffer) and the next unit's id.
+  __shared__ __align__(1024) int s_desc[2][kDescMaxBytes / 4];
+  __shared__ int s_next[2];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int r16 = lane & 15, kg = lane >> 4;
-  const int64_t n_work = a.counters[0] * a.Hkv;
+  const int n_work = (int)(a.counters[0] * a.Hkv);
   const float NEG_INF = -__builtin_huge_valf();
   const unsigned char* pool = static_cast<const unsigned char*>(a.pool);
   const T* qbase = static_cast<const T*>(a.q);
   const unsigned lds_ring =
       (unsigned)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)smem;
+  const unsigned lds_desc =
+      (unsigned)(uintptr_t)(__attribute__((address_space(3))) int*)&s_desc[0][0];
+  const int dins = (a.desc_words * 4 + 1023) / 1024;      // copy instructions per descriptor
+  const int br_word = kDescHead + a.chunk_pages;          // first branch id in a descriptor
+
+  // Wave 0 copies the descriptor of unit v (if v < n_work) into buffer nb and publishes v (or
+  // -1: queue exhausted) there; the copy is waited for before the next end-of-unit barrier.
+  auto fetch_desc = [&](int v, int nb) {
+    const bool ok = v < n_work;
+    if (lane == 0) s_next[nb] = ok ? v : -1;
+    if (ok) {
+      const int* src = a.desc + (int64_t)(v / a.Hkv) * a.desc_words;
+      const unsigned dst = lds_desc + nb * kDescMaxBytes;
+      for (int i = 0; i < dins; ++i)
+        dma16(1024 * i + 16 * lane, src, __builtin_amdgcn_readfirstlane(dst + 1024 * i));
+    }
+  };
 
   // Per-lane source offsets inside a page block for this wave's copies: copy i of a stage covers
   // bytes [1024 j, 1024 j + 1024) with j = wave + 4 i, i.e. page i / IPW of the stage, piece
@@ -174,20 +322,28 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
     c_rest[i] = kv * C::KVB + ((pc ^ (tok & (C::CPR - 1))) << 4);
   }
 
-  for (;;) {
-    if (tid == 0) s_work = (int64_t)atomicAdd((unsigned long long*)&a.counters[2], 1ull);
-    __syncthreads();
-    const int64_t w = uniform64(s_work);
-    if (w >= n_work) break;
-    const int64_t item = w / a.Hkv;
-    const int kvh = (int)(w - item * a.Hkv);
-    // One record per item (written by the scheduler): pages, last page, its valid tokens,
-    // |B(s)|, row block, group offset, page-table offset, first partial row.
-    const int4 rec0 = a.recs[2 * item], rec1 = a.recs[2 * item + 1];
-    const int np = rec0.x, last_pg = rec0.y, last_valid = rec0.z, cnt = rec0.w;
-    const int rb = rec1.x, goff = rec1.y, prow_base = rec1.w;
-    const int* pages = a.seg_pages + rec1.z;
-    for (int i = tid; i < np; i += kAttnThreads) s_pages[i] = pages[i];
+  // The first unit: claimed and its descriptor copied before the loop.
+  if (wave == 0) {
+    int v = 0;
+    if (lane == 0) v = atomicAdd(reinterpret_cast<int*>(&a.counters[2]), 1);
+    fetch_desc(__builtin_amdgcn_readfirstlane(v), 0);
+    wait_vmcnt(0);
+  }
+  __syncthreads();
+
+  for (int b = 0;; b ^= 1) {
+    // Unit fields from its descriptor (the scheduler's record, then the chunk's page ids and the
+    // row block's branch ids).
+    const int w = __builtin_amdgcn_readfirstlane(s_next[b]);
+    if (w < 0) break;
+    const int* dsc = &s_desc[b][0];
+    const int kvh = w % a.Hkv;
+    const int np = __builtin_amdgcn_readfirstlane(dsc[0]);
+    const int last_pg = __builtin_amdgcn_readfirstlane(dsc[1]);
+    const int last_valid = __builtin_amdgcn_readfirstlane(dsc[2]);
+    const int cnt = __builtin_amdgcn_readfirstlane(dsc[3]);
+    const int rb = __builtin_amdgcn_readfirstlane(dsc[4]);
+    const int prow_base = __builtin_amdgcn_readfirstlane(dsc[7]);
     const int row0 = rb * kRowsPerBlock;
     const int R = min(kRowsPerBlock, cnt * a.group - row0);
     const int nrt = (R + 15) >> 4;
@@ -204,7 +360,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
     }
 
     // Q operand (B of S^T = K Q^T): lane holds row r16 of the tile, head_dim slice by kg.
-    QOp<BF16> qop[2][C::QR];
+    auto load_q = [&](QOp<BF16> (&qop)[2][C::QR]) {
 #pragma unroll
     for (int k = 0; k < 2; ++k) {
       const int r = (t0 + 4 * k) * 16 + r16;
@@ -214,8 +370,8 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
         const int gr = row0 + r;
         const int j = gr / a.group;
         const int h = kvh * a.group + (gr - j * a.group);
-        const int b = a.grp_br[goff + j];
-        qp = qbase + ((int64_t)b * a.Hq + h) * D;
+        const int br = dsc[br_word + j - row0 / a.group];
+        qp = qbase + ((int64_t)br * a.Hq + h) * D;
       }
 #pragma unroll
       for (int jj = 0; jj < C::QR; ++jj) {
@@ -228,6 +384,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
         }
       }
     }
+    };
 
     float m[2] = {NEG_INF, NEG_INF}, l[2] = {0.f, 0.f};
     f32x4 O[2][C::NB];
@@ -256,7 +413,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
         const int pis = i / C::IPW;
         if (pis < npst) {
           const int pg = st * C::SP + pis;
-          const int pid = __builtin_amdgcn_readfirstlane(s_pages[pg]);
+          const int pid = __builtin_amdgcn_readfirstlane(s_desc[b][kDescHead + pg]);
           const unsigned char* base = pool_h + (int64_t)pid * blk_stride;
           dma16(pg == last_pg ? off_last[i] : off_full[i], base,
                 __builtin_amdgcn_readfirstlane(dst + i * 4096));
@@ -264,12 +421,18 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
       }
     };
 
-    // The queries must have arrived before the first copy is issued: the compiler cannot see the
-    // copies, so a wait it placed for its own loads inside the stage loop would also drain them.
-    wait_vmcnt(0);
-    __syncthreads();                       // s_pages visible; nothing of the last item in flight
+    // The first stages are issued right away; the queries and the next unit's claim are loaded
+    // behind them, and one wait covers all three (the compiler cannot see the copies, so a wait
+    // it placed for its own loads inside the stage loop would also drain them).
     const int nst = (np + C::SP - 1) / C::SP;
     for (int st = 0; st < C::NBUF - 1 && st < nst; ++st) issue(st);
+    QOp<BF16> qop[2][C::QR];
+    load_q(qop);
+    int claim = 0;
+    if (wave == 0 && lane == 0) claim = atomicAdd(reinterpret_cast<int*>(&a.counters[2]), 1);
+    wait_vmcnt(0);
+    // Wave 0 fetches the next unit's descriptor while this one streams.
+    if (wave == 0) fetch_desc(__builtin_amdgcn_readfirstlane(claim), b ^ 1);
     for (int st = 0; st < nst; ++st) {
       // Wait until this wave's copies of stage st have landed (copies of later stages may stay
       // in flight), then make every wave's copies visible.
@@ -283,89 +446,19 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
       const int buf = st % C::NBUF;
       const int npst = min(C::SP, np - st * C::SP);
       if (ntile > 0) {
-        for (int pis = split; pis < npst; pis += ks) {
-          const unsigned char* kb = smem + buf * C::STAGE + pis * C::PB;
-          const unsigned char* vb = kb + C::KVB;
-          const bool last = st * C::SP + pis == last_pg;
-          f32x4 S[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
-#pragma unroll
-          for (int jj = 0; jj < C::QR; ++jj) {
-            if constexpr (BF16) {
-              const bf16x8 ka = *reinterpret_cast<const bf16x8*>(kb + swz<D, BF16>(r16, 4 * jj + kg));
-              S[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qop[0][jj].v, S[0], 0, 0, 0);
-              if (ntile > 1)
-                S[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qop[1][jj].v, S[1], 0, 0, 0);
-            } else {
-              const float ka = *reinterpret_cast<const float*>(kb + swz<D, BF16>(r16, jj) + kg * 4);
-              S[0] = __builtin_amdgcn_mfma_f32_16x16x4f32(ka, qop[0][jj].v, S[0], 0, 0, 0);
-              if (ntile > 1)
-                S[1] = __builtin_amdgcn_mfma_f32_16x16x4f32(ka, qop[1][jj].v, S[1], 0, 0, 0);
-            }
-          }
-          // Online softmax (log2 domain) over this page's 16 tokens for each of the wave's tiles.
-          // The row reference m only moves when some score exceeds it by more than 2^kTau, so
-          // the common page needs no cross-lane reduction and no rescale of O.
-          float p[2][4];
-#pragma unroll
-          for (int k = 0; k < 2; ++k) {
-            if (k >= ntile) break;
-            if (last) {
-#pragma unroll
-              for (int i = 0; i < 4; ++i)
-                if (4 * kg + i >= last_valid) S[k][i] = NEG_INF;
-            }
-            const float lm =
-                fmaxf(fmaxf(S[k][0], S[k][1]), fmaxf(S[k][2], S[k][3])) * a.scale_log2;
-            if (__any(lm > m[k] + kTau)) {
-              const float mn = fmaxf(m[k], xmax(lm));
-              const float alpha = exp2_(m[k] - mn);
-              m[k] = mn;
-              l[k] *= alpha;
-#pragma unroll
-              for (int n = 0; n < C::NB; ++n) O[k][n] *= alpha;
-            }
-            const float nm = -m[k];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) p[k][i] = exp2_(fmaf(S[k][i], a.scale_log2, nm));
-            l[k] += (p[k][0] + p[k][1]) + (p[k][2] + p[k][3]);
-          }
-          if constexpr (BF16) {
-            s16x4 pb[2];
-#pragma unroll
-            for (int k = 0; k < 2; ++k)
-#pragma unroll
-              for (int i = 0; i < 4; ++i)
-                pb[k][i] = __builtin_bit_cast(short, (__bf16)(k < ntile ? p[k][i] : 0.f));
-            const int tv = 4 * kg + (r16 >> 2);
-#pragma unroll
-            for (int n = 0; n < C::NB; ++n) {
-              const int off = tv * C::ROW +
-                              (((2 * n + ((r16 & 3) >> 1)) ^ (tv & (C::CPR - 1))) << 4) +
-                              (r16 & 1) * 8;
-              const s16x4 va = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                  (lds_s16x4*)(vb + off));
-              O[0][n] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pb[0], O[0][n], 0, 0, 0);
-              if (ntile > 1)
-                O[1][n] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, pb[1], O[1][n], 0, 0, 0);
-            }
-          } else {
-#pragma unroll
-            for (int n = 0; n < C::NB; ++n) {
-#pragma unroll
-              for (int i = 0; i < 4; ++i) {
-                const int tv = 4 * kg + i;
-                const float va = *reinterpret_cast<const float*>(
-                    vb + swz<D, BF16>(tv, 4 * n + (r16 >> 2)) + (r16 & 3) * 4);
-                O[0][n] = __builtin_amdgcn_mfma_f32_16x16x4f32(va, p[0][i], O[0][n], 0, 0, 0);
-                if (ntile > 1)
-                  O[1][n] = __builtin_amdgcn_mfma_f32_16x16x4f32(va, p[1][i], O[1][n], 0, 0, 0);
-              }
-            }
-          }
-        }
+        const unsigned char* sb = smem + buf * C::STAGE;
+        if (ntile > 1)
+          kv_stage<D, BF16, 2, C::NB>(sb, st * C::SP, split, ks, npst, last_pg, last_valid,
+                                      a.scale_log2, r16, kg, 0, qop, m, l, O);
+        else
+          kv_stage<D, BF16, 1, C::NB>(sb, st * C::SP, split, ks, npst, last_pg, last_valid,
+                                      a.scale_log2, r16, kg, 0, qop, m, l, O);
       }
     }
-    __syncthreads();                       // every wave done with the ring
+    // Every wave is done with the ring; wave 0's copy of the next descriptor has landed (the
+    // partial stores of earlier units need not have).
+    if (wave == 0) wait_vmcnt(0);
+    lds_barrier();
 
     // Row sums: reduce the per-lane partials across the four lane groups.
     float L[2];
@@ -383,7 +476,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
       for (int n = 0; n < C::NB; ++n)
 #pragma unroll
         for (int i = 0; i < 4; ++i) mine[(2 + 4 * n + i) * 64 + lane] = O[0][n][i];
-      __syncthreads();
+      lds_barrier();
       if (split == 0) {
         float M = NEG_INF;
         for (int sp = 0; sp < ks; ++sp) M = fmaxf(M, cb[(t0 + nrt * sp) * NV * 64 + lane]);
@@ -426,7 +519,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
         }
       }
     }
-    __syncthreads();                       // smem and s_work are reused by the next item
+    lds_barrier();                         // the ring is refilled by the next unit
   }
 }
 

@@ -200,7 +200,7 @@ struct Layout {
 enum {
   L_SEG_LEN, L_SEG_PAGE_OFF, L_SEG_PAGES, L_PATH_OFF, L_PATH_SEGS,  // uploaded graph (contiguous)
   L_GRP_CNT, L_GRP_FILL, L_GRP_OFF, L_GRP_TMP, L_GRP_BR, L_ENTRY_BR, L_ENTRY_RANK, L_SEG_NCH,
-  L_SEG_ITEM_OFF, L_SEG_PROW_OFF, L_ITEMS, L_DESC, L_COUNTERS, L_ENTRY_PART, L_BPART_OFF, L_BPART,
+  L_SEG_ITEM_OFF, L_SEG_PROW_OFF, L_SEG_ORDER, L_ORDER_ITEM_OFF, L_ITEMS, L_DESC, L_COUNTERS, L_ENTRY_PART, L_BPART_OFF, L_BPART,
   L_PO, L_PLSE, L_COUNT
 };
 
@@ -221,6 +221,8 @@ Layout layout(const Sizes& z, const ga_params& p) {
   sz[L_SEG_NCH] = sizeof(int32_t) * z.S;
   sz[L_SEG_ITEM_OFF] = sizeof(int64_t) * (z.S + 1);
   sz[L_SEG_PROW_OFF] = sizeof(int64_t) * (z.S + 1);
+  sz[L_SEG_ORDER] = sizeof(int32_t) * (z.S > 0 ? z.S : 1);
+  sz[L_ORDER_ITEM_OFF] = sizeof(int64_t) * (z.S + 1);
   sz[L_ITEMS] = sizeof(int4) * (z.max_items > 0 ? z.max_items : 1);
   // (padded so that whole-slot copies of the last descriptor stay inside the allocation)
   sz[L_DESC] = sizeof(int32_t) * (size_t)z.desc_words * (z.max_items > 0 ? z.max_items : 1) +
@@ -266,6 +268,8 @@ void bind(ga_plan* pl, const Layout& L) {
   pl->sc.seg_nchunk = reinterpret_cast<int32_t*>(d + L.off[L_SEG_NCH]);
   pl->sc.seg_item_off = reinterpret_cast<int64_t*>(d + L.off[L_SEG_ITEM_OFF]);
   pl->sc.seg_prow_off = reinterpret_cast<int64_t*>(d + L.off[L_SEG_PROW_OFF]);
+  pl->sc.seg_order = reinterpret_cast<int32_t*>(d + L.off[L_SEG_ORDER]);
+  pl->sc.order_item_off = reinterpret_cast<int64_t*>(d + L.off[L_ORDER_ITEM_OFF]);
   pl->sc.items = reinterpret_cast<int4*>(d + L.off[L_ITEMS]);
   pl->sc.desc = reinterpret_cast<int32_t*>(d + L.off[L_DESC]);
   pl->sc.desc_words = z.desc_words;

@@ -54,6 +54,8 @@ struct DevSchedule {
   int32_t* seg_nchunk;     // [S]   page chunks of each segment
   int64_t* seg_item_off;   // [S+1] first work item of each segment
   int64_t* seg_prow_off;   // [S+1] first partial row (per q-head) of each segment
+  int32_t* seg_order;      // [S]   segments in work-list order
+  int64_t* order_item_off; // [S+1] first work item of the segment at each work-list position
   int4* items;             // [max_items] (segment, chunk, row block, unused)
   int32_t* desc;           // [max_items * desc_words (+ kDescMaxBytes of padding)] descriptors
   int32_t desc_words;      // descriptor stride in int32 words (a multiple of 4)

@@ -60,6 +60,17 @@ __device__ __forceinline__ uint32_t item_cost(int npg, int cnt, int group, int c
   return (uint32_t)(min(npg, chunk_pages) * (2 + tiles));
 }
 
+// Cost class of a work item: half-octave bins of item_cost (0 for a segment without items).
+// The work list is ordered by descending class, ties by segment id: longest first, to within a
+// factor of 1.5, and a pure function of the graph.
+constexpr int kCostClasses = 32;
+__device__ __forceinline__ int cost_class(uint32_t cost) {
+  if (cost == 0) return 0;
+  const int e = 31 - __builtin_clz(cost);
+  const int m = e > 0 ? (int)((cost >> (e - 1)) & 1u) : 0;
+  return min(kCostClasses - 1, 1 + 2 * e + m);
+}
+
 #ifndef GA_SORT_CAP
 #define GA_SORT_CAP 8192
 #endif
@@ -120,7 +131,7 @@ __device__ void scan_segments(const DevGraph& g, const DevSchedule& sc, int32_t 
     sc.counters[1] = sh[2][1023];
   }
 
-  // 2. Work-list order: segments by descending item cost, ties by segment id (bitonic sort of
+  // 2. Work-list order: segments by descending cost class, ties by segment id (bitonic sort of
   //    unique 64-bit keys, so the order is a pure function of the graph).
   const bool sorted = S <= kSortCap;
   if (sorted) {
@@ -132,7 +143,7 @@ __device__ void scan_segments(const DevGraph& g, const DevSchedule& sc, int32_t 
         int cnt, nch, nrb, npg;
         seg_info(i, cnt, nch, nrb, npg);
         const uint32_t cost = cnt > 0 ? item_cost(npg, cnt, group, chunk_pages) : 0u;
-        key = ((uint64_t)(0xffffffffu - cost) << 32) | (uint32_t)i;
+        key = ((uint64_t)(kCostClasses - cost_class(cost)) << 32) | (uint32_t)i;
       }
       keys[i] = key;
     }
@@ -263,21 +274,26 @@ __global__ __launch_bounds__(1024) void k_sched_small(DevGraph g, DevSchedule sc
   __shared__ int l_cnt[kSmallSegs];         // |B(s)|
   __shared__ int l_goff[kSmallSegs];        // group offsets (scatter cursors in phase 5)
   __shared__ int l_len[kSmallSegs];         // segment lengths
-  __shared__ uint32_t l_key[kSmallSegs];    // sort keys, later partial-row offsets
+  __shared__ uint32_t l_key[kSmallSegs];    // sort keys
   __shared__ int sh[3][1024];
   const int t = threadIdx.x;
   const int S = g.S, E = g.E, B = g.B;
-  auto block_scan = [&](int a, int b, int c) {   // inclusive over threads -> sh
+  __shared__ int l_wsum[3][16];
+  // Inclusive scan over threads of three values at once -> sh[k][t] (sh[k][1023] is the total):
+  // a shuffle scan inside each wave, then each thread adds the totals of the waves before it.
+  auto block_scan = [&](int a, int b, int c) {
+    const int lane = t & 63, wv = t >> 6;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int ya = __shfl_up(a, off), yb = __shfl_up(b, off), yc = __shfl_up(c, off);
+      if (lane >= off) { a += ya; b += yb; c += yc; }
+    }
+    lds_barrier();                               // earlier readers of sh / l_wsum are done
+    if (lane == 63) { l_wsum[0][wv] = a; l_wsum[1][wv] = b; l_wsum[2][wv] = c; }
     lds_barrier();
+    for (int w = 0; w < wv; ++w) { a += l_wsum[0][w]; b += l_wsum[1][w]; c += l_wsum[2][w]; }
     sh[0][t] = a; sh[1][t] = b; sh[2][t] = c;
     lds_barrier();
-    for (int off = 1; off < 1024; off <<= 1) {
-      int x0 = 0, x1 = 0, x2 = 0;
-      if (t >= off) { x0 = sh[0][t - off]; x1 = sh[1][t - off]; x2 = sh[2][t - off]; }
-      lds_barrier();
-      sh[0][t] += x0; sh[1][t] += x1; sh[2][t] += x2;
-      lds_barrier();
-    }
   };
   auto nch_of = [&](int s) {
     const int npg = (l_len[s] + kPageTokens - 1) / kPageTokens;
@@ -315,7 +331,6 @@ __global__ __launch_bounds__(1024) void k_sched_small(DevGraph g, DevSchedule sc
   //    the sort keys.
   const int per = (S + 1023) / 1024;
   const int s0 = min(S, t * per), s1 = min(S, s0 + per);
-  int prow_r[SPT];
   {
     int a = 0, c = 0;
     for (int s = s0; s < s1; ++s) {
@@ -331,13 +346,12 @@ __global__ __launch_bounds__(1024) void k_sched_small(DevGraph g, DevSchedule sc
         const int cnt = l_cnt[s], nch = nch_of(s);
         const int npg = (l_len[s] + kPageTokens - 1) / kPageTokens;
         l_goff[s] = ra;
-        prow_r[u] = rc;
         sc.grp_cnt[s] = cnt;
         sc.grp_off[s] = ra;
         sc.seg_prow_off[s] = rc;
         sc.seg_nchunk[s] = nch;
         const uint32_t cost = cnt > 0 ? item_cost(npg, cnt, group, chunk_pages) : 0u;
-        l_key[s] = ((0xffffu - min(cost, 0xffffu)) << 16) | (uint32_t)s;   // S <= 65536
+        l_key[s] = ((uint32_t)(kCostClasses - 1 - cost_class(cost)) << 16) | (uint32_t)s;
         ra += cnt;
         rc += nch * cnt;
       }
@@ -350,61 +364,95 @@ __global__ __launch_bounds__(1024) void k_sched_small(DevGraph g, DevSchedule sc
   }
   lds_barrier();
 
-  // 3. Work-list order: descending cost, ties by id (bitonic sort of the unique keys, one
-  //    compare-exchange per thread per pass; the sorted keys carry the segment ids).
+  // 3. Work-list order: a stable counting sort of the segments by cost bucket (l_key >> 16,
+  //    bucket 0 = largest class), ties by segment id.  Segments are taken in slots of 1024
+  //    (s = 1024 u + t), so id order is slot-major, then wave, then lane.  Lanes of a wave with
+  //    equal buckets are matched with five bit ballots; the per-(slot, wave) bucket counts are
+  //    prefix-summed per bucket by one wave each.
   {
-    int n = 1;
-    while (n < S) n <<= 1;
-    for (int i = S + t; i < n; i += 1024) l_key[i] = 0xffffffffu;
+    constexpr int NBK = kCostClasses;
+    const int lane = t & 63, wv = t >> 6;
+    const uint64_t lt = lane ? (~0ull >> (64 - lane)) : 0ull;
+    const int nslots = (S + 1023) >> 10;         // <= kSmallSegs / 1024
+    int* cw = &sh[0][0];                         // [(slot * 16 + wave) * NBK + bucket]
+    int* tot = &sh[2][0];                        // [bucket] totals, then [NBK + bucket] offsets
+    for (int i = t; i < 2048; i += 1024) cw[i] = 0;
     lds_barrier();
-    for (int k = 2; k <= n; k <<= 1) {
-      for (int j = k >> 1; j > 0; j >>= 1) {
-        for (int pr = t; pr < (n >> 1); pr += 1024) {
-          const int i = ((pr / j) * 2 * j) + (pr % j);
-          const int l = i + j;
-          const uint32_t x = l_key[i], y = l_key[l];
-          if ((x > y) == ((i & k) == 0)) { l_key[i] = y; l_key[l] = x; }
+    int bk[SPT], wr[SPT];
+#pragma unroll
+    for (int u = 0; u < SPT; ++u) {
+      bk[u] = 0;
+      wr[u] = 0;
+      if (u < nslots) {
+        const int sg = 1024 * u + t;
+        const bool valid = sg < S;
+        const int bucket = valid ? (int)(l_key[sg] >> 16) : 0;
+        uint64_t m = __ballot(valid);
+#pragma unroll
+        for (int bit = 0; bit < 5; ++bit) {
+          const bool on = (bucket >> bit) & 1;
+          const uint64_t bb = __ballot(valid && on);
+          m &= on ? bb : ~bb;
         }
-        lds_barrier();
+        bk[u] = bucket;
+        wr[u] = __popcll(m & lt);
+        if (valid && (m & lt) == 0) cw[(u * 16 + wv) * NBK + bucket] = __popcll(m);
       }
     }
-    for (int i = t; i < S; i += 1024) l_tmp[i] = (int)(l_key[i] & 0xffffu);
+    lds_barrier();
+    // Exclusive prefix over the (slot, wave) pairs of each bucket: wave wv owns buckets wv and
+    // wv + 16, lane = pair index.
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int c = wv + 16 * h;
+      const int v = cw[lane * NBK + c];
+      int x = v;
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const int y = __shfl_up(x, off);
+        if (lane >= off) x += y;
+      }
+      cw[lane * NBK + c] = x - v;
+      if (lane == 63) tot[c] = x;
+    }
+    lds_barrier();
+    if (t < 64) {                                // bucket offsets: exclusive scan of the totals
+      const int v = t < NBK ? tot[t] : 0;
+      int x = v;
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const int y = __shfl_up(x, off);
+        if (t >= off) x += y;
+      }
+      if (t < NBK) tot[NBK + t] = x - v;
+    }
+    lds_barrier();
+#pragma unroll
+    for (int u = 0; u < SPT; ++u) {
+      const int sg = 1024 * u + t;
+      if (u < nslots && sg < S) l_tmp[tot[NBK + bk[u]] + cw[(u * 16 + wv) * NBK + bk[u]] + wr[u]] = sg;
+    }
   }
   lds_barrier();
-#pragma unroll
-  for (int u = 0; u < SPT; ++u)
-    if (s0 + u < s1) l_key[s0 + u] = (uint32_t)prow_r[u];   // keys done: partial-row offsets
-  // 4. Item offsets in work-list order, and the items (each thread owns <= 4 positions).
+  // 4. Item offsets in work-list order (each thread owns <= 4 positions); the items themselves
+  //    are written by k_emit.
   {
     int b = 0;
     for (int i = s0; i < s1; ++i) b += nch_of(l_tmp[i]) * nrb_of(l_tmp[i]);
     block_scan(0, b, 0);                         // (also publishes the partial-row offsets)
-    int64_t poff_r[SPT];
-#pragma unroll
-    for (int u = 0; u < SPT; ++u) poff_r[u] = s0 + u < s1 ? g.seg_page_off[l_tmp[s0 + u]] : 0;
-    int64_t w = t ? sh[1][t - 1] : 0;
+    int w = t ? sh[1][t - 1] : 0;
 #pragma unroll
     for (int u = 0; u < SPT; ++u) {
       if (s0 + u >= s1) break;
       const int s = l_tmp[s0 + u];
-      const int cnt = l_cnt[s], len = l_len[s];
-      const int npg = (len + kPageTokens - 1) / kPageTokens;
-      const int nch = nch_of(s), nrb = nrb_of(s);
-      const int last_valid = len - (npg - 1) * kPageTokens;
       sc.seg_item_off[s] = w;
-      for (int c = 0; c < nch; ++c) {
-        const int p0 = c * chunk_pages;
-        const int np = min(npg, p0 + chunk_pages) - p0;
-        for (int rbk = 0; rbk < nrb; ++rbk, ++w) {
-          sc.items[w] = make_int4(s, c, rbk, 0);
-          int4* d = reinterpret_cast<int4*>(sc.desc + w * sc.desc_words);
-          d[0] = make_int4(np, npg - 1 - p0, last_valid, cnt);
-          d[1] = make_int4(rbk, l_goff[s], (int)(poff_r[u] + p0), (int)(l_key[s] + c * cnt));
-        }
-      }
+      sc.seg_order[s0 + u] = s;
+      sc.order_item_off[s0 + u] = w;
+      w += nch_of(s) * nrb_of(s);
     }
     if (t == 1023) {
       sc.seg_item_off[S] = sh[1][1023];
+      sc.order_item_off[S] = sh[1][1023];
       sc.counters[0] = sh[1][1023];
     }
   }
@@ -416,31 +464,92 @@ __global__ __launch_bounds__(1024) void k_sched_small(DevGraph g, DevSchedule sc
       const int s = l_segs[e];
       l_tmp[atomicAdd(&l_goff[s], 1)] = bb;
     }
-  // 6. Ranks inside each group, and each entry's slot in the branch partial lists (exclusive
-  //    scan of chunk counts over entries; each thread owns a contiguous run of branches).
+  // 6. Each entry's branch and its slot in the branch partial lists (exclusive scan of chunk
+  //    counts over entries; each thread owns a contiguous run of branches).  The ranks, the
+  //    ascending groups and the lists themselves are written by k_emit.
   const int pb = (B + 1023) / 1024;
   const int b0 = min(B, t * pb), b1 = min(B, b0 + pb);
   int ne = 0;
   for (int e = l_poff[b0]; e < l_poff[b1]; ++e) ne += nch_of(l_segs[e]);
-  block_scan(ne, 0, 0);                          // (also orders the scatter before the ranks)
+  block_scan(ne, 0, 0);                          // (also orders the scatter before the copy)
   int slot = t ? sh[0][t - 1] : 0;
   for (int bb = b0; bb < b1; ++bb) {
     sc.bpart_off[bb] = slot;
     for (int e = l_poff[bb]; e < l_poff[bb + 1]; ++e) {
-      const int s = l_segs[e];
-      const int cnt = l_cnt[s], off = l_goff[s] - cnt, nch = nch_of(s);
-      int r = 0;
-      for (int k = 0; k < cnt; ++k) r += l_tmp[off + k] < bb;
-      sc.grp_br[off + r] = bb;
-      sc.entry_rank[e] = r;
       sc.entry_branch[e] = bb;
       sc.entry_part[e] = slot;
-      const int base = (int)l_key[s] + r;       // the branch's partials: segment chunks in order
-      for (int c = 0; c < nch; ++c) sc.bpart[slot + c] = base + c * cnt;
-      slot += nch;
+      slot += nch_of(l_segs[e]);
     }
   }
   if (t == 1023) sc.bpart_off[B] = sh[0][1023];
+  for (int i = t; i < E; i += 1024) sc.grp_tmp[i] = l_tmp[i];
+}
+
+// Outputs of the single-workgroup scheduler that are independent per path entry and per item,
+// written in parallel with coalesced stores.
+//   Blocks [0, eblocks), one thread per path entry (b, s): the rank r of b inside B(s) (count
+//   of smaller branch ids), B(s) in ascending order, the entry's rank, its partial rows (one per
+//   chunk of s, in chunk order) and b's place in the branch list of every descriptor whose row
+//   block holds b's rows.
+//   Later blocks, one wave per work item: the item (found by binary search over the item
+//   offsets in work-list order), the head of its descriptor and the chunk's page ids.
+__global__ void k_emit(DevGraph g, DevSchedule sc, int32_t group, int32_t chunk_pages,
+                       int32_t eblocks) {
+  if ((int)blockIdx.x < eblocks) {
+    const int e = blockIdx.x * kT + threadIdx.x;
+    if (e >= g.E) return;
+    const int s = g.path_segs[e];
+    const int b = sc.entry_branch[e];
+    const int off = (int)sc.grp_off[s];
+    const int cnt = sc.grp_cnt[s];
+    int r = 0, k = 0;
+    for (; k + 4 <= cnt; k += 4)
+      r += (sc.grp_tmp[off + k] < b) + (sc.grp_tmp[off + k + 1] < b) +
+           (sc.grp_tmp[off + k + 2] < b) + (sc.grp_tmp[off + k + 3] < b);
+    for (; k < cnt; ++k) r += sc.grp_tmp[off + k] < b;
+    sc.grp_br[off + r] = b;
+    sc.entry_rank[e] = r;
+    const int nch = sc.seg_nchunk[s];
+    const int slot = (int)sc.entry_part[e];
+    const int prow = (int)sc.seg_prow_off[s] + r;
+    for (int c = 0; c < nch; ++c) sc.bpart[slot + c] = prow + c * cnt;
+    const int nrb = (cnt * group + kRowsPerBlock - 1) / kRowsPerBlock;
+    const int rb_lo = (r * group) / kRowsPerBlock;
+    const int rb_hi = (r * group + group - 1) / kRowsPerBlock;
+    const int w0 = (int)sc.seg_item_off[s];
+    for (int c = 0; c < nch; ++c)
+      for (int rb = rb_lo; rb <= rb_hi; ++rb) {
+        const int64_t w = w0 + c * nrb + rb;
+        const int j0 = (rb * kRowsPerBlock) / group;
+        sc.desc[w * sc.desc_words + kDescHead + chunk_pages + (r - j0)] = b;
+      }
+    return;
+  }
+  const int64_t w = (int64_t)(blockIdx.x - eblocks) * (kT / 64) + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (w >= sc.counters[0]) return;
+  int lo = 0, hi = g.S;                          // order_item_off[lo] <= w < order_item_off[hi]
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (sc.order_item_off[mid] <= w) lo = mid; else hi = mid;
+  }
+  const int s = sc.seg_order[lo];
+  const int kk = (int)(w - sc.order_item_off[lo]);
+  const int cnt = sc.grp_cnt[s], len = g.seg_len[s];
+  const int npg = (len + kPageTokens - 1) / kPageTokens;
+  const int nrb = (cnt * group + kRowsPerBlock - 1) / kRowsPerBlock;
+  const int c = kk / nrb, rb = kk - c * nrb;
+  const int p0 = c * chunk_pages;
+  const int np = min(npg, p0 + chunk_pages) - p0;
+  const int poff = (int)g.seg_page_off[s] + p0;
+  int32_t* d = sc.desc + w * sc.desc_words;
+  if (lane == 0) {
+    sc.items[w] = make_int4(s, c, rb, 0);
+    reinterpret_cast<int4*>(d)[0] = make_int4(np, npg - 1 - p0, len - (npg - 1) * kPageTokens, cnt);
+    reinterpret_cast<int4*>(d)[1] =
+        make_int4(rb, (int)sc.grp_off[s], poff, (int)sc.seg_prow_off[s] + c * cnt);
+  }
+  for (int i = lane; i < np; i += 64) d[kDescHead + i] = g.seg_pages[poff + i];
 }
 
 __global__ void k_scatter(DevGraph g, DevSchedule sc) {
@@ -497,9 +606,10 @@ hipError_t launch_schedule(const DevGraph& g, const DevSchedule& sc, int32_t gro
   const int fill_blocks = (int)((max_items + kT / 64 - 1) / (kT / 64));
   if (g.S <= kSmallSegs && g.E <= kSmallEntries && g.B < kSmallBranches) {
     hipLaunchKernelGGL(k_sched_small, dim3(1), dim3(1024), 0, stream, g, sc, group, chunk_pages);
-    if (fill_blocks > 0)
-      hipLaunchKernelGGL(k_fill_desc, dim3(fill_blocks), dim3(kT), 0, stream, g, sc, group,
-                         chunk_pages);
+    const int eblocks = blocks(g.E);
+    if (eblocks + fill_blocks > 0)
+      hipLaunchKernelGGL(k_emit, dim3(eblocks + fill_blocks), dim3(kT), 0, stream, g, sc, group,
+                         chunk_pages, eblocks);
     return hipGetLastError();
   }
   hipLaunchKernelGGL(k_init, dim3(blocks(g.S > 4 ? g.S : 4)), dim3(kT), 0, stream, g, sc);

@@ -18,9 +18,20 @@ pytestmark = pytest.mark.gpu
 ROWS_PER_BLOCK = 128
 
 
+def cost_class(cost):
+    """Half-octave bins of the per-item cost: 1 + 2 floor(log2 c) + (the bit below the leading
+    one), capped at 31; 0 for no cost."""
+    cost = int(cost)
+    if cost == 0:
+        return 0
+    e = cost.bit_length() - 1
+    m = (cost >> (e - 1)) & 1 if e > 0 else 0
+    return min(31, 1 + 2 * e + m)
+
+
 def expected_items(g, group, chunk_pages, cnt):
-    """Work list: items grouped by segment, segments by descending per-item cost
-    (chunk pages x (2 + row tiles)), ties by segment id; within a segment chunk-major."""
+    """Work list: items grouped by segment, segments by descending cost class of the per-item
+    cost (chunk pages x (2 + row tiles)), ties by segment id; within a segment chunk-major."""
     def npg(s):
         return (int(g.seg_len[s]) + 15) // 16
 
@@ -28,7 +39,8 @@ def expected_items(g, group, chunk_pages, cnt):
         tiles = (min(cnt[s] * group, ROWS_PER_BLOCK) + 15) // 16
         return min(npg(s), chunk_pages) * (2 + tiles)
 
-    order = sorted((s for s in range(g.num_segments) if cnt[s] > 0), key=lambda s: (-cost(s), s))
+    order = sorted((s for s in range(g.num_segments) if cnt[s] > 0),
+                   key=lambda s: (-cost_class(cost(s)), s))
     items = []
     for s in order:
         nch = (npg(s) + chunk_pages - 1) // chunk_pages

@@ -85,6 +85,10 @@ __device__ __forceinline__ void dma16(unsigned off, const void* base, unsigned l
 // encoding splits vmcnt into bits [3:0] and [15:14].
 #define GA_VMCNT(k) (((k) & 15) | (7 << 4) | (15 << 8) | (((k) >> 4) << 14))
 __device__ __forceinline__ void wait_vmcnt(int n) {
+  // Loads placed before the wait in the source must be issued before it: the s_waitcnt builtin
+  // alone does not order ordinary loads, and a load sunk below it would be waited for later,
+  // inside the stage loop, draining the copy ring.
+  asm volatile("" ::: "memory");
 #define GA_VMW(k) case k: __builtin_amdgcn_s_waitcnt(GA_VMCNT(k)); break;
 #define GA_VMW8(b) GA_VMW(b) GA_VMW(b + 1) GA_VMW(b + 2) GA_VMW(b + 3) GA_VMW(b + 4) \
                    GA_VMW(b + 5) GA_VMW(b + 6) GA_VMW(b + 7)
@@ -97,7 +101,10 @@ __device__ __forceinline__ void wait_vmcnt(int n) {
 }
 
 template <int N>
-__device__ __forceinline__ void wait_vmcnt_const() { __builtin_amdgcn_s_waitcnt(GA_VMCNT(N)); }
+__device__ __forceinline__ void wait_vmcnt_const() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(GA_VMCNT(N));
+}
 
 // Workgroup barrier without a memory fence: LDS-DMA completion is ordered by the explicit
 // vmcnt wait before it; the empty asm statements keep the compiler from moving LDS accesses
@@ -153,8 +160,8 @@ constexpr float kTau = 8.0f;
 // tokens past the segment end, and moves a row's reference m only when some score exceeds it by
 // more than 2^kTau, so the common page needs no cross-lane reduction and no rescale of O.
 template <int NT, int NBW, int NBT>
-__device__ __forceinline__ void softmax_page(f32x4 (&S)[NT], float (&p)[NT][4], float (&m)[2],
-                                             float (&l)[2], f32x4 (&O)[2][NBT], bool last,
+__device__ __forceinline__ void softmax_page(f32x4 (&S)[NT], float (&p)[NT][4], float (&m)[NT],
+                                             float (&l)[NT], f32x4 (&O)[NT][NBT], bool last,
                                              int last_valid, int kg, float sl2) {
   const float NEG_INF = -__builtin_huge_valf();
 #pragma unroll
@@ -188,11 +195,12 @@ template <int D, bool BF16, int NT, int NBW>
 __device__ __forceinline__ void kv_stage(const unsigned char* sb, int pg0, int p0, int pstep,
                                          int npst, int last_pg, int last_valid, float sl2,
                                          int r16, int kg, int n0,
-                                         const QOp<BF16> (&qop)[2][Cfg<D, BF16>::QR],
-                                         float (&m)[2], float (&l)[2],
-                                         f32x4 (&O)[2][Cfg<D, BF16>::NB]) {
+                                         const QOp<BF16> (&qop)[NT][Cfg<D, BF16>::QR],
+                                         float (&m)[NT], float (&l)[NT],
+                                         f32x4 (&O)[NT][Cfg<D, BF16>::NB]) {
   using C = Cfg<D, BF16>;
   const float NEG_INF = -__builtin_huge_valf();
+  asm volatile("" : "+v"(r16), "+v"(kg));   // per-lane offsets recomputed per call, not hoisted
   for (int pis = p0; pis < npst; pis += pstep) {
     const unsigned char* kb = sb + pis * C::PB;
     const unsigned char* vb = kb + C::KVB;
@@ -359,166 +367,172 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
       ks = C::SP < 4 ? C::SP : 4; split = wave; t0 = 0; ntile = split < ks;
     }
 
-    // Q operand (B of S^T = K Q^T): lane holds row r16 of the tile, head_dim slice by kg.
-    auto load_q = [&](QOp<BF16> (&qop)[2][C::QR]) {
-#pragma unroll
-    for (int k = 0; k < 2; ++k) {
-      const int r = (t0 + 4 * k) * 16 + r16;
-      const bool live = k < ntile && r < R;
-      const T* qp = qbase;
-      if (live) {
-        const int gr = row0 + r;
-        const int j = gr / a.group;
-        const int h = kvh * a.group + (gr - j * a.group);
-        const int br = dsc[br_word + j - row0 / a.group];
-        qp = qbase + ((int64_t)br * a.Hq + h) * D;
-      }
-#pragma unroll
-      for (int jj = 0; jj < C::QR; ++jj) {
-        if constexpr (BF16) {
-          bf16x8 v = {};
-          if (live) v = *reinterpret_cast<const bf16x8*>(qp + 32 * jj + 8 * kg);
-          qop[k][jj].v = v;
-        } else {
-          qop[k][jj].v = live ? qp[4 * jj + kg] : 0.f;
-        }
-      }
-    }
-    };
-
-    float m[2] = {NEG_INF, NEG_INF}, l[2] = {0.f, 0.f};
-    f32x4 O[2][C::NB];
-#pragma unroll
-    for (int k = 0; k < 2; ++k)
-#pragma unroll
-      for (int n = 0; n < C::NB; ++n) O[k][n] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    // Offsets for the segment's last page: slots past its end re-read its last valid token
-    // (finite data; their scores are masked).
-    unsigned off_full[NI], off_last[NI];
-#pragma unroll
-    for (int i = 0; i < NI; ++i) {
-      off_full[i] = c_tok[i] * C::ROW + c_rest[i];
-      off_last[i] = min(c_tok[i], last_valid - 1) * C::ROW + c_rest[i];
-    }
-    const int64_t blk_stride = (int64_t)a.Hkv * 2 * C::KVB;
-    const unsigned char* pool_h = (const unsigned char*)uniform64(
-        (int64_t)(uintptr_t)(pool + (int64_t)kvh * 2 * C::KVB));
-
-    auto issue = [&](int st) {
-      const unsigned dst = lds_ring + (st % C::NBUF) * C::STAGE + wave * 1024;
-      const int npst = min(C::SP, np - st * C::SP);
-#pragma unroll
-      for (int i = 0; i < NI; ++i) {
-        const int pis = i / C::IPW;
-        if (pis < npst) {
-          const int pg = st * C::SP + pis;
-          const int pid = __builtin_amdgcn_readfirstlane(s_desc[b][kDescHead + pg]);
-          const unsigned char* base = pool_h + (int64_t)pid * blk_stride;
-          dma16(pg == last_pg ? off_last[i] : off_full[i], base,
-                __builtin_amdgcn_readfirstlane(dst + i * 4096));
-        }
-      }
-    };
-
-    // The first stages are issued right away; the queries and the next unit's claim are loaded
-    // behind them, and one wait covers all three (the compiler cannot see the copies, so a wait
-    // it placed for its own loads inside the stage loop would also drain them).
-    const int nst = (np + C::SP - 1) / C::SP;
-    for (int st = 0; st < C::NBUF - 1 && st < nst; ++st) issue(st);
-    QOp<BF16> qop[2][C::QR];
-    load_q(qop);
-    int claim = 0;
-    if (wave == 0 && lane == 0) claim = atomicAdd(reinterpret_cast<int*>(&a.counters[2]), 1);
-    wait_vmcnt(0);
-    // Wave 0 fetches the next unit's descriptor while this one streams.
-    if (wave == 0) fetch_desc(__builtin_amdgcn_readfirstlane(claim), b ^ 1);
-    for (int st = 0; st < nst; ++st) {
-      // Wait until this wave's copies of stage st have landed (copies of later stages may stay
-      // in flight), then make every wave's copies visible.
-      const int ahead = min(nst - 1 - st, C::NBUF - 2);
-      const int pend = C::IPW * (min(np, (st + 1 + ahead) * C::SP) - (st + 1) * C::SP);
-      if (pend == (C::NBUF - 2) * NI) wait_vmcnt_const<(C::NBUF - 2) * NI>();
-      else wait_vmcnt(pend);
-      wg_barrier();
-      // All waves are done with stage st - 1, so its buffer can be refilled.
-      if (st + C::NBUF - 1 < nst) issue(st + C::NBUF - 1);
-      const int buf = st % C::NBUF;
-      const int npst = min(C::SP, np - st * C::SP);
-      if (ntile > 0) {
-        const unsigned char* sb = smem + buf * C::STAGE;
-        if (ntile > 1)
-          kv_stage<D, BF16, 2, C::NB>(sb, st * C::SP, split, ks, npst, last_pg, last_valid,
-                                      a.scale_log2, r16, kg, 0, qop, m, l, O);
-        else
-          kv_stage<D, BF16, 1, C::NB>(sb, st * C::SP, split, ks, npst, last_pg, last_valid,
-                                      a.scale_log2, r16, kg, 0, qop, m, l, O);
-      }
-    }
-    // Every wave is done with the ring; wave 0's copy of the next descriptor has landed (the
-    // partial stores of earlier units need not have).
-    if (wave == 0) wait_vmcnt(0);
-    lds_barrier();
-
-    // Row sums: reduce the per-lane partials across the four lane groups.
-    float L[2];
-#pragma unroll
-    for (int k = 0; k < 2; ++k) L[k] = xsum(l[k]);
-
-    if (ks > 1) {
-      // Waves that split one tile's pages combine through LDS (the stage buffers are free).
-      constexpr int NV = C::NB * 4 + 2;
-      float* cb = reinterpret_cast<float*>(smem);
-      float* mine = cb + wave * NV * 64;
-      mine[0 * 64 + lane] = m[0];
-      mine[1 * 64 + lane] = L[0];
-#pragma unroll
-      for (int n = 0; n < C::NB; ++n)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) mine[(2 + 4 * n + i) * 64 + lane] = O[0][n][i];
-      lds_barrier();
-      if (split == 0) {
-        float M = NEG_INF;
-        for (int sp = 0; sp < ks; ++sp) M = fmaxf(M, cb[(t0 + nrt * sp) * NV * 64 + lane]);
-        float Lc = 0.f;
-        f32x4 Oc[C::NB];
-#pragma unroll
-        for (int n = 0; n < C::NB; ++n) Oc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
-        for (int sp = 0; sp < ks; ++sp) {
-          const float* o = cb + (t0 + nrt * sp) * NV * 64;
-          const float wgt = exp2_(o[lane] - M);
-          Lc += wgt * o[64 + lane];
-#pragma unroll
-          for (int n = 0; n < C::NB; ++n)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) Oc[n][i] += wgt * o[(2 + 4 * n + i) * 64 + lane];
-        }
-        m[0] = M;
-        L[0] = Lc;
-#pragma unroll
-        for (int n = 0; n < C::NB; ++n) O[0][n] = Oc[n];
-      }
-    }
-
-    if (split == 0) {
-#pragma unroll
-      for (int k = 0; k < 2; ++k) {
-        if (k >= ntile) break;
+    // The rest of the unit, specialised on the number of row tiles this wave owns (the
+    // second tile's registers exist only where they are used).
+    auto run_unit = [&](auto nt_tag) {
+      constexpr int NT = decltype(nt_tag)::value;
+      // Q operand (B of S^T = K Q^T): lane holds row r16 of the tile, head_dim slice by kg.
+      auto load_q = [&](QOp<BF16> (&qop)[NT][C::QR]) {
+  #pragma unroll
+      for (int k = 0; k < NT; ++k) {
         const int r = (t0 + 4 * k) * 16 + r16;
-        if (r < R) {
+        const bool live = k < ntile && r < R;
+        const T* qp = qbase;
+        if (live) {
           const int gr = row0 + r;
           const int j = gr / a.group;
           const int h = kvh * a.group + (gr - j * a.group);
-          const int64_t row = ((int64_t)prow_base + j) * a.Hq + h;
-          const float inv = 1.f / L[k];
-          float* dst = a.po + row * D + 4 * kg;
-#pragma unroll
-          for (int n = 0; n < C::NB; ++n)
-            *reinterpret_cast<f32x4*>(dst + 16 * n) = O[k][n] * inv;
-          if (kg == 0) a.plse[row] = m[k] + log2_(L[k]);
+          const int br = dsc[br_word + j - row0 / a.group];
+          qp = qbase + ((int64_t)br * a.Hq + h) * D;
+        }
+  #pragma unroll
+        for (int jj = 0; jj < C::QR; ++jj) {
+          if constexpr (BF16) {
+            bf16x8 v = {};
+            if (live) v = *reinterpret_cast<const bf16x8*>(qp + 32 * jj + 8 * kg);
+            qop[k][jj].v = v;
+          } else {
+            qop[k][jj].v = live ? qp[4 * jj + kg] : 0.f;
+          }
         }
       }
-    }
+      };
+  
+      float m[NT], l[NT];
+      f32x4 O[NT][C::NB];
+  #pragma unroll
+      for (int k = 0; k < NT; ++k) {
+        m[k] = NEG_INF;
+        l[k] = 0.f;
+  #pragma unroll
+        for (int n = 0; n < C::NB; ++n) O[k][n] = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+  
+      // Offsets for the segment's last page: slots past its end re-read its last valid token
+      // (finite data; their scores are masked).
+      unsigned off_full[NI], off_last[NI];
+  #pragma unroll
+      for (int i = 0; i < NI; ++i) {
+        off_full[i] = c_tok[i] * C::ROW + c_rest[i];
+        off_last[i] = min(c_tok[i], last_valid - 1) * C::ROW + c_rest[i];
+      }
+      const int64_t blk_stride = (int64_t)a.Hkv * 2 * C::KVB;
+      const unsigned char* pool_h = (const unsigned char*)uniform64(
+          (int64_t)(uintptr_t)(pool + (int64_t)kvh * 2 * C::KVB));
+  
+      auto issue = [&](int st) {
+        const unsigned dst = lds_ring + (st % C::NBUF) * C::STAGE + wave * 1024;
+        const int npst = min(C::SP, np - st * C::SP);
+  #pragma unroll
+        for (int i = 0; i < NI; ++i) {
+          const int pis = i / C::IPW;
+          if (pis < npst) {
+            const int pg = st * C::SP + pis;
+            const int pid = __builtin_amdgcn_readfirstlane(s_desc[b][kDescHead + pg]);
+            const unsigned char* base = pool_h + (int64_t)pid * blk_stride;
+            dma16(pg == last_pg ? off_last[i] : off_full[i], base,
+                  __builtin_amdgcn_readfirstlane(dst + i * 4096));
+          }
+        }
+      };
+  
+      // The first stages are issued right away; the queries and the next unit's claim are loaded
+      // behind them, and one wait covers all three (the compiler cannot see the copies, so a wait
+      // it placed for its own loads inside the stage loop would also drain them).
+      const int nst = (np + C::SP - 1) / C::SP;
+      for (int st = 0; st < C::NBUF - 1 && st < nst; ++st) issue(st);
+      QOp<BF16> qop[NT][C::QR];
+      load_q(qop);
+      int claim = 0;
+      if (wave == 0 && lane == 0) claim = atomicAdd(reinterpret_cast<int*>(&a.counters[2]), 1);
+      wait_vmcnt(0);
+      // Wave 0 fetches the next unit's descriptor while this one streams.
+      if (wave == 0) fetch_desc(__builtin_amdgcn_readfirstlane(claim), b ^ 1);
+      for (int st = 0; st < nst; ++st) {
+        // Wait until this wave's copies of stage st have landed (copies of later stages may stay
+        // in flight), then make every wave's copies visible.
+        const int ahead = min(nst - 1 - st, C::NBUF - 2);
+        const int pend = C::IPW * (min(np, (st + 1 + ahead) * C::SP) - (st + 1) * C::SP);
+        if (pend == (C::NBUF - 2) * NI) wait_vmcnt_const<(C::NBUF - 2) * NI>();
+        else wait_vmcnt(pend);
+        wg_barrier();
+        // All waves are done with stage st - 1, so its buffer can be refilled.
+        if (st + C::NBUF - 1 < nst) issue(st + C::NBUF - 1);
+        const int buf = st % C::NBUF;
+        const int npst = min(C::SP, np - st * C::SP);
+        if (ntile > 0) {
+          const unsigned char* sb = smem + buf * C::STAGE;
+          kv_stage<D, BF16, NT, C::NB>(sb, st * C::SP, split, ks, npst, last_pg, last_valid,
+                                       a.scale_log2, r16, kg, 0, qop, m, l, O);
+        }
+      }
+      // Every wave is done with the ring; wave 0's copy of the next descriptor has landed (the
+      // partial stores of earlier units need not have).
+      if (wave == 0) wait_vmcnt(0);
+      lds_barrier();
+  
+      // Row sums: reduce the per-lane partials across the four lane groups.
+      float L[NT];
+  #pragma unroll
+      for (int k = 0; k < NT; ++k) L[k] = xsum(l[k]);
+  
+      if (ks > 1) {
+        // Waves that split one tile's pages combine through LDS (the stage buffers are free).
+        constexpr int NV = C::NB * 4 + 2;
+        float* cb = reinterpret_cast<float*>(smem);
+        float* mine = cb + wave * NV * 64;
+        mine[0 * 64 + lane] = m[0];
+        mine[1 * 64 + lane] = L[0];
+  #pragma unroll
+        for (int n = 0; n < C::NB; ++n)
+  #pragma unroll
+          for (int i = 0; i < 4; ++i) mine[(2 + 4 * n + i) * 64 + lane] = O[0][n][i];
+        lds_barrier();
+        if (split == 0) {
+          float M = NEG_INF;
+          for (int sp = 0; sp < ks; ++sp) M = fmaxf(M, cb[(t0 + nrt * sp) * NV * 64 + lane]);
+          float Lc = 0.f;
+          f32x4 Oc[C::NB];
+  #pragma unroll
+          for (int n = 0; n < C::NB; ++n) Oc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
+          for (int sp = 0; sp < ks; ++sp) {
+            const float* o = cb + (t0 + nrt * sp) * NV * 64;
+            const float wgt = exp2_(o[lane] - M);
+            Lc += wgt * o[64 + lane];
+  #pragma unroll
+            for (int n = 0; n < C::NB; ++n)
+  #pragma unroll
+              for (int i = 0; i < 4; ++i) Oc[n][i] += wgt * o[(2 + 4 * n + i) * 64 + lane];
+          }
+          m[0] = M;
+          L[0] = Lc;
+  #pragma unroll
+          for (int n = 0; n < C::NB; ++n) O[0][n] = Oc[n];
+        }
+      }
+  
+      if (split == 0) {
+  #pragma unroll
+        for (int k = 0; k < NT; ++k) {
+          if (k >= ntile) break;
+          const int r = (t0 + 4 * k) * 16 + r16;
+          if (r < R) {
+            const int gr = row0 + r;
+            const int j = gr / a.group;
+            const int h = kvh * a.group + (gr - j * a.group);
+            const int64_t row = ((int64_t)prow_base + j) * a.Hq + h;
+            const float inv = 1.f / L[k];
+            float* dst = a.po + row * D + 4 * kg;
+  #pragma unroll
+            for (int n = 0; n < C::NB; ++n)
+              *reinterpret_cast<f32x4*>(dst + 16 * n) = O[k][n] * inv;
+            if (kg == 0) a.plse[row] = m[k] + log2_(L[k]);
+          }
+        }
+      }
+    };
+    if (ntile == 2) run_unit(std::integral_constant<int, 2>{});
+    else run_unit(std::integral_constant<int, 1>{});
     lds_barrier();                         // the ring is refilled by the next unit
   }
 }

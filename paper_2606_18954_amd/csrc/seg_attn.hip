@@ -286,7 +286,14 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
   __shared__ __align__(1024) unsigned char smem[C::NBUF * C::STAGE];
   // Descriptors of the current and the next work unit (double buffer) and the next unit's id.
   __shared__ __align__(1024) int s_desc[2][kDescMaxBytes / 4];
+  __shared__ float s_ml[4][2][64];
   __shared__ int s_next[2];
+  // Waves that split one tile's pages hand their (m, l, O) to the tile's split-0 wave through the
+  // last ring slot: at most MAXW hand-overs of NB KiB each.
+  constexpr int MAXW = (C::SP < 4 ? C::SP : 4) - 1 > 2 * ((C::SP < 2 ? C::SP : 2) - 1)
+                           ? (C::SP < 4 ? C::SP : 4) - 1
+                           : 2 * ((C::SP < 2 ? C::SP : 2) - 1);
+  static_assert(MAXW <= 4 && MAXW * C::NB * 1024 <= C::STAGE, "hand-over must fit one stage");
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -423,12 +430,19 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
       auto issue = [&](int st) {
         const unsigned dst = lds_ring + (st % C::NBUF) * C::STAGE + wave * 1024;
         const int npst = min(C::SP, np - st * C::SP);
+        // All page ids of the stage are read before the first copy: one LDS round trip (the
+        // copies' memory clobber would otherwise force a re-read before each of them).  Ids past
+        // the chunk are read but unused.
+        int pids[C::SP];
+  #pragma unroll
+        for (int q = 0; q < C::SP; ++q)
+          pids[q] = __builtin_amdgcn_readfirstlane(s_desc[b][kDescHead + st * C::SP + q]);
   #pragma unroll
         for (int i = 0; i < NI; ++i) {
           const int pis = i / C::IPW;
           if (pis < npst) {
             const int pg = st * C::SP + pis;
-            const int pid = __builtin_amdgcn_readfirstlane(s_desc[b][kDescHead + pg]);
+            const int pid = pids[pis];
             const unsigned char* base = pool_h + (int64_t)pid * blk_stride;
             dma16(pg == last_pg ? off_last[i] : off_full[i], base,
                   __builtin_amdgcn_readfirstlane(dst + i * 4096));
@@ -477,32 +491,39 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
       for (int k = 0; k < NT; ++k) L[k] = xsum(l[k]);
   
       if (ks > 1) {
-        // Waves that split one tile's pages combine through LDS (the stage buffers are free).
-        constexpr int NV = C::NB * 4 + 2;
-        float* cb = reinterpret_cast<float*>(smem);
-        float* mine = cb + wave * NV * 64;
-        mine[0 * 64 + lane] = m[0];
-        mine[1 * 64 + lane] = L[0];
+        // Waves that split one tile's pages hand (m, l, O) to the tile's split-0 wave through
+        // the last ring slot: the next unit's first stages go to the other slots, and this one
+        // is refilled only after that unit's first barrier.
+        constexpr int NV = C::NB * 4;
+        float* cb = reinterpret_cast<float*>(smem + (C::NBUF - 1) * C::STAGE);
+        if (split > 0 && ntile > 0) {
+          const int wi = (split - 1) * nrt + t0;
+          float* mine = cb + wi * NV * 64;
+          s_ml[wi][0][lane] = m[0];
+          s_ml[wi][1][lane] = L[0];
   #pragma unroll
-        for (int n = 0; n < C::NB; ++n)
+          for (int n = 0; n < C::NB; ++n)
   #pragma unroll
-          for (int i = 0; i < 4; ++i) mine[(2 + 4 * n + i) * 64 + lane] = O[0][n][i];
+            for (int i = 0; i < 4; ++i) mine[(4 * n + i) * 64 + lane] = O[0][n][i];
+        }
         lds_barrier();
-        if (split == 0) {
-          float M = NEG_INF;
-          for (int sp = 0; sp < ks; ++sp) M = fmaxf(M, cb[(t0 + nrt * sp) * NV * 64 + lane]);
-          float Lc = 0.f;
+        if (split == 0 && ntile > 0) {
+          float M = m[0];
+          for (int sp = 1; sp < ks; ++sp) M = fmaxf(M, s_ml[(sp - 1) * nrt + t0][0][lane]);
+          const float w0 = exp2_(m[0] - M);
+          float Lc = w0 * L[0];
           f32x4 Oc[C::NB];
   #pragma unroll
-          for (int n = 0; n < C::NB; ++n) Oc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
-          for (int sp = 0; sp < ks; ++sp) {
-            const float* o = cb + (t0 + nrt * sp) * NV * 64;
-            const float wgt = exp2_(o[lane] - M);
-            Lc += wgt * o[64 + lane];
+          for (int n = 0; n < C::NB; ++n) Oc[n] = O[0][n] * w0;
+          for (int sp = 1; sp < ks; ++sp) {
+            const int wi = (sp - 1) * nrt + t0;
+            const float* o = cb + wi * NV * 64;
+            const float wgt = exp2_(s_ml[wi][0][lane] - M);
+            Lc += wgt * s_ml[wi][1][lane];
   #pragma unroll
             for (int n = 0; n < C::NB; ++n)
   #pragma unroll
-              for (int i = 0; i < 4; ++i) Oc[n][i] += wgt * o[(2 + 4 * n + i) * 64 + lane];
+              for (int i = 0; i < 4; ++i) Oc[n][i] += wgt * o[(4 * n + i) * 64 + lane];
           }
           m[0] = M;
           L[0] = Lc;
@@ -531,9 +552,11 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
         }
       }
     };
+    // No barrier here: the next unit's first copies go to slots every wave is done with (the
+    // barrier after the stage loop), its descriptor was published by that barrier, and nothing
+    // reads this unit's descriptor buffer after the unit's start.
     if (ntile == 2) run_unit(std::integral_constant<int, 2>{});
     else run_unit(std::integral_constant<int, 1>{});
-    lds_barrier();                         // the ring is refilled by the next unit
   }
 }
 

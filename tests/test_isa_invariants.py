@@ -47,7 +47,7 @@ def test_every_m0_write_feeds_a_direct_to_lds_copy(asm):
         copies = 0
         for i, l in enumerate(lines):
             if re.search(r"\bm0\b", l):
-                assert l.startswith("s_mov_b32 m0, s"), (name, l)
+                assert re.match(r"s_mov_b32 m0, (s\d+|vcc_lo|vcc_hi)$", l), (name, l)
                 assert lines[i + 1].startswith("global_load_lds_dwordx4"), (name, lines[i + 1])
                 copies += 1
         assert copies >= 1, name
@@ -70,3 +70,4 @@ def test_no_compiler_vector_memory_waits_in_the_compute(asm):
         mixed = [w for w in re.findall(r"s_waitcnt vmcnt\((\d+)\)(?: expcnt\(\d+\))? lgkmcnt\((\d+)\)", body)
                  if int(w[0]) < 63 and int(w[1]) < 15]     # (63, 15) is "wait for nothing"
         assert not mixed, (name, mixed[:3])
+

@@ -71,12 +71,14 @@ struct Cfg {
 // as inline assembly so that the compiler's wait-count pass does not treat every later LDS read
 // as a possible alias of the copy (it would drain the whole pipeline before each stage);
 // ordering is explicit instead: wait_vmcnt() before the barrier that publishes a stage.  M0
-// holds the LDS base; the kernel keeps no other value in M0.
+// holds the LDS base; the kernel keeps no other value in M0.  The copies are non-temporal (nt):
+// every K/V byte is read once per step, and streaming it through the caches at normal priority
+// would evict the partial rows this kernel writes and the merge kernel reads back.
 // (tests/test_isa_invariants.py checks in the built assembly that every M0 write is one of these.)
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
 __device__ __forceinline__ void dma16(unsigned off, const void* base, unsigned lds_base) {
-  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1 nt"
                :: "v"(off), "s"(base), "s"(lds_base) : "memory", "m0");
 }
 #pragma clang diagnostic pop

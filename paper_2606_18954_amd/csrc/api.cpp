@@ -72,7 +72,7 @@ struct ga_plan {
   int num_cus = 256;
   ga::DevGraph g{};
   ga::DevSchedule sc{};
-  float* po = nullptr;
+  void* po = nullptr;
   float* plse = nullptr;
   // Kernel timing (graphattn_plan_profile): events for up to prof_cap schedule / run calls.
   int32_t prof_cap = 0, prof_sched = 0, prof_runs = 0;
@@ -231,8 +231,10 @@ Layout layout(const Sizes& z, const ga_params& p) {
   sz[L_ENTRY_PART] = sizeof(int64_t) * z.E;
   sz[L_BPART_OFF] = sizeof(int64_t) * (z.B + 1);
   sz[L_BPART] = sizeof(int32_t) * z.prows;
-  sz[L_PO] = sizeof(float) * (size_t)z.prows * p.num_q_heads * p.head_dim;
-  sz[L_PLSE] = sizeof(float) * (size_t)z.prows * p.num_q_heads;
+  // Partials: fp16 values + (lambda, scale) for bf16 inputs, fp32 values + lambda for fp32.
+  const bool f16_parts = p.dtype == GA_BF16;
+  sz[L_PO] = (f16_parts ? 2 : 4) * (size_t)z.prows * p.num_q_heads * p.head_dim;
+  sz[L_PLSE] = (f16_parts ? 8 : 4) * (size_t)z.prows * p.num_q_heads;
   Layout L{};
   size_t o = 0;
   for (int i = 0; i < L_COUNT; ++i) {
@@ -277,7 +279,7 @@ void bind(ga_plan* pl, const Layout& L) {
   pl->sc.entry_part = reinterpret_cast<int64_t*>(d + L.off[L_ENTRY_PART]);
   pl->sc.bpart_off = reinterpret_cast<int64_t*>(d + L.off[L_BPART_OFF]);
   pl->sc.bpart = reinterpret_cast<int32_t*>(d + L.off[L_BPART]);
-  pl->po = reinterpret_cast<float*>(d + L.off[L_PO]);
+  pl->po = d + L.off[L_PO];
   pl->plse = reinterpret_cast<float*>(d + L.off[L_PLSE]);
 }
 
@@ -403,7 +405,8 @@ ga_status do_run(ga_plan* pl, const void* q, const void* pool, void* out, float*
   m.counters = pl->sc.counters;
   m.B = pl->z.B;
   m.Hq = pl->p.num_q_heads;
-  GA_HIP(ga::launch_merge(m, pl->p.head_dim, bf16 && !pl->p.out_f32, stream), "merge launch");
+  GA_HIP(ga::launch_merge(m, pl->p.head_dim, bf16 && !pl->p.out_f32, bf16, stream),
+         "merge launch");
   if (rec) {
     GA_HIP(hipEventRecord(ev[2], stream), "profile event");
     pl->ev_last = ev[2];

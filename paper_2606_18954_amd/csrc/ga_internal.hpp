@@ -65,13 +65,22 @@ struct DevSchedule {
   int32_t* bpart;          // [partial rows] partial rows of each branch: path order, then chunk
 };
 
+// Partial rows (one per partial row and q-head), in one of two formats:
+// * fp32 inputs: po [rows][Hq][D] fp32, the normalised partial output o in column order;
+//   plse [rows][Hq] fp32, its log2-domain log-sum-exp lambda.
+// * bf16 inputs: po [rows][Hq][D] fp16, o scaled by 2^(15 - e) (e: the binary exponent of the
+//   row's largest |o|, so every value is below 2^15) and stored in lane order: column
+//   16 n + 4 g + i (n < D/16, g < 4, i < 4) at position g * D/4 + 4 n + i; plse [rows][Hq][2]
+//   fp32, (lambda, 2^(e - 15)), the second being the factor that undoes the scaling.
+constexpr int kPartScaleBits = 15;
+
 struct AttnArgs {
   const void* q;
   const void* pool;
   const int32_t* desc;     // work-item descriptors (layout above)
   int64_t* counters;       // [0] items, [2] work-queue head (units claimed so far, as int32)
-  float* po;               // [partial rows][Hq][D] normalised partial outputs
-  float* plse;             // [partial rows][Hq] log2-domain log-sum-exp of each partial
+  void* po;                // partial outputs (format above)
+  float* plse;             // partial log-sum-exps (format above)
   int32_t Hq, Hkv, group, chunk_pages;
   int32_t desc_words;      // descriptor stride (int32 words)
   float scale_log2;        // softmax scale * log2(e)
@@ -80,7 +89,7 @@ struct AttnArgs {
 struct MergeArgs {
   const int64_t* bpart_off;
   const int32_t* bpart;
-  const float* po;
+  const void* po;          // partial outputs (format above)
   const float* plse;
   void* out;
   float* lse;
@@ -93,7 +102,8 @@ hipError_t launch_schedule(const DevGraph& g, const DevSchedule& sc, int32_t gro
                            int32_t chunk_pages, int64_t max_items, hipStream_t stream);
 hipError_t launch_seg_attn(const AttnArgs& a, int head_dim, bool bf16, int grid,
                            hipStream_t stream);
-hipError_t launch_merge(const MergeArgs& a, int head_dim, bool out_bf16, hipStream_t stream);
+hipError_t launch_merge(const MergeArgs& a, int head_dim, bool out_bf16, bool part_f16,
+                        hipStream_t stream);
 // Number of co-resident attention workgroups the persistent grid uses on this device.
 int seg_attn_grid(int head_dim, bool bf16, int num_cus);
 

@@ -28,7 +28,8 @@
 // l <- alpha * l + sum_j 2^(s_j - m); O <- alpha * O + P V.  The row maximum is reduced across
 // the four lane groups of the wave; l is kept as per-lane partial sums and reduced once at the
 // end.  Each work item writes normalised partials o = O / l and lambda = m + log2(l) for every
-// row; the merge kernel folds them along each branch's path.
+// row (fp16 with a per-row power-of-two scale for bf16 inputs, fp32 otherwise); the merge kernel
+// folds them along each branch's path.
 #include "ga_internal.hpp"
 
 #include <type_traits>
@@ -539,17 +540,54 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
         for (int k = 0; k < NT; ++k) {
           if (k >= ntile) break;
           const int r = (t0 + 4 * k) * 16 + r16;
-          if (r < R) {
-            const int gr = row0 + r;
-            const int j = gr / a.group;
-            const int h = kvh * a.group + (gr - j * a.group);
-            const int64_t row = ((int64_t)prow_base + j) * a.Hq + h;
-            const float inv = 1.f / L[k];
-            float* dst = a.po + row * D + 4 * kg;
+          const float inv = 1.f / L[k];
+          if constexpr (BF16) {
+            // fp16 partial in lane order, scaled so the row's largest |o| is below 2^15 (the
+            // four lanes of a row agree on the scale; L >= 1, so |o| <= max |V|).
+            float amax = 0.f;
   #pragma unroll
             for (int n = 0; n < C::NB; ++n)
-              *reinterpret_cast<f32x4*>(dst + 16 * n) = O[k][n] * inv;
-            if (kg == 0) a.plse[row] = m[k] + log2_(L[k]);
+  #pragma unroll
+              for (int i = 0; i < 4; ++i) amax = fmaxf(amax, fabsf(O[k][n][i]));
+            amax = xmax(amax) * inv;
+            const int e = max(__builtin_amdgcn_frexp_expf(amax), -100);
+            const float up = __builtin_amdgcn_ldexpf(inv, kPartScaleBits - e);
+            if (r < R) {
+              const int gr = row0 + r;
+              const int j = gr / a.group;
+              const int h = kvh * a.group + (gr - j * a.group);
+              const int64_t row = ((int64_t)prow_base + j) * a.Hq + h;
+              typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+              f16x8* dst = reinterpret_cast<f16x8*>(static_cast<_Float16*>(a.po) + row * D +
+                                                    kg * (D / 4));
+  #pragma unroll
+              for (int c = 0; c < C::NB / 2; ++c) {
+                f16x8 v;
+  #pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                  v[i] = (_Float16)(O[k][2 * c][i] * up);
+                  v[4 + i] = (_Float16)(O[k][2 * c + 1][i] * up);
+                }
+                dst[c] = v;
+              }
+              if (kg == 0) {
+                typedef float f32x2 __attribute__((ext_vector_type(2)));
+                *reinterpret_cast<f32x2*>(a.plse + 2 * row) =
+                    f32x2{m[k] + log2_(L[k]), __builtin_amdgcn_ldexpf(1.f, e - kPartScaleBits)};
+              }
+            }
+          } else {
+            if (r < R) {
+              const int gr = row0 + r;
+              const int j = gr / a.group;
+              const int h = kvh * a.group + (gr - j * a.group);
+              const int64_t row = ((int64_t)prow_base + j) * a.Hq + h;
+              float* dst = static_cast<float*>(a.po) + row * D + 4 * kg;
+  #pragma unroll
+              for (int n = 0; n < C::NB; ++n)
+                *reinterpret_cast<f32x4*>(dst + 16 * n) = O[k][n] * inv;
+              if (kg == 0) a.plse[row] = m[k] + log2_(L[k]);
+            }
           }
         }
       }

@@ -70,7 +70,8 @@ struct DevSchedule {
 //   plse [rows][Hq] fp32, its log2-domain log-sum-exp lambda.
 // * bf16 inputs: po [rows][Hq][D] fp16, o scaled by 2^(15 - e) (e: the binary exponent of the
 //   row's largest |o|, so every value is below 2^15) and stored in lane order: column
-//   16 n + 4 g + i (n < D/16, g < 4, i < 4) at position g * D/4 + 4 n + i; plse [rows][Hq][2]
+//   16 n + 4 g + i (n < D/16, g < 4, i < 4) at position 32 (n / 2) + 8 g + 4 (n % 2) + i, so
+//   the four lanes that hold a tile row write 64 contiguous bytes per store; plse [rows][Hq][2]
 //   fp32, (lambda, 2^(e - 15)), the second being the factor that undoes the scaling.
 constexpr int kPartScaleBits = 15;
 

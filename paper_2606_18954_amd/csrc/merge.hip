@@ -30,9 +30,10 @@ __global__ __launch_bounds__(256) void k_merge(MergeArgs a) {
   const int h = (int)(row % a.Hq);
   const float NEG_INF = -__builtin_huge_valf();
   const int64_t k0 = a.bpart_off[b], k1 = a.bpart_off[b + 1];
-  // This lane's 4 columns 4 sub .. 4 sub + 3; in the fp16 format they sit at position
-  // (sub % 4) * D/4 + 4 (sub / 4) of the row (lane order of the attention kernel's tiles).
-  const int pos = PF16 ? (sub % 4) * (D / 4) + 4 * (sub / 4) : 4 * sub;
+  // This lane's 4 columns 4 sub .. 4 sub + 3 = 16 n + 4 g + (0 .. 3) with n = sub / 4, g = sub % 4;
+  // in the fp16 format they sit at position 32 (n / 2) + 8 g + 4 (n % 2) of the row (the lane
+  // order of the attention kernel's tiles).
+  const int pos = PF16 ? (sub / 8) * 32 + (sub % 4) * 8 + ((sub / 4) % 2) * 4 : 4 * sub;
   // Pass 1: the largest partial log-sum-exp of the row.
   float M = NEG_INF;
 #pragma unroll 4

@@ -559,7 +559,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
               const int64_t row = ((int64_t)prow_base + j) * a.Hq + h;
               typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
               f16x8* dst = reinterpret_cast<f16x8*>(static_cast<_Float16*>(a.po) + row * D +
-                                                    kg * (D / 4));
+                                                    8 * kg);
   #pragma unroll
               for (int c = 0; c < C::NB / 2; ++c) {
                 f16x8 v;
@@ -568,7 +568,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
                   v[i] = (_Float16)(O[k][2 * c][i] * up);
                   v[4 + i] = (_Float16)(O[k][2 * c + 1][i] * up);
                 }
-                dst[c] = v;
+                dst[4 * c] = v;           // the row's four lanes fill 64 contiguous bytes
               }
               if (kg == 0) {
                 typedef float f32x2 __attribute__((ext_vector_type(2)));

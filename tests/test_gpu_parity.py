@@ -226,3 +226,19 @@ def test_scale_override():
     oo, ol = O.decode(wl.q_bits(), wl.pool_bits(), g.seg_len, g.seg_page_offsets, g.seg_pages,
                       g.path_offsets, g.path_segs, 28, 4, 128, "bf16", scale=0.05)
     compare("scale 0.05", out.double().cpu().numpy(), lse.double().cpu().numpy(), oo, ol)
+
+
+@pytest.mark.parametrize("k", [-100, -40, 40, 100])
+def test_value_magnitudes(k):
+    """Scaling V by 2^k (exact in bf16) scales out by 2^k and leaves lse unchanged.
+
+    Pins the per-row power-of-two scale of the fp16 partials of bf16 inputs at magnitudes far
+    from 1, against the oracle on the unscaled values."""
+    wl = W.config3_merged_dag(prompts=2)
+    q, pool = to_device(wl)
+    pool_k = pool.clone()
+    pool_k[:, :, 1] = (pool_k[:, :, 1].float() * 2.0 ** k).to(torch.bfloat16)
+    assert torch.equal((pool_k[:, :, 1].float() * 2.0 ** -k).to(torch.bfloat16), pool[:, :, 1])
+    go, gl = gpu_decode(wl, q=q, pool=pool_k, out_f32=True)
+    oo, ol = oracle_decode(wl)
+    compare(f"V x 2^{k}", go * 2.0 ** -k, gl, oo, ol)

@@ -4,8 +4,8 @@
 // chunks), so with lambda_i = log2 sum_{j in piece i} 2^(s_j) and o_i the piece's normalised
 // output, the exact result over the whole context is
 //   Lambda = log2 sum_i 2^(lambda_i),  out = sum_i 2^(lambda_i - Lambda) o_i.
-// The scheduler lists each branch's partials in path order, then chunk order; the merge takes
-// their maximum first and then folds them in that order, so the result is deterministic.  The
+// The scheduler lists each branch's partials in path order, then chunk order; the merge folds them
+// in that order in one pass with a running maximum, so the result is deterministic.  The
 // natural-log lse is Lambda * ln 2.  Partials of bf16 inputs are fp16 values with a power-of-two
 // scale per row (format in ga_internal.hpp); the scale is folded into the row's weight.
 #include "ga_internal.hpp"
@@ -34,29 +34,33 @@ __global__ __launch_bounds__(256) void k_merge(MergeArgs a) {
   // in the fp16 format they sit at position 32 (n / 2) + 8 g + 4 (n % 2) of the row (the lane
   // order of the attention kernel's tiles).
   const int pos = PF16 ? (sub / 8) * 32 + (sub % 4) * 8 + ((sub / 4) % 2) * 4 : 4 * sub;
-  // Pass 1: the largest partial log-sum-exp of the row.
-  float M = NEG_INF;
-#pragma unroll 4
-  for (int64_t k = k0; k < k1; ++k) M = fmaxf(M, a.plse[((int64_t)a.bpart[k] * a.Hq + h) * PS]);
-  // Pass 2: fold the partials in list order (path order, then chunk order).
-  float W = 0.f;
+  // One pass in list order (path order, then chunk order) with a running maximum: when a
+  // partial's log-sum-exp exceeds it, the sums so far are rescaled.
+  float M = NEG_INF, W = 0.f;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll 4
   for (int64_t k = k0; k < k1; ++k) {
     const int64_t idx = (int64_t)a.bpart[k] * a.Hq + h;
-    const float wl = __builtin_amdgcn_exp2f(a.plse[idx * PS] - M);
+    const float lam = a.plse[idx * PS];
     f32x4 o;
-    float wo = wl;
+    float sc = 1.f;
     if constexpr (PF16) {
       typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
       const f16x4 v =
           *reinterpret_cast<const f16x4*>(static_cast<const _Float16*>(a.po) + idx * D + pos);
       o = f32x4{(float)v[0], (float)v[1], (float)v[2], (float)v[3]};
-      wo = wl * a.plse[idx * PS + 1];      // undo the partial's power-of-two scaling
+      sc = a.plse[idx * PS + 1];                // undoes the partial's power-of-two scaling
     } else {
       o = *reinterpret_cast<const f32x4*>(static_cast<const float*>(a.po) + idx * D + pos);
     }
-    acc += o * wo;
+    if (lam > M) {                               // the same for the row's lanes
+      const float r = __builtin_amdgcn_exp2f(M - lam);
+      W *= r;
+      acc *= r;
+      M = lam;
+    }
+    const float wl = __builtin_amdgcn_exp2f(lam - M);
+    acc += o * (wl * sc);
     W += wl;
   }
   const f32x4 r = acc * (1.f / W);

@@ -272,9 +272,13 @@ __global__ __launch_bounds__(1024) void k_sched_small(DevGraph g, DevSchedule sc
   __shared__ int l_tmp[kSmallEntries];      // work-list order, later B(s) in arrival order
   __shared__ int l_poff[kSmallBranches];    // path_off
   __shared__ int l_cnt[kSmallSegs];         // |B(s)|
-  __shared__ int l_goff[kSmallSegs];        // group offsets (scatter cursors in phase 5)
   __shared__ int l_len[kSmallSegs];         // segment lengths
-  __shared__ uint32_t l_key[kSmallSegs];    // sort keys
+  // Group offsets (scatter cursors in phase 5) and sort keys; after the scatter, each entry's
+  // slot in the branch partial lists.
+  __shared__ int l_aux[2 * kSmallSegs];
+  static_assert(2 * kSmallSegs >= kSmallEntries, "entry slots must fit the reused arrays");
+  int* const l_goff = l_aux;
+  uint32_t* const l_key = reinterpret_cast<uint32_t*>(l_aux + kSmallSegs);
   __shared__ int sh[3][1024];
   const int t = threadIdx.x;
   const int S = g.S, E = g.E, B = g.B;
@@ -473,16 +477,24 @@ __global__ __launch_bounds__(1024) void k_sched_small(DevGraph g, DevSchedule sc
   for (int e = l_poff[b0]; e < l_poff[b1]; ++e) ne += nch_of(l_segs[e]);
   block_scan(ne, 0, 0);                          // (also orders the scatter before the copy)
   int slot = t ? sh[0][t - 1] : 0;
+  // Per-entry results go to LDS first (the entry's own slot of l_segs, which only this thread
+  // reads, and l_aux), then out in one coalesced pass.
   for (int bb = b0; bb < b1; ++bb) {
     sc.bpart_off[bb] = slot;
     for (int e = l_poff[bb]; e < l_poff[bb + 1]; ++e) {
-      sc.entry_branch[e] = bb;
-      sc.entry_part[e] = slot;
-      slot += nch_of(l_segs[e]);
+      const int nch = nch_of(l_segs[e]);
+      l_segs[e] = bb;
+      l_aux[e] = slot;
+      slot += nch;
     }
   }
   if (t == 1023) sc.bpart_off[B] = sh[0][1023];
-  for (int i = t; i < E; i += 1024) sc.grp_tmp[i] = l_tmp[i];
+  lds_barrier();
+  for (int i = t; i < E; i += 1024) {
+    sc.entry_branch[i] = l_segs[i];
+    sc.entry_part[i] = l_aux[i];
+    sc.grp_tmp[i] = l_tmp[i];
+  }
 }
 
 // Outputs of the single-workgroup scheduler that are independent per path entry and per item,

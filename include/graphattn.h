@@ -61,7 +61,7 @@ typedef enum { GA_F32 = 0, GA_BF16 = 1 } ga_dtype;
 /* The rollout graph's segments: one segment per generated step (edge) plus the prompt (root).
  * seg_len[s] >= 1 tokens; seg_page_offsets is CSR into seg_pages with seg_page_offsets[0] = 0,
  * non-decreasing, and at least ceil(seg_len[s] / 16) pages per segment.  Page ids lie in
- * [0, num_pages).  Host memory. */
+ * [0, num_pages), num_pages <= 2^27 (GA_EUNSUPPORTED beyond).  Host memory. */
 typedef struct {
   int32_t num_segments;
   const int32_t* seg_len;           /* [S] */
@@ -125,13 +125,18 @@ ga_status graphattn_schedule(ga_plan* plan, void* hip_stream);
 ga_status graphattn_run(ga_plan* plan, const void* q, const void* kv_page_pool, void* out,
                         float* lse, void* hip_stream);
 
-/* Sizes of the schedule, available after plan_create: */
+/* Sizes of the schedule, available after plan_create.  The plan schedules chains: maximal runs
+ * of consecutive path segments whose branch sets are identical (every branch through s continues
+ * with s', and no other branch enters s') are attended as one segment, which is exact (attention
+ * over disjoint token sets merges by log-sum-exp) and leaves one partial per branch and chunk of
+ * the chain. */
 typedef struct {
-  int32_t num_segments, num_branches, num_entries;  /* S, B, E = path_offsets[B] */
+  int32_t num_segments, num_branches, num_entries;  /* S, B, E = path_offsets[B] (as given) */
   int32_t chunk_pages;        /* maximum pages per work item */
   int32_t rows_per_block;     /* maximum query rows (branch x q-head-in-group) per work item */
   int64_t num_items;          /* work items per kv-head */
   int64_t num_partial_rows;   /* partial results per q-head: sum over entries of chunks */
+  int32_t num_chains;         /* chains scheduled (segments on some path, after merging runs) */
 } ga_plan_info;
 ga_status graphattn_plan_info(const ga_plan* plan, ga_plan_info* info);
 
@@ -139,7 +144,9 @@ ga_status graphattn_plan_info(const ga_plan* plan, ga_plan_info* info);
  * pointer may be NULL to skip that array.  Sizes: group_offsets [S+1] and group_branches [E]
  * (B(s) as CSR, ascending ids), entry_ranks [E] (position of each path entry's branch inside
  * its segment's group), items [3 * num_items] as (segment, chunk, row block) triples, and
- * segment_chunks [S]. */
+ * segment_chunks [S].  Groups and ranks are per given segment and path entry.  Items and chunk
+ * counts are per chain: an item names its chain by the chain's first segment, and
+ * segment_chunks holds a chain's chunk count at its first segment and 0 at the others. */
 ga_status graphattn_plan_debug_dump(const ga_plan* plan, void* hip_stream,
                                     int64_t* group_offsets, int32_t* group_branches,
                                     int32_t* entry_ranks, int32_t* items,

@@ -48,6 +48,23 @@ int device_cus() {
   return n;
 }
 
+// The graph as uploaded.  Consecutive segments whose branch sets are identical (every branch
+// through s continues with s', and |B(s)| = |B(s')|) form a chain; attention over a chain's
+// concatenated tokens equals the log-sum-exp merge of its segments, so each chain is scheduled
+// as one segment: one partial per branch and chunk, and longer work items.  A chain's page list
+// concatenates its segments' pages; every page id carries its valid token count in the bits
+// from ga::kPageValidShift up, so the pages where a segment ends mid-page are masked.
+struct CGraph {
+  int32_t S0 = 0;                  // segments and path entries as given
+  int64_t E0 = 0;
+  std::vector<int32_t> seg_len, seg_pages, path_segs, npg;
+  std::vector<int64_t> seg_page_off, path_off;
+  std::vector<int32_t> vid;        // [S0] chain of each segment (-1: on no path)
+  std::vector<int32_t> ventry;     // [E0] uploaded entry of the chain the path entry belongs to
+  std::vector<int32_t> head;       // [chains] first segment of each chain
+  std::vector<char> first;         // [S0] the segment starts its chain
+};
+
 struct Sizes {
   int32_t S = 0, B = 0, E = 0;
   int64_t P = 0;               // entries of seg_pages
@@ -70,6 +87,7 @@ struct ga_plan {
   bool owns_memory = true;
   bool scheduled = false;
   int num_cus = 256;
+  CGraph cg;                   // the uploaded (chain) graph and its map to the given one
   ga::DevGraph g{};
   ga::DevSchedule sc{};
   void* po = nullptr;
@@ -102,6 +120,9 @@ ga_status validate_params(const ga_params* p) {
   if (p->dtype != GA_F32 && p->dtype != GA_BF16)
     return fail(GA_EUNSUPPORTED, "dtype %d unsupported", p->dtype);
   if (p->num_pages < 0) return fail(GA_EINVAL, "num_pages is negative");
+  if (p->num_pages > (1LL << ga::kPageValidShift))
+    return fail(GA_EUNSUPPORTED, "num_pages %lld exceeds 2^%d", (long long)p->num_pages,
+                ga::kPageValidShift);
   if (!std::isfinite(p->softmax_scale) || p->softmax_scale < 0.f)
     return fail(GA_EINVAL, "softmax_scale must be finite and >= 0");
   if (p->out_f32 != 0 && p->out_f32 != 1) return fail(GA_EINVAL, "out_f32 must be 0 or 1");
@@ -160,6 +181,86 @@ ga_status validate_graph(const ga_segment_table* st, const ga_branch_paths* bp,
   z->B = B;
   z->E = (int32_t)E;
   z->P = P;
+  return GA_OK;
+}
+
+// Builds the chain graph (CGraph above) from a validated graph; npg0 = pages of each segment.
+ga_status compress_chains(const ga_segment_table* st, const ga_branch_paths* bp,
+                          const std::vector<int32_t>& npg0, CGraph* c) {
+  const int32_t S = st->num_segments, B = bp->num_branches;
+  const int64_t E = bp->path_offsets[B];
+  c->S0 = S;
+  c->E0 = E;
+  // succ[s]: the segment every path continues with after s (-1: none or not unique).
+  std::vector<int32_t> cnt(S, 0), succ(S, -2), link(S, -1);
+  std::vector<char> haspred(S, 0);
+  for (int32_t b = 0; b < B; ++b)
+    for (int64_t e = bp->path_offsets[b]; e < bp->path_offsets[b + 1]; ++e) {
+      const int32_t s = bp->path_segs[e];
+      const int32_t n = e + 1 < bp->path_offsets[b + 1] ? bp->path_segs[e + 1] : -1;
+      ++cnt[s];
+      succ[s] = succ[s] == -2 ? n : (succ[s] == n ? n : -1);
+    }
+  // s links to s' when every branch through s continues with s' and no other branch enters s',
+  // so B(s) = B(s').  Each segment has at most one link in and out, and paths never revisit a
+  // segment, so the links form disjoint chains.
+  for (int32_t s = 0; s < S; ++s) {
+    const int32_t n = succ[s];
+    if (cnt[s] > 0 && n >= 0 && cnt[n] == cnt[s]) {
+      link[s] = n;
+      haspred[n] = 1;
+    }
+  }
+  c->vid.assign(S, -1);
+  c->first.assign(S, 0);
+  c->head.clear();
+  c->seg_len.clear();
+  c->npg.clear();
+  c->seg_pages.clear();
+  c->seg_page_off.assign(1, 0);
+  for (int32_t s = 0; s < S; ++s) {
+    if (cnt[s] == 0 || haspred[s]) continue;
+    const int32_t v = (int32_t)c->head.size();
+    c->head.push_back(s);
+    c->first[s] = 1;
+    int64_t pages = 0;
+    int32_t last_valid = ga::kPageTokens;
+    for (int32_t x = s; x >= 0; x = link[x]) {
+      c->vid[x] = v;
+      const int32_t len = st->seg_len[x], n = npg0[x];
+      const int64_t off = st->seg_page_offsets[x];
+      for (int32_t i = 0; i < n; ++i) {
+        const int32_t valid = i == n - 1 ? len - (n - 1) * ga::kPageTokens : ga::kPageTokens;
+        c->seg_pages.push_back(st->seg_pages[off + i] | ((valid - 1) << ga::kPageValidShift));
+      }
+      pages += n;
+      last_valid = len - (n - 1) * ga::kPageTokens;
+    }
+    const int64_t tokens = (pages - 1) * ga::kPageTokens + last_valid;
+    if (tokens > 0x7fffffffLL)
+      return fail(GA_EUNSUPPORTED, "segment chain from segment %d spans %lld tokens", s,
+                  (long long)tokens);
+    c->seg_len.push_back((int32_t)tokens);
+    c->npg.push_back((int32_t)pages);
+    c->seg_page_off.push_back((int64_t)c->seg_pages.size());
+  }
+  // Paths over chains: a chain's first segment stands for the chain; the rest of the chain
+  // follows it immediately in every path through it.
+  c->path_segs.clear();
+  c->path_off.assign(1, 0);
+  c->ventry.assign(E, -1);
+  for (int32_t b = 0; b < B; ++b) {
+    int32_t cur = -1;
+    for (int64_t e = bp->path_offsets[b]; e < bp->path_offsets[b + 1]; ++e) {
+      const int32_t s = bp->path_segs[e];
+      if (c->first[s]) {
+        cur = (int32_t)c->path_segs.size();
+        c->path_segs.push_back(c->vid[s]);
+      }
+      c->ventry[e] = cur;
+    }
+    c->path_off.push_back((int64_t)c->path_segs.size());
+  }
   return GA_OK;
 }
 
@@ -312,10 +413,18 @@ ga_status plan_init(const ga_segment_table* st, const ga_branch_paths* bp, const
   std::vector<int32_t> npg;
   rc = validate_graph(st, bp, p, &pl->z, &npg);
   if (rc) return rc;
+  rc = compress_chains(st, bp, npg, &pl->cg);
+  if (rc) return rc;
+  const CGraph& c = pl->cg;
+  pl->z.S = (int32_t)c.head.size();
+  pl->z.E = (int32_t)c.path_segs.size();
+  pl->z.P = (int64_t)c.seg_pages.size();
+  const ga_segment_table cst{pl->z.S, c.seg_len.data(), c.seg_page_off.data(), c.seg_pages.data()};
+  const ga_branch_paths cbp{pl->z.B, c.path_off.data(), c.path_segs.data()};
   pl->p = *p;
   if (pl->p.softmax_scale == 0.f) pl->p.softmax_scale = 1.f / std::sqrt((float)p->head_dim);
   pl->num_cus = device_cus();
-  size_schedule(st, bp, p, npg, pl->num_cus, &pl->z);
+  size_schedule(&cst, &cbp, p, c.npg, pl->num_cus, &pl->z);
   if (pl->z.prows > 0x7fffffffLL)
     return fail(GA_EINVAL, "too many partial rows (%lld)", (long long)pl->z.prows);
   if (pl->z.P > 0x7fffffffLL)
@@ -329,9 +438,11 @@ ga_status plan_init(const ga_segment_table* st, const ga_branch_paths* bp, const
   return GA_OK;
 }
 
-ga_status upload(ga_plan* pl, const ga_segment_table* st, const ga_branch_paths* bp,
-                 const Layout& L, hipStream_t stream) {
-  pack_upload(st, bp, L, pl->z, static_cast<char*>(pl->pin));
+ga_status upload(ga_plan* pl, const Layout& L, hipStream_t stream) {
+  const CGraph& c = pl->cg;
+  const ga_segment_table cst{pl->z.S, c.seg_len.data(), c.seg_page_off.data(), c.seg_pages.data()};
+  const ga_branch_paths cbp{pl->z.B, c.path_off.data(), c.path_segs.data()};
+  pack_upload(&cst, &cbp, L, pl->z, static_cast<char*>(pl->pin));
   GA_HIP(hipMemcpyAsync(pl->dev, pl->pin, upload_bytes(L), hipMemcpyHostToDevice, stream),
          "graph upload");
   return GA_OK;
@@ -457,7 +568,7 @@ ga_status graphattn_plan_create(const ga_segment_table* segment_table,
     return fail(GA_ENOMEM, "pinned staging of %zu bytes", pl->pin_bytes);
   }
   bind(pl, L);
-  rc = upload(pl, segment_table, branch_paths, L, static_cast<hipStream_t>(hip_stream));
+  rc = upload(pl, L, static_cast<hipStream_t>(hip_stream));
   if (rc) {
     graphattn_plan_destroy(pl);
     return rc;
@@ -482,9 +593,10 @@ ga_status graphattn_run(ga_plan* plan, const void* q, const void* kv_page_pool, 
 ga_status graphattn_plan_info(const ga_plan* plan, ga_plan_info* info) {
   g_err.clear();
   if (!plan || !info) return fail(GA_EINVAL, "plan or info is NULL");
-  info->num_segments = plan->z.S;
+  info->num_segments = plan->cg.S0;
   info->num_branches = plan->z.B;
-  info->num_entries = plan->z.E;
+  info->num_entries = (int32_t)plan->cg.E0;
+  info->num_chains = plan->z.S;
   info->chunk_pages = plan->z.chunk_pages;
   info->rows_per_block = ga::kRowsPerBlock;
   info->num_items = -1;
@@ -507,18 +619,35 @@ ga_status graphattn_plan_debug_dump(const ga_plan* plan, void* hip_stream,
   hipStream_t s = static_cast<hipStream_t>(hip_stream);
   GA_HIP(hipStreamSynchronize(s), "synchronise");
   const Sizes& z = plan->z;
-  if (group_offsets)
-    GA_HIP(hipMemcpy(group_offsets, plan->sc.grp_off, sizeof(int64_t) * (z.S + 1),
-                     hipMemcpyDeviceToHost), "dump group offsets");
-  if (group_branches && z.E)
-    GA_HIP(hipMemcpy(group_branches, plan->sc.grp_br, sizeof(int32_t) * z.E,
-                     hipMemcpyDeviceToHost), "dump groups");
-  if (entry_ranks && z.E)
-    GA_HIP(hipMemcpy(entry_ranks, plan->sc.entry_rank, sizeof(int32_t) * z.E,
+  const CGraph& c = plan->cg;
+  // The schedule is over chains; groups, ranks and chunk counts are reported per given segment
+  // and path entry (a segment's group is its chain's).
+  std::vector<int64_t> vgoff(z.S + 1);
+  std::vector<int32_t> vgbr(z.E), vrank(z.E), vnch(z.S);
+  GA_HIP(hipMemcpy(vgoff.data(), plan->sc.grp_off, sizeof(int64_t) * (z.S + 1),
+                   hipMemcpyDeviceToHost), "dump group offsets");
+  if (z.E) {
+    GA_HIP(hipMemcpy(vgbr.data(), plan->sc.grp_br, sizeof(int32_t) * z.E, hipMemcpyDeviceToHost),
+           "dump groups");
+    GA_HIP(hipMemcpy(vrank.data(), plan->sc.entry_rank, sizeof(int32_t) * z.E,
                      hipMemcpyDeviceToHost), "dump ranks");
-  if (segment_chunks && z.S)
-    GA_HIP(hipMemcpy(segment_chunks, plan->sc.seg_nchunk, sizeof(int32_t) * z.S,
+  }
+  if (z.S)
+    GA_HIP(hipMemcpy(vnch.data(), plan->sc.seg_nchunk, sizeof(int32_t) * z.S,
                      hipMemcpyDeviceToHost), "dump chunks");
+  int64_t off = 0;
+  for (int32_t sg = 0; sg < c.S0; ++sg) {
+    const int32_t v = c.vid[sg];
+    const int64_t n = v >= 0 ? vgoff[v + 1] - vgoff[v] : 0;
+    if (group_offsets) group_offsets[sg] = off;
+    if (group_branches)
+      for (int64_t k = 0; k < n; ++k) group_branches[off + k] = vgbr[vgoff[v] + k];
+    if (segment_chunks) segment_chunks[sg] = c.first[sg] ? vnch[v] : 0;
+    off += n;
+  }
+  if (group_offsets) group_offsets[c.S0] = off;
+  if (entry_ranks)
+    for (int64_t e = 0; e < c.E0; ++e) entry_ranks[e] = vrank[c.ventry[e]];
   if (items) {
     int64_t n = 0;
     GA_HIP(hipMemcpy(&n, plan->sc.counters, sizeof n, hipMemcpyDeviceToHost), "dump count");
@@ -528,7 +657,7 @@ ga_status graphattn_plan_debug_dump(const ga_plan* plan, void* hip_stream,
       GA_HIP(hipMemcpy(tmp.data(), plan->sc.items, sizeof(int4) * n, hipMemcpyDeviceToHost),
              "dump items");
     for (int64_t i = 0; i < n; ++i) {
-      items[3 * i] = tmp[i].x;
+      items[3 * i] = c.head[tmp[i].x];
       items[3 * i + 1] = tmp[i].y;
       items[3 * i + 2] = tmp[i].z;
     }
@@ -648,7 +777,7 @@ ga_status graphattn_decode(const void* q, const void* kv_page_pool,
   pl.pin = g_cache.pin;
   bind(&pl, L);
   GA_HIP(hipStreamWaitEvent(stream, g_cache.done, 0), "order after previous decode");
-  rc = upload(&pl, segment_table, branch_paths, L, stream);
+  rc = upload(&pl, L, stream);
   if (rc) return rc;
   GA_HIP(hipEventRecord(g_cache.uploaded, stream), "record upload");
   rc = do_schedule(&pl, stream);

@@ -7,6 +7,9 @@
 namespace ga {
 
 constexpr int kPageTokens = 16;
+// Page-table words: page id in bits [0, 27), valid tokens of the page minus one above.
+constexpr int kPageValidShift = 27;
+constexpr int32_t kPageIdMask = (1 << kPageValidShift) - 1;
 // Query rows (branch x q-head-in-group) handled by one work item: 8 MFMA row tiles of 16.
 constexpr int kRowsPerBlock = 128;
 // Upper bound on pages per work item (the chunk's page ids are staged in LDS).
@@ -18,7 +21,7 @@ constexpr int kAttnThreads = 256;        // 4 wave64 per workgroup
 //   [0..3]  pages in the chunk, index of the segment's last page relative to the chunk start,
 //           valid tokens of that last page, |B(s)|
 //   [4..7]  row block, group offset of B(s), page-table offset of the chunk, first partial row
-//   [8 .. 8 + chunk_pages)            physical page ids of the chunk
+//   [8 .. 8 + chunk_pages)            page words of the chunk (page id | (valid tokens - 1) << 27)
 //   [8 + chunk_pages .. + branches)   branch ids of the row block's rows (B(s) from row0/group)
 constexpr int kDescHead = 8;
 constexpr int kDescMaxBytes = 3072;      // LDS slot per descriptor

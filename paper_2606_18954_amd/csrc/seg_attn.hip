@@ -195,8 +195,8 @@ __device__ __forceinline__ void softmax_page(f32x4 (&S)[NT], float (&p)[NT][4], 
 // NBW output column blocks (O[t][i] holds column block n0 + i).  All LDS operand reads of a page
 // are issued before its first MFMA, so the V reads overlap S = K Q^T and the softmax.
 template <int D, bool BF16, int NT, int NBW>
-__device__ __forceinline__ void kv_stage(const unsigned char* sb, int pg0, int p0, int pstep,
-                                         int npst, int last_pg, int last_valid, float sl2,
+__device__ __forceinline__ void kv_stage(const unsigned char* sb, const int* pwords, int p0,
+                                         int pstep, int npst, float sl2,
                                          int r16, int kg, int n0,
                                          const QOp<BF16> (&qop)[NT][Cfg<D, BF16>::QR],
                                          float (&m)[NT], float (&l)[NT],
@@ -207,7 +207,10 @@ __device__ __forceinline__ void kv_stage(const unsigned char* sb, int pg0, int p
   for (int pis = p0; pis < npst; pis += pstep) {
     const unsigned char* kb = sb + pis * C::PB;
     const unsigned char* vb = kb + C::KVB;
-    const bool last = pg0 + pis == last_pg;
+    // Valid tokens of this page (a segment of the chain may end inside it): from its page word.
+    const int vm1 = (int)((unsigned)__builtin_amdgcn_readfirstlane(pwords[pis]) >> kPageValidShift);
+    const bool last = vm1 < kPageTokens - 1;
+    const int last_valid = vm1 + 1;
     f32x4 S[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) S[t] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -350,15 +353,13 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
   __syncthreads();
 
   for (int b = 0;; b ^= 1) {
-    // Unit fields from its descriptor (the scheduler's record, then the chunk's page ids and the
-    // row block's branch ids).
+    // Unit fields from its descriptor (the scheduler's record, then the chunk's page words and
+    // the row block's branch ids; each page word carries the page's valid tokens).
     const int w = __builtin_amdgcn_readfirstlane(s_next[b]);
     if (w < 0) break;
     const int* dsc = &s_desc[b][0];
     const int kvh = w % a.Hkv;
     const int np = __builtin_amdgcn_readfirstlane(dsc[0]);
-    const int last_pg = __builtin_amdgcn_readfirstlane(dsc[1]);
-    const int last_valid = __builtin_amdgcn_readfirstlane(dsc[2]);
     const int cnt = __builtin_amdgcn_readfirstlane(dsc[3]);
     const int rb = __builtin_amdgcn_readfirstlane(dsc[4]);
     const int prow_base = __builtin_amdgcn_readfirstlane(dsc[7]);
@@ -418,14 +419,6 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
         for (int n = 0; n < C::NB; ++n) O[k][n] = f32x4{0.f, 0.f, 0.f, 0.f};
       }
   
-      // Offsets for the segment's last page: slots past its end re-read its last valid token
-      // (finite data; their scores are masked).
-      unsigned off_full[NI], off_last[NI];
-  #pragma unroll
-      for (int i = 0; i < NI; ++i) {
-        off_full[i] = c_tok[i] * C::ROW + c_rest[i];
-        off_last[i] = min(c_tok[i], last_valid - 1) * C::ROW + c_rest[i];
-      }
       const int64_t blk_stride = (int64_t)a.Hkv * 2 * C::KVB;
       const unsigned char* pool_h = (const unsigned char*)uniform64(
           (int64_t)(uintptr_t)(pool + (int64_t)kvh * 2 * C::KVB));
@@ -436,18 +429,20 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
         // All page ids of the stage are read before the first copy: one LDS round trip (the
         // copies' memory clobber would otherwise force a re-read before each of them).  Ids past
         // the chunk are read but unused.
-        int pids[C::SP];
+        int pw[C::SP];
   #pragma unroll
         for (int q = 0; q < C::SP; ++q)
-          pids[q] = __builtin_amdgcn_readfirstlane(s_desc[b][kDescHead + st * C::SP + q]);
+          pw[q] = __builtin_amdgcn_readfirstlane(s_desc[b][kDescHead + st * C::SP + q]);
   #pragma unroll
         for (int i = 0; i < NI; ++i) {
           const int pis = i / C::IPW;
           if (pis < npst) {
-            const int pg = st * C::SP + pis;
-            const int pid = pids[pis];
+            // Token rows past the page's valid tokens re-read its last valid token (finite
+            // data; their scores are masked).
+            const int pid = pw[pis] & kPageIdMask;
+            const int vm1 = (int)((unsigned)pw[pis] >> kPageValidShift);
             const unsigned char* base = pool_h + (int64_t)pid * blk_stride;
-            dma16(pg == last_pg ? off_last[i] : off_full[i], base,
+            dma16(min(c_tok[i], vm1) * C::ROW + c_rest[i], base,
                   __builtin_amdgcn_readfirstlane(dst + i * 4096));
           }
         }
@@ -479,7 +474,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
         const int npst = min(C::SP, np - st * C::SP);
         if (ntile > 0) {
           const unsigned char* sb = smem + buf * C::STAGE;
-          kv_stage<D, BF16, NT, C::NB>(sb, st * C::SP, split, ks, npst, last_pg, last_valid,
+          kv_stage<D, BF16, NT, C::NB>(sb, &s_desc[b][kDescHead + st * C::SP], split, ks, npst,
                                        a.scale_log2, r16, kg, 0, qop, m, l, O);
         }
       }

@@ -53,7 +53,7 @@ class PlanInfo(ctypes.Structure):
     _fields_ = [("num_segments", ctypes.c_int32), ("num_branches", ctypes.c_int32),
                 ("num_entries", ctypes.c_int32), ("chunk_pages", ctypes.c_int32),
                 ("rows_per_block", ctypes.c_int32), ("num_items", ctypes.c_int64),
-                ("num_partial_rows", ctypes.c_int64)]
+                ("num_partial_rows", ctypes.c_int64), ("num_chains", ctypes.c_int32)]
 
 
 class Profile(ctypes.Structure):

@@ -242,3 +242,19 @@ def test_value_magnitudes(k):
     go, gl = gpu_decode(wl, q=q, pool=pool_k, out_f32=True)
     oo, ol = oracle_decode(wl)
     compare(f"V x 2^{k}", go * 2.0 ** -k, gl, oo, ol)
+
+
+def test_segment_chains_with_ragged_pages():
+    """Runs of segments with identical branch sets are attended as one chain; segments ending
+    inside a page (NaN in the unused slots) must be masked page by page.  Segments 0-5 carry
+    branches 0-2 only (one chain), 6-8 are private to one branch each, 9 and 10 form a chain of
+    branch 3, and segment 11 is entered by two different predecessors (no chain link)."""
+    lens = [1, 15, 16, 17, 2, 33, 5, 40, 3, 9, 14, 21]
+    paths = [[0, 1, 2, 3, 4, 5, 6], [0, 1, 2, 3, 4, 5, 7], [0, 1, 2, 3, 4, 5, 8, 11],
+             [9, 10, 11]]
+    for dtype, D in [("bf16", 128), ("f32", 64)]:
+        wl = _mk(lens, paths, 28 if D == 128 else 8, 4 if D == 128 else 2, D, dtype, 11)
+        hg = G.HostGraph.from_graph(wl.graph)
+        with G.Plan(hg, params_of(wl)) as plan:
+            assert plan.info().num_chains == 6     # {0-5}, 6, 7, 8, {9, 10}, 11
+        check_workload(wl, out_f32=True)

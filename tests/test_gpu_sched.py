@@ -29,25 +29,52 @@ def cost_class(cost):
     return min(31, 1 + 2 * e + m)
 
 
+def chains(g):
+    """Chains of path segments with identical branch sets: s links to s' when every branch
+    through s continues with s' and |B(s)| = |B(s')|.  Returns the chains (lists of segments, in
+    path order) ordered by their first segment's id."""
+    S = g.num_segments
+    cnt = [0] * S
+    succ = [None] * S
+    for b in range(g.num_branches):
+        p = [int(x) for x in g.path_segs[g.path_offsets[b]:g.path_offsets[b + 1]]]
+        for i, s in enumerate(p):
+            cnt[s] += 1
+            n = p[i + 1] if i + 1 < len(p) else -1
+            succ[s] = n if succ[s] is None else (n if succ[s] == n else -1)
+    link = {s: succ[s] for s in range(S)
+            if cnt[s] and succ[s] is not None and succ[s] >= 0 and cnt[succ[s]] == cnt[s]}
+    has_pred = set(link.values())
+    out = []
+    for s in range(S):
+        if cnt[s] and s not in has_pred:
+            c = [s]
+            while c[-1] in link:
+                c.append(link[c[-1]])
+            out.append(c)
+    return out
+
+
 def expected_items(g, group, chunk_pages, cnt):
-    """Work list: items grouped by segment, segments by descending cost class of the per-item
-    cost (chunk pages x (2 + row tiles)), ties by segment id; within a segment chunk-major."""
+    """Work list: items grouped by chain, chains by descending cost class of the per-item cost
+    (chunk pages x (2 + row tiles)), ties by first segment; within a chain chunk-major.  An item
+    names its chain by the chain's first segment."""
     def npg(s):
         return (int(g.seg_len[s]) + 15) // 16
 
-    def cost(s):
-        tiles = (min(cnt[s] * group, ROWS_PER_BLOCK) + 15) // 16
-        return min(npg(s), chunk_pages) * (2 + tiles)
+    def cost(c):
+        tiles = (min(cnt[c[0]] * group, ROWS_PER_BLOCK) + 15) // 16
+        return min(sum(npg(s) for s in c), chunk_pages) * (2 + tiles)
 
-    order = sorted((s for s in range(g.num_segments) if cnt[s] > 0),
-                   key=lambda s: (-cost_class(cost(s)), s))
+    order = sorted(chains(g), key=lambda c: (-cost_class(cost(c)), c[0]))
     items = []
-    for s in order:
-        nch = (npg(s) + chunk_pages - 1) // chunk_pages
-        nrb = (cnt[s] * group + ROWS_PER_BLOCK - 1) // ROWS_PER_BLOCK
-        for c in range(nch):
+    for c in order:
+        pages = sum(npg(s) for s in c)
+        nch = (pages + chunk_pages - 1) // chunk_pages
+        nrb = (cnt[c[0]] * group + ROWS_PER_BLOCK - 1) // ROWS_PER_BLOCK
+        for ch in range(nch):
             for rb in range(nrb):
-                items.append((s, c, rb))
+                items.append((c[0], ch, rb))
     return np.array(items, dtype=np.int32).reshape(-1, 3)
 
 
@@ -70,8 +97,13 @@ def check_schedule(wl):
     group = wl.num_q_heads // wl.num_kv_heads
     exp_items = expected_items(g, group, info.chunk_pages, cnt)
     assert np.array_equal(d["items"], exp_items)
-    chunks = np.array([((int(g.seg_len[s]) + 15) // 16 + info.chunk_pages - 1) // info.chunk_pages
-                       if cnt[s] else 0 for s in range(g.num_segments)], dtype=np.int32)
+    # Chunks of each chain at its first segment, 0 elsewhere.
+    chunks = np.zeros(g.num_segments, dtype=np.int32)
+    ch = chains(g)
+    for c in ch:
+        pages = sum((int(g.seg_len[s]) + 15) // 16 for s in c)
+        chunks[c[0]] = (pages + info.chunk_pages - 1) // info.chunk_pages
+    assert info.num_chains == len(ch)
     assert np.array_equal(d["segment_chunks"], chunks)
     assert info.num_partial_rows == int(sum(chunks[s] for s in g.path_segs))
     for k in d:

@@ -20,14 +20,22 @@ What it computes (the passages it follows):
   z_j = scale * <q, k_j>, p = softmax(z), out = sum_j p_j v_j, lse = ln sum_j exp(z_j).
 * Grouped-query attention: q-head h reads kv-head floor(h / (Hq / Hkv)).
 
+* Extend: the queries of a branch are the newest tokens of its last path segment, each
+  attending causally (Alg. S.1, Stage 1: a continuation is predicted token by token from
+  prefix(u)); append and copy store tokens into page slots and move them between slots.
+
 Readings where the paper is silent (each also listed in the design notes):
 all tokens of every segment on the path are attended, including the branch's own leaf segment;
 no causal mask (a single query at the end of the path); scale = 1/sqrt(D) unless given;
 lse is the natural log; segment order along a path does not change the result.
+For extend: the query segment is the path's last entry, a query sees itself, and a query at
+position P of that segment sees exactly its tokens 0 .. P. A slot word is page * 16 + slot.
 
 Parity status: every function below is pinned by CPU tests against brute force, a library
 routine on a special case, closed forms and invariants (softmax rows sum to 1, merge
-associativity, the K=0 tag closed form, the single-token case).
+associativity, the K=0 tag closed form, the single-token case); extend against torch's causal
+SDPA and a token-by-token walk, append by reading the stored segment back, copy by splitting a
+segment inside a page without changing attention.
 """
 from __future__ import annotations
 
@@ -208,3 +216,119 @@ def branch_slot_ranks(path_offsets, path_segs, num_segments: int) -> np.ndarray:
             grp = list(ids[offs[s]:offs[s + 1]])
             ranks[e] = grp.index(b)
     return ranks
+
+
+# ----------------------------------------------------------------------------------------------
+# Multi-query attention over a branch's newest segment ("extend")
+# ----------------------------------------------------------------------------------------------
+
+def query_context_length(context_tokens: int, n_queries: int, i: int) -> int:
+    """Tokens seen by query i of a branch whose context (its whole path) has context_tokens
+    tokens and whose newest segment, last in the path, holds its n_queries queries at the end:
+    all but the segment's n_queries - 1 - i final tokens (the query sees itself)."""
+    return context_tokens - (n_queries - 1 - i)
+
+
+def extend(q_raw: np.ndarray, pool_raw: np.ndarray, seg_len, seg_page_offsets, seg_pages,
+           path_offsets, path_segs, query_counts, num_q_heads: int, num_kv_heads: int,
+           head_dim: int, dtype: str, scale: Optional[float] = None,
+           rows: Optional[Iterable[int]] = None) -> Tuple[np.ndarray, np.ndarray]:
+    """Several query tokens per branch, causal inside the branch's newest segment.
+
+    Continuations are sampled from pi_theta(. | prefix(u)) (Alg. S.1, Stage 1): every token of a
+    new step segment is predicted from the state's prefix plus the step's earlier tokens. Branch
+    b's last path segment is that step; its queries are the last n_b = query_counts[b] tokens of
+    it, so query i (0 <= i < n_b) sits at position P_i = len(last) - n_b + i of the segment and
+    attends to every token of the other path segments and to tokens 0 .. P_i of the last one
+    (itself included). With n_b = 1 the single query sees the whole context, which is decode.
+
+    q_raw holds one row per query, [sum_b n_b][Hq][D], branch-major and ascending i within a
+    branch. Returns out [n][Hq][D] and lse [n][Hq] (float64) for the n requested query rows
+    (all rows if ``rows`` is None).
+    """
+    if num_q_heads % num_kv_heads:
+        raise ValueError("Hq must be a multiple of Hkv")
+    if scale is None or scale == 0.0:
+        scale = 1.0 / math.sqrt(head_dim)
+    B = len(path_offsets) - 1
+    counts = [int(c) for c in query_counts]
+    if len(counts) != B:
+        raise ValueError("one query count per branch")
+    row_branch: List[Tuple[int, int]] = []
+    for b in range(B):
+        last = int(path_segs[path_offsets[b + 1] - 1])
+        if not 1 <= counts[b] <= int(seg_len[last]):
+            raise ValueError(f"branch {b}: query count outside [1, len(last segment)]")
+        row_branch += [(b, i) for i in range(counts[b])]
+    ids = list(range(len(row_branch))) if rows is None else [int(r) for r in rows]
+    out = np.empty((len(ids), num_q_heads, head_dim), dtype=np.float64)
+    lse = np.empty((len(ids), num_q_heads), dtype=np.float64)
+    ctx_cache = {}
+    for k, r in enumerate(ids):
+        b, i = row_branch[r]
+        if b not in ctx_cache:
+            path = path_segs[path_offsets[b]:path_offsets[b + 1]]
+            ctx_cache = {b: branch_context(pool_raw, dtype, seg_len, seg_page_offsets,
+                                           seg_pages, path)}
+        K, V = ctx_cache[b]
+        visible = query_context_length(K.shape[0], counts[b], i)
+        qi = to_f64(q_raw[r], dtype)
+        out[k], lse[k] = attend(qi, K[:visible], V[:visible], scale)
+    return out, lse
+
+
+# ----------------------------------------------------------------------------------------------
+# Writing K/V into the page pool
+# ----------------------------------------------------------------------------------------------
+
+def _slot_ok(word: int, num_pages: int) -> bool:
+    return 0 <= word < num_pages * PAGE_TOKENS
+
+
+def kv_append(pool_raw: np.ndarray, k_new_raw: np.ndarray, v_new_raw: np.ndarray,
+              slot_words) -> np.ndarray:
+    """Store new tokens' K and V in the pool; returns the updated copy of the pool.
+
+    Each decode step extends every active branch's leaf segment by the token it produced, and a
+    state's continuation splits into new step segments (Alg. S.1, Stage 1); a token of a segment
+    lives in one page slot. slot_words[j] = page * 16 + slot names token j's destination;
+    k_new_raw / v_new_raw are [n][Hkv][D] raw storage values (bf16 bits or float32). Words
+    outside [0, num_pages * 16) are skipped (a negative word pads a batch). Destinations must be
+    distinct.
+    """
+    out = np.array(pool_raw, copy=True)
+    seen = set()
+    for j, w in enumerate(int(x) for x in slot_words):
+        if not _slot_ok(w, pool_raw.shape[0]):
+            continue
+        if w in seen:
+            raise ValueError("destination slots must be distinct")
+        seen.add(w)
+        page, slot = divmod(w, PAGE_TOKENS)
+        out[page, :, 0, slot, :] = k_new_raw[j]
+        out[page, :, 1, slot, :] = v_new_raw[j]
+    return out
+
+
+def kv_copy(pool_raw: np.ndarray, src_words, dst_words) -> np.ndarray:
+    """Copy tokens between page slots (every kv-head, K and V); returns the updated pool.
+
+    Needed where a generated run of tokens is cut into step segments inside a page (Alg. S.1,
+    Stage 1, "split them into segment-level transitions"): a segment begins at slot 0 of its
+    own page, so the tokens after the cut move to fresh pages; a fork that lets children keep
+    writing into a shared, partly filled page copies that page the same way. Pairs with either
+    word outside the pool are skipped; sources are read as they were before the call, and
+    destinations must be distinct and disjoint from the sources.
+    """
+    out = np.array(pool_raw, copy=True)
+    Np = pool_raw.shape[0]
+    pairs = [(int(s), int(d)) for s, d in zip(src_words, dst_words)
+             if _slot_ok(int(s), Np) and _slot_ok(int(d), Np)]
+    dsts = [d for _, d in pairs]
+    if len(set(dsts)) != len(dsts) or set(dsts) & {s for s, _ in pairs}:
+        raise ValueError("destinations must be distinct and disjoint from the sources")
+    for s, d in pairs:
+        sp, ss = divmod(s, PAGE_TOKENS)
+        dp, ds = divmod(d, PAGE_TOKENS)
+        out[dp, :, :, ds, :] = pool_raw[sp, :, :, ss, :]
+    return out

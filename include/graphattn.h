@@ -104,12 +104,40 @@ ga_status graphattn_decode(const void* q, const void* kv_page_pool,
                            const ga_branch_paths* branch_paths, void* out, float* lse,
                            const ga_params* params, void* hip_stream);
 
+/* Multi-query ("extend") attention: several query tokens per branch, causal inside the branch's
+ * newest segment.  A continuation is predicted token by token from prefix(u) (Alg. S.1, Stage 1),
+ * so prefilling a new step segment, or checking several drafted tokens at once, gives each of its
+ * tokens one query over the path's earlier segments plus the segment's tokens up to itself.
+ * Branch b's newest segment is the LAST entry of its path and must be on no other path; its
+ * K/V are already in the pool (graphattn_kv_append).  query_counts[b] = n_b in [1, len(last)]
+ * (host array): the queries are the segment's last n_b tokens, query i at position
+ * len(last) - n_b + i, seeing every token of the other path segments and tokens 0 .. that
+ * position of the newest one (itself included).  With n_b = 1 this is graphattn_decode.
+ *   q    [R][Hq][D]  R = sum_b n_b query rows, branch-major, ascending i within a branch
+ *   out  [R][Hq][D], lse [R][Hq]  (as for decode, per query row)
+ * Rows of one branch share its path's segments with each other and with every branch on them,
+ * so a segment's K/V are read once per kv-head for all of those rows.  GA_EINVAL for a NULL
+ * query_counts with branches, a count outside [1, len(last)] or a newest segment shared with
+ * another path.  Otherwise as graphattn_decode. */
+ga_status graphattn_extend(const void* q, const void* kv_page_pool,
+                           const ga_segment_table* segment_table,
+                           const ga_branch_paths* branch_paths, const int32_t* query_counts,
+                           void* out, float* lse, const ga_params* params, void* hip_stream);
+
 /* Validate the graph and parameters, allocate the plan's device workspace (sized for this
  * graph) and enqueue the upload of the index arrays on hip_stream.  The host arrays may be
  * released when the call returns.  *plan receives a new plan (NULL on error). */
 ga_status graphattn_plan_create(const ga_segment_table* segment_table,
                                 const ga_branch_paths* branch_paths, const ga_params* params,
                                 void* hip_stream, ga_plan** plan);
+
+/* A plan for graphattn_extend's problem (same arguments and checks): graphattn_schedule and
+ * graphattn_run then take q / out / lse with R = sum_b n_b rows.  In the schedule (plan_info,
+ * debug dump) every query row is a branch with its branch's path. */
+ga_status graphattn_plan_create_extend(const ga_segment_table* segment_table,
+                                       const ga_branch_paths* branch_paths,
+                                       const int32_t* query_counts, const ga_params* params,
+                                       void* hip_stream, ga_plan** plan);
 
 /* Segment scheduler, on the GPU: transpose branch->segments into segment->branches (B(s) in
  * ascending branch order), give each path entry the branch's position inside B(s), split long
@@ -131,12 +159,15 @@ ga_status graphattn_run(ga_plan* plan, const void* q, const void* kv_page_pool, 
  * over disjoint token sets merges by log-sum-exp) and leaves one partial per branch and chunk of
  * the chain. */
 typedef struct {
-  int32_t num_segments, num_branches, num_entries;  /* S, B, E = path_offsets[B] (as given) */
+  /* S and B as given; E = path entries of the schedule: path_offsets[B] for decode plans,
+   * sum_b n_b |path_b| for multi-query plans */
+  int32_t num_segments, num_branches, num_entries;
   int32_t chunk_pages;        /* maximum pages per work item */
   int32_t rows_per_block;     /* maximum query rows (branch x q-head-in-group) per work item */
   int64_t num_items;          /* work items per kv-head */
   int64_t num_partial_rows;   /* partial results per q-head: sum over entries of chunks */
   int32_t num_chains;         /* chains scheduled (segments on some path, after merging runs) */
+  int32_t num_query_rows;     /* rows of q / out / lse: B for decode plans, sum_b n_b for extend */
 } ga_plan_info;
 ga_status graphattn_plan_info(const ga_plan* plan, ga_plan_info* info);
 
@@ -165,6 +196,32 @@ typedef struct {
 } ga_profile;
 ga_status graphattn_plan_profile(ga_plan* plan, int32_t max_calls);
 ga_status graphattn_plan_profile_read(ga_plan* plan, ga_profile* out);
+
+/* Page-pool writes (Alg. S.1, Stage 1: each decode step extends the newest segment of every
+ * active branch by its token; a continuation is split into step segments).  A slot word
+ * w = page * 16 + slot names one token slot of kv_page_pool.  Slot words are DEVICE arrays (one
+ * mapping serves every layer's pool), so they are range-checked in the kernel: a token whose
+ * word lies outside [0, num_pages * 16) is skipped and nothing outside the pool is written
+ * (negative words pad a batch).  Only params->num_kv_heads, head_dim, dtype and num_pages are
+ * used; the call validates params like the others and is asynchronous on hip_stream.
+ *
+ * graphattn_kv_append: token j's K and V, k_new / v_new [num_tokens][Hkv][D] (device, the pool's
+ * dtype), are stored for every kv-head at slot_words[j].  Destinations must be distinct
+ * (otherwise which token lands is unspecified).
+ *
+ * graphattn_kv_copy: every kv-head's K and V of slot src_slot_words[j] are copied to slot
+ * dst_slot_words[j].  Since each segment starts at slot 0 of a page of its own, a fork needs no
+ * copy (children open new pages); cutting a generated run into step segments inside a page moves
+ * the tokens after the cut to fresh pages with this call.  Destinations must be distinct and
+ * disjoint from the sources (otherwise the result is unspecified).
+ *
+ * Both: pool, k_new and v_new 16-byte aligned; num_tokens >= 0 (0: nothing is launched). */
+ga_status graphattn_kv_append(void* kv_page_pool, const void* k_new, const void* v_new,
+                              const int32_t* slot_words, int32_t num_tokens,
+                              const ga_params* params, void* hip_stream);
+ga_status graphattn_kv_copy(void* kv_page_pool, const int32_t* src_slot_words,
+                            const int32_t* dst_slot_words, int32_t num_tokens,
+                            const ga_params* params, void* hip_stream);
 
 /* Release the plan and its device workspace (waits for work still using it). */
 void graphattn_plan_destroy(ga_plan* plan);

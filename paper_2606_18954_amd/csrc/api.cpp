@@ -63,6 +63,7 @@ struct CGraph {
   std::vector<int32_t> ventry;     // [E0] uploaded entry of the chain the path entry belongs to
   std::vector<int32_t> head;       // [chains] first segment of each chain
   std::vector<char> first;         // [S0] the segment starts its chain
+  std::vector<int32_t> causal;     // [chains] causal origin (multi-query plans), else kNoCausal
 };
 
 struct Sizes {
@@ -86,6 +87,8 @@ struct ga_plan {
   size_t pin_bytes = 0;
   bool owns_memory = true;
   bool scheduled = false;
+  bool causal = false;         // a multi-query plan (graphattn_plan_create_extend)
+  int32_t B0 = 0;              // branches as given (z.B counts query rows)
   int num_cus = 256;
   CGraph cg;                   // the uploaded (chain) graph and its map to the given one
   ga::DevGraph g{};
@@ -214,6 +217,7 @@ ga_status compress_chains(const ga_segment_table* st, const ga_branch_paths* bp,
   c->vid.assign(S, -1);
   c->first.assign(S, 0);
   c->head.clear();
+  c->causal.clear();
   c->seg_len.clear();
   c->npg.clear();
   c->seg_pages.clear();
@@ -242,6 +246,7 @@ ga_status compress_chains(const ga_segment_table* st, const ga_branch_paths* bp,
                   (long long)tokens);
     c->seg_len.push_back((int32_t)tokens);
     c->npg.push_back((int32_t)pages);
+    c->causal.push_back(ga::kNoCausal);
     c->seg_page_off.push_back((int64_t)c->seg_pages.size());
   }
   // Paths over chains: a chain's first segment stands for the chain; the rest of the chain
@@ -299,7 +304,7 @@ struct Layout {
 
 // Device workspace layout (byte offsets of every array in the single allocation).
 enum {
-  L_SEG_LEN, L_SEG_PAGE_OFF, L_SEG_PAGES, L_PATH_OFF, L_PATH_SEGS,  // uploaded graph (contiguous)
+  L_SEG_LEN, L_SEG_PAGE_OFF, L_SEG_PAGES, L_PATH_OFF, L_PATH_SEGS, L_SEG_CAUSAL,  // uploaded
   L_GRP_CNT, L_GRP_FILL, L_GRP_OFF, L_GRP_TMP, L_GRP_BR, L_ENTRY_BR, L_ENTRY_RANK, L_SEG_NCH,
   L_SEG_ITEM_OFF, L_SEG_PROW_OFF, L_SEG_ORDER, L_ORDER_ITEM_OFF, L_ITEMS, L_DESC, L_COUNTERS, L_ENTRY_PART, L_BPART_OFF, L_BPART,
   L_PO, L_PLSE, L_COUNT
@@ -312,6 +317,7 @@ Layout layout(const Sizes& z, const ga_params& p) {
   sz[L_SEG_PAGES] = sizeof(int32_t) * z.P;
   sz[L_PATH_OFF] = sizeof(int64_t) * (z.B + 1);
   sz[L_PATH_SEGS] = sizeof(int32_t) * z.E;
+  sz[L_SEG_CAUSAL] = sizeof(int32_t) * z.S;
   sz[L_GRP_CNT] = sizeof(int32_t) * z.S;
   sz[L_GRP_FILL] = sizeof(int32_t) * z.S;
   sz[L_GRP_OFF] = sizeof(int64_t) * (z.S + 1);
@@ -340,7 +346,7 @@ Layout layout(const Sizes& z, const ga_params& p) {
   size_t o = 0;
   for (int i = 0; i < L_COUNT; ++i) {
     // The uploaded graph arrays are packed back to back (8-byte aligned) so one copy moves them.
-    o = align_up(o, i <= L_PATH_SEGS ? 8 : 256);
+    o = align_up(o, i <= L_SEG_CAUSAL ? 8 : 256);
     L.off[i] = o;
     o += sz[i];
   }
@@ -361,6 +367,7 @@ void bind(ga_plan* pl, const Layout& L) {
   pl->g.seg_pages = reinterpret_cast<const int32_t*>(d + L.off[L_SEG_PAGES]);
   pl->g.path_off = reinterpret_cast<const int64_t*>(d + L.off[L_PATH_OFF]);
   pl->g.path_segs = reinterpret_cast<const int32_t*>(d + L.off[L_PATH_SEGS]);
+  pl->g.seg_causal = reinterpret_cast<const int32_t*>(d + L.off[L_SEG_CAUSAL]);
   pl->sc.grp_cnt = reinterpret_cast<int32_t*>(d + L.off[L_GRP_CNT]);
   pl->sc.grp_fill = reinterpret_cast<int32_t*>(d + L.off[L_GRP_FILL]);
   pl->sc.grp_off = reinterpret_cast<int64_t*>(d + L.off[L_GRP_OFF]);
@@ -384,13 +391,14 @@ void bind(ga_plan* pl, const Layout& L) {
   pl->plse = reinterpret_cast<float*>(d + L.off[L_PLSE]);
 }
 
-void pack_upload(const ga_segment_table* st, const ga_branch_paths* bp, const Layout& L,
-                 const Sizes& z, char* h) {
+void pack_upload(const ga_segment_table* st, const ga_branch_paths* bp, const int32_t* causal,
+                 const Layout& L, const Sizes& z, char* h) {
   if (z.S) std::memcpy(h + L.off[L_SEG_LEN], st->seg_len, sizeof(int32_t) * z.S);
   std::memcpy(h + L.off[L_SEG_PAGE_OFF], st->seg_page_offsets, sizeof(int64_t) * (z.S + 1));
   if (z.P) std::memcpy(h + L.off[L_SEG_PAGES], st->seg_pages, sizeof(int32_t) * z.P);
   std::memcpy(h + L.off[L_PATH_OFF], bp->path_offsets, sizeof(int64_t) * (z.B + 1));
   if (z.E) std::memcpy(h + L.off[L_PATH_SEGS], bp->path_segs, sizeof(int32_t) * z.E);
+  if (z.S) std::memcpy(h + L.off[L_SEG_CAUSAL], causal, sizeof(int32_t) * z.S);
 }
 
 // Process-wide workspace reused by graphattn_decode.
@@ -406,15 +414,81 @@ struct DecodeCache {
 };
 DecodeCache g_cache;
 
+// Multi-query plans: query row i of branch b becomes a branch of its own with b's path (the rows
+// of one branch are consecutive, in query order), so every segment a branch shares is attended
+// once for all of the rows that share it.  b's newest segment (its path's last entry) is on no
+// other path, so its group is exactly b's rows and a row's rank there is its query index i; the
+// causal limit inside that segment is a per-rank token bound (DevGraph::seg_causal).
+ga_status expand_queries(const ga_segment_table* st, const ga_branch_paths* bp,
+                         const int32_t* counts, std::vector<int64_t>* vpo,
+                         std::vector<int32_t>* vps) {
+  const int32_t S = st->num_segments, B = bp->num_branches;
+  if (B > 0 && !counts) return fail(GA_EINVAL, "query_counts is NULL");
+  std::vector<int32_t> occ(S, 0);
+  for (int64_t e = 0; e < bp->path_offsets[B]; ++e) ++occ[bp->path_segs[e]];
+  int64_t rows = 0, entries = 0;
+  for (int32_t b = 0; b < B; ++b) {
+    const int64_t a = bp->path_offsets[b], e1 = bp->path_offsets[b + 1];
+    const int32_t last = bp->path_segs[e1 - 1];
+    if (occ[last] != 1)
+      return fail(GA_EINVAL, "query segment %d of branch %d is on another path", last, b);
+    if (counts[b] < 1 || counts[b] > st->seg_len[last])
+      return fail(GA_EINVAL, "branch %d: query count %d outside [1, %d]", b, counts[b],
+                  st->seg_len[last]);
+    rows += counts[b];
+    entries += (int64_t)counts[b] * (e1 - a);
+  }
+  if (rows > 0x7fffffffLL || entries > 0x7fffffffLL)
+    return fail(GA_EINVAL, "too many query rows (%lld) or row path entries (%lld)",
+                (long long)rows, (long long)entries);
+  vpo->assign(1, 0);
+  vpo->reserve(rows + 1);
+  vps->clear();
+  vps->reserve(entries);
+  for (int32_t b = 0; b < B; ++b)
+    for (int32_t i = 0; i < counts[b]; ++i) {
+      vps->insert(vps->end(), bp->path_segs + bp->path_offsets[b],
+                  bp->path_segs + bp->path_offsets[b + 1]);
+      vpo->push_back((int64_t)vps->size());
+    }
+  return GA_OK;
+}
+
 ga_status plan_init(const ga_segment_table* st, const ga_branch_paths* bp, const ga_params* p,
-                    ga_plan* pl, Layout* L) {
+                    const int32_t* query_counts, ga_plan* pl, Layout* L) {
   ga_status rc = validate_params(p);
   if (rc) return rc;
   std::vector<int32_t> npg;
   rc = validate_graph(st, bp, p, &pl->z, &npg);
   if (rc) return rc;
-  rc = compress_chains(st, bp, npg, &pl->cg);
+  pl->B0 = bp->num_branches;
+  std::vector<int64_t> vpo;
+  std::vector<int32_t> vps;
+  ga_branch_paths vbp{};
+  if (query_counts) {
+    rc = expand_queries(st, bp, query_counts, &vpo, &vps);
+    if (rc) return rc;
+    vbp = ga_branch_paths{(int32_t)(vpo.size() - 1), vpo.data(), vps.data()};
+    rc = validate_graph(st, &vbp, p, &pl->z, &npg);
+    if (rc) return rc;
+    pl->causal = true;
+  }
+  rc = compress_chains(st, query_counts ? &vbp : bp, npg, &pl->cg);
   if (rc) return rc;
+  if (query_counts) {
+    // The newest segment closes its chain (it is the last entry of every path through it), and
+    // starts on a page of its own: its token t is chain token 16 x (chain pages before it) + t,
+    // and query i sits at t = len - n + i.
+    for (int32_t b = 0; b < bp->num_branches; ++b) {
+      const int32_t last = bp->path_segs[bp->path_offsets[b + 1] - 1];
+      const int32_t v = pl->cg.vid[last];
+      if (pl->cg.seg_len[v] >= ga::kNoCausal)
+        return fail(GA_EUNSUPPORTED, "segment chain of branch %d spans %d tokens", b,
+                    pl->cg.seg_len[v]);
+      pl->cg.causal[v] =
+          (pl->cg.npg[v] - npg[last]) * ga::kPageTokens + st->seg_len[last] - query_counts[b];
+    }
+  }
   const CGraph& c = pl->cg;
   pl->z.S = (int32_t)c.head.size();
   pl->z.E = (int32_t)c.path_segs.size();
@@ -442,7 +516,7 @@ ga_status upload(ga_plan* pl, const Layout& L, hipStream_t stream) {
   const CGraph& c = pl->cg;
   const ga_segment_table cst{pl->z.S, c.seg_len.data(), c.seg_page_off.data(), c.seg_pages.data()};
   const ga_branch_paths cbp{pl->z.B, c.path_off.data(), c.path_segs.data()};
-  pack_upload(&cst, &cbp, L, pl->z, static_cast<char*>(pl->pin));
+  pack_upload(&cst, &cbp, c.causal.data(), L, pl->z, static_cast<char*>(pl->pin));
   GA_HIP(hipMemcpyAsync(pl->dev, pl->pin, upload_bytes(L), hipMemcpyHostToDevice, stream),
          "graph upload");
   return GA_OK;
@@ -504,7 +578,8 @@ ga_status do_run(ga_plan* pl, const void* q, const void* pool, void* out, float*
   hipEvent_t* ev = rec ? &pl->ev_run[3 * pl->prof_runs] : nullptr;
   if (rec) GA_HIP(hipEventRecord(ev[0], stream), "profile event");
   if (grid > 0)
-    GA_HIP(ga::launch_seg_attn(a, pl->p.head_dim, bf16, (int)grid, stream), "attention launch");
+    GA_HIP(ga::launch_seg_attn(a, pl->p.head_dim, bf16, pl->causal, (int)grid, stream),
+           "attention launch");
   if (rec) GA_HIP(hipEventRecord(ev[1], stream), "profile event");
   ga::MergeArgs m{};
   m.bpart_off = pl->sc.bpart_off;
@@ -541,15 +616,15 @@ extern "C" {
 
 const char* graphattn_last_error(void) { return g_err.c_str(); }
 
-ga_status graphattn_plan_create(const ga_segment_table* segment_table,
-                                const ga_branch_paths* branch_paths, const ga_params* params,
-                                void* hip_stream, ga_plan** plan) {
+static ga_status plan_create(const ga_segment_table* segment_table,
+                             const ga_branch_paths* branch_paths, const int32_t* query_counts,
+                             const ga_params* params, void* hip_stream, ga_plan** plan) {
   g_err.clear();
   if (!plan) return fail(GA_EINVAL, "plan out-pointer is NULL");
   *plan = nullptr;
   ga_plan* pl = new ga_plan();
   Layout L;
-  ga_status rc = plan_init(segment_table, branch_paths, params, pl, &L);
+  ga_status rc = plan_init(segment_table, branch_paths, params, query_counts, pl, &L);
   if (rc) {
     delete pl;
     return rc;
@@ -577,6 +652,26 @@ ga_status graphattn_plan_create(const ga_segment_table* segment_table,
   return GA_OK;
 }
 
+ga_status graphattn_plan_create(const ga_segment_table* segment_table,
+                                const ga_branch_paths* branch_paths, const ga_params* params,
+                                void* hip_stream, ga_plan** plan) {
+  return plan_create(segment_table, branch_paths, nullptr, params, hip_stream, plan);
+}
+
+ga_status graphattn_plan_create_extend(const ga_segment_table* segment_table,
+                                       const ga_branch_paths* branch_paths,
+                                       const int32_t* query_counts, const ga_params* params,
+                                       void* hip_stream, ga_plan** plan) {
+  if (!query_counts && branch_paths && branch_paths->num_branches > 0) {
+    g_err.clear();
+    if (plan) *plan = nullptr;
+    return fail(GA_EINVAL, "query_counts is NULL");
+  }
+  static const int32_t none = 0;
+  return plan_create(segment_table, branch_paths, query_counts ? query_counts : &none, params,
+                     hip_stream, plan);
+}
+
 ga_status graphattn_schedule(ga_plan* plan, void* hip_stream) {
   g_err.clear();
   if (!plan) return fail(GA_EINVAL, "plan is NULL");
@@ -594,7 +689,8 @@ ga_status graphattn_plan_info(const ga_plan* plan, ga_plan_info* info) {
   g_err.clear();
   if (!plan || !info) return fail(GA_EINVAL, "plan or info is NULL");
   info->num_segments = plan->cg.S0;
-  info->num_branches = plan->z.B;
+  info->num_branches = plan->B0;
+  info->num_query_rows = plan->z.B;
   info->num_entries = (int32_t)plan->cg.E0;
   info->num_chains = plan->z.S;
   info->chunk_pages = plan->z.chunk_pages;
@@ -719,15 +815,15 @@ void graphattn_plan_destroy(ga_plan* plan) {
   delete plan;
 }
 
-ga_status graphattn_decode(const void* q, const void* kv_page_pool,
-                           const ga_segment_table* segment_table,
-                           const ga_branch_paths* branch_paths, void* out, float* lse,
-                           const ga_params* params, void* hip_stream) {
+static ga_status one_shot(const void* q, const void* kv_page_pool,
+                          const ga_segment_table* segment_table,
+                          const ga_branch_paths* branch_paths, const int32_t* query_counts,
+                          void* out, float* lse, const ga_params* params, void* hip_stream) {
   g_err.clear();
   hipStream_t stream = static_cast<hipStream_t>(hip_stream);
   ga_plan pl;
   Layout L;
-  ga_status rc = plan_init(segment_table, branch_paths, params, &pl, &L);
+  ga_status rc = plan_init(segment_table, branch_paths, params, query_counts, &pl, &L);
   if (rc) return rc;
   rc = check_run_ptrs(&pl, q, kv_page_pool, out, lse);
   if (rc) return rc;
@@ -786,6 +882,76 @@ ga_status graphattn_decode(const void* q, const void* kv_page_pool,
   if (rc) return rc;
   GA_HIP(hipEventRecord(g_cache.done, stream), "record decode");
   return GA_OK;
+}
+
+ga_status graphattn_decode(const void* q, const void* kv_page_pool,
+                           const ga_segment_table* segment_table,
+                           const ga_branch_paths* branch_paths, void* out, float* lse,
+                           const ga_params* params, void* hip_stream) {
+  return one_shot(q, kv_page_pool, segment_table, branch_paths, nullptr, out, lse, params,
+                  hip_stream);
+}
+
+static ga_status kv_write(void* pool, const void* k_new, const void* v_new, const int32_t* src,
+                          const int32_t* dst, int32_t n, const ga_params* params,
+                          void* hip_stream) {
+  g_err.clear();
+  ga_status rc = validate_params(params);
+  if (rc) return rc;
+  if (n < 0) return fail(GA_EINVAL, "num_tokens is negative");
+  if (n == 0) return GA_OK;
+  if (!pool || !dst || (src == nullptr && (!k_new || !v_new)))
+    return fail(GA_EINVAL, "device pointers must be non-NULL");
+  if ((reinterpret_cast<uintptr_t>(pool) | reinterpret_cast<uintptr_t>(k_new) |
+       reinterpret_cast<uintptr_t>(v_new)) & 15)
+    return fail(GA_EINVAL, "kv_page_pool, k_new and v_new must be 16-byte aligned");
+  if ((reinterpret_cast<uintptr_t>(dst) | reinterpret_cast<uintptr_t>(src)) & 3)
+    return fail(GA_EINVAL, "slot word arrays must be 4-byte aligned");
+  ga::KvWriteArgs a{};
+  a.pool = static_cast<unsigned char*>(pool);
+  a.k_new = static_cast<const unsigned char*>(k_new);
+  a.v_new = static_cast<const unsigned char*>(v_new);
+  a.src_words = src;
+  a.dst_words = dst;
+  a.num_slots = params->num_pages * ga::kPageTokens;
+  a.n = n;
+  a.Hkv = params->num_kv_heads;
+  a.row_bytes = params->head_dim * (params->dtype == GA_BF16 ? 2 : 4);
+  if ((int64_t)n * a.Hkv * 2 * (a.row_bytes / 16) > 0x7fffffffLL * 256)
+    return fail(GA_EINVAL, "too many tokens (%d)", n);
+  GA_HIP(ga::launch_kv_write(a, static_cast<hipStream_t>(hip_stream)), "kv write launch");
+  return GA_OK;
+}
+
+ga_status graphattn_kv_append(void* kv_page_pool, const void* k_new, const void* v_new,
+                              const int32_t* slot_words, int32_t num_tokens,
+                              const ga_params* params, void* hip_stream) {
+  return kv_write(kv_page_pool, k_new, v_new, nullptr, slot_words, num_tokens, params,
+                  hip_stream);
+}
+
+ga_status graphattn_kv_copy(void* kv_page_pool, const int32_t* src_slot_words,
+                            const int32_t* dst_slot_words, int32_t num_tokens,
+                            const ga_params* params, void* hip_stream) {
+  if (!src_slot_words && num_tokens > 0) {
+    g_err.clear();
+    return fail(GA_EINVAL, "src_slot_words is NULL");
+  }
+  return kv_write(kv_page_pool, nullptr, nullptr, src_slot_words, dst_slot_words, num_tokens,
+                  params, hip_stream);
+}
+
+ga_status graphattn_extend(const void* q, const void* kv_page_pool,
+                           const ga_segment_table* segment_table,
+                           const ga_branch_paths* branch_paths, const int32_t* query_counts,
+                           void* out, float* lse, const ga_params* params, void* hip_stream) {
+  if (!query_counts && branch_paths && branch_paths->num_branches > 0) {
+    g_err.clear();
+    return fail(GA_EINVAL, "query_counts is NULL");
+  }
+  static const int32_t none = 0;
+  return one_shot(q, kv_page_pool, segment_table, branch_paths,
+                  query_counts ? query_counts : &none, out, lse, params, hip_stream);
 }
 
 }  // extern "C"

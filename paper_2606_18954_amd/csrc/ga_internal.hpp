@@ -18,12 +18,14 @@ constexpr int kAttnThreads = 256;        // 4 wave64 per workgroup
 
 // Work-item descriptor (int32 words, one per item, fixed stride), written by the scheduler and
 // copied whole into LDS by the attention kernel:
-//   [0..3]  pages in the chunk, index of the segment's last page relative to the chunk start,
-//           valid tokens of that last page, |B(s)|
+//   [0..3]  pages in the chunk, causal word (kNoCausal, or for a multi-query segment c such that
+//           the row of group rank j sees chunk token 16 x page + slot only up to c + j), valid
+//           tokens of the segment's last page, |B(s)|
 //   [4..7]  row block, group offset of B(s), page-table offset of the chunk, first partial row
 //   [8 .. 8 + chunk_pages)            page words of the chunk (page id | (valid tokens - 1) << 27)
 //   [8 + chunk_pages .. + branches)   branch ids of the row block's rows (B(s) from row0/group)
 constexpr int kDescHead = 8;
+constexpr int32_t kNoCausal = 0x40000000;
 constexpr int kDescMaxBytes = 3072;      // LDS slot per descriptor
 __host__ __device__ inline int desc_branch_max(int group) {
   const int n = (kRowsPerBlock + group - 1) / group + 1;
@@ -43,6 +45,9 @@ struct DevGraph {
   const int32_t* seg_pages;      // [P]
   const int64_t* path_off;       // [B+1]
   const int32_t* path_segs;      // [E]
+  const int32_t* seg_causal;     // [S]  causal origin of a multi-query segment, else kNoCausal:
+                                 //      the row of group rank j sees token 16 x page + slot of
+                                 //      the segment's page list only up to seg_causal + j
 };
 
 // Scheduler outputs (device memory owned by the plan).
@@ -101,13 +106,27 @@ struct MergeArgs {
   int32_t B, Hq;
 };
 
+// Page-pool writes (kv_write.hip): token j goes to slot word dst_words[j] (page * 16 + slot),
+// from k_new / v_new [n][Hkv][D] (append, src_words == nullptr) or from the pool slot
+// src_words[j] (copy).  Tokens whose words fall outside [0, num_slots) are skipped.
+struct KvWriteArgs {
+  unsigned char* pool;
+  const unsigned char* k_new;
+  const unsigned char* v_new;
+  const int32_t* src_words;
+  const int32_t* dst_words;
+  int64_t num_slots;       // num_pages * 16
+  int32_t n, Hkv, row_bytes;
+};
+
 // Launchers (each returns the launch status).
 hipError_t launch_schedule(const DevGraph& g, const DevSchedule& sc, int32_t group,
                            int32_t chunk_pages, int64_t max_items, hipStream_t stream);
-hipError_t launch_seg_attn(const AttnArgs& a, int head_dim, bool bf16, int grid,
+hipError_t launch_seg_attn(const AttnArgs& a, int head_dim, bool bf16, bool causal, int grid,
                            hipStream_t stream);
 hipError_t launch_merge(const MergeArgs& a, int head_dim, bool out_bf16, bool part_f16,
                         hipStream_t stream);
+hipError_t launch_kv_write(const KvWriteArgs& a, hipStream_t stream);
 // Number of co-resident attention workgroups the persistent grid uses on this device.
 int seg_attn_grid(int head_dim, bool bf16, int num_cus);
 

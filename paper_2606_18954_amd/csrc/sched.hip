@@ -220,6 +220,12 @@ __device__ void scan_entries(const DevGraph& g, const DevSchedule& sc, int64_t (
     sc.bpart_off[b] = b < g.B ? sc.entry_part[g.path_off[b]] : sh[0][1023];
 }
 
+// Descriptor causal word of the chunk of segment s that starts at page p0.
+__device__ __forceinline__ int causal_word(const DevGraph& g, int s, int p0) {
+  const int c = g.seg_causal[s];
+  return c == kNoCausal ? kNoCausal : c - p0 * kPageTokens;
+}
+
 // Partial rows of path entry e (its segment's chunks, in order) into the branch list.
 __device__ __forceinline__ void write_entry_parts(const DevGraph& g, const DevSchedule& sc,
                                                   int e, int rank, int cnt) {
@@ -252,7 +258,7 @@ __device__ __forceinline__ void emit_items(const DevGraph& g, const DevSchedule&
     for (int rbk = 0; rbk < nrb; ++rbk, ++w) {
       sc.items[w] = make_int4(s, c, rbk, 0);
       int4* d = reinterpret_cast<int4*>(sc.desc + w * sc.desc_words);
-      d[0] = make_int4(np, npg - 1 - p0, last_valid, cnt);
+      d[0] = make_int4(np, causal_word(g, s, p0), last_valid, cnt);
       d[1] = make_int4(rbk, (int)goff, (int)(poff + p0), (int)(prow_off + (int64_t)c * cnt));
     }
   }
@@ -557,7 +563,8 @@ __global__ void k_emit(DevGraph g, DevSchedule sc, int32_t group, int32_t chunk_
   int32_t* d = sc.desc + w * sc.desc_words;
   if (lane == 0) {
     sc.items[w] = make_int4(s, c, rb, 0);
-    reinterpret_cast<int4*>(d)[0] = make_int4(np, npg - 1 - p0, len - (npg - 1) * kPageTokens, cnt);
+    reinterpret_cast<int4*>(d)[0] =
+        make_int4(np, causal_word(g, s, p0), len - (npg - 1) * kPageTokens, cnt);
     reinterpret_cast<int4*>(d)[1] =
         make_int4(rb, (int)sc.grp_off[s], poff, (int)sc.seg_prow_off[s] + c * cnt);
   }

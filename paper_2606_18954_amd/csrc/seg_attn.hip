@@ -162,10 +162,14 @@ constexpr float kTau = 8.0f;
 // Online softmax (log2 domain) over one page's 16 tokens for each of the wave's NT tiles: masks
 // tokens past the segment end, and moves a row's reference m only when some score exceeds it by
 // more than 2^kTau, so the common page needs no cross-lane reduction and no rescale of O.
-template <int NT, int NBW, int NBT>
+// CAUSAL (multi-query units): when cm is set, the lane's score i of tile t is also masked for
+// i > thr[t] (the row's last visible token, relative to token 4 kg of the page).  A row may then
+// have seen no token yet (m = -inf, l = 0, O = 0); the guards keep it at exactly that.
+template <int NT, int NBW, int NBT, bool CAUSAL>
 __device__ __forceinline__ void softmax_page(f32x4 (&S)[NT], float (&p)[NT][4], float (&m)[NT],
                                              float (&l)[NT], f32x4 (&O)[NT][NBT], bool last,
-                                             int last_valid, int kg, float sl2) {
+                                             int last_valid, bool cm, const int (&thr)[NT],
+                                             int kg, float sl2) {
   const float NEG_INF = -__builtin_huge_valf();
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
@@ -174,16 +178,25 @@ __device__ __forceinline__ void softmax_page(f32x4 (&S)[NT], float (&p)[NT][4], 
       for (int i = 0; i < 4; ++i)
         if (4 * kg + i >= last_valid) S[t][i] = NEG_INF;
     }
+    if constexpr (CAUSAL) {
+      if (cm) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (i > thr[t]) S[t][i] = NEG_INF;
+      }
+    }
     const float lm = fmaxf(fmaxf(S[t][0], S[t][1]), fmaxf(S[t][2], S[t][3])) * sl2;
     if (__any(lm > m[t] + kTau)) {
       const float mn = fmaxf(m[t], xmax(lm));
-      const float alpha = exp2_(m[t] - mn);
+      float alpha = exp2_(m[t] - mn);
+      if constexpr (CAUSAL) alpha = mn == NEG_INF ? 1.f : alpha;
       m[t] = mn;
       l[t] *= alpha;
 #pragma unroll
       for (int i = 0; i < NBW; ++i) O[t][i] *= alpha;
     }
-    const float nm = -m[t];
+    float nm = -m[t];
+    if constexpr (CAUSAL) nm = m[t] == NEG_INF ? 0.f : nm;
 #pragma unroll
     for (int i = 0; i < 4; ++i) p[t][i] = exp2_(fmaf(S[t][i], sl2, nm));
     l[t] += (p[t][0] + p[t][1]) + (p[t][2] + p[t][3]);
@@ -191,13 +204,14 @@ __device__ __forceinline__ void softmax_page(f32x4 (&S)[NT], float (&p)[NT][4], 
 }
 
 // One K/V stage for one wave: NT row tiles (qop[0 .. NT-1]) against pages p0, p0 + pstep, ... of
-// the stage, producing
+// the stage (for CAUSAL units, cl[t] is the lane's row limit relative to the stage's first page),
+// producing
 // NBW output column blocks (O[t][i] holds column block n0 + i).  All LDS operand reads of a page
 // are issued before its first MFMA, so the V reads overlap S = K Q^T and the softmax.
-template <int D, bool BF16, int NT, int NBW>
+template <int D, bool BF16, int NT, int NBW, bool CAUSAL>
 __device__ __forceinline__ void kv_stage(const unsigned char* sb, const int* pwords, int p0,
                                          int pstep, int npst, float sl2,
-                                         int r16, int kg, int n0,
+                                         int r16, int kg, int n0, bool cm, const int (&cl)[NT],
                                          const QOp<BF16> (&qop)[NT][Cfg<D, BF16>::QR],
                                          float (&m)[NT], float (&l)[NT],
                                          f32x4 (&O)[NT][Cfg<D, BF16>::NB]) {
@@ -211,6 +225,9 @@ __device__ __forceinline__ void kv_stage(const unsigned char* sb, const int* pwo
     const int vm1 = (int)((unsigned)__builtin_amdgcn_readfirstlane(pwords[pis]) >> kPageValidShift);
     const bool last = vm1 < kPageTokens - 1;
     const int last_valid = vm1 + 1;
+    int thr[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) thr[t] = CAUSAL ? cl[t] - kPageTokens * pis : 0;
     f32x4 S[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) S[t] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -238,7 +255,8 @@ __device__ __forceinline__ void kv_stage(const unsigned char* sb, const int* pwo
 #pragma unroll
         for (int t = 0; t < NT; ++t)
           S[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[jj], qop[t][jj].v, S[t], 0, 0, 0);
-      softmax_page<NT, NBW, Cfg<D, BF16>::NB>(S, p, m, l, O, last, last_valid, kg, sl2);
+      softmax_page<NT, NBW, Cfg<D, BF16>::NB, CAUSAL>(S, p, m, l, O, last, last_valid, cm, thr,
+                                                       kg, sl2);
       s16x4 pb[NT];
 #pragma unroll
       for (int t = 0; t < NT; ++t)
@@ -265,7 +283,8 @@ __device__ __forceinline__ void kv_stage(const unsigned char* sb, const int* pwo
         for (int t = 0; t < NT; ++t)
           S[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(ka, qop[t][jj].v, S[t], 0, 0, 0);
       }
-      softmax_page<NT, NBW, Cfg<D, BF16>::NB>(S, p, m, l, O, last, last_valid, kg, sl2);
+      softmax_page<NT, NBW, Cfg<D, BF16>::NB, CAUSAL>(S, p, m, l, O, last, last_valid, cm, thr,
+                                                       kg, sl2);
 #pragma unroll
       for (int i = 0; i < NBW; ++i) {
         const int n = n0 + i;
@@ -284,7 +303,10 @@ __device__ __forceinline__ void kv_stage(const unsigned char* sb, const int* pwo
   }
 }
 
-template <int D, bool BF16>
+// CAUSAL: the multi-query variant.  A unit whose descriptor carries a causal word c (word 1;
+// kNoCausal otherwise) lets the row of group rank j see token t of the chunk (t counted as
+// 16 x page index + slot) only for t <= c + j.
+template <int D, bool BF16, bool CAUSAL>
 __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
   using C = Cfg<D, BF16>;
   using T = typename std::conditional<BF16, __bf16, float>::type;
@@ -409,6 +431,20 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
       }
       };
   
+      // Causal limits: the lane's row (group rank j) sees chunk token t for t <= cw + j; cl[k]
+      // holds that bound relative to token 4 kg of the chunk's first page.
+      bool cm = false;
+      int cl[NT];
+  #pragma unroll
+      for (int k = 0; k < NT; ++k) cl[k] = 0;
+      if constexpr (CAUSAL) {
+        const int cw = __builtin_amdgcn_readfirstlane(dsc[1]);
+        cm = cw != kNoCausal;
+  #pragma unroll
+        for (int k = 0; k < NT; ++k)
+          cl[k] = cw + (row0 + (t0 + 4 * k) * 16 + r16) / a.group - 4 * kg;
+      }
+
       float m[NT], l[NT];
       f32x4 O[NT][C::NB];
   #pragma unroll
@@ -474,8 +510,12 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
         const int npst = min(C::SP, np - st * C::SP);
         if (ntile > 0) {
           const unsigned char* sb = smem + buf * C::STAGE;
-          kv_stage<D, BF16, NT, C::NB>(sb, &s_desc[b][kDescHead + st * C::SP], split, ks, npst,
-                                       a.scale_log2, r16, kg, 0, qop, m, l, O);
+          int cls[NT];
+  #pragma unroll
+          for (int k = 0; k < NT; ++k) cls[k] = cl[k] - kPageTokens * C::SP * st;
+          kv_stage<D, BF16, NT, C::NB, CAUSAL>(sb, &s_desc[b][kDescHead + st * C::SP], split, ks,
+                                               npst, a.scale_log2, r16, kg, 0, cm, cls, qop, m,
+                                               l, O);
         }
       }
       // Every wave is done with the ring; wave 0's copy of the next descriptor has landed (the
@@ -508,7 +548,9 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
         if (split == 0 && ntile > 0) {
           float M = m[0];
           for (int sp = 1; sp < ks; ++sp) M = fmaxf(M, s_ml[(sp - 1) * nrt + t0][0][lane]);
-          const float w0 = exp2_(m[0] - M);
+          // (a causal row that saw no token in any split has M = -inf and stays empty)
+          const float Ms = CAUSAL && M == NEG_INF ? 0.f : M;
+          const float w0 = exp2_(m[0] - Ms);
           float Lc = w0 * L[0];
           f32x4 Oc[C::NB];
   #pragma unroll
@@ -516,7 +558,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
           for (int sp = 1; sp < ks; ++sp) {
             const int wi = (sp - 1) * nrt + t0;
             const float* o = cb + wi * NV * 64;
-            const float wgt = exp2_(s_ml[wi][0][lane] - M);
+            const float wgt = exp2_(s_ml[wi][0][lane] - Ms);
             Lc += wgt * s_ml[wi][1][lane];
   #pragma unroll
             for (int n = 0; n < C::NB; ++n)
@@ -535,7 +577,8 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
         for (int k = 0; k < NT; ++k) {
           if (k >= ntile) break;
           const int r = (t0 + 4 * k) * 16 + r16;
-          const float inv = 1.f / L[k];
+          // A causal row that saw no token of the chunk (L = 0) stores o = 0, lambda = -inf.
+          const float inv = CAUSAL && !(L[k] > 0.f) ? 0.f : 1.f / L[k];
           if constexpr (BF16) {
             // fp16 partial in lane order, scaled so the row's largest |o| is below 2^15 (the
             // four lanes of a row agree on the scale; L >= 1, so |o| <= max |V|).
@@ -596,8 +639,11 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
 }
 
 template <int D, bool BF16>
-hipError_t launch_t(const AttnArgs& a, int grid, hipStream_t stream) {
-  hipLaunchKernelGGL((k_seg_attn<D, BF16>), dim3(grid), dim3(kAttnThreads), 0, stream, a);
+hipError_t launch_t(const AttnArgs& a, bool causal, int grid, hipStream_t stream) {
+  if (causal)
+    hipLaunchKernelGGL((k_seg_attn<D, BF16, true>), dim3(grid), dim3(kAttnThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL((k_seg_attn<D, BF16, false>), dim3(grid), dim3(kAttnThreads), 0, stream, a);
   return hipGetLastError();
 }
 
@@ -609,14 +655,14 @@ int seg_attn_grid(int head_dim, bool bf16, int num_cus) {
   return num_cus * 2;                      // two 256-thread workgroups fit per CU (LDS-bound)
 }
 
-hipError_t launch_seg_attn(const AttnArgs& a, int head_dim, bool bf16, int grid,
+hipError_t launch_seg_attn(const AttnArgs& a, int head_dim, bool bf16, bool causal, int grid,
                            hipStream_t stream) {
   if (bf16) {
-    if (head_dim == 64) return launch_t<64, true>(a, grid, stream);
-    if (head_dim == 128) return launch_t<128, true>(a, grid, stream);
+    if (head_dim == 64) return launch_t<64, true>(a, causal, grid, stream);
+    if (head_dim == 128) return launch_t<128, true>(a, causal, grid, stream);
   } else {
-    if (head_dim == 64) return launch_t<64, false>(a, grid, stream);
-    if (head_dim == 128) return launch_t<128, false>(a, grid, stream);
+    if (head_dim == 64) return launch_t<64, false>(a, causal, grid, stream);
+    if (head_dim == 128) return launch_t<128, false>(a, causal, grid, stream);
   }
   return hipErrorInvalidValue;
 }

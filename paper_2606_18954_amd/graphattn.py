@@ -53,7 +53,8 @@ class PlanInfo(ctypes.Structure):
     _fields_ = [("num_segments", ctypes.c_int32), ("num_branches", ctypes.c_int32),
                 ("num_entries", ctypes.c_int32), ("chunk_pages", ctypes.c_int32),
                 ("rows_per_block", ctypes.c_int32), ("num_items", ctypes.c_int64),
-                ("num_partial_rows", ctypes.c_int64), ("num_chains", ctypes.c_int32)]
+                ("num_partial_rows", ctypes.c_int64), ("num_chains", ctypes.c_int32),
+                ("num_query_rows", ctypes.c_int32)]
 
 
 class Profile(ctypes.Structure):
@@ -80,6 +81,16 @@ def load_library() -> ctypes.CDLL:
     lib.graphattn_decode.restype = ctypes.c_int
     lib.graphattn_plan_create.argtypes = [P(SegmentTable), P(BranchPaths), P(Params), vp, P(vp)]
     lib.graphattn_plan_create.restype = ctypes.c_int
+    lib.graphattn_extend.argtypes = [vp, vp, P(SegmentTable), P(BranchPaths), P(i32), vp, vp,
+                                     P(Params), vp]
+    lib.graphattn_extend.restype = ctypes.c_int
+    lib.graphattn_plan_create_extend.argtypes = [P(SegmentTable), P(BranchPaths), P(i32),
+                                                 P(Params), vp, P(vp)]
+    lib.graphattn_plan_create_extend.restype = ctypes.c_int
+    lib.graphattn_kv_append.argtypes = [vp, vp, vp, vp, i32, P(Params), vp]
+    lib.graphattn_kv_append.restype = ctypes.c_int
+    lib.graphattn_kv_copy.argtypes = [vp, vp, vp, i32, P(Params), vp]
+    lib.graphattn_kv_copy.restype = ctypes.c_int
     lib.graphattn_schedule.argtypes = [vp, vp]
     lib.graphattn_schedule.restype = ctypes.c_int
     lib.graphattn_run.argtypes = [vp, vp, vp, vp, vp, vp]
@@ -169,17 +180,71 @@ def decode(q, pool, graph: HostGraph, params: Params, out=None, lse=None, stream
     return out, lse
 
 
-class Plan:
-    """graphattn_plan_create / schedule / run / destroy."""
+def _counts(query_counts) -> np.ndarray:
+    return np.ascontiguousarray(query_counts, dtype=np.int32)
 
-    def __init__(self, graph: HostGraph, params: Params, stream=None):
+
+def extend(q, pool, graph: HostGraph, query_counts, params: Params, out=None, lse=None,
+           stream=None):
+    """graphattn_extend on torch tensors: q [R, Hq, D] with R = sum(query_counts); returns
+    (out [R, Hq, D], lse [R, Hq] float32)."""
+    import torch
+    lib = load_library()
+    cnt = _counts(query_counts)
+    if len(cnt) != graph.bp.num_branches:
+        raise ValueError("one query count per branch")
+    R = int(cnt.sum())
+    if out is None:
+        odt = torch.float32 if params.out_f32 else q.dtype
+        out = torch.empty((R, params.num_q_heads, params.head_dim), dtype=odt, device=q.device)
+    if lse is None:
+        lse = torch.empty((R, params.num_q_heads), dtype=torch.float32, device=q.device)
+    _check(lib.graphattn_extend(_dev_ptr(q), _dev_ptr(pool), ctypes.byref(graph.st),
+                                ctypes.byref(graph.bp), _ptr(cnt, ctypes.c_int32), _dev_ptr(out),
+                                _dev_ptr(lse), ctypes.byref(params), _stream_handle(stream)))
+    return out, lse
+
+
+def kv_append(pool, k_new, v_new, slot_words, params: Params, stream=None):
+    """graphattn_kv_append: k_new / v_new [n, Hkv, D], slot_words int32 [n] (device)."""
+    lib = load_library()
+    n = int(slot_words.numel())
+    if k_new.shape[0] != n or v_new.shape[0] != n:
+        raise ValueError("one K row and one V row per slot word")
+    _check(lib.graphattn_kv_append(_dev_ptr(pool), _dev_ptr(k_new), _dev_ptr(v_new),
+                                   _dev_ptr(slot_words), n, ctypes.byref(params),
+                                   _stream_handle(stream)))
+
+
+def kv_copy(pool, src_words, dst_words, params: Params, stream=None):
+    """graphattn_kv_copy: src_words / dst_words int32 [n] (device)."""
+    lib = load_library()
+    n = int(dst_words.numel())
+    if src_words.numel() != n:
+        raise ValueError("one source word per destination word")
+    _check(lib.graphattn_kv_copy(_dev_ptr(pool), _dev_ptr(src_words), _dev_ptr(dst_words), n,
+                                 ctypes.byref(params), _stream_handle(stream)))
+
+
+class Plan:
+    """graphattn_plan_create (or _create_extend with query_counts) / schedule / run /
+    destroy."""
+
+    def __init__(self, graph: HostGraph, params: Params, stream=None, query_counts=None):
         self.lib = load_library()
         self.graph = graph
         self.params = params
         h = ctypes.c_void_p()
-        _check(self.lib.graphattn_plan_create(ctypes.byref(graph.st), ctypes.byref(graph.bp),
-                                              ctypes.byref(params), _stream_handle(stream),
-                                              ctypes.byref(h)))
+        if query_counts is None:
+            _check(self.lib.graphattn_plan_create(ctypes.byref(graph.st), ctypes.byref(graph.bp),
+                                                  ctypes.byref(params), _stream_handle(stream),
+                                                  ctypes.byref(h)))
+        else:
+            self.query_counts = _counts(query_counts)
+            _check(self.lib.graphattn_plan_create_extend(
+                ctypes.byref(graph.st), ctypes.byref(graph.bp),
+                _ptr(self.query_counts, ctypes.c_int32), ctypes.byref(params),
+                _stream_handle(stream), ctypes.byref(h)))
         self.handle = h
 
     def schedule(self, stream=None):
@@ -238,13 +303,18 @@ class Plan:
             pass
 
 
-def validate_only(graph: HostGraph, params: Params) -> int:
-    """Run the library's host-side validation through graphattn_decode with NULL device
-    buffers and no branches to compute; used by CPU tests of the error paths.  Returns the
+def validate_only(graph: HostGraph, params: Params, query_counts=None) -> int:
+    """Run the library's host-side validation through graphattn_decode (graphattn_extend with
+    query_counts) with NULL device buffers; used by CPU tests of the error paths.  Returns the
     status (only meaningful for invalid inputs, which are rejected before any HIP call)."""
     lib = load_library()
-    return lib.graphattn_decode(None, None, ctypes.byref(graph.st), ctypes.byref(graph.bp), None,
-                                None, ctypes.byref(params), None)
+    if query_counts is None:
+        return lib.graphattn_decode(None, None, ctypes.byref(graph.st), ctypes.byref(graph.bp),
+                                    None, None, ctypes.byref(params), None)
+    cnt = _counts(query_counts)
+    return lib.graphattn_extend(None, None, ctypes.byref(graph.st), ctypes.byref(graph.bp),
+                                _ptr(cnt, ctypes.c_int32) if len(cnt) else None, None, None,
+                                ctypes.byref(params), None)
 
 
 def last_error() -> str:

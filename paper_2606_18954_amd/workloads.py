@@ -86,6 +86,8 @@ class Workload:
     q: torch.Tensor               # CPU [B][Hq][D], torch.bfloat16 or torch.float32
     pool: torch.Tensor            # CPU [Np][Hkv][2][16][D]
     seed: int
+    # Multi-query (extend) workloads: queries per branch; q then holds sum(query_counts) rows.
+    query_counts: Optional[np.ndarray] = None
 
     @property
     def elt_bytes(self) -> int:
@@ -344,12 +346,7 @@ def merged_dag_prompt(rng, schedule=(2, 2, 2, 2, 1, 1), root_lo=512, root_hi=102
     return lens, paths, {"merges": merges, "step_nodes": step_nodes, "merged_nodes": merged_nodes}
 
 
-def config3_merged_dag(prompts: int = 64, slack_pages: int = 0, poison: bool = False,
-                       kzero_tags: bool = False, seed: Optional[int] = None,
-                       merge_p: float = 0.25) -> Workload:
-    """Merged-DAG rollout, 7B shape: 64 prompts, root U{512..1024}, depth-6 graph with 16 leaves,
-    steps U{64..1024}, per-node merge probability 0.25; 1024 branches of 7 segments."""
-    seed = SEED_BASE + 3 if seed is None else seed
+def _merged_dag_structure(prompts: int, seed: int, merge_p: float):
     rng = np.random.default_rng(seed)
     lens: List[int] = []
     paths: List[List[int]] = []
@@ -363,6 +360,16 @@ def config3_merged_dag(prompts: int = 64, slack_pages: int = 0, poison: bool = F
         merged += st["merged_nodes"]
     info = {"config": 3, "prompts": prompts, "merge_p": merge_p,
             "merged_fraction": merged / max(1, step_nodes)}
+    return lens, paths, info
+
+
+def config3_merged_dag(prompts: int = 64, slack_pages: int = 0, poison: bool = False,
+                       kzero_tags: bool = False, seed: Optional[int] = None,
+                       merge_p: float = 0.25) -> Workload:
+    """Merged-DAG rollout, 7B shape: 64 prompts, root U{512..1024}, depth-6 graph with 16 leaves,
+    steps U{64..1024}, per-node merge probability 0.25; 1024 branches of 7 segments."""
+    seed = SEED_BASE + 3 if seed is None else seed
+    lens, paths, info = _merged_dag_structure(prompts, seed, merge_p)
     g = assemble_graph(lens, paths, seed, slack_pages, info)
     return make_workload(f"merged-DAG rollout, 7B shape (28/4/128, {prompts} prompts, "
                          f"{len(paths)} branches)", g, 28, 4, 128, "bf16", seed, poison, kzero_tags)
@@ -471,6 +478,45 @@ def config5_graph(prompts: int = 32, slack_pages: int = 0, poison: bool = False,
     g = assemble_graph(lens, paths, seed, slack_pages, {"config": "5-graph", "prompts": prompts})
     return make_workload(f"equal-budget graph, 7B shape ({prompts} prompts, {len(paths)} "
                          f"branches)", g, 28, 4, 128, "bf16", seed, poison, kzero_tags)
+
+
+def with_new_steps(lens: Sequence[int], paths: Sequence[Sequence[int]],
+                   step_lens: Sequence[int]):
+    """Give every branch a new private segment (the step being extended) at the end of its
+    path: branch b's new segment has step_lens[b] tokens."""
+    lens = list(lens)
+    out = []
+    for p, n in zip(paths, step_lens):
+        out.append(list(p) + [len(lens)])
+        lens.append(int(n))
+    return lens, out
+
+
+def make_extend_workload(name: str, graph: RolloutGraph, query_counts: Sequence[int], Hq: int,
+                         Hkv: int, D: int, dtype: str, seed: int,
+                         poison: bool = False) -> Workload:
+    """Pool as in draw_data; q [sum(query_counts)][Hq][D] from the data stream after the
+    decode queries (i.i.d. N(0,1) rounded to dtype)."""
+    _, pool = draw_data(graph, Hq, Hkv, D, dtype, seed, poison=poison)
+    counts = np.asarray(query_counts, dtype=np.int32)
+    nchunks = (graph.num_pages + _DRAW_CHUNK_PAGES - 1) // _DRAW_CHUNK_PAGES
+    q = _randn(seed, nchunks + 1, (int(counts.sum()), Hq, D))
+    q = _bf16_rne(q) if dtype == "bf16" else q
+    return Workload(name, graph, Hq, Hkv, D, dtype, q, pool, seed, counts)
+
+
+def config3_extend(prompts: int = 64, n_query: int = 16, slack_pages: int = 0,
+                   poison: bool = False, seed: Optional[int] = None) -> Workload:
+    """The merged-DAG rollout (7B shape) where every branch extends a new private step of
+    n_query tokens, all of them queries (a multi-token step: drafted tokens checked at once)."""
+    seed = SEED_BASE + 13 if seed is None else seed
+    lens, paths, info = _merged_dag_structure(prompts, seed, 0.25)
+    lens, paths = with_new_steps(lens, paths, [n_query] * len(paths))
+    info.update({"config": "3-extend", "n_query": n_query})
+    g = assemble_graph(lens, paths, seed, slack_pages, info)
+    return make_extend_workload(f"merged-DAG rollout, 7B shape (28/4/128, {prompts} prompts, "
+                                f"{len(paths)} branches), {n_query}-token extend", g,
+                                [n_query] * len(paths), 28, 4, 128, "bf16", seed, poison)
 
 
 CONFIGS = {

@@ -15,7 +15,9 @@ def test_library_exports_every_declared_symbol():
     assert set(syms) == {"graphattn_decode", "graphattn_plan_create", "graphattn_schedule",
                          "graphattn_run", "graphattn_plan_info", "graphattn_plan_debug_dump",
                          "graphattn_plan_destroy", "graphattn_last_error",
-                         "graphattn_plan_profile", "graphattn_plan_profile_read"}
+                         "graphattn_plan_profile", "graphattn_plan_profile_read",
+                         "graphattn_extend", "graphattn_plan_create_extend",
+                         "graphattn_kv_append", "graphattn_kv_copy"}
     for s in syms:
         assert hasattr(lib, s), s
 
@@ -120,3 +122,54 @@ def test_null_device_buffers_with_branches():
     p = G.make_params(8, 2, 64, n, "f32")
     assert G.validate_only(g, p) == G.GA_EINVAL
     assert "non-NULL" in G.last_error()
+
+
+def test_extend_errors():
+    """Multi-query validation: counts per branch, the newest segment is private to its branch."""
+    lib = G.load_library()
+    g, n = _graph()                                   # paths (0, 1) and (0, 2): 7 and 33 tokens
+    p = G.make_params(8, 2, 64, n, "f32")
+    assert lib.graphattn_extend(None, None, ctypes.byref(g.st), ctypes.byref(g.bp), None, None,
+                                None, ctypes.byref(p), None) == G.GA_EINVAL
+    assert "query_counts" in G.last_error()
+    for counts in ([0, 1], [8, 1], [1, 34], [-1, 1]):
+        assert G.validate_only(g, p, counts) == G.GA_EINVAL, counts
+        assert "query count" in G.last_error()
+    assert G.validate_only(g, p, [7, 33]) == G.GA_EINVAL   # valid counts, NULL device buffers
+    assert "non-NULL" in G.last_error()
+    g2, n2 = _graph(paths=((0, 1), (1, 2)))            # segment 1 is newest on path 0, shared
+    assert G.validate_only(g2, p, [1, 1]) == G.GA_EINVAL
+    assert "another path" in G.last_error()
+    g3, n3 = _graph(paths=((0,), (0, 1)))              # the root is newest on path 0
+    assert G.validate_only(g3, p, [3, 1]) == G.GA_EINVAL
+    g4, n4 = _graph(paths=((0, 3),))
+    assert G.validate_only(g4, p, [1]) == G.GA_ERANGE   # graph errors come first
+    h = ctypes.c_void_p(1)
+    assert lib.graphattn_plan_create_extend(ctypes.byref(g.st), ctypes.byref(g.bp), None,
+                                            ctypes.byref(p), None, ctypes.byref(h)) == G.GA_EINVAL
+    assert h.value is None
+
+
+def test_kv_write_errors():
+    """Append and copy validate on the host; no tokens is a no-op that touches no device."""
+    lib = G.load_library()
+    p = G.make_params(8, 2, 64, 4, "bf16")
+    dummy = ctypes.c_void_p(1 << 20)                  # never dereferenced: rejected or n = 0
+    assert lib.graphattn_kv_append(dummy, dummy, dummy, dummy, 0, ctypes.byref(p), None) == 0
+    assert lib.graphattn_kv_copy(None, None, None, 0, ctypes.byref(p), None) == 0
+    assert lib.graphattn_kv_append(dummy, dummy, dummy, dummy, -1, ctypes.byref(p),
+                                   None) == G.GA_EINVAL
+    assert lib.graphattn_kv_append(dummy, None, dummy, dummy, 3, ctypes.byref(p),
+                                   None) == G.GA_EINVAL
+    assert lib.graphattn_kv_append(dummy, dummy, dummy, None, 3, ctypes.byref(p),
+                                   None) == G.GA_EINVAL
+    assert lib.graphattn_kv_copy(dummy, None, dummy, 3, ctypes.byref(p), None) == G.GA_EINVAL
+    assert lib.graphattn_kv_append(ctypes.c_void_p((1 << 20) + 8), dummy, dummy, dummy, 3,
+                                   ctypes.byref(p), None) == G.GA_EINVAL
+    assert "aligned" in G.last_error()
+    assert lib.graphattn_kv_copy(dummy, ctypes.c_void_p((1 << 20) + 2), dummy, 3, ctypes.byref(p),
+                                 None) == G.GA_EINVAL
+    bad = G.make_params(8, 2, 96, 4, "bf16")
+    assert lib.graphattn_kv_append(dummy, dummy, dummy, dummy, 3, ctypes.byref(bad),
+                                   None) == G.GA_EUNSUPPORTED
+    assert lib.graphattn_kv_append(dummy, dummy, dummy, dummy, 3, None, None) == G.GA_EINVAL

@@ -9,6 +9,11 @@ workload is the merged-DAG rollout (64 prompts, 1024 branches, 7B attention shap
 Prints one JSON line: branch-tokens/s (one decode token per branch per step), the attention
 kernel's achieved fraction of the HBM roofline counting unique K/V bytes, and the CPU oracle
 timed on a bounded sample of the same workload.
+
+--op extend times the multi-query variant instead (every branch of the merged-DAG rollout extends
+a new step of --n-query tokens, all of them queries, causal inside the step): query-tokens/s and
+the attention kernel's fraction of the bf16 MFMA roofline on the attention flops.  --op append
+times storing one decode step's new K/V (one token per branch) into the page pool.
 """
 import argparse
 import hashlib
@@ -20,8 +25,10 @@ import time
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0
 METRIC = "branch-tokens/s per decode step; % of HBM roofline on unique KV bytes"
 COUNTERS_MD = os.path.join(ROOT, "profiles", "seg_attn_merged_dag_counters.md")
+EXT_COUNTERS_MD = os.path.join(ROOT, "profiles", "seg_attn_extend_counters.md")
 KERNEL_SRC = os.path.join(ROOT, "paper_2606_18954_amd", "csrc", "seg_attn.hip")
 
 
@@ -34,12 +41,12 @@ def kernel_hash():
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def measured_counters(config):
+def measured_counters(config, path=COUNTERS_MD):
     """HBM traffic and MFMA busy fraction from the committed rocprofv3 counter summary, only
     if it was taken on this exact attention kernel source and workload."""
-    if not os.path.exists(COUNTERS_MD):
+    if not os.path.exists(path):
         return None
-    txt = open(COUNTERS_MD).read()
+    txt = open(path).read()
     kv = dict(re.findall(r"^- (\w+): (\S+)", txt, flags=re.M))
     if kv.get("kernel_source_sha256_16") != kernel_hash() or kv.get("workload") != config:
         return None
@@ -70,6 +77,182 @@ def cpu_baseline(wl, n_sample):
             "attended_tokens_per_s": toks / dt}
 
 
+def extend_flops(wl):
+    """Attention flops of an extend step: 2 D per visible token for S = Q K^T and 2 D for O = P V,
+    per query row and q-head; query i of branch b sees its path's other segments whole and
+    len(last) - n_b + i + 1 tokens of the newest one."""
+    g = wl.graph
+    vis = 0
+    for b in range(g.num_branches):
+        n = int(wl.query_counts[b])
+        L = g.path_tokens(b)
+        vis += n * (L - n) + n * (n + 1) // 2
+    return 4 * wl.head_dim * wl.num_q_heads * vis, vis
+
+
+def cpu_baseline_extend(wl, n_sample):
+    sys.path.insert(0, ROOT)
+    import numpy as np
+    from oracle import graphattn_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = 1
+    g = wl.graph
+    R = int(wl.query_counts.sum())
+    rows = sorted(np.random.default_rng(11).choice(R, min(n_sample, R), replace=False).tolist())
+    t0 = time.perf_counter()
+    O.extend(wl.q_bits(), wl.pool_bits(), g.seg_len, g.seg_page_offsets, g.seg_pages,
+             g.path_offsets, g.path_segs, wl.query_counts, wl.num_q_heads, wl.num_kv_heads,
+             wl.head_dim, wl.dtype, rows=rows)
+    dt = time.perf_counter() - t0
+    return {"value": len(rows) / dt, "unit": "query-tokens/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{len(rows)} seeded query rows of the same workload, fp64 NumPy, "
+                      f"{dt:.1f} s wall"}
+
+
+def calibrate_copy(torch, dev):
+    """A plain elementwise copy of 1 GiB (bf16) three times: a kernel of known HBM traffic to
+    scale the FETCH_SIZE / WRITE_SIZE counters against."""
+    n = 1 << 29                                   # 1 GiB of bf16 read, 1 GiB written
+    a = torch.ones(n, dtype=torch.bfloat16, device=dev)
+    b = torch.empty_like(a)
+    for _ in range(3):
+        torch.mul(a, 1.0, out=b)
+    torch.cuda.synchronize()
+    log("copy calibration: 3 launches of a 1 GiB elementwise copy")
+    del a, b
+    torch.cuda.empty_cache()
+
+
+def run_extend(args, torch, G, W):
+    t0 = time.time()
+    wl = W.config3_extend(n_query=args.n_query)
+    g = wl.graph
+    R = int(wl.query_counts.sum())
+    log(f"workload {wl.name}: B={g.num_branches} rows={R} pages={g.num_pages} generated in "
+        f"{time.time() - t0:.1f}s")
+    dev = torch.device("cuda:0")
+    q, pool = wl.q.to(dev), wl.pool.to(dev)
+    Hq, D = wl.num_q_heads, wl.head_dim
+    out = torch.empty((R, Hq, D), dtype=q.dtype, device=dev)
+    lse = torch.empty((R, Hq), dtype=torch.float32, device=dev)
+    hg = G.HostGraph.from_graph(g)
+    params = G.make_params(Hq, wl.num_kv_heads, D, g.num_pages, wl.dtype)
+    plan = G.Plan(hg, params, query_counts=wl.query_counts)
+    info = plan.info()
+
+    def step():
+        plan.schedule()
+        plan.run(q, pool, out, lse)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    plan.profile(args.steps)
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record()
+    for _ in range(args.steps):
+        step()
+    ev1.record()
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / args.steps
+    prof = plan.profile_read()
+    attn_ms = prof.attn_ms / max(1, prof.runs)
+    merge_ms = prof.merge_ms / max(1, prof.runs)
+    sched_ms = prof.sched_ms / max(1, prof.schedules)
+    log(f"timed {args.steps} steps: {ms:.4f} ms/step (attention {attn_ms:.4f} ms, merge "
+        f"{merge_ms:.4f} ms, scheduler {sched_ms:.4f} ms)")
+    flops, vis = extend_flops(wl)
+    achieved = flops / (attn_ms * 1e-3) / 1e12
+    ukv = wl.unique_kv_bytes()
+    cnt = measured_counters("extend", EXT_COUNTERS_MD)
+    traffic = None
+    if cnt:
+        traffic = float(cnt["fetch_bytes_per_launch"]) + float(cnt["write_bytes_per_launch"])
+    res = {
+        "metric": "query-tokens/s per extend step; % of bf16 MFMA roofline on attention flops",
+        "value": R / (ms * 1e-3), "unit": "query-tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": wl.dtype,
+        "data": "synthetic (seeded N(0,1) K/V/Q, seeded rollout graph)",
+        "config": {"workload": wl.name, "branches": g.num_branches, "query_rows": R,
+                   "n_query": args.n_query, "segments": g.num_segments,
+                   "unique_tokens": g.unique_tokens(), "visible_token_pairs": vis,
+                   "q_heads": Hq, "kv_heads": wl.num_kv_heads, "head_dim": D,
+                   "page_tokens": 16, "chunk_pages": info.chunk_pages},
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": MFMA_BF16_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": achieved / MFMA_BF16_PEAK_TFLOPS,
+                     "traffic": traffic},
+        "kernel_ms": {"scheduler": sched_ms, "attention": attn_ms, "merge": merge_ms},
+        "attention_flops": flops,
+        "unique_kv_bytes": ukv,
+        "unique_kv_hbm_frac": ukv / (attn_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+    }
+    plan.close()
+    del q, pool, out, lse
+    torch.cuda.empty_cache()
+    if args.calibrate_copy:
+        calibrate_copy(torch, dev)
+    if args.cpu_sample > 0:
+        n = min(args.cpu_sample, 1024)
+        log(f"timing the CPU oracle on {n} query rows")
+        res["cpu_baseline"] = cpu_baseline_extend(wl, n)
+    print(json.dumps(res), flush=True)
+
+
+def run_append(args, torch, G, W):
+    """One decode step's new K/V: the token of every branch of the merged-DAG rollout, stored
+    at the next slot of its newest segment (a page of its own per branch)."""
+    import numpy as np
+    wl = W.config3_merged_dag()
+    g = wl.graph
+    B, Hkv, D = g.num_branches, wl.num_kv_heads, wl.head_dim
+    dev = torch.device("cuda:0")
+    pool = wl.pool.to(dev)
+    words = np.empty(B, dtype=np.int32)
+    for b in range(B):
+        s = int(g.path(b)[-1])
+        t = int(g.seg_len[s]) % 16            # the slot after the segment's last token
+        words[b] = int(g.seg_pages[g.seg_page_offsets[s + 1] - 1]) * 16 + t if t else -1
+    keep = words >= 0
+    gen = torch.Generator().manual_seed(7)
+    kn = torch.randn((B, Hkv, D), generator=gen).to(torch.bfloat16).to(dev)
+    vn = torch.randn((B, Hkv, D), generator=gen).to(torch.bfloat16).to(dev)
+    wd = torch.from_numpy(words).to(dev)
+    params = G.make_params(wl.num_q_heads, Hkv, D, g.num_pages, "bf16")
+    for _ in range(args.warmup):
+        G.kv_append(pool, kn, vn, wd, params)
+    torch.cuda.synchronize()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    for _ in range(args.steps):
+        G.kv_append(pool, kn, vn, wd, params)
+    ev1.record()
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / args.steps
+    n = int(keep.sum())
+    moved = n * Hkv * 2 * D * 2 * 2                 # read + written
+    achieved = moved / (ms * 1e-3) / 1e9
+    res = {
+        "metric": "tokens/s stored per K/V append call; % of HBM roofline on bytes moved",
+        "value": n / (ms * 1e-3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "one decode step of the merged-DAG rollout (1024 branches, "
+                               "28/4/128): one new token per branch", "tokens": n,
+                   "padded_words": int(B - n)},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None},
+    }
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -77,6 +260,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="c3",
                     choices=["c1", "c2", "c3", "c4", "c5chain", "c5graph"])
+    ap.add_argument("--op", default="decode", choices=["decode", "extend", "append"])
+    ap.add_argument("--n-query", type=int, default=16,
+                    help="query tokens per branch for --op extend")
     ap.add_argument("--cpu-sample", type=int, default=1024,
                     help="branches the CPU oracle is timed on (0 skips it)")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -94,6 +280,10 @@ def main():
     from paper_2606_18954_amd import graphattn as G
     from paper_2606_18954_amd import workloads as W
 
+    if args.op == "extend":
+        return run_extend(args, torch, G, W)
+    if args.op == "append":
+        return run_append(args, torch, G, W)
     t0 = time.time()
     wl = W.CONFIGS[args.config]()
     g = wl.graph
@@ -167,15 +357,7 @@ def main():
     del q, pool, out, lse
     torch.cuda.empty_cache()
     if args.calibrate_copy:
-        n = 1 << 29                                   # 1 GiB of bf16 read, 1 GiB written
-        a = torch.ones(n, dtype=torch.bfloat16, device=dev)
-        b = torch.empty_like(a)
-        for _ in range(3):
-            torch.mul(a, 1.0, out=b)
-        torch.cuda.synchronize()
-        log("copy calibration: 3 launches of a 1 GiB elementwise copy")
-        del a, b
-        torch.cuda.empty_cache()
+        calibrate_copy(torch, dev)
     if args.cpu_sample > 0:
         log(f"timing the CPU oracle on {args.cpu_sample} branches")
         res["cpu_baseline"] = cpu_baseline(wl, args.cpu_sample)

@@ -306,7 +306,7 @@ struct Layout {
 enum {
   L_SEG_LEN, L_SEG_PAGE_OFF, L_SEG_PAGES, L_PATH_OFF, L_PATH_SEGS, L_SEG_CAUSAL,  // uploaded
   L_GRP_CNT, L_GRP_FILL, L_GRP_OFF, L_GRP_TMP, L_GRP_BR, L_ENTRY_BR, L_ENTRY_RANK, L_SEG_NCH,
-  L_SEG_ITEM_OFF, L_SEG_PROW_OFF, L_SEG_ORDER, L_ORDER_ITEM_OFF, L_ITEMS, L_DESC, L_COUNTERS, L_ENTRY_PART, L_BPART_OFF, L_BPART,
+  L_SEG_ITEM_OFF, L_SEG_PROW_OFF, L_SEG_ORDER, L_ORDER_ITEM_OFF, L_ITEMS, L_DESC, L_COUNTERS, L_ENTRY_PART, L_BPART_OFF, L_BPART, L_BLK_SUM,
   L_PO, L_PLSE, L_COUNT
 };
 
@@ -338,6 +338,7 @@ Layout layout(const Sizes& z, const ga_params& p) {
   sz[L_ENTRY_PART] = sizeof(int64_t) * z.E;
   sz[L_BPART_OFF] = sizeof(int64_t) * (z.B + 1);
   sz[L_BPART] = sizeof(int32_t) * z.prows;
+  sz[L_BLK_SUM] = sizeof(int64_t) * ((z.E + 1023) / 1024 + 1);
   // Partials: fp16 values + (lambda, scale) for bf16 inputs, fp32 values + lambda for fp32.
   const bool f16_parts = p.dtype == GA_BF16;
   sz[L_PO] = (f16_parts ? 2 : 4) * (size_t)z.prows * p.num_q_heads * p.head_dim;
@@ -387,6 +388,7 @@ void bind(ga_plan* pl, const Layout& L) {
   pl->sc.entry_part = reinterpret_cast<int64_t*>(d + L.off[L_ENTRY_PART]);
   pl->sc.bpart_off = reinterpret_cast<int64_t*>(d + L.off[L_BPART_OFF]);
   pl->sc.bpart = reinterpret_cast<int32_t*>(d + L.off[L_BPART]);
+  pl->sc.blk_sum = reinterpret_cast<int64_t*>(d + L.off[L_BLK_SUM]);
   pl->po = d + L.off[L_PO];
   pl->plse = reinterpret_cast<float*>(d + L.off[L_PLSE]);
 }

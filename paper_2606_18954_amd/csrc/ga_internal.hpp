@@ -71,6 +71,7 @@ struct DevSchedule {
   int64_t* entry_part;     // [E]   first slot of each path entry in the branch partial lists
   int64_t* bpart_off;      // [B+1] CSR offsets of each branch's partial rows
   int32_t* bpart;          // [partial rows] partial rows of each branch: path order, then chunk
+  int64_t* blk_sum;        // [ceil(E / 1024)] per-block totals of the entry scan
 };
 
 // Partial rows (one per partial row and q-head), in one of two formats:

@@ -194,30 +194,62 @@ __global__ __launch_bounds__(1024) void k_scan(DevGraph g, DevSchedule sc, int32
 
 // Exclusive scan over path entries of their chunk counts (one 1024-thread workgroup): the slot
 // of each entry's first partial in the flat per-branch lists, and the branch CSR offsets.
-__device__ void scan_entries(const DevGraph& g, const DevSchedule& sc, int64_t (*sh)[1024]) {
-  const int t = threadIdx.x;
-  const int E = g.E;
-  const int per = (E + 1023) / 1024;
-  const int e0 = min(E, t * per), e1 = min(E, e0 + per);
-  int64_t a = 0;
-  for (int e = e0; e < e1; ++e) a += sc.seg_nchunk[g.path_segs[e]];
+// Exclusive scan of the partial rows of every path entry (its segment's chunk count), in entry
+// order, over many workgroups: k_entry_sums totals each block of kScanBlock entries,
+// k_entry_scan gives each block the sum of the blocks before it and scans inside the block, and
+// k_bpart_off reads each branch's first slot.  All loads are coalesced.
+constexpr int kScanBlock = 1024;
+
+__device__ __forceinline__ int64_t block_sum_1024(int64_t v, int64_t* red) {
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  if (lane == 0) red[w] = v;
   __syncthreads();
-  sh[0][t] = a;
+  int64_t tot = 0;
+  for (int i = 0; i < kScanBlock / 64; ++i) tot += red[i];
   __syncthreads();
-  for (int off = 1; off < 1024; off <<= 1) {
-    const int64_t x = t >= off ? sh[0][t - off] : 0;
-    __syncthreads();
-    sh[0][t] += x;
-    __syncthreads();
+  return tot;
+}
+
+__global__ __launch_bounds__(kScanBlock) void k_entry_sums(DevGraph g, DevSchedule sc) {
+  __shared__ int64_t red[kScanBlock / 64];
+  const int64_t e = (int64_t)blockIdx.x * kScanBlock + threadIdx.x;
+  const int64_t v = e < g.E ? sc.seg_nchunk[g.path_segs[e]] : 0;
+  const int64_t tot = block_sum_1024(v, red);
+  if (threadIdx.x == 0) sc.blk_sum[blockIdx.x] = tot;
+}
+
+__global__ __launch_bounds__(kScanBlock) void k_entry_scan(DevGraph g, DevSchedule sc) {
+  __shared__ int64_t red[kScanBlock / 64];
+  __shared__ int64_t wsum[kScanBlock / 64];
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  // Offset of this block: the sum of the block totals before it.
+  int64_t pre = 0;
+  for (int k = t; k < (int)blockIdx.x; k += kScanBlock) pre += sc.blk_sum[k];
+  const int64_t base = block_sum_1024(pre, red);
+  const int64_t e = (int64_t)blockIdx.x * kScanBlock + t;
+  const int64_t v = e < g.E ? sc.seg_nchunk[g.path_segs[e]] : 0;
+  int64_t x = v;                                   // inclusive scan inside the wave
+  for (int o = 1; o < 64; o <<= 1) {
+    const int64_t y = __shfl_up(x, o);
+    if (lane >= o) x += y;
   }
-  int64_t r = t ? sh[0][t - 1] : 0;
-  for (int e = e0; e < e1; ++e) {
-    sc.entry_part[e] = r;
-    r += sc.seg_nchunk[g.path_segs[e]];
-  }
+  if (lane == 63) wsum[w] = x;
   __syncthreads();
-  for (int b = t; b <= g.B; b += 1024)
-    sc.bpart_off[b] = b < g.B ? sc.entry_part[g.path_off[b]] : sh[0][1023];
+  int64_t before = 0;
+  for (int i = 0; i < w; ++i) before += wsum[i];
+  if (e < g.E) sc.entry_part[e] = base + before + x - v;
+}
+
+__global__ void k_bpart_off(DevGraph g, DevSchedule sc) {
+  const int64_t b = (int64_t)blockIdx.x * kT + threadIdx.x;
+  if (b > g.B) return;
+  if (b < g.B) {
+    sc.bpart_off[b] = sc.entry_part[g.path_off[b]];
+  } else {
+    sc.bpart_off[b] =
+        g.E > 0 ? sc.entry_part[g.E - 1] + sc.seg_nchunk[g.path_segs[g.E - 1]] : 0;
+  }
 }
 
 // Descriptor causal word of the chunk of segment s that starts at page p0.
@@ -234,11 +266,6 @@ __device__ __forceinline__ void write_entry_parts(const DevGraph& g, const DevSc
   const int64_t base = sc.seg_prow_off[s] + rank;
   const int64_t slot = sc.entry_part[e];
   for (int c = 0; c < nch; ++c) sc.bpart[slot + c] = (int32_t)(base + (int64_t)c * cnt);
-}
-
-__global__ __launch_bounds__(1024) void k_scan_entries(DevGraph g, DevSchedule sc) {
-  __shared__ int64_t sh[1][1024];
-  scan_entries(g, sc, sh);
 }
 
 // Emits the work items of segment s at work-list offset w (chunk-major, then row block): the
@@ -635,7 +662,12 @@ hipError_t launch_schedule(const DevGraph& g, const DevSchedule& sc, int32_t gro
   if (g.E > 0)
     hipLaunchKernelGGL(k_count, dim3(blocks(g.E)), dim3(kT), 0, stream, g, sc);
   hipLaunchKernelGGL(k_scan, dim3(1), dim3(1024), 0, stream, g, sc, group, chunk_pages);
-  hipLaunchKernelGGL(k_scan_entries, dim3(1), dim3(1024), 0, stream, g, sc);
+  const int64_t sblocks = ((int64_t)g.E + kScanBlock - 1) / kScanBlock;
+  if (sblocks > 0) {
+    hipLaunchKernelGGL(k_entry_sums, dim3((unsigned)sblocks), dim3(kScanBlock), 0, stream, g, sc);
+    hipLaunchKernelGGL(k_entry_scan, dim3((unsigned)sblocks), dim3(kScanBlock), 0, stream, g, sc);
+  }
+  hipLaunchKernelGGL(k_bpart_off, dim3(blocks((int64_t)g.B + 1)), dim3(kT), 0, stream, g, sc);
   if (g.E > 0)
     hipLaunchKernelGGL(k_scatter, dim3(blocks(g.E)), dim3(kT), 0, stream, g, sc);
   const int64_t n = g.E > g.S ? g.E : g.S;

@@ -75,11 +75,17 @@ struct Cfg {
 // holds the LDS base; the kernel keeps no other value in M0.  The copies are non-temporal (nt):
 // every K/V byte is read once per step, and streaming it through the caches at normal priority
 // would evict the partial rows this kernel writes and the merge kernel reads back.
+// The multi-query (causal) variant copies with the normal cache policy instead: there the row
+// blocks of one chunk read the same pages, and the later ones find them in the caches.
 // (tests/test_isa_invariants.py checks in the built assembly that every M0 write is one of these.)
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
 __device__ __forceinline__ void dma16(unsigned off, const void* base, unsigned lds_base) {
   asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1 nt"
+               :: "v"(off), "s"(base), "s"(lds_base) : "memory", "m0");
+}
+__device__ __forceinline__ void dma16_cached(unsigned off, const void* base, unsigned lds_base) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
                :: "v"(off), "s"(base), "s"(lds_base) : "memory", "m0");
 }
 #pragma clang diagnostic pop
@@ -478,8 +484,12 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
             const int pid = pw[pis] & kPageIdMask;
             const int vm1 = (int)((unsigned)pw[pis] >> kPageValidShift);
             const unsigned char* base = pool_h + (int64_t)pid * blk_stride;
-            dma16(min(c_tok[i], vm1) * C::ROW + c_rest[i], base,
-                  __builtin_amdgcn_readfirstlane(dst + i * 4096));
+            if constexpr (CAUSAL)
+              dma16_cached(min(c_tok[i], vm1) * C::ROW + c_rest[i], base,
+                     __builtin_amdgcn_readfirstlane(dst + i * 4096));
+            else
+              dma16(min(c_tok[i], vm1) * C::ROW + c_rest[i], base,
+                    __builtin_amdgcn_readfirstlane(dst + i * 4096));
           }
         }
       };

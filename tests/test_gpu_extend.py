@@ -229,3 +229,31 @@ def test_append_then_extend():
     oo, ol = O.extend(wl.q_bits(), pool_ref, g.seg_len, g.seg_page_offsets, g.seg_pages,
                       g.path_offsets, g.path_segs, new, 28, 4, 128, "bf16")
     compare("append then extend", out.double().cpu().numpy(), lse.double().cpu().numpy(), oo, ol)
+
+
+def test_kv_append_replayed_from_a_graph():
+    """Append calls captured in a HIP graph: each replay (after eager work that restores the
+    pool) must store exactly what the eager call stores."""
+    require_gpu()
+    Np, n, Hkv, D = 24, 200, 4, 128
+    pool, k, v = _pool_and_rows(Np, Hkv, D, "bf16", n, 41)
+    words = np.random.default_rng(41).choice(Np * 16, n, replace=False).astype(np.int32)
+    ref = O.kv_append(_raw(pool), _raw(k), _raw(v), words)
+    p = G.make_params(Hkv, Hkv, D, Np, "bf16")
+    pg, kg, vg = pool.cuda(), k.cuda(), v.cuda()
+    wd = torch.from_numpy(words).cuda()
+    graph = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(graph, stream=side):
+            G.kv_append(pg, kg, vg, wd, p)
+    torch.cuda.current_stream().wait_stream(side)
+    orig = pool.cuda()
+    for rep in range(3):
+        pg.copy_(orig)                       # eager work between replays
+        torch.cuda.synchronize()
+        assert not np.array_equal(_raw(pg.cpu()), ref)
+        graph.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(_raw(pg.cpu()), ref), rep

@@ -20,6 +20,10 @@ What it computes (the passages it follows):
   z_j = scale * <q, k_j>, p = softmax(z), out = sum_j p_j v_j, lse = ln sum_j exp(z_j).
 * Grouped-query attention: q-head h reads kv-head floor(h / (Hq / Hkv)).
 
+* Equivalence detection (Sec. 3.2; Alg. S.1, Stage 1): states of one prompt's graph that are
+  not ancestor and descendant are compared by the cosine of their embeddings; pairs at or above
+  kappa are joined by union-find into classes Q(v); the graph suffix C_g(u) adds the direct
+  successors of the other class members that lie deeper than u.
 * Extend: the queries of a branch are the newest tokens of its last path segment, each
   attending causally (Alg. S.1, Stage 1: a continuation is predicted token by token from
   prefix(u)); append and copy store tokens into page slots and move them between slots.
@@ -30,12 +34,16 @@ no causal mask (a single query at the end of the path); scale = 1/sqrt(D) unless
 lse is the natural log; segment order along a path does not change the result.
 For extend: the query segment is the path's last entry, a query sees itself, and a query at
 position P of that segment sees exactly its tokens 0 .. P. A slot word is page * 16 + slot.
+For equivalence detection: ancestry is that of the generation tree (p(v)); a class is labelled
+by its smallest state id; pairs of different prompts are never compared.
 
 Parity status: every function below is pinned by CPU tests against brute force, a library
 routine on a special case, closed forms and invariants (softmax rows sum to 1, merge
 associativity, the K=0 tag closed form, the single-token case); extend against torch's causal
 SDPA and a token-by-token walk, append by reading the stored segment back, copy by splitting a
-segment inside a page without changing attention.
+segment inside a page without changing attention; equivalence classes against scipy's connected
+components of an independently built link graph, threshold extremes and the ancestor rule;
+the graph suffix against a hand-derived fixture and the no-merge identity.
 """
 from __future__ import annotations
 
@@ -332,3 +340,132 @@ def kv_copy(pool_raw: np.ndarray, src_words, dst_words) -> np.ndarray:
         dp, ds = divmod(d, PAGE_TOKENS)
         out[dp, :, :, ds, :] = pool_raw[sp, :, :, ss, :]
     return out
+
+
+# ----------------------------------------------------------------------------------------------
+# Equivalence detection over rollout states (graph construction)
+# ----------------------------------------------------------------------------------------------
+
+def state_depths(parent) -> np.ndarray:
+    """Depth of every state in its prompt's generation tree (a prompt's root has depth 0)."""
+    par = [int(x) for x in parent]
+    depth = np.zeros(len(par), dtype=np.int64)
+    for v, p in enumerate(par):
+        depth[v] = 0 if p < 0 else depth[p] + 1
+    return depth
+
+
+def is_ancestor(parent, u: int, v: int) -> bool:
+    """True when u lies on v's generation path (u == v counts): walk v's predecessors."""
+    x = int(v)
+    while x >= 0:
+        if x == u:
+            return True
+        x = int(parent[x])
+    return False
+
+
+def prompts_of(parent) -> List[List[int]]:
+    """The states of each prompt's graph (grouped by the root their generation path starts at),
+    in ascending id order."""
+    root = {}
+    groups: dict = {}
+    for v in range(len(parent)):
+        x = v
+        while int(parent[x]) >= 0:
+            x = int(parent[x])
+        root[v] = x
+        groups.setdefault(x, []).append(v)
+    return [groups[r] for r in sorted(groups)]
+
+
+def compared_pairs(parent) -> List[Tuple[int, int]]:
+    """The pairs the method compares (Sec. 3.2): two states of the same prompt's graph, neither
+    an ancestor of the other (comparing a state with its own ancestors could close a cycle)."""
+    out = []
+    for ids in prompts_of(parent):
+        for i, u in enumerate(ids):
+            for v in ids[i + 1:]:
+                if not is_ancestor(parent, u, v) and not is_ancestor(parent, v, u):
+                    out.append((u, v))
+    return out
+
+
+def similarity_matrix(z_raw: np.ndarray, dtype: str, ids: Sequence[int]) -> np.ndarray:
+    """sim(u, v) = z_u . z_v / (|z_u| |z_v|) for all u, v in ids, float64 on the stored values
+    (one matrix product of the row-normalised embeddings)."""
+    z = to_f64(z_raw[np.asarray(ids, dtype=np.int64)], dtype)
+    zn = z / np.sqrt((z * z).sum(axis=1, keepdims=True))
+    return zn @ zn.T
+
+
+def cosine(z_raw: np.ndarray, dtype: str, u: int, v: int) -> float:
+    """sim(u, v) of one pair."""
+    return float(similarity_matrix(z_raw, dtype, [u, v])[0, 1])
+
+
+def _compared_similarities(z_raw, dtype, parent):
+    for ids in prompts_of(parent):
+        pos = {v: i for i, v in enumerate(ids)}
+        sim = similarity_matrix(z_raw, dtype, ids)
+        for i, u in enumerate(ids):
+            for v in ids[i + 1:]:
+                if not is_ancestor(parent, u, v) and not is_ancestor(parent, v, u):
+                    yield u, v, float(sim[i, pos[v]])
+
+
+def equivalence_classes(z_raw: np.ndarray, dtype: str, parent, kappa: float) -> np.ndarray:
+    """Class label of every state: the smallest state id of its equivalence class Q(v).
+
+    Compared pairs with sim(u, v) >= kappa are linked by union-find (Sec. 3.2; Alg. S.1,
+    Stage 1), so the classes are the connected components of those links. Plain union-find
+    with the smaller root kept as the representative, so a root is its class's minimum.
+    """
+    N = len(parent)
+    rep = list(range(N))
+
+    def find(x):
+        while rep[x] != x:
+            x = rep[x]
+        return x
+
+    for u, v, sim in _compared_similarities(z_raw, dtype, parent):
+        if sim >= kappa:
+            ru, rv = find(u), find(v)
+            if ru != rv:
+                rep[max(ru, rv)] = min(ru, rv)
+    return np.array([find(v) for v in range(N)], dtype=np.int32)
+
+
+def similarity_margin(z_raw: np.ndarray, dtype: str, parent, kappa: float) -> float:
+    """Smallest |sim(u, v) - kappa| over the compared pairs (inf if there are none): how far
+    the inputs keep every decision from the threshold."""
+    m = math.inf
+    for _, _, sim in _compared_similarities(z_raw, dtype, parent):
+        m = min(m, abs(sim - kappa))
+    return m
+
+
+def graph_suffix(labels, parent) -> Tuple[np.ndarray, np.ndarray]:
+    """Graph suffix C_g(u) of every state as CSR (offsets [N+1], ascending state ids).
+
+    C_g(u) = C(u) together with the direct successors of the other members of Q(u) (Sec. 3.2,
+    the equation of the graph suffix); a shared successor must lie deeper than u, which keeps
+    the graph acyclic (the virtual merge only adds edges that point deeper).
+    """
+    N = len(parent)
+    depth = state_depths(parent)
+    out: List[List[int]] = []
+    for u in range(N):
+        cu = []
+        for c in range(N):
+            p = int(parent[c])
+            if p < 0:
+                continue
+            if p == u or (labels[p] == labels[u] and depth[c] > depth[u]):
+                cu.append(c)
+        out.append(cu)
+    offs = np.zeros(N + 1, dtype=np.int64)
+    for u in range(N):
+        offs[u + 1] = offs[u] + len(out[u])
+    return offs, np.array([c for cu in out for c in cu], dtype=np.int32)

@@ -519,6 +519,96 @@ def config3_extend(prompts: int = 64, n_query: int = 16, slack_pages: int = 0,
                                 [n_query] * len(paths), 28, 4, 128, "bf16", seed, poison)
 
 
+# ----------------------------------------------------------------------------------------------
+# Rollout states and their embeddings (equivalence detection)
+# ----------------------------------------------------------------------------------------------
+
+@dataclasses.dataclass
+class StateWorkload:
+    """States of a batch of prompts' rollout graphs: generation predecessors (each prompt's
+    states consecutive, root first, p(v) < v) and one embedding per state."""
+    name: str
+    parent: np.ndarray            # int32 [N], -1 for a prompt's root
+    z: torch.Tensor               # CPU [N][dim] bfloat16
+    kappa: float
+    seed: int
+
+    def z_bits(self) -> np.ndarray:
+        return self.z.view(torch.int16).numpy().view(np.uint16)
+
+
+def state_forest(prompts: int, schedule: Sequence[int]) -> np.ndarray:
+    """Full trees with the per-layer branching `schedule` (each state at depth h-1 samples
+    schedule[h-1] continuations), numbered breadth first inside each prompt."""
+    parent: List[int] = []
+    for _ in range(prompts):
+        root = len(parent)
+        parent.append(-1)
+        level = [root]
+        for b in schedule:
+            nxt = []
+            for u in level:
+                for _ in range(b):
+                    nxt.append(len(parent))
+                    parent.append(u)
+            level = nxt
+    return np.asarray(parent, dtype=np.int32)
+
+
+def draw_state_embeddings(parent: np.ndarray, dim: int, seed: int, share: float = 3.0,
+                          stay: float = 0.1, sigma: float = 0.2) -> torch.Tensor:
+    """Clustered synthetic embeddings, bf16 [N][dim].
+
+    Within a prompt, the n_h states of depth h >= 1 each draw a semantic centre from a pool of
+    ceil(share * n_h) centres, except that with probability `stay` a state of depth >= 2 keeps
+    its predecessor's centre (a step that does not change the summarised state); z_v is its
+    centre plus sigma-scaled noise, all components N(0, 1).  States with one centre have
+    cosine near 1 / (1 + sigma^2) (0.96 at sigma = 0.2), others near 0.
+    """
+    rng = np.random.default_rng(seed)
+    N = len(parent)
+    depth = np.zeros(N, dtype=np.int64)
+    prompt = np.zeros(N, dtype=np.int64)
+    for v in range(N):
+        p = int(parent[v])
+        depth[v] = 0 if p < 0 else depth[p] + 1
+        prompt[v] = v if p < 0 else prompt[p]
+    groups: Dict = {}
+    for v in range(N):
+        groups.setdefault((int(prompt[v]), int(depth[v])), []).append(v)
+    center = np.zeros(N, dtype=np.int64)
+    ncent = 0
+    for (_, h), ids in groups.items():          # insertion order: by prompt, then depth
+        if h == 0:
+            center[ids[0]] = ncent
+            ncent += 1
+            continue
+        pool = max(1, int(math.ceil(share * len(ids))))
+        pick = rng.integers(0, pool, size=len(ids))
+        keep = rng.random(len(ids)) < stay
+        for u, k, kp in zip(ids, pick, keep):
+            center[u] = center[parent[u]] if (kp and h > 1) else ncent + int(k)
+        ncent += pool
+    gen = torch.Generator(device="cpu")
+    gen.manual_seed(_chunk_seed(seed, 0))
+    centres = torch.randn((ncent, dim), generator=gen, dtype=torch.float32)
+    gen.manual_seed(_chunk_seed(seed, 1))
+    noise = torch.randn((N, dim), generator=gen, dtype=torch.float32)
+    z = centres[torch.from_numpy(center)] + sigma * noise
+    return _bf16_rne(z)
+
+
+def equiv_batch(prompts: int = 512, schedule: Sequence[int] = (4, 5, 3, 2), dim: int = 4096,
+                kappa: float = 0.92, seed: Optional[int] = None) -> StateWorkload:
+    """One training batch's states: `prompts` rollout graphs with branching schedule T (205
+    states per prompt at T = {4, 5, 3, 2}), embeddings of width `dim`, threshold kappa."""
+    seed = SEED_BASE + 21 if seed is None else seed
+    parent = state_forest(prompts, schedule)
+    z = draw_state_embeddings(parent, dim, seed)
+    return StateWorkload(f"rollout states ({prompts} prompts, T={tuple(schedule)}, "
+                         f"{len(parent)} states, dim {dim})", parent, z, kappa, seed)
+
+
 CONFIGS = {
     "c1": config1_tiny,
     "c2": config2_tree,

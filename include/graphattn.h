@@ -223,6 +223,40 @@ ga_status graphattn_kv_copy(void* kv_page_pool, const int32_t* src_slot_words,
                             const int32_t* dst_slot_words, int32_t num_tokens,
                             const ga_params* params, void* hip_stream);
 
+/* Rollout states for equivalence detection: the generation tree of every prompt in a batch.
+ * parent[v] = p(v), the state v was generated from (-1 for a prompt's root).  Each prompt's
+ * states are consecutive, its root first, and p(v) < v (GA_EINVAL otherwise).  Host memory. */
+typedef struct {
+  int32_t num_states;
+  const int32_t* parent;   /* [N] */
+} ga_state_forest;
+
+/* Equivalence classes of rollout states (Sec. 3.2 "Graph Construction"; Alg. S.1, Stage 1).
+ * Two states of the same prompt that are neither ancestor nor descendant of each other are
+ * compared by the cosine of their embeddings; pairs with cosine >= kappa are joined by
+ * union-find, so the classes Q(v) are the connected components of those links.  A state with a
+ * zero embedding is never joined.
+ *   embeddings  [N][dim] device, bf16 (dtype = GA_BF16; GA_EUNSUPPORTED otherwise), 16-byte
+ *               aligned; dim a positive multiple of 64 (GA_EUNSUPPORTED otherwise)
+ *   labels      [N] device int32, written: the smallest state id of each state's class
+ * The cosine is computed from fp32 sums of the bf16 products (error below 2.5e-4 at
+ * dim = 4096), so a pair within that distance of kappa may be decided either way.  Host
+ * validation first; asynchronous on hip_stream. */
+ga_status graphattn_equivalence_classes(const void* embeddings, int32_t dim, int32_t dtype,
+                                        const ga_state_forest* forest, float kappa,
+                                        int32_t* labels, void* hip_stream);
+
+/* Graph suffix (Sec. 3.2, the equation of C_g): C_g(u) = u's direct successors plus those of
+ * the other members of Q(u) that lie deeper than u (shared edges only point deeper, so the
+ * graph stays acyclic).  labels [N] device int32 (as written by graphattn_equivalence_classes).
+ * Output as CSR: suffix_offsets [N + 1] device int64, suffix_states [*total] device int32,
+ * ascending state ids per state.  The call synchronises hip_stream to learn the size: *total
+ * (host) receives it; if it exceeds capacity the call returns GA_ERANGE and writes neither
+ * output array (call again with a larger buffer). */
+ga_status graphattn_graph_suffix(const int32_t* labels, const ga_state_forest* forest,
+                                 int64_t* suffix_offsets, int32_t* suffix_states,
+                                 int64_t capacity, int64_t* total, void* hip_stream);
+
 /* Release the plan and its device workspace (waits for work still using it). */
 void graphattn_plan_destroy(ga_plan* plan);
 

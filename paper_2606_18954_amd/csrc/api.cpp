@@ -77,6 +77,13 @@ struct Sizes {
 
 }  // namespace
 
+namespace ga {
+// Error reporting for the other host source files (equiv_api.cpp).
+ga_status host_fail(ga_status st, const char* msg) { return fail(st, "%s", msg); }
+ga_status host_hip_fail(hipError_t e, const char* what) { return hip_fail(e, what); }
+void host_clear_error() { g_err.clear(); }
+}  // namespace ga
+
 struct ga_plan {
   ga_params p{};
   Sizes z;

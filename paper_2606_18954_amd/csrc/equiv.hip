@@ -1,0 +1,248 @@
+// Equivalence detection over rollout states and the graph suffix (Sec. 3.2, "Graph
+// Construction"; Alg. S.1, Stage 1).
+//
+// Two states of one prompt's graph that are neither ancestor nor descendant of each other are
+// compared by the cosine of their embeddings; pairs at or above kappa are linked, and the
+// classes Q(v) are the connected components of the links.  The similarity is a dense
+// contraction over the embedding width, so it runs on bf16 MFMA: one workgroup per 64 x 64
+// tile (row states i0.., column states j0.., both of one prompt, i0 <= j0), the width streamed
+// through LDS in 64-wide stages, each wave holding a 32 x 32 quadrant as 2 x 2 MFMA tiles.  The
+// epilogue tests every pair of the quadrant (u < v, same prompt, not ancestor-related by the
+// Euler intervals of the generation tree, z_u.z_v >= kappa |z_u| |z_v|) and links the qualifying
+// ones at once with a lock-free union-find on a global parent array: the larger root is hooked
+// under the smaller with a compare-and-swap, so every class's final root is its smallest state
+// (a deterministic label, whatever order the links land in).
+//
+// Graph suffix: C_g(u) is u's direct successors plus those of the other members of Q(u) that lie
+// deeper than u (shared edges only point deeper, so the graph stays acyclic).  One thread per
+// state counts them over its prompt's states, a scan gives the CSR offsets, and a second pass
+// writes them in ascending state order.
+#include "ga_internal.hpp"
+
+namespace ga {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kTile = 64;       // states per tile side
+constexpr int kKC = 64;         // embedding components per LDS stage (128 bytes per state row)
+
+__device__ __forceinline__ int load_rep(const int* rep, int x) {
+  return __hip_atomic_load(rep + x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ int find_root(const int* rep, int x) {
+  int p = load_rep(rep, x);
+  while (p != x) {
+    x = p;
+    p = load_rep(rep, x);
+  }
+  return x;
+}
+
+// Links the classes of a and b: the larger root is hooked under the smaller one.  A failed
+// compare-and-swap means another link changed that root first; the roots are looked up again.
+__device__ void unite(int* rep, int a, int b) {
+  while (true) {
+    a = find_root(rep, a);
+    b = find_root(rep, b);
+    if (a == b) return;
+    if (a > b) {
+      const int t = a;
+      a = b;
+      b = t;
+    }
+    if (atomicCAS(rep + b, b, a) == b) return;
+  }
+}
+
+// Inverse norm of every embedding (NaN for a zero vector, which is then never linked) and the
+// union-find parent array reset to singletons.  One wave per state.
+__global__ __launch_bounds__(256) void k_norms(EquivArgs a) {
+  const int64_t w = ((int64_t)blockIdx.x * 256 + threadIdx.x) >> 6;
+  const int lane = threadIdx.x & 63;
+  if (w >= a.N) return;
+  const bf16x8* row = reinterpret_cast<const bf16x8*>(a.z + w * a.dim);
+  float s = 0.f;
+  for (int c = lane; c < a.dim / 8; c += 64) {
+    const bf16x8 v = row[c];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) s = fmaf((float)v[i], (float)v[i], s);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
+  if (lane == 0) {
+    a.inv_norm[w] = s > 0.f ? 1.f / sqrtf(s) : __builtin_nanf("");
+    a.rep[w] = (int)w;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_sim_union(EquivArgs a) {
+  __shared__ __align__(16) unsigned char sA[kTile * kKC * 2];
+  __shared__ __align__(16) unsigned char sB[kTile * kKC * 2];
+  const int4 it = a.items[blockIdx.x];        // (first row state, first column state, prompt end)
+  const int i0 = it.x, j0 = it.y, pend = it.z;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r16 = lane & 15, kg = lane >> 4;
+  const int wm = wave >> 1, wn = wave & 1;
+  // Global -> LDS: thread t moves 16-byte chunk t % 8 of state rows t / 8 and t / 8 + 32 of both
+  // tiles; chunks are XOR-permuted by row so the MFMA operand reads are conflict-free.
+  const int lr = tid >> 3, lc = tid & 7;
+  auto gload = [&](int s0, int r, int kc) {
+    const int s = s0 + r;
+    uint4 v = make_uint4(0u, 0u, 0u, 0u);
+    if (s < pend) v = *reinterpret_cast<const uint4*>(a.z + (int64_t)s * a.dim + kc * kKC + lc * 8);
+    return v;
+  };
+  auto lds_off = [](int row, int chunk) { return row * (kKC * 2) + ((chunk ^ (row & 7)) << 4); };
+  uint4 ra0 = gload(i0, lr, 0), ra1 = gload(i0, lr + 32, 0);
+  uint4 rb0 = gload(j0, lr, 0), rb1 = gload(j0, lr + 32, 0);
+  f32x4 acc[2][2];
+#pragma unroll
+  for (int x = 0; x < 2; ++x)
+#pragma unroll
+    for (int y = 0; y < 2; ++y) acc[x][y] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int nk = a.dim / kKC;
+  for (int kc = 0; kc < nk; ++kc) {
+    __syncthreads();                            // every wave is done with the previous stage
+    *reinterpret_cast<uint4*>(sA + lds_off(lr, lc)) = ra0;
+    *reinterpret_cast<uint4*>(sA + lds_off(lr + 32, lc)) = ra1;
+    *reinterpret_cast<uint4*>(sB + lds_off(lr, lc)) = rb0;
+    *reinterpret_cast<uint4*>(sB + lds_off(lr + 32, lc)) = rb1;
+    __syncthreads();
+    if (kc + 1 < nk) {                          // next stage's loads overlap this stage's MFMAs
+      ra0 = gload(i0, lr, kc + 1);
+      ra1 = gload(i0, lr + 32, kc + 1);
+      rb0 = gload(j0, lr, kc + 1);
+      rb1 = gload(j0, lr + 32, kc + 1);
+    }
+#pragma unroll
+    for (int ks = 0; ks < kKC / 32; ++ks) {
+      bf16x8 av[2], bv[2];
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        av[t] = *reinterpret_cast<const bf16x8*>(sA + lds_off(wm * 32 + t * 16 + r16, ks * 4 + kg));
+        bv[t] = *reinterpret_cast<const bf16x8*>(sB + lds_off(wn * 32 + t * 16 + r16, ks * 4 + kg));
+      }
+#pragma unroll
+      for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int y = 0; y < 2; ++y)
+          acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[x], bv[y], acc[x][y], 0, 0, 0);
+    }
+  }
+  // acc[x][y][i] = z_u . z_v with u the row state (4 kg + i of row tile x), v the column state
+  // (r16 of column tile y).
+#pragma unroll
+  for (int y = 0; y < 2; ++y) {
+    const int v = j0 + wn * 32 + y * 16 + r16;
+    if (v >= pend) continue;
+    const int tin_v = a.tin[v], tout_v = a.tout[v];
+    const float nv = a.inv_norm[v];
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int u = i0 + wm * 32 + x * 16 + 4 * kg + i;
+        if (u >= v) continue;
+        const int tin_u = a.tin[u], tout_u = a.tout[u];
+        const bool related = (tin_u <= tin_v && tin_v < tout_u) || (tin_v <= tin_u && tin_u < tout_v);
+        if (!related && acc[x][y][i] * a.inv_norm[u] * nv >= a.kappa) unite(a.rep, u, v);
+      }
+  }
+}
+
+// Final labels: every state's root (all links have landed: kernel boundary).
+__global__ void k_labels(EquivArgs a) {
+  const int64_t v = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (v >= a.N) return;
+  a.labels[v] = find_root(a.rep, (int)v);
+}
+
+// Graph suffix, pass 1 (count into cnt[u]) or pass 2 (write from off[u]).
+template <bool FILL>
+__global__ void k_suffix(SuffixArgs a) {
+  const int64_t u = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (u >= a.N) return;
+  const int lu = a.labels[u], du = a.depth[u];
+  int64_t k = FILL ? a.off[u] : 0;
+  for (int c = a.pstart[u]; c < a.pend[u]; ++c) {
+    const int p = a.parent[c];
+    if (p < 0) continue;
+    if (p == (int)u || (a.labels[p] == lu && a.depth[c] > du)) {
+      if (FILL) a.states[k] = c;
+      ++k;
+    }
+  }
+  if (!FILL) a.cnt[u] = k;
+}
+
+// Exclusive scan of cnt[0..N) into off[0..N] (off[N] = total) over many workgroups.
+__global__ __launch_bounds__(1024) void k_scan_sums(SuffixArgs a) {
+  __shared__ int64_t red[16];
+  const int64_t i = (int64_t)blockIdx.x * 1024 + threadIdx.x;
+  int64_t v = i < a.N ? a.cnt[i] : 0;
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int64_t t = 0;
+    for (int w = 0; w < 16; ++w) t += red[w];
+    a.blk[blockIdx.x] = t;
+  }
+}
+
+__global__ __launch_bounds__(1024) void k_scan_apply(SuffixArgs a) {
+  __shared__ int64_t red[16], wsum[16];
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  int64_t pre = 0;
+  for (int k = t; k < (int)blockIdx.x; k += 1024) pre += a.blk[k];
+  for (int o = 32; o > 0; o >>= 1) pre += __shfl_xor(pre, o);
+  if (lane == 0) red[w] = pre;
+  __syncthreads();
+  int64_t base = 0;
+  for (int k = 0; k < 16; ++k) base += red[k];
+  const int64_t i = (int64_t)blockIdx.x * 1024 + t;
+  const int64_t v = i < a.N ? a.cnt[i] : 0;
+  int64_t x = v;
+  for (int o = 1; o < 64; o <<= 1) {
+    const int64_t y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) wsum[w] = x;
+  __syncthreads();
+  int64_t before = 0;
+  for (int k = 0; k < w; ++k) before += wsum[k];
+  if (i < a.N) a.off[i] = base + before + x - v;
+  if (i == a.N - 1) a.off[a.N] = base + before + x;
+}
+
+}  // namespace
+
+hipError_t launch_equivalence(const EquivArgs& a, hipStream_t stream) {
+  if (a.N == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_norms, dim3((unsigned)((a.N * 64 + 255) / 256)), dim3(256), 0, stream, a);
+  if (a.n_items > 0)
+    hipLaunchKernelGGL(k_sim_union, dim3((unsigned)a.n_items), dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(k_labels, dim3((unsigned)((a.N + 255) / 256)), dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_suffix_count(const SuffixArgs& a, hipStream_t stream) {
+  if (a.N == 0) return hipSuccess;
+  const unsigned g = (unsigned)((a.N + 255) / 256);
+  hipLaunchKernelGGL(k_suffix<false>, dim3(g), dim3(256), 0, stream, a);
+  const unsigned sb = (unsigned)((a.N + 1023) / 1024);
+  hipLaunchKernelGGL(k_scan_sums, dim3(sb), dim3(1024), 0, stream, a);
+  hipLaunchKernelGGL(k_scan_apply, dim3(sb), dim3(1024), 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_suffix_fill(const SuffixArgs& a, hipStream_t stream) {
+  if (a.N == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_suffix<true>, dim3((unsigned)((a.N + 255) / 256)), dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace ga

@@ -120,6 +120,34 @@ struct KvWriteArgs {
   int32_t n, Hkv, row_bytes;
 };
 
+// Equivalence detection (equiv.hip).  z [N][dim] bf16 bits; items: (first row state, first
+// column state, end of their prompt's states, unused) per 64 x 64 tile, row tile <= column tile.
+struct EquivArgs {
+  const unsigned short* z;
+  float* inv_norm;         // [N]
+  int* rep;                // [N]  union-find parents
+  const int32_t* tin;      // [N]  Euler interval of each state in its generation tree
+  const int32_t* tout;     // [N]
+  const int4* items;       // [n_items]
+  int32_t* labels;         // [N]  output: smallest state of the class
+  int64_t N, n_items;
+  int32_t dim;
+  float kappa;
+};
+
+struct SuffixArgs {
+  const int32_t* labels;   // [N]
+  const int32_t* parent;   // [N]
+  const int32_t* depth;    // [N]
+  const int32_t* pstart;   // [N]  first state of the state's prompt
+  const int32_t* pend;     // [N]  one past its last state
+  int64_t* cnt;            // [N]  |C_g(u)|
+  int64_t* off;            // [N + 1] CSR offsets
+  int64_t* blk;            // [ceil(N / 1024)] scan block totals
+  int32_t* states;         // [total] output
+  int64_t N;
+};
+
 // Launchers (each returns the launch status).
 hipError_t launch_schedule(const DevGraph& g, const DevSchedule& sc, int32_t group,
                            int32_t chunk_pages, int64_t max_items, hipStream_t stream);
@@ -128,6 +156,9 @@ hipError_t launch_seg_attn(const AttnArgs& a, int head_dim, bool bf16, bool caus
 hipError_t launch_merge(const MergeArgs& a, int head_dim, bool out_bf16, bool part_f16,
                         hipStream_t stream);
 hipError_t launch_kv_write(const KvWriteArgs& a, hipStream_t stream);
+hipError_t launch_equivalence(const EquivArgs& a, hipStream_t stream);
+hipError_t launch_suffix_count(const SuffixArgs& a, hipStream_t stream);
+hipError_t launch_suffix_fill(const SuffixArgs& a, hipStream_t stream);
 // Number of co-resident attention workgroups the persistent grid uses on this device.
 int seg_attn_grid(int head_dim, bool bf16, int num_cus);
 

@@ -57,6 +57,10 @@ class PlanInfo(ctypes.Structure):
                 ("num_query_rows", ctypes.c_int32)]
 
 
+class StateForest(ctypes.Structure):
+    _fields_ = [("num_states", ctypes.c_int32), ("parent", ctypes.POINTER(ctypes.c_int32))]
+
+
 class Profile(ctypes.Structure):
     _fields_ = [("schedules", ctypes.c_int32), ("runs", ctypes.c_int32),
                 ("sched_ms", ctypes.c_double), ("attn_ms", ctypes.c_double),
@@ -91,6 +95,11 @@ def load_library() -> ctypes.CDLL:
     lib.graphattn_kv_append.restype = ctypes.c_int
     lib.graphattn_kv_copy.argtypes = [vp, vp, vp, i32, P(Params), vp]
     lib.graphattn_kv_copy.restype = ctypes.c_int
+    lib.graphattn_equivalence_classes.argtypes = [vp, i32, i32, P(StateForest), ctypes.c_float,
+                                                  vp, vp]
+    lib.graphattn_equivalence_classes.restype = ctypes.c_int
+    lib.graphattn_graph_suffix.argtypes = [vp, P(StateForest), vp, vp, i64, P(i64), vp]
+    lib.graphattn_graph_suffix.restype = ctypes.c_int
     lib.graphattn_schedule.argtypes = [vp, vp]
     lib.graphattn_schedule.restype = ctypes.c_int
     lib.graphattn_run.argtypes = [vp, vp, vp, vp, vp, vp]
@@ -224,6 +233,53 @@ def kv_copy(pool, src_words, dst_words, params: Params, stream=None):
         raise ValueError("one source word per destination word")
     _check(lib.graphattn_kv_copy(_dev_ptr(pool), _dev_ptr(src_words), _dev_ptr(dst_words), n,
                                  ctypes.byref(params), _stream_handle(stream)))
+
+
+class HostForest:
+    """The states' generation predecessors as the C struct (keeps the array alive)."""
+
+    def __init__(self, parent):
+        self.parent = np.ascontiguousarray(parent, dtype=np.int32)
+        self.c = StateForest(len(self.parent), _ptr(self.parent, ctypes.c_int32))
+
+
+def equivalence_classes(z, forest: HostForest, kappa: float, labels=None, stream=None):
+    """graphattn_equivalence_classes: z [N, dim] bf16 (device); returns labels int32 [N]."""
+    import torch
+    lib = load_library()
+    N = forest.c.num_states
+    if z.dim() != 2 or z.shape[0] != N:
+        raise ValueError("one embedding row per state")
+    if labels is None:
+        labels = torch.empty(N, dtype=torch.int32, device=z.device)
+    _check(lib.graphattn_equivalence_classes(_dev_ptr(z), int(z.shape[1]),
+                                             GA_BF16 if z.dtype == torch.bfloat16 else GA_F32,
+                                             ctypes.byref(forest.c), float(kappa),
+                                             _dev_ptr(labels), _stream_handle(stream)))
+    return labels
+
+
+def graph_suffix(labels, forest: HostForest, capacity=None, stream=None):
+    """graphattn_graph_suffix: returns (offsets int64 [N + 1], states int32 [total]) on the
+    device; sized by a first call when capacity is not given."""
+    import torch
+    lib = load_library()
+    N = forest.c.num_states
+    total = ctypes.c_int64(0)
+    offs = torch.empty(N + 1, dtype=torch.int64, device=labels.device)
+    cap = int(capacity) if capacity is not None else 0
+    states = torch.empty(max(cap, 1), dtype=torch.int32, device=labels.device)
+    st = lib.graphattn_graph_suffix(_dev_ptr(labels), ctypes.byref(forest.c), _dev_ptr(offs),
+                                    _dev_ptr(states), cap, ctypes.byref(total),
+                                    _stream_handle(stream))
+    if st == GA_ERANGE and capacity is None:
+        cap = int(total.value)
+        states = torch.empty(max(cap, 1), dtype=torch.int32, device=labels.device)
+        st = lib.graphattn_graph_suffix(_dev_ptr(labels), ctypes.byref(forest.c), _dev_ptr(offs),
+                                        _dev_ptr(states), cap, ctypes.byref(total),
+                                        _stream_handle(stream))
+    _check(st)
+    return offs, states[:int(total.value)]
 
 
 class Plan:

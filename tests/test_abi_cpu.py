@@ -17,7 +17,8 @@ def test_library_exports_every_declared_symbol():
                          "graphattn_plan_destroy", "graphattn_last_error",
                          "graphattn_plan_profile", "graphattn_plan_profile_read",
                          "graphattn_extend", "graphattn_plan_create_extend",
-                         "graphattn_kv_append", "graphattn_kv_copy"}
+                         "graphattn_kv_append", "graphattn_kv_copy",
+                         "graphattn_equivalence_classes", "graphattn_graph_suffix"}
     for s in syms:
         assert hasattr(lib, s), s
 
@@ -173,3 +174,38 @@ def test_kv_write_errors():
     assert lib.graphattn_kv_append(dummy, dummy, dummy, dummy, 3, ctypes.byref(bad),
                                    None) == G.GA_EUNSUPPORTED
     assert lib.graphattn_kv_append(dummy, dummy, dummy, dummy, 3, None, None) == G.GA_EINVAL
+
+
+def test_equivalence_errors():
+    """Forest and argument validation of equivalence detection and the graph suffix."""
+    lib = G.load_library()
+    dummy = ctypes.c_void_p(1 << 20)                  # never dereferenced: rejected first
+    good = G.HostForest([-1, 0, 0, 1, -1, 4])
+
+    def eq(forest, dim=64, dtype=G.GA_BF16, kappa=0.9, z=dummy, labels=dummy):
+        return lib.graphattn_equivalence_classes(z, dim, dtype,
+                                                 ctypes.byref(forest.c) if forest else None,
+                                                 kappa, labels, None)
+    assert eq(None) == G.GA_EINVAL
+    assert eq(good, dim=96) == G.GA_EUNSUPPORTED
+    assert eq(good, dim=0) == G.GA_EUNSUPPORTED
+    assert eq(good, dtype=G.GA_F32) == G.GA_EUNSUPPORTED
+    assert eq(good, kappa=float("nan")) == G.GA_EINVAL
+    assert eq(good, z=None) == G.GA_EINVAL
+    assert eq(good, labels=None) == G.GA_EINVAL
+    assert eq(good, z=ctypes.c_void_p((1 << 20) + 8)) == G.GA_EINVAL
+    for bad in ([0, -1], [-1, 1], [-1, 0, -1, 1], [-2], [-1, 0, 5]):
+        assert eq(G.HostForest(bad)) == G.GA_EINVAL, bad
+    assert "consecutive" in (eq(G.HostForest([-1, 0, -1, 1])) and G.last_error())
+    assert eq(G.HostForest([])) == G.GA_OK            # no states: nothing to do
+    tot = ctypes.c_int64(7)
+
+    def sfx(forest, offs=dummy, states=dummy, cap=10, total=ctypes.byref(tot), labels=dummy):
+        return lib.graphattn_graph_suffix(labels, ctypes.byref(forest.c) if forest else None,
+                                          offs, states, cap, total, None)
+    assert sfx(good, total=None) == G.GA_EINVAL
+    assert sfx(None) == G.GA_EINVAL
+    assert sfx(good, offs=None) == G.GA_EINVAL
+    assert sfx(good, cap=-1) == G.GA_EINVAL
+    assert sfx(G.HostForest([-1, 1])) == G.GA_EINVAL
+    assert tot.value == 0

@@ -274,6 +274,94 @@ def run_append(args, torch, G, W):
     print(json.dumps(res), flush=True)
 
 
+def compared_pairs_count(parent):
+    """Pairs the method compares: same prompt, neither an ancestor of the other.  A prompt with n
+    states has n (n - 1) / 2 pairs, of which sum over states of (depth) are ancestor pairs."""
+    import numpy as np
+    N = len(parent)
+    depth = np.zeros(N, dtype=np.int64)
+    for v in range(N):
+        depth[v] = 0 if parent[v] < 0 else depth[parent[v]] + 1
+    roots = np.nonzero(parent < 0)[0].tolist() + [N]
+    pairs = sum((b - a) * (b - a - 1) // 2 for a, b in zip(roots[:-1], roots[1:]))
+    return pairs - int(depth.sum())
+
+
+def run_equiv(args, torch, G, W):
+    """Equivalence detection for one training batch's states: classes (the timed step), and the
+    graph suffix timed on its own (it synchronises to size its output)."""
+    import numpy as np
+    t0 = time.time()
+    wl = W.equiv_batch()
+    N, dim = wl.z.shape
+    log(f"workload {wl.name} generated in {time.time() - t0:.1f}s")
+    dev = torch.device("cuda:0")
+    z = wl.z.to(dev)
+    f = G.Forest(wl.parent)
+    labels = torch.empty(N, dtype=torch.int32, device=dev)
+    for _ in range(args.warmup):
+        f.classes(z, wl.kappa, labels)
+    torch.cuda.synchronize()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    for _ in range(args.steps):
+        f.classes(z, wl.kappa, labels)
+    ev1.record()
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / args.steps
+    lab = labels.cpu().numpy()
+    offs = torch.empty(N + 1, dtype=torch.int64, device=dev)
+    total = f.suffix_total(labels, offs)
+    states = torch.empty(max(1, total), dtype=torch.int32, device=dev)
+    f.suffix(labels, offs, states)
+    torch.cuda.synchronize()
+    ev0.record()
+    for _ in range(args.steps):
+        f.suffix(labels, offs, states)
+    ev1.record()
+    torch.cuda.synchronize()
+    suffix_ms = ev0.elapsed_time(ev1) / args.steps
+    log(f"timed {args.steps} steps: classes {ms:.4f} ms, graph suffix {suffix_ms:.4f} ms "
+        f"(with its host synchronisation)")
+    zbytes = N * dim * 2
+    pairs = compared_pairs_count(wl.parent)
+    achieved = zbytes / (ms * 1e-3) / 1e9
+    merged = int((lab != np.arange(N)).sum())
+    res = {
+        "metric": "rollout states/s classified per equivalence-detection call; % of HBM "
+                  "roofline on embedding bytes",
+        "value": N / (ms * 1e-3), "unit": "states/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded clustered N(0,1) embeddings, seeded state forest)",
+        "config": {"workload": wl.name, "states": int(N), "dim": int(dim), "kappa": wl.kappa,
+                   "compared_pairs": pairs, "classes": int(len(set(lab.tolist()))),
+                   "merged_states": merged, "suffix_entries": total},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None},
+        "compared_pair_tflops": pairs * 2 * dim / (ms * 1e-3) / 1e12,
+        "kernel_ms": {"classes": ms, "graph_suffix": suffix_ms},
+    }
+    f.close()
+    if args.cpu_sample > 0:
+        from oracle import graphattn_oracle as O
+        per = 205
+        n = min(64, N // per)
+        t1 = time.perf_counter()
+        for p in range(n):
+            a, b = p * per, (p + 1) * per
+            sub = wl.parent[a:b].copy()
+            sub[1:] -= a
+            O.equivalence_classes(wl.z_bits()[a:b], "bf16", sub, wl.kappa)
+        dt = time.perf_counter() - t1
+        res["cpu_baseline"] = {"value": n * per / dt, "unit": "states/s", "cores": 1,
+                               "kind": "oracle",
+                               "sample": f"{n} prompts ({n * per} states) of the same batch, "
+                                         f"fp64 NumPy, {dt:.1f} s wall"}
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -281,7 +369,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="c3",
                     choices=["c1", "c2", "c3", "c4", "c5chain", "c5graph"])
-    ap.add_argument("--op", default="decode", choices=["decode", "extend", "append"])
+    ap.add_argument("--op", default="decode", choices=["decode", "extend", "append", "equiv"])
     ap.add_argument("--n-query", type=int, default=16,
                     help="query tokens per branch for --op extend")
     ap.add_argument("--cpu-sample", type=int, default=1024,
@@ -305,6 +393,8 @@ def main():
         return run_extend(args, torch, G, W)
     if args.op == "append":
         return run_append(args, torch, G, W)
+    if args.op == "equiv":
+        return run_equiv(args, torch, G, W)
     t0 = time.time()
     wl = W.CONFIGS[args.config]()
     g = wl.graph

@@ -231,6 +231,21 @@ typedef struct {
   const int32_t* parent;   /* [N] */
 } ga_state_forest;
 
+/* A forest validated and uploaded once (its Euler intervals, depths, prompt ranges and the tile
+ * list of the similarity), plus the kernels' scratch; the graph_suffix / equivalence_classes
+ * calls below are forest_create + one call + forest_destroy.  Create enqueues the upload on
+ * hip_stream (the host arrays may be released on return); destroy waits for the device. */
+typedef struct ga_forest ga_forest;
+ga_status graphattn_forest_create(const ga_state_forest* forest, void* hip_stream,
+                                  ga_forest** out);
+ga_status graphattn_forest_classes(ga_forest* forest, const void* embeddings, int32_t dim,
+                                   int32_t dtype, float kappa, int32_t* labels,
+                                   void* hip_stream);
+ga_status graphattn_forest_suffix(ga_forest* forest, const int32_t* labels,
+                                  int64_t* suffix_offsets, int32_t* suffix_states,
+                                  int64_t capacity, int64_t* total, void* hip_stream);
+void graphattn_forest_destroy(ga_forest* forest);
+
 /* Equivalence classes of rollout states (Sec. 3.2 "Graph Construction"; Alg. S.1, Stage 1).
  * Two states of the same prompt that are neither ancestor nor descendant of each other are
  * compared by the cosine of their embeddings; pairs with cosine >= kappa are joined by
@@ -241,7 +256,8 @@ typedef struct {
  *   labels      [N] device int32, written: the smallest state id of each state's class
  * The cosine is computed from fp32 sums of the bf16 products (error below 2.5e-4 at
  * dim = 4096), so a pair within that distance of kappa may be decided either way.  Host
- * validation first; asynchronous on hip_stream. */
+ * validation first; returns after the device work (its workspace is freed on return; the
+ * forest calls above are asynchronous). */
 ga_status graphattn_equivalence_classes(const void* embeddings, int32_t dim, int32_t dtype,
                                         const ga_state_forest* forest, float kappa,
                                         int32_t* labels, void* hip_stream);

@@ -57,12 +57,14 @@ __device__ void unite(int* rep, int a, int b) {
   }
 }
 
-// Inverse norm of every embedding (NaN for a zero vector, which is then never linked) and the
-// union-find parent array reset to singletons.  One wave per state.
+// Prompts of more than 256 states: inverse norm of each of their embeddings (NaN for a zero
+// vector, which is then never linked) and the union-find parent reset to a singleton.  One wave
+// per state of the list a.big.
 __global__ __launch_bounds__(256) void k_norms(EquivArgs a) {
-  const int64_t w = ((int64_t)blockIdx.x * 256 + threadIdx.x) >> 6;
+  const int64_t wi = ((int64_t)blockIdx.x * 256 + threadIdx.x) >> 6;
   const int lane = threadIdx.x & 63;
-  if (w >= a.N) return;
+  if (wi >= a.n_big) return;
+  const int64_t w = a.big[wi];
   const bf16x8* row = reinterpret_cast<const bf16x8*>(a.z + w * a.dim);
   float s = 0.f;
   for (int c = lane; c < a.dim / 8; c += 64) {
@@ -153,11 +155,149 @@ __global__ __launch_bounds__(256) void k_sim_union(EquivArgs a) {
   }
 }
 
+// One prompt of at most 256 states in one workgroup (8 waves): the prompt's embeddings are
+// streamed through LDS once, 64 components per stage (256 rows x 128 bytes, double-buffered),
+// while each thread also sums the squares of the 4 row pieces it loads (the norms).  The upper
+// triangle of the 16 x 16 grid of 16 x 16 tiles (136 tiles) is dealt out as strips: wave w owns
+// row strips w and 15 - w, i.e. the 16 - w tiles (w, w..15) and the w + 1 tiles
+// (15 - w, 15 - w..15), 17 per wave.  Links are made with a union-find in LDS and the labels
+// written at the end, so nothing else is needed for these prompts.
+constexpr int kPromptMax = 256;
+
+__device__ __forceinline__ int lds_find(int* r, int x) {
+  int p = __hip_atomic_load(r + x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  while (p != x) {
+    x = p;
+    p = __hip_atomic_load(r + x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  }
+  return x;
+}
+
+__device__ void lds_unite(int* r, int a, int b) {
+  while (true) {
+    a = lds_find(r, a);
+    b = lds_find(r, b);
+    if (a == b) return;
+    if (a > b) {
+      const int t = a;
+      a = b;
+      b = t;
+    }
+    if (atomicCAS(r + b, b, a) == b) return;
+  }
+}
+
+__global__ __launch_bounds__(512, 2) void k_prompt_classes(EquivArgs a) {
+  __shared__ __align__(16) unsigned char stage[2][kPromptMax * kKC * 2];
+  __shared__ float s_inv[kPromptMax];
+  __shared__ int s_tin[kPromptMax], s_tout[kPromptMax], s_rep[kPromptMax];
+  const int2 pr = a.prompts[blockIdx.x];          // (first state, states)
+  const int s0 = pr.x, n = pr.y;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int r16 = lane & 15, kg = lane >> 4;
+  const int nt = (n + 15) >> 4;                   // 16-row tiles holding states
+  // Loads: thread t moves chunk t % 8 of rows t / 8 + 64 j (j < 4) of every stage.
+  const int lc = tid & 7, lr = tid >> 3;
+  auto lds_off = [](int row, int chunk) { return row * (kKC * 2) + ((chunk ^ (row & 7)) << 4); };
+  uint4 pf[4];
+  float ss[4] = {0.f, 0.f, 0.f, 0.f};
+  auto gload = [&](int kc) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int row = lr + 64 * j;
+      pf[j] = make_uint4(0u, 0u, 0u, 0u);
+      if (row < n)
+        pf[j] = *reinterpret_cast<const uint4*>(a.z + (int64_t)(s0 + row) * a.dim + kc * kKC +
+                                                lc * 8);
+    }
+  };
+  auto lstore = [&](int buf) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int row = lr + 64 * j;
+      *reinterpret_cast<uint4*>(&stage[buf][lds_off(row, lc)]) = pf[j];
+      const bf16x8 v = __builtin_bit_cast(bf16x8, pf[j]);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) ss[j] = fmaf((float)v[i], (float)v[i], ss[j]);
+    }
+  };
+  // Strips of this wave and the 17 tiles (strip, column) it owns.
+  const int sa = wave, sb = 15 - wave;
+  auto tile_strip = [&](int k) { return k < 16 - sa ? sa : sb; };
+  auto tile_col = [&](int k) { return k < 16 - sa ? sa + k : k - 1; };
+  f32x4 acc[17];
+#pragma unroll
+  for (int k = 0; k < 17; ++k) acc[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  if (tid < kPromptMax) {
+    s_rep[tid] = tid;
+    s_tin[tid] = tid < n ? a.tin[s0 + tid] : 0;
+    s_tout[tid] = tid < n ? a.tout[s0 + tid] : 0;
+  }
+  const int nk = a.dim / kKC;
+  gload(0);
+  lstore(0);
+  if (nk > 1) gload(1);
+  for (int kc = 0; kc < nk; ++kc) {
+    __syncthreads();                              // stage kc is in LDS; stage kc - 1 is done
+    const unsigned char* st = stage[kc & 1];
+#pragma unroll
+    for (int ks = 0; ks < kKC / 32; ++ks) {
+      const bf16x8 a0 = *reinterpret_cast<const bf16x8*>(st + lds_off(sa * 16 + r16, ks * 4 + kg));
+      const bf16x8 a1 = *reinterpret_cast<const bf16x8*>(st + lds_off(sb * 16 + r16, ks * 4 + kg));
+#pragma unroll
+      for (int k = 0; k < 17; ++k) {
+        const int srow = tile_strip(k), col = tile_col(k);
+        if (srow < nt && col < nt) {
+          const bf16x8 b = *reinterpret_cast<const bf16x8*>(st + lds_off(col * 16 + r16, ks * 4 + kg));
+          acc[k] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(srow == sa ? a0 : a1, b, acc[k], 0, 0, 0);
+        }
+      }
+    }
+    if (kc + 1 < nk) {
+      lstore((kc + 1) & 1);                       // the other buffer: nobody reads it now
+      if (kc + 2 < nk) gload(kc + 2);
+    }
+  }
+  // Norms: the 8 threads that load one row hold its partial sums (lanes 8q .. 8q + 7).
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    float v = ss[j];
+    v += __shfl_xor(v, 1);
+    v += __shfl_xor(v, 2);
+    v += __shfl_xor(v, 4);
+    if (lc == 0) s_inv[lr + 64 * j] = v > 0.f ? 1.f / sqrtf(v) : __builtin_nanf("");
+  }
+  __syncthreads();
+  // acc[k][i] = z_u . z_v, u = 16 strip + 4 kg + i, v = 16 col + r16 (prompt-local).
+#pragma unroll
+  for (int k = 0; k < 17; ++k) {
+    const int srow = tile_strip(k), col = tile_col(k);
+    if (srow >= nt || col >= nt) continue;
+    const int v = col * 16 + r16;
+    if (v >= n) continue;
+    const int tin_v = s_tin[v], tout_v = s_tout[v];
+    const float nv = s_inv[v];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int u = srow * 16 + 4 * kg + i;
+      if (u >= v) continue;
+      const int tin_u = s_tin[u], tout_u = s_tout[u];
+      const bool related = (tin_u <= tin_v && tin_v < tout_u) || (tin_v <= tin_u && tin_u < tout_v);
+      if (!related && acc[k][i] * s_inv[u] * nv >= a.kappa) lds_unite(s_rep, u, v);
+    }
+  }
+  __syncthreads();
+  if (tid < n) a.labels[s0 + tid] = s0 + lds_find(s_rep, tid);
+}
+
 // Final labels: every state's root (all links have landed: kernel boundary).
 __global__ void k_labels(EquivArgs a) {
-  const int64_t v = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (v >= a.N) return;
-  a.labels[v] = find_root(a.rep, (int)v);
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= a.n_big) return;
+  const int v = a.big[i];
+  a.labels[v] = find_root(a.rep, v);
 }
 
 // Graph suffix, pass 1 (count into cnt[u]) or pass 2 (write from off[u]).
@@ -221,11 +361,15 @@ __global__ __launch_bounds__(1024) void k_scan_apply(SuffixArgs a) {
 }  // namespace
 
 hipError_t launch_equivalence(const EquivArgs& a, hipStream_t stream) {
-  if (a.N == 0) return hipSuccess;
-  hipLaunchKernelGGL(k_norms, dim3((unsigned)((a.N * 64 + 255) / 256)), dim3(256), 0, stream, a);
-  if (a.n_items > 0)
-    hipLaunchKernelGGL(k_sim_union, dim3((unsigned)a.n_items), dim3(256), 0, stream, a);
-  hipLaunchKernelGGL(k_labels, dim3((unsigned)((a.N + 255) / 256)), dim3(256), 0, stream, a);
+  if (a.n_prompts > 0)
+    hipLaunchKernelGGL(k_prompt_classes, dim3((unsigned)a.n_prompts), dim3(512), 0, stream, a);
+  if (a.n_big > 0) {
+    hipLaunchKernelGGL(k_norms, dim3((unsigned)((a.n_big * 64 + 255) / 256)), dim3(256), 0, stream,
+                       a);
+    if (a.n_items > 0)
+      hipLaunchKernelGGL(k_sim_union, dim3((unsigned)a.n_items), dim3(256), 0, stream, a);
+    hipLaunchKernelGGL(k_labels, dim3((unsigned)((a.n_big + 255) / 256)), dim3(256), 0, stream, a);
+  }
   return hipGetLastError();
 }
 

@@ -42,8 +42,12 @@ size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 struct Forest {
   int64_t N = 0;
   std::vector<int32_t> parent, depth, tin, tout, pstart, pend;
-  std::vector<int4> items;
+  std::vector<int4> items;       // 64 x 64 tiles of the prompts of more than 256 states
+  std::vector<int2> prompts;     // (first state, states) of the prompts of at most 256 states
+  std::vector<int32_t> big;      // the states of the larger prompts
 };
+
+constexpr int32_t kPromptMax = 256;   // states one workgroup classifies on its own
 
 // Each prompt's states are consecutive, its root first; p(v) < v.  Depths, prompt ranges and
 // Euler intervals (tin <= tin' < tout exactly when the state is an ancestor of the other).
@@ -103,63 +107,20 @@ ga_status build_forest(const ga_state_forest* f, bool with_items, Forest* fo) {
     }
   }
   fo->items.clear();
+  fo->prompts.clear();
+  fo->big.clear();
   if (with_items) {
     for (int32_t r = 0; r < N; r = fo->pend[r]) {
       const int32_t e = fo->pend[r];
+      if (e - r <= kPromptMax) {
+        fo->prompts.push_back(make_int2(r, e - r));
+        continue;
+      }
+      for (int32_t v = r; v < e; ++v) fo->big.push_back(v);
       for (int32_t i0 = r; i0 < e; i0 += 64)
         for (int32_t j0 = i0; j0 < e; j0 += 64) fo->items.push_back(make_int4(i0, j0, e, 0));
     }
   }
-  return GA_OK;
-}
-
-// Process-wide device workspace and pinned staging for these calls (grown on demand; a call
-// waits for the previous one's upload and kernels before reusing them).
-struct Cache {
-  std::mutex mu;
-  void* dev = nullptr;
-  size_t dev_bytes = 0;
-  void* pin = nullptr;
-  size_t pin_bytes = 0;
-  int device = -1;
-  hipEvent_t done = nullptr;
-};
-Cache g_eq;
-
-ga_status acquire(size_t dev_bytes, size_t pin_bytes, hipStream_t stream) {
-  int dev = 0;
-  EQ_HIP(hipGetDevice(&dev), "current device");
-  if (g_eq.device != dev) {
-    g_eq.dev = g_eq.pin = nullptr;
-    g_eq.dev_bytes = g_eq.pin_bytes = 0;
-    g_eq.done = nullptr;
-    g_eq.device = dev;
-  }
-  if (!g_eq.done) EQ_HIP(hipEventCreateWithFlags(&g_eq.done, hipEventDisableTiming), "event");
-  // The staging buffer is refilled on the host, so everything the previous call enqueued
-  // (its upload included) must be done.
-  EQ_HIP(hipEventSynchronize(g_eq.done), "wait for the previous call");
-  if (g_eq.dev_bytes < dev_bytes) {
-    if (g_eq.dev) (void)hipFree(g_eq.dev);
-    g_eq.dev = nullptr;
-    g_eq.dev_bytes = 0;
-    if (hipMalloc(&g_eq.dev, dev_bytes) != hipSuccess) {
-      (void)hipGetLastError();
-      return efail(GA_ENOMEM, "device workspace of %zu bytes", dev_bytes);
-    }
-    g_eq.dev_bytes = dev_bytes;
-  }
-  if (g_eq.pin_bytes < pin_bytes || !g_eq.pin) {
-    if (g_eq.pin) (void)hipHostFree(g_eq.pin);
-    g_eq.pin = nullptr;
-    g_eq.pin_bytes = 0;
-    if (hipHostMalloc(&g_eq.pin, pin_bytes > 0 ? pin_bytes : 1) != hipSuccess) {
-      (void)hipGetLastError();
-      return efail(GA_ENOMEM, "pinned staging of %zu bytes", pin_bytes);
-    }
-    g_eq.pin_bytes = pin_bytes;
-  }
-  (void)stream;
   return GA_OK;
 }
 
@@ -171,7 +132,205 @@ void put(char* pin, size_t& o, const std::vector<T>& v) {
 
 }  // namespace
 
+// A validated forest on the device: its arrays (uploaded once) and the scratch of the kernels.
+struct ga_forest {
+  Forest fo;
+  void* dev = nullptr;
+  void* pin = nullptr;
+  int32_t *tin = nullptr, *tout = nullptr, *parent = nullptr, *depth = nullptr;
+  int32_t *pstart = nullptr, *pend = nullptr;
+  int4* items = nullptr;
+  int2* prompts = nullptr;
+  int32_t* big = nullptr;
+  float* inv_norm = nullptr;
+  int* rep = nullptr;
+  int64_t *cnt = nullptr, *off = nullptr, *blk = nullptr;
+};
+
+namespace {
+
+void forest_free(ga_forest* f) {
+  if (!f) return;
+  if (f->dev) {
+    (void)hipDeviceSynchronize();
+    (void)hipFree(f->dev);
+  }
+  if (f->pin) (void)hipHostFree(f->pin);
+  delete f;
+}
+
+ga_status forest_create(const ga_state_forest* forest, hipStream_t stream, ga_forest** out) {
+  if (!out) return efail(GA_EINVAL, "forest out-pointer is NULL");
+  *out = nullptr;
+  ga_forest* f = new ga_forest();
+  ga_status rc = build_forest(forest, true, &f->fo);
+  if (rc) {
+    delete f;
+    return rc;
+  }
+  const Forest& fo = f->fo;
+  if ((int64_t)fo.items.size() > 0x7fffffffLL) {
+    delete f;
+    return efail(GA_EINVAL, "too many tiles");
+  }
+  const size_t n4 = align256(4 * fo.N), n8 = align256(8 * fo.N);
+  const size_t up = 6 * n4 + align256(sizeof(int4) * fo.items.size()) +
+                    align256(sizeof(int2) * fo.prompts.size()) + align256(4 * fo.big.size());
+  const size_t nblk = (size_t)((fo.N + 1023) / 1024);
+  const size_t total = up + 2 * n4 + n8 + align256(8 * (fo.N + 1)) + align256(8 * (nblk + 1));
+  if (hipMalloc(&f->dev, total) != hipSuccess) {
+    (void)hipGetLastError();
+    f->dev = nullptr;
+    forest_free(f);
+    return efail(GA_ENOMEM, "device workspace of %zu bytes", total);
+  }
+  if (hipHostMalloc(&f->pin, up > 0 ? up : 1) != hipSuccess) {
+    (void)hipGetLastError();
+    f->pin = nullptr;
+    forest_free(f);
+    return efail(GA_ENOMEM, "pinned staging of %zu bytes", up);
+  }
+  char* pin = static_cast<char*>(f->pin);
+  size_t o = 0;
+  put(pin, o, fo.tin);
+  put(pin, o, fo.tout);
+  put(pin, o, fo.parent);
+  put(pin, o, fo.depth);
+  put(pin, o, fo.pstart);
+  put(pin, o, fo.pend);
+  put(pin, o, fo.items);
+  put(pin, o, fo.prompts);
+  put(pin, o, fo.big);
+  char* d = static_cast<char*>(f->dev);
+  f->tin = reinterpret_cast<int32_t*>(d);
+  f->tout = reinterpret_cast<int32_t*>(d + n4);
+  f->parent = reinterpret_cast<int32_t*>(d + 2 * n4);
+  f->depth = reinterpret_cast<int32_t*>(d + 3 * n4);
+  f->pstart = reinterpret_cast<int32_t*>(d + 4 * n4);
+  f->pend = reinterpret_cast<int32_t*>(d + 5 * n4);
+  f->items = reinterpret_cast<int4*>(d + 6 * n4);
+  const size_t oi = 6 * n4 + align256(sizeof(int4) * fo.items.size());
+  f->prompts = reinterpret_cast<int2*>(d + oi);
+  f->big = reinterpret_cast<int32_t*>(d + oi + align256(sizeof(int2) * fo.prompts.size()));
+  f->inv_norm = reinterpret_cast<float*>(d + up);
+  f->rep = reinterpret_cast<int*>(d + up + n4);
+  f->cnt = reinterpret_cast<int64_t*>(d + up + 2 * n4);
+  f->off = reinterpret_cast<int64_t*>(d + up + 2 * n4 + n8);
+  f->blk = reinterpret_cast<int64_t*>(d + up + 2 * n4 + n8 + align256(8 * (fo.N + 1)));
+  if (up > 0) {
+    const hipError_t e = hipMemcpyAsync(d, pin, up, hipMemcpyHostToDevice, stream);
+    if (e != hipSuccess) {
+      forest_free(f);
+      return ga::host_hip_fail(e, "forest upload");
+    }
+  }
+  *out = f;
+  return GA_OK;
+}
+
+ga_status forest_classes(ga_forest* f, const void* embeddings, int32_t dim, int32_t dtype,
+                         float kappa, int32_t* labels, hipStream_t stream) {
+  if (!f) return efail(GA_EINVAL, "forest is NULL");
+  if (dtype != GA_BF16) return efail(GA_EUNSUPPORTED, "embeddings must be bf16");
+  if (dim < 64 || dim % 64) return efail(GA_EUNSUPPORTED, "dim %d unsupported (a multiple of 64)", dim);
+  if (!std::isfinite(kappa)) return efail(GA_EINVAL, "kappa must be finite");
+  if (f->fo.N == 0) return GA_OK;
+  if (!embeddings || !labels) return efail(GA_EINVAL, "embeddings and labels must be non-NULL");
+  if (reinterpret_cast<uintptr_t>(embeddings) & 15)
+    return efail(GA_EINVAL, "embeddings must be 16-byte aligned");
+  if (reinterpret_cast<uintptr_t>(labels) & 3) return efail(GA_EINVAL, "labels must be 4-byte aligned");
+  ga::EquivArgs a{};
+  a.z = static_cast<const unsigned short*>(embeddings);
+  a.tin = f->tin;
+  a.tout = f->tout;
+  a.items = f->items;
+  a.prompts = f->prompts;
+  a.big = f->big;
+  a.n_prompts = (int64_t)f->fo.prompts.size();
+  a.n_big = (int64_t)f->fo.big.size();
+  a.inv_norm = f->inv_norm;
+  a.rep = f->rep;
+  a.labels = labels;
+  a.N = f->fo.N;
+  a.n_items = (int64_t)f->fo.items.size();
+  a.dim = dim;
+  a.kappa = kappa;
+  EQ_HIP(ga::launch_equivalence(a, stream), "equivalence launch");
+  return GA_OK;
+}
+
+ga_status forest_suffix(ga_forest* f, const int32_t* labels, int64_t* suffix_offsets,
+                        int32_t* suffix_states, int64_t capacity, int64_t* total,
+                        hipStream_t stream) {
+  if (!total) return efail(GA_EINVAL, "total is NULL");
+  *total = 0;
+  if (!f) return efail(GA_EINVAL, "forest is NULL");
+  if (!suffix_offsets) return efail(GA_EINVAL, "suffix_offsets is NULL");
+  if (capacity < 0) return efail(GA_EINVAL, "capacity is negative");
+  const int64_t N = f->fo.N;
+  if (N > 0 && !labels) return efail(GA_EINVAL, "labels is NULL");
+  if ((reinterpret_cast<uintptr_t>(suffix_offsets) & 7) ||
+      (reinterpret_cast<uintptr_t>(labels) & 3) || (reinterpret_cast<uintptr_t>(suffix_states) & 3))
+    return efail(GA_EINVAL, "misaligned output or label array");
+  ga::SuffixArgs a{};
+  a.labels = labels;
+  a.parent = f->parent;
+  a.depth = f->depth;
+  a.pstart = f->pstart;
+  a.pend = f->pend;
+  a.cnt = f->cnt;
+  a.off = f->off;
+  a.blk = f->blk;
+  a.states = suffix_states;
+  a.N = N;
+  int64_t n = 0;
+  if (N > 0) {
+    EQ_HIP(ga::launch_suffix_count(a, stream), "suffix count launch");
+    EQ_HIP(hipMemcpyAsync(&n, a.off + N, sizeof n, hipMemcpyDeviceToHost, stream), "total");
+  }
+  EQ_HIP(hipStreamSynchronize(stream), "synchronise");
+  *total = n;
+  if (n > capacity)
+    return efail(GA_ERANGE, "graph suffix needs %lld entries, capacity is %lld", (long long)n,
+                 (long long)capacity);
+  if (n > 0 && !suffix_states) return efail(GA_EINVAL, "suffix_states is NULL");
+  if (N == 0) {
+    EQ_HIP(hipMemsetAsync(suffix_offsets, 0, sizeof(int64_t), stream), "offsets");
+    return GA_OK;
+  }
+  EQ_HIP(hipMemcpyAsync(suffix_offsets, a.off, sizeof(int64_t) * (N + 1),
+                        hipMemcpyDeviceToDevice, stream), "offsets");
+  EQ_HIP(ga::launch_suffix_fill(a, stream), "suffix fill launch");
+  return GA_OK;
+}
+
+}  // namespace
+
 extern "C" {
+
+ga_status graphattn_forest_create(const ga_state_forest* forest, void* hip_stream,
+                                  ga_forest** out) {
+  ga::host_clear_error();
+  return forest_create(forest, static_cast<hipStream_t>(hip_stream), out);
+}
+
+ga_status graphattn_forest_classes(ga_forest* forest, const void* embeddings, int32_t dim,
+                                   int32_t dtype, float kappa, int32_t* labels,
+                                   void* hip_stream) {
+  ga::host_clear_error();
+  return forest_classes(forest, embeddings, dim, dtype, kappa, labels,
+                        static_cast<hipStream_t>(hip_stream));
+}
+
+ga_status graphattn_forest_suffix(ga_forest* forest, const int32_t* labels,
+                                  int64_t* suffix_offsets, int32_t* suffix_states,
+                                  int64_t capacity, int64_t* total, void* hip_stream) {
+  ga::host_clear_error();
+  return forest_suffix(forest, labels, suffix_offsets, suffix_states, capacity, total,
+                       static_cast<hipStream_t>(hip_stream));
+}
+
+void graphattn_forest_destroy(ga_forest* forest) { forest_free(forest); }
 
 ga_status graphattn_equivalence_classes(const void* embeddings, int32_t dim, int32_t dtype,
                                         const ga_state_forest* forest, float kappa,
@@ -180,44 +339,21 @@ ga_status graphattn_equivalence_classes(const void* embeddings, int32_t dim, int
   if (dtype != GA_BF16) return efail(GA_EUNSUPPORTED, "embeddings must be bf16");
   if (dim < 64 || dim % 64) return efail(GA_EUNSUPPORTED, "dim %d unsupported (a multiple of 64)", dim);
   if (!std::isfinite(kappa)) return efail(GA_EINVAL, "kappa must be finite");
-  Forest fo;
-  ga_status rc = build_forest(forest, true, &fo);
+  Forest probe;
+  ga_status rc = build_forest(forest, false, &probe);
   if (rc) return rc;
-  if (fo.N == 0) return GA_OK;
+  if (probe.N == 0) return GA_OK;
   if (!embeddings || !labels) return efail(GA_EINVAL, "embeddings and labels must be non-NULL");
   if (reinterpret_cast<uintptr_t>(embeddings) & 15)
     return efail(GA_EINVAL, "embeddings must be 16-byte aligned");
   if (reinterpret_cast<uintptr_t>(labels) & 3) return efail(GA_EINVAL, "labels must be 4-byte aligned");
-  if ((int64_t)fo.items.size() > 0x7fffffffLL) return efail(GA_EINVAL, "too many tiles");
   hipStream_t stream = static_cast<hipStream_t>(hip_stream);
-  std::lock_guard<std::mutex> lock(g_eq.mu);
-  // Uploaded (pinned, one copy): tin, tout, items.  Device only: inverse norms, parents.
-  const size_t up = align256(4 * fo.N) * 2 + align256(sizeof(int4) * fo.items.size());
-  const size_t total = up + align256(4 * fo.N) * 2;
-  rc = acquire(total, up, stream);
+  ga_forest* f = nullptr;
+  rc = forest_create(forest, stream, &f);
   if (rc) return rc;
-  char* pin = static_cast<char*>(g_eq.pin);
-  size_t o = 0;
-  put(pin, o, fo.tin);
-  put(pin, o, fo.tout);
-  put(pin, o, fo.items);
-  char* d = static_cast<char*>(g_eq.dev);
-  EQ_HIP(hipMemcpyAsync(d, pin, up, hipMemcpyHostToDevice, stream), "forest upload");
-  ga::EquivArgs a{};
-  a.z = static_cast<const unsigned short*>(embeddings);
-  a.tin = reinterpret_cast<const int32_t*>(d);
-  a.tout = reinterpret_cast<const int32_t*>(d + align256(4 * fo.N));
-  a.items = reinterpret_cast<const int4*>(d + 2 * align256(4 * fo.N));
-  a.inv_norm = reinterpret_cast<float*>(d + up);
-  a.rep = reinterpret_cast<int*>(d + up + align256(4 * fo.N));
-  a.labels = labels;
-  a.N = fo.N;
-  a.n_items = (int64_t)fo.items.size();
-  a.dim = dim;
-  a.kappa = kappa;
-  EQ_HIP(ga::launch_equivalence(a, stream), "equivalence launch");
-  EQ_HIP(hipEventRecord(g_eq.done, stream), "record");
-  return GA_OK;
+  rc = forest_classes(f, embeddings, dim, dtype, kappa, labels, stream);
+  forest_free(f);
+  return rc;
 }
 
 ga_status graphattn_graph_suffix(const int32_t* labels, const ga_state_forest* forest,
@@ -226,65 +362,19 @@ ga_status graphattn_graph_suffix(const int32_t* labels, const ga_state_forest* f
   ga::host_clear_error();
   if (!total) return efail(GA_EINVAL, "total is NULL");
   *total = 0;
-  Forest fo;
-  ga_status rc = build_forest(forest, false, &fo);
+  Forest probe;
+  ga_status rc = build_forest(forest, false, &probe);
   if (rc) return rc;
   if (!suffix_offsets) return efail(GA_EINVAL, "suffix_offsets is NULL");
   if (capacity < 0) return efail(GA_EINVAL, "capacity is negative");
+  if (probe.N > 0 && !labels) return efail(GA_EINVAL, "labels is NULL");
   hipStream_t stream = static_cast<hipStream_t>(hip_stream);
-  if (fo.N == 0) {
-    const int64_t zero = 0;
-    EQ_HIP(hipMemcpyAsync(suffix_offsets, &zero, sizeof zero, hipMemcpyHostToDevice, stream),
-           "offsets");
-    EQ_HIP(hipStreamSynchronize(stream), "synchronise");
-    return GA_OK;
-  }
-  if (!labels) return efail(GA_EINVAL, "labels is NULL");
-  if ((reinterpret_cast<uintptr_t>(suffix_offsets) & 7) ||
-      (reinterpret_cast<uintptr_t>(labels) & 3) || (reinterpret_cast<uintptr_t>(suffix_states) & 3))
-    return efail(GA_EINVAL, "misaligned output or label array");
-  std::lock_guard<std::mutex> lock(g_eq.mu);
-  const size_t n4 = align256(4 * fo.N);
-  const size_t up = 4 * n4;                          // parent, depth, pstart, pend
-  const size_t nblk = (size_t)((fo.N + 1023) / 1024);
-  const size_t tot = up + align256(8 * fo.N) + align256(8 * (fo.N + 1)) + align256(8 * nblk);
-  rc = acquire(tot, up, stream);
+  ga_forest* f = nullptr;
+  rc = forest_create(forest, stream, &f);
   if (rc) return rc;
-  char* pin = static_cast<char*>(g_eq.pin);
-  size_t o = 0;
-  put(pin, o, fo.parent);
-  put(pin, o, fo.depth);
-  put(pin, o, fo.pstart);
-  put(pin, o, fo.pend);
-  char* d = static_cast<char*>(g_eq.dev);
-  EQ_HIP(hipMemcpyAsync(d, pin, up, hipMemcpyHostToDevice, stream), "forest upload");
-  ga::SuffixArgs a{};
-  a.labels = labels;
-  a.parent = reinterpret_cast<const int32_t*>(d);
-  a.depth = reinterpret_cast<const int32_t*>(d + n4);
-  a.pstart = reinterpret_cast<const int32_t*>(d + 2 * n4);
-  a.pend = reinterpret_cast<const int32_t*>(d + 3 * n4);
-  a.cnt = reinterpret_cast<int64_t*>(d + up);
-  a.off = reinterpret_cast<int64_t*>(d + up + align256(8 * fo.N));
-  a.blk = reinterpret_cast<int64_t*>(d + up + align256(8 * fo.N) + align256(8 * (fo.N + 1)));
-  a.states = suffix_states;
-  a.N = fo.N;
-  EQ_HIP(ga::launch_suffix_count(a, stream), "suffix count launch");
-  int64_t n = 0;
-  EQ_HIP(hipMemcpyAsync(&n, a.off + fo.N, sizeof n, hipMemcpyDeviceToHost, stream), "total");
-  EQ_HIP(hipStreamSynchronize(stream), "synchronise");
-  *total = n;
-  if (n > capacity) {
-    EQ_HIP(hipEventRecord(g_eq.done, stream), "record");
-    return efail(GA_ERANGE, "graph suffix needs %lld entries, capacity is %lld", (long long)n,
-                 (long long)capacity);
-  }
-  if (n > 0 && !suffix_states) return efail(GA_EINVAL, "suffix_states is NULL");
-  EQ_HIP(hipMemcpyAsync(suffix_offsets, a.off, sizeof(int64_t) * (fo.N + 1),
-                        hipMemcpyDeviceToDevice, stream), "offsets");
-  EQ_HIP(ga::launch_suffix_fill(a, stream), "suffix fill launch");
-  EQ_HIP(hipEventRecord(g_eq.done, stream), "record");
-  return GA_OK;
+  rc = forest_suffix(f, labels, suffix_offsets, suffix_states, capacity, total, stream);
+  forest_free(f);
+  return rc;
 }
 
 }  // extern "C"

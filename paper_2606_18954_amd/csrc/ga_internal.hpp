@@ -128,9 +128,11 @@ struct EquivArgs {
   int* rep;                // [N]  union-find parents
   const int32_t* tin;      // [N]  Euler interval of each state in its generation tree
   const int32_t* tout;     // [N]
-  const int4* items;       // [n_items]
+  const int4* items;       // [n_items] tiles of the prompts of more than 256 states
+  const int2* prompts;     // [n_prompts] (first state, states) of the prompts of <= 256 states
+  const int32_t* big;      // [n_big] the states of the larger prompts
   int32_t* labels;         // [N]  output: smallest state of the class
-  int64_t N, n_items;
+  int64_t N, n_items, n_prompts, n_big;
   int32_t dim;
   float kappa;
 };

@@ -100,6 +100,14 @@ def load_library() -> ctypes.CDLL:
     lib.graphattn_equivalence_classes.restype = ctypes.c_int
     lib.graphattn_graph_suffix.argtypes = [vp, P(StateForest), vp, vp, i64, P(i64), vp]
     lib.graphattn_graph_suffix.restype = ctypes.c_int
+    lib.graphattn_forest_create.argtypes = [P(StateForest), vp, P(vp)]
+    lib.graphattn_forest_create.restype = ctypes.c_int
+    lib.graphattn_forest_classes.argtypes = [vp, vp, i32, i32, ctypes.c_float, vp, vp]
+    lib.graphattn_forest_classes.restype = ctypes.c_int
+    lib.graphattn_forest_suffix.argtypes = [vp, vp, vp, vp, i64, P(i64), vp]
+    lib.graphattn_forest_suffix.restype = ctypes.c_int
+    lib.graphattn_forest_destroy.argtypes = [vp]
+    lib.graphattn_forest_destroy.restype = None
     lib.graphattn_schedule.argtypes = [vp, vp]
     lib.graphattn_schedule.restype = ctypes.c_int
     lib.graphattn_run.argtypes = [vp, vp, vp, vp, vp, vp]
@@ -280,6 +288,63 @@ def graph_suffix(labels, forest: HostForest, capacity=None, stream=None):
                                         _stream_handle(stream))
     _check(st)
     return offs, states[:int(total.value)]
+
+
+class Forest:
+    """graphattn_forest_create / classes / suffix / destroy."""
+
+    def __init__(self, parent, stream=None):
+        self.lib = load_library()
+        self.host = HostForest(parent)
+        h = ctypes.c_void_p()
+        _check(self.lib.graphattn_forest_create(ctypes.byref(self.host.c), _stream_handle(stream),
+                                                ctypes.byref(h)))
+        self.handle = h
+
+    def classes(self, z, kappa: float, labels=None, stream=None):
+        import torch
+        N = self.host.c.num_states
+        if labels is None:
+            labels = torch.empty(N, dtype=torch.int32, device=z.device)
+        _check(self.lib.graphattn_forest_classes(
+            self.handle, _dev_ptr(z), int(z.shape[1]),
+            GA_BF16 if z.dtype == torch.bfloat16 else GA_F32, float(kappa), _dev_ptr(labels),
+            _stream_handle(stream)))
+        return labels
+
+    def suffix(self, labels, offsets, states, stream=None) -> int:
+        total = ctypes.c_int64(0)
+        _check(self.lib.graphattn_forest_suffix(self.handle, _dev_ptr(labels), _dev_ptr(offsets),
+                                                _dev_ptr(states), int(states.numel()),
+                                                ctypes.byref(total), _stream_handle(stream)))
+        return int(total.value)
+
+    def suffix_total(self, labels, offsets, stream=None) -> int:
+        """Entries the graph suffix needs (a call with no output buffer)."""
+        total = ctypes.c_int64(0)
+        st = self.lib.graphattn_forest_suffix(self.handle, _dev_ptr(labels), _dev_ptr(offsets),
+                                              None, 0, ctypes.byref(total),
+                                              _stream_handle(stream))
+        if st not in (GA_OK, GA_ERANGE):
+            _check(st)
+        return int(total.value)
+
+    def close(self):
+        if self.handle:
+            self.lib.graphattn_forest_destroy(self.handle)
+            self.handle = None
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 class Plan:

@@ -589,13 +589,33 @@ def draw_state_embeddings(parent: np.ndarray, dim: int, seed: int, share: float 
         for u, k, kp in zip(ids, pick, keep):
             center[u] = center[parent[u]] if (kp and h > 1) else ncent + int(k)
         ncent += pool
-    gen = torch.Generator(device="cpu")
-    gen.manual_seed(_chunk_seed(seed, 0))
-    centres = torch.randn((ncent, dim), generator=gen, dtype=torch.float32)
-    gen.manual_seed(_chunk_seed(seed, 1))
-    noise = torch.randn((N, dim), generator=gen, dtype=torch.float32)
-    z = centres[torch.from_numpy(center)] + sigma * noise
-    return _bf16_rne(z)
+    # Centres and noise in chunks of rows, chunk c from its own generator (seed, stream), so
+    # the chunks are drawn in parallel and the values do not depend on the thread count.
+    import concurrent.futures
+    CH = 4096
+    centres = torch.empty((ncent, dim), dtype=torch.float32)
+    z = torch.empty((N, dim), dtype=torch.bfloat16)
+    cidx = torch.from_numpy(center)
+
+    def draw_centres(c):
+        gen = torch.Generator(device="cpu")
+        gen.manual_seed(_chunk_seed(seed, 2 * c))
+        r0, r1 = c * CH, min(ncent, (c + 1) * CH)
+        centres[r0:r1] = torch.randn((r1 - r0, dim), generator=gen, dtype=torch.float32)
+
+    def draw_rows(c):
+        gen = torch.Generator(device="cpu")
+        gen.manual_seed(_chunk_seed(seed, 2 * c + 1))
+        r0, r1 = c * CH, min(N, (c + 1) * CH)
+        x = torch.randn((r1 - r0, dim), generator=gen, dtype=torch.float32).mul_(sigma)
+        x += centres[cidx[r0:r1]]
+        z[r0:r1] = _bf16_rne(x)
+
+    workers = max(1, min(16, os.cpu_count() or 1))
+    with concurrent.futures.ThreadPoolExecutor(max_workers=workers) as ex:
+        list(ex.map(draw_centres, range((ncent + CH - 1) // CH)))
+        list(ex.map(draw_rows, range((N + CH - 1) // CH)))
+    return z
 
 
 def equiv_batch(prompts: int = 512, schedule: Sequence[int] = (4, 5, 3, 2), dim: int = 4096,

@@ -18,7 +18,9 @@ def test_library_exports_every_declared_symbol():
                          "graphattn_plan_profile", "graphattn_plan_profile_read",
                          "graphattn_extend", "graphattn_plan_create_extend",
                          "graphattn_kv_append", "graphattn_kv_copy",
-                         "graphattn_equivalence_classes", "graphattn_graph_suffix"}
+                         "graphattn_equivalence_classes", "graphattn_graph_suffix",
+                         "graphattn_forest_create", "graphattn_forest_classes",
+                         "graphattn_forest_suffix", "graphattn_forest_destroy"}
     for s in syms:
         assert hasattr(lib, s), s
 
@@ -209,3 +211,20 @@ def test_equivalence_errors():
     assert sfx(good, cap=-1) == G.GA_EINVAL
     assert sfx(G.HostForest([-1, 1])) == G.GA_EINVAL
     assert tot.value == 0
+
+
+def test_forest_plan_errors():
+    lib = G.load_library()
+    h = ctypes.c_void_p(1)
+    assert lib.graphattn_forest_create(ctypes.byref(G.HostForest([0]).c), None,
+                                       ctypes.byref(h)) == G.GA_EINVAL
+    assert h.value is None
+    assert lib.graphattn_forest_create(None, None, ctypes.byref(h)) == G.GA_EINVAL
+    assert lib.graphattn_forest_create(ctypes.byref(G.HostForest([-1]).c), None,
+                                       None) == G.GA_EINVAL
+    assert lib.graphattn_forest_classes(None, None, 64, G.GA_BF16, 0.9, None, None) == G.GA_EINVAL
+    tot = ctypes.c_int64(3)
+    assert lib.graphattn_forest_suffix(None, None, None, None, 0, ctypes.byref(tot),
+                                       None) == G.GA_EINVAL
+    assert tot.value == 0
+    lib.graphattn_forest_destroy(None)            # no-op

@@ -101,3 +101,25 @@ def test_full_batch_sampled_prompts():
         ref = O.equivalence_classes(zb, "bf16", sub, wl.kappa) + a
         say(f"[equiv] prompt {p}: {len(set(ref.tolist()))} classes")
         assert np.array_equal(got[a:b], ref), p
+
+
+def test_forest_plan_serves_several_thresholds():
+    """One uploaded forest, classes at two thresholds and the suffix of each, against the
+    one-shot calls and the oracle."""
+    wl = W.equiv_batch(prompts=3, schedule=(4, 5, 3, 2), dim=512, seed=19)
+    z = wl.z.cuda()
+    with G.Forest(wl.parent) as f:
+        for kappa in (0.92, 0.5):
+            assert O.similarity_margin(wl.z_bits(), "bf16", wl.parent, kappa) >= MARGIN
+            lab = f.classes(z, kappa)
+            torch.cuda.synchronize()
+            ref = O.equivalence_classes(wl.z_bits(), "bf16", wl.parent, kappa)
+            assert np.array_equal(lab.cpu().numpy(), ref)
+            ro, rs = O.graph_suffix(ref, wl.parent)
+            offs = torch.empty(len(wl.parent) + 1, dtype=torch.int64, device="cuda")
+            st = torch.empty(len(rs) + 5, dtype=torch.int32, device="cuda")
+            n = f.suffix(lab, offs, st)
+            torch.cuda.synchronize()
+            assert n == len(rs)
+            assert np.array_equal(offs.cpu().numpy(), ro)
+            assert np.array_equal(st[:n].cpu().numpy(), rs)

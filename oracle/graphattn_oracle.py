@@ -24,6 +24,11 @@ What it computes (the passages it follows):
   not ancestor and descendant are compared by the cosine of their embeddings; pairs at or above
   kappa are joined by union-find into classes Q(v); the graph suffix C_g(u) adds the direct
   successors of the other class members that lie deeper than u.
+* Graph reward and dual-group advantage (Sec. 3.3-3.4; Alg. S.1, Stages 2-3): terminal
+  outcomes summed over each state's subtree, pooled over its class with weight w, step rewards
+  from score gains discounted by endpoint similarity, correctness z-scores within each source's
+  group E_cor, efficiency z-scores of route lengths within each class, gated by the class's
+  mean score and spread over the route's edges.
 * Extend: the queries of a branch are the newest tokens of its last path segment, each
   attending causally (Alg. S.1, Stage 1: a continuation is predicted token by token from
   prefix(u)); append and copy store tokens into page slots and move them between slots.
@@ -36,6 +41,10 @@ For extend: the query segment is the path's last entry, a query sees itself, and
 position P of that segment sees exactly its tokens 0 .. P. A slot word is page * 16 + slot.
 For equivalence detection: ancestry is that of the generation tree (p(v)); a class is labelled
 by its smallest state id; pairs of different prompts are never compared.
+For the graph reward: S(v) is undefined (NaN) without evidence, and such edges sit out of their
+group with advantage 0; an edge's correctness advantage is taken in its own source's group;
+std is the population standard deviation and a zero spread gives 0; a_Q is the deepest proper
+ancestor of every member; an edge on several efficiency routes receives the sum.
 
 Parity status: every function below is pinned by CPU tests against brute force, a library
 routine on a special case, closed forms and invariants (softmax rows sum to 1, merge
@@ -43,7 +52,9 @@ associativity, the K=0 tag closed form, the single-token case); extend against t
 SDPA and a token-by-token walk, append by reading the stored segment back, copy by splitting a
 segment inside a page without changing attention; equivalence classes against scipy's connected
 components of an independently built link graph, threshold extremes and the ancestor rule;
-the graph suffix against a hand-derived fixture and the no-merge identity.
+the graph suffix against a hand-derived fixture and the no-merge identity; the graph reward and
+advantages against a hand-derived fixture, the Monte Carlo rate (no merges, or w = 0), the
+pooled rate at w = 1 and the z-score invariants of unshared groups.
 """
 from __future__ import annotations
 
@@ -469,3 +480,143 @@ def graph_suffix(labels, parent) -> Tuple[np.ndarray, np.ndarray]:
     for u in range(N):
         offs[u + 1] = offs[u] + len(out[u])
     return offs, np.array([c for cu in out for c in cu], dtype=np.int32)
+
+
+# ----------------------------------------------------------------------------------------------
+# Graph reward and the dual-group advantage
+# ----------------------------------------------------------------------------------------------
+
+def subtree_outcomes(parent, reward) -> Tuple[np.ndarray, np.ndarray]:
+    """c_own(v) = sum of R(z) and t_own(v) = |Z(v)| over the terminal states z reachable from v
+    through direct generation edges (v's own subtree, v included): Sec. 3.3. reward[v] is R(v)
+    in {0, 1} for a terminal state and -1 for any other state. Plain bottom-up accumulation."""
+    N = len(parent)
+    c = np.zeros(N, dtype=np.int64)
+    t = np.zeros(N, dtype=np.int64)
+    for v in range(N):
+        if reward[v] >= 0:
+            x = v
+            while x >= 0:                       # v is in the subtree of each of its ancestors
+                c[x] += int(reward[v])
+                t[x] += 1
+                x = int(parent[x])
+    return c, t
+
+
+def node_scores(parent, labels, reward, w: float) -> np.ndarray:
+    """S(v) = (c_own(v) + w sum_{q in Q(v), q != v} c_own(q)) /
+              (t_own(v) + w sum_{q in Q(v), q != v} t_own(q))   (Sec. 3.3, the pooled score).
+    Defined where the denominator is positive; NaN (no evidence) elsewhere."""
+    c, t = subtree_outcomes(parent, reward)
+    N = len(parent)
+    S = np.full(N, np.nan)
+    for v in range(N):
+        cs = float(c[v])
+        ts = float(t[v])
+        for q in range(N):
+            if q != v and labels[q] == labels[v]:
+                cs += w * float(c[q])
+                ts += w * float(t[q])
+        if ts > 0:
+            S[v] = cs / ts
+    return S
+
+
+def step_rewards(parent, S, edge_sim) -> np.ndarray:
+    """r_step(p(v), v) = (S(v) - S(p(v))) (1 - max(0, sim(p(v), v))) for the direct edge into
+    each non-root state v (Sec. 3.3); edge_sim[v] = sim(p(v), v). NaN for a root and where a
+    score is undefined."""
+    N = len(parent)
+    r = np.full(N, np.nan)
+    for v in range(N):
+        p = int(parent[v])
+        if p >= 0:
+            r[v] = (S[v] - S[p]) * (1.0 - max(0.0, float(edge_sim[v])))
+    return r
+
+
+def _zscores(values: Sequence[float]) -> List[float]:
+    """(x - mean) / std over a group, population std; 0 for every member if std = 0."""
+    n = len(values)
+    m = math.fsum(values) / n
+    sd = math.sqrt(math.fsum((x - m) ** 2 for x in values) / n)
+    return [0.0 if sd == 0 else (x - m) / sd for x in values]
+
+
+def correctness_advantage(parent, labels, r) -> np.ndarray:
+    """A_cor of the edge into every state (Sec. 3.4, the step correctness group).
+
+    The group of source state u is E_cor(u) = {(p(v), v) : v in C_g(u)}; groups exist for
+    |C_g(u)| > 1 (Alg. S.1, Stage 3). An edge's advantage is taken in the group of its own
+    source p(v); edges with an undefined reward take no part and get 0.
+    """
+    offs, states = graph_suffix(labels, parent)
+    N = len(parent)
+    A = np.zeros(N)
+    for v in range(N):
+        u = int(parent[v])
+        if u < 0 or np.isnan(r[v]):
+            continue
+        grp = [int(x) for x in states[offs[u]:offs[u + 1]]]
+        if len(grp) <= 1:
+            continue
+        vals = [float(r[x]) for x in grp if not np.isnan(r[x])]
+        z = _zscores(vals)
+        A[v] = z[[x for x in grp if not np.isnan(r[x])].index(v)]
+    return A
+
+
+def class_anchor(parent, members: Sequence[int]) -> int:
+    """a_Q: the deepest state that is a predecessor (a proper ancestor) of every member."""
+    def chain(v):
+        out = []
+        x = int(parent[v])
+        while x >= 0:
+            out.append(x)
+            x = int(parent[x])
+        return out
+    common = set(chain(members[0]))
+    for v in members[1:]:
+        common &= set(chain(v))
+    depth = state_depths(parent)
+    return max(common, key=lambda x: depth[x])
+
+
+def efficiency_advantage(parent, labels, S) -> np.ndarray:
+    """A_eff on the edge into every state (Sec. 3.4, the efficiency group).
+
+    For each class Q with |Q| >= 2: a_Q = class_anchor, l_v = d(v) - d(a_Q), the gate
+    S_bar = mean of the defined S over Q (0 if none), A_eff(v) = S_bar z(-l_v) over Q, and
+    A_eff(v) is given to every direct edge on the route from a_Q to v; an edge on several such
+    routes receives their sum.
+    """
+    N = len(parent)
+    depth = state_depths(parent)
+    E = np.zeros(N)
+    classes: dict = {}
+    for v in range(N):
+        classes.setdefault(int(labels[v]), []).append(v)
+    for members in classes.values():
+        if len(members) < 2:
+            continue
+        a = class_anchor(parent, members)
+        ell = [int(depth[v] - depth[a]) for v in members]
+        defined = [float(S[v]) for v in members if not np.isnan(S[v])]
+        gate = math.fsum(defined) / len(defined) if defined else 0.0
+        z = _zscores([-float(x) for x in ell])
+        for v, zv in zip(members, z):
+            x = v
+            while x != a:                        # edges (p(x), x) from a_Q down to v
+                E[x] += gate * zv
+                x = int(parent[x])
+    return E
+
+
+def graph_advantages(parent, labels, reward, edge_sim, w: float, lam: float) -> dict:
+    """The graph reward and dual-group advantage of every state's incoming edge (Sec. 3.3-3.4;
+    Alg. S.1, Stages 2-3): S, r_step, A_cor, A_eff and A_dual = A_cor + lam A_eff."""
+    S = node_scores(parent, labels, reward, w)
+    r = step_rewards(parent, S, edge_sim)
+    A_cor = correctness_advantage(parent, labels, r)
+    A_eff = efficiency_advantage(parent, labels, S)
+    return {"S": S, "r": r, "A_cor": A_cor, "A_eff": A_eff, "A_dual": A_cor + lam * A_eff}

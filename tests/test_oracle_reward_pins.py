@@ -1,0 +1,172 @@
+"""Pins of the oracle's graph reward (node scores, step rewards) and dual-group advantage
+against facts that do not come from the oracle itself: a hand-derived fixture, the Monte Carlo
+rate it reduces to without merges or with w = 0, the pooled closed form at w = 1, and the
+z-score invariants of the correctness groups.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+from oracle import graphattn_oracle as O
+from paper_2606_18954_amd import workloads as W
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _fixture():
+    with open(os.path.join(GOLDEN, "graph_reward_small.json")) as f:
+        return json.load(f)
+
+
+def _euler(parent):
+    N = len(parent)
+    kids = [[] for _ in range(N)]
+    for v, p in enumerate(parent):
+        if p >= 0:
+            kids[p].append(v)
+    tin, tout, clock = [0] * N, [0] * N, 0
+    for r in [v for v in range(N) if parent[v] < 0]:
+        stack = [(r, 0)]
+        while stack:
+            v, i = stack.pop()
+            if i == 0:
+                tin[v] = clock
+                clock += 1
+            if i < len(kids[v]):
+                stack.append((v, i + 1))
+                stack.append((kids[v][i], 0))
+            else:
+                tout[v] = clock
+    return tin, tout
+
+
+def _random_rollout(seed, prompts=3, sched=(3, 3, 2), merge_every=5):
+    rng = np.random.default_rng(seed)
+    parent = W.state_forest(prompts, sched)
+    N = len(parent)
+    kids = np.bincount(parent[parent >= 0], minlength=N)
+    reward = np.where(kids == 0, rng.integers(0, 2, N), -1)
+    reward[rng.random(N) < 0.1] = -1                # some leaves stopped early
+    labels = np.arange(N, dtype=np.int32)
+    depth = O.state_depths(parent)
+    roots = np.nonzero(parent < 0)[0].tolist() + [N]
+    for a, b in zip(roots[:-1], roots[1:]):         # link a few same-depth states per prompt
+        for v in range(a + 1, b, merge_every):
+            same = [u for u in range(a + 1, b) if depth[u] == depth[v] and u != v]
+            if same:
+                u = int(rng.choice(same))
+                lo, hi = min(labels[u], labels[v]), max(labels[u], labels[v])
+                labels[labels == hi] = lo
+    sim = rng.uniform(-0.3, 1.0, N)
+    return parent, reward, labels, sim
+
+
+def check_fixture(mod):
+    fx = _fixture()
+    res = mod.graph_advantages(np.array(fx["parent"]), np.array(fx["labels"]),
+                               np.array(fx["reward"]), np.array(fx["edge_sim"]), fx["w"],
+                               fx["lambda_eff"])
+    for k in ["S", "r", "A_cor", "A_eff", "A_dual"]:
+        exp = np.array([np.nan if x is None else x for x in fx[k]])
+        assert np.allclose(res[k], exp, rtol=0, atol=1e-12, equal_nan=True), k
+
+
+def check_monte_carlo_rate(mod, seed=61):
+    """Without merges, and with merges at w = 0, S(v) is the share of correct terminal states
+    in v's subtree (counted here with the test's own Euler intervals)."""
+    parent, reward, labels, sim = _random_rollout(seed)
+    tin, tout = _euler(parent)
+    N = len(parent)
+    for lab, w in [(np.arange(N), 0.7), (labels, 0.0)]:
+        S = mod.node_scores(parent, lab, reward, w)
+        for v in range(N):
+            under = [z for z in range(N) if reward[z] >= 0 and tin[v] <= tin[z] < tout[v]]
+            if under:
+                assert abs(S[v] - sum(reward[z] for z in under) / len(under)) < 1e-15
+            else:
+                assert np.isnan(S[v])
+
+
+def check_full_pooling(mod, seed=62):
+    """At w = 1 every member of a class gets the class's pooled rate."""
+    parent, reward, labels, sim = _random_rollout(seed)
+    c, t = mod.subtree_outcomes(parent, reward)
+    S = mod.node_scores(parent, labels, reward, 1.0)
+    for lab in set(labels.tolist()):
+        m = labels == lab
+        if t[m].sum() > 0:
+            assert np.allclose(S[m], c[m].sum() / t[m].sum(), rtol=0, atol=1e-15)
+
+
+def check_step_reward_discount(mod):
+    parent = np.array([-1, 0, 0, 0])
+    S = np.array([0.5, 1.0, 0.0, 0.25])
+    r = mod.step_rewards(parent, S, np.array([0.0, -0.4, 1.0, 0.5]))
+    assert np.isnan(r[0]) and r[1] == 0.5 and r[2] == 0.0 and r[3] == -0.125
+
+
+def check_correctness_groups(mod, seed=63):
+    """In a group without shared successors (C_g(u) = C(u)), the advantages of u's edges are the
+    z-scores of their rewards: mean 0 and population variance 1 (or all 0)."""
+    parent, reward, labels, sim = _random_rollout(seed)
+    N = len(parent)
+    res = mod.graph_advantages(parent, np.arange(N), reward, sim, 0.7, 0.3)
+    for u in range(N):
+        kids = [v for v in range(N) if parent[v] == u and not np.isnan(res["r"][v])]
+        if len(kids) < 2 or len([v for v in range(N) if parent[v] == u]) < 2:
+            continue
+        a = res["A_cor"][kids]
+        assert abs(a.mean()) < 1e-12
+        assert abs(np.mean(a * a) - 1) < 1e-12 or np.all(a == 0)
+    assert np.all(res["A_eff"] == 0)                  # no class of two or more
+
+
+PINS = [check_fixture, check_monte_carlo_rate, check_full_pooling, check_step_reward_discount,
+        check_correctness_groups]
+
+
+@pytest.mark.parametrize("pin", PINS, ids=[p.__name__ for p in PINS])
+def test_reward_pin(pin):
+    pin(O)
+
+
+ORIG_SCORES = O.node_scores
+ORIG_SUFFIX = O.graph_suffix
+ORIG_EFF = O.efficiency_advantage
+
+
+def _sample_std(values):
+    n = len(values)
+    m = sum(values) / n
+    sd = math.sqrt(sum((x - m) ** 2 for x in values) / max(1, n - 1))
+    return [0.0 if sd == 0 else (x - m) / sd for x in values]
+
+
+def _own_children_only(labels, parent):
+    return ORIG_SUFFIX(np.arange(len(parent)), parent)
+
+
+@pytest.mark.parametrize("name,attr,repl", [
+    ("no_pooling", "node_scores", lambda p, l, r, w: ORIG_SCORES(p, l, r, 0.0)),
+    ("sample_std", "_zscores", _sample_std),
+    ("shared_successors_ignored", "graph_suffix", _own_children_only),
+    ("similarity_not_clipped", "step_rewards",
+     lambda parent, S, sim: np.array([np.nan if parent[v] < 0 else
+                                      (S[v] - S[parent[v]]) * (1 - sim[v])
+                                      for v in range(len(parent))])),
+    ("gate_ignored", "efficiency_advantage",
+     lambda parent, labels, S: ORIG_EFF(parent, labels, np.ones_like(S))),
+])
+def test_planted_mistake_is_caught(monkeypatch, name, attr, repl):
+    monkeypatch.setattr(O, attr, repl)
+    caught = False
+    for pin in PINS:
+        try:
+            pin(O)
+        except (AssertionError, IndexError, ValueError):
+            caught = True
+            break
+    assert caught, f"planted mistake {name} went unnoticed"

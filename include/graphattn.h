@@ -238,8 +238,11 @@ typedef struct {
 typedef struct ga_forest ga_forest;
 ga_status graphattn_forest_create(const ga_state_forest* forest, void* hip_stream,
                                   ga_forest** out);
+/* forest_classes also writes, when edge_sim is not NULL, edge_sim[v] = sim(p(v), v) (device
+ * float [N], 0 for a root): the cosine of each state with its predecessor, from the same
+ * products (the graph reward's endpoint similarity). */
 ga_status graphattn_forest_classes(ga_forest* forest, const void* embeddings, int32_t dim,
-                                   int32_t dtype, float kappa, int32_t* labels,
+                                   int32_t dtype, float kappa, int32_t* labels, float* edge_sim,
                                    void* hip_stream);
 ga_status graphattn_forest_suffix(ga_forest* forest, const int32_t* labels,
                                   int64_t* suffix_offsets, int32_t* suffix_states,
@@ -272,6 +275,40 @@ ga_status graphattn_equivalence_classes(const void* embeddings, int32_t dim, int
 ga_status graphattn_graph_suffix(const int32_t* labels, const ga_state_forest* forest,
                                  int64_t* suffix_offsets, int32_t* suffix_states,
                                  int64_t capacity, int64_t* total, void* hip_stream);
+
+/* Graph reward and dual-group advantage (Sec. 3.3-3.4; Alg. S.1, Stages 2-3) for every
+ * state v and the direct edge (p(v), v) into it.  Device inputs of N entries:
+ *   labels    classes as written by forest_classes (a label outside [v's prompt's first state,
+ *             v] is read as v itself)
+ *   reward    R(v) (0 or 1) for a terminal state, any negative value for other states
+ *   edge_sim  sim(p(v), v), e.g. from forest_classes (roots ignored)
+ * w in [0, 1] pools the outcomes of class partners; lambda_eff >= 0 weighs efficiency.
+ * Outputs (device double [N] each):
+ *   score        S(v) = (c_own(v) + w sum_{q in Q(v)\v} c_own(q)) / (t_own(v) + w sum t_own(q)),
+ *                c_own / t_own = correct / all terminal states in v's subtree; NaN when the
+ *                denominator is 0 (no evidence)
+ *   step_reward  r(v) = (S(v) - S(p(v))) (1 - max(0, edge_sim(v))); NaN for a root or an
+ *                undefined score
+ *   a_cor        z-score of r(v) (population std) among the defined rewards of the group
+ *                E_cor(p(v)) = edges into C_g(p(v)), when that group has two or more edges and a
+ *                non-zero spread; 0 otherwise
+ *   a_eff        sum, over the classes Q of two or more and their members x whose route from
+ *                a_Q (the deepest proper ancestor of all of Q) passes through this edge, of
+ *                mean_Q(S) z(-l_x), l_x = d(x) - d(a_Q) (z over Q, population std; 0 if no
+ *                spread)
+ *   a_dual       a_cor + lambda_eff a_eff
+ * Asynchronous on hip_stream; deterministic. */
+typedef struct {
+  double* score;
+  double* step_reward;
+  double* a_cor;
+  double* a_eff;
+  double* a_dual;
+} ga_advantages;
+ga_status graphattn_forest_advantages(ga_forest* forest, const int32_t* labels,
+                                      const int32_t* reward, const float* edge_sim, double w,
+                                      double lambda_eff, const ga_advantages* out,
+                                      void* hip_stream);
 
 /* Release the plan and its device workspace (waits for work still using it). */
 void graphattn_plan_destroy(ga_plan* plan);

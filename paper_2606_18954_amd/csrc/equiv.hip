@@ -150,7 +150,9 @@ __global__ __launch_bounds__(256) void k_sim_union(EquivArgs a) {
         if (u >= v) continue;
         const int tin_u = a.tin[u], tout_u = a.tout[u];
         const bool related = (tin_u <= tin_v && tin_v < tout_u) || (tin_v <= tin_u && tin_u < tout_v);
-        if (!related && acc[x][y][i] * a.inv_norm[u] * nv >= a.kappa) unite(a.rep, u, v);
+        const float cs = acc[x][y][i] * a.inv_norm[u] * nv;
+        if (!related && cs >= a.kappa) unite(a.rep, u, v);
+        if (a.edge_sim && a.parent[v] == u) a.edge_sim[v] = cs;
       }
   }
 }
@@ -190,7 +192,7 @@ __device__ void lds_unite(int* r, int a, int b) {
 __global__ __launch_bounds__(512, 2) void k_prompt_classes(EquivArgs a) {
   __shared__ __align__(16) unsigned char stage[2][kPromptMax * kKC * 2];
   __shared__ float s_inv[kPromptMax];
-  __shared__ int s_tin[kPromptMax], s_tout[kPromptMax], s_rep[kPromptMax];
+  __shared__ int s_tin[kPromptMax], s_tout[kPromptMax], s_rep[kPromptMax], s_par[kPromptMax];
   const int2 pr = a.prompts[blockIdx.x];          // (first state, states)
   const int s0 = pr.x, n = pr.y;
   const int tid = threadIdx.x, lane = tid & 63;
@@ -234,6 +236,7 @@ __global__ __launch_bounds__(512, 2) void k_prompt_classes(EquivArgs a) {
     s_rep[tid] = tid;
     s_tin[tid] = tid < n ? a.tin[s0 + tid] : 0;
     s_tout[tid] = tid < n ? a.tout[s0 + tid] : 0;
+    s_par[tid] = tid < n ? a.parent[s0 + tid] - s0 : -1;   // prompt-local (-1 - s0 for the root)
   }
   const int nk = a.dim / kKC;
   gload(0);
@@ -285,11 +288,16 @@ __global__ __launch_bounds__(512, 2) void k_prompt_classes(EquivArgs a) {
       if (u >= v) continue;
       const int tin_u = s_tin[u], tout_u = s_tout[u];
       const bool related = (tin_u <= tin_v && tin_v < tout_u) || (tin_v <= tin_u && tin_u < tout_v);
-      if (!related && acc[k][i] * s_inv[u] * nv >= a.kappa) lds_unite(s_rep, u, v);
+      const float cs = acc[k][i] * s_inv[u] * nv;
+      if (!related && cs >= a.kappa) lds_unite(s_rep, u, v);
+      if (a.edge_sim && s_par[v] == u) a.edge_sim[s0 + v] = cs;
     }
   }
   __syncthreads();
-  if (tid < n) a.labels[s0 + tid] = s0 + lds_find(s_rep, tid);
+  if (tid < n) {
+    a.labels[s0 + tid] = s0 + lds_find(s_rep, tid);
+    if (a.edge_sim && s_par[tid] < 0) a.edge_sim[s0 + tid] = 0.f;
+  }
 }
 
 // Final labels: every state's root (all links have landed: kernel boundary).
@@ -298,6 +306,7 @@ __global__ void k_labels(EquivArgs a) {
   if (i >= a.n_big) return;
   const int v = a.big[i];
   a.labels[v] = find_root(a.rep, v);
+  if (a.edge_sim && a.parent[v] < 0) a.edge_sim[v] = 0.f;
 }
 
 // Graph suffix, pass 1 (count into cnt[u]) or pass 2 (write from off[u]).

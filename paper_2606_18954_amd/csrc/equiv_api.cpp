@@ -145,6 +145,10 @@ struct ga_forest {
   float* inv_norm = nullptr;
   int* rep = nullptr;
   int64_t *cnt = nullptr, *off = nullptr, *blk = nullptr;
+  // graph reward scratch
+  int32_t *lab = nullptr, *anchor = nullptr;
+  int64_t *euler = nullptr, *pre = nullptr, *own = nullptr, *ctot = nullptr;
+  double *aeff_node = nullptr, *gmean = nullptr, *gstd = nullptr;
 };
 
 namespace {
@@ -177,7 +181,9 @@ ga_status forest_create(const ga_state_forest* forest, hipStream_t stream, ga_fo
   const size_t up = 6 * n4 + align256(sizeof(int4) * fo.items.size()) +
                     align256(sizeof(int2) * fo.prompts.size()) + align256(4 * fo.big.size());
   const size_t nblk = (size_t)((fo.N + 1023) / 1024);
-  const size_t total = up + 2 * n4 + n8 + align256(8 * (fo.N + 1)) + align256(8 * (nblk + 1));
+  const size_t scan = align256(8 * (fo.N + 1));
+  const size_t total = up + 2 * n4 + n8 + scan + align256(8 * (nblk + 1))   // classes, suffix
+                       + 2 * n4 + 3 * n8 + scan + 3 * n8;                     // graph reward
   if (hipMalloc(&f->dev, total) != hipSuccess) {
     (void)hipGetLastError();
     f->dev = nullptr;
@@ -216,7 +222,17 @@ ga_status forest_create(const ga_state_forest* forest, hipStream_t stream, ga_fo
   f->rep = reinterpret_cast<int*>(d + up + n4);
   f->cnt = reinterpret_cast<int64_t*>(d + up + 2 * n4);
   f->off = reinterpret_cast<int64_t*>(d + up + 2 * n4 + n8);
-  f->blk = reinterpret_cast<int64_t*>(d + up + 2 * n4 + n8 + align256(8 * (fo.N + 1)));
+  f->blk = reinterpret_cast<int64_t*>(d + up + 2 * n4 + n8 + scan);
+  char* r = d + up + 2 * n4 + n8 + scan + align256(8 * (nblk + 1));
+  f->lab = reinterpret_cast<int32_t*>(r);
+  f->anchor = reinterpret_cast<int32_t*>(r + n4);
+  f->euler = reinterpret_cast<int64_t*>(r + 2 * n4);
+  f->own = reinterpret_cast<int64_t*>(r + 2 * n4 + n8);
+  f->ctot = reinterpret_cast<int64_t*>(r + 2 * n4 + 2 * n8);
+  f->pre = reinterpret_cast<int64_t*>(r + 2 * n4 + 3 * n8);
+  f->aeff_node = reinterpret_cast<double*>(r + 2 * n4 + 3 * n8 + scan);
+  f->gmean = reinterpret_cast<double*>(r + 2 * n4 + 4 * n8 + scan);
+  f->gstd = reinterpret_cast<double*>(r + 2 * n4 + 5 * n8 + scan);
   if (up > 0) {
     const hipError_t e = hipMemcpyAsync(d, pin, up, hipMemcpyHostToDevice, stream);
     if (e != hipSuccess) {
@@ -229,7 +245,7 @@ ga_status forest_create(const ga_state_forest* forest, hipStream_t stream, ga_fo
 }
 
 ga_status forest_classes(ga_forest* f, const void* embeddings, int32_t dim, int32_t dtype,
-                         float kappa, int32_t* labels, hipStream_t stream) {
+                         float kappa, int32_t* labels, float* edge_sim, hipStream_t stream) {
   if (!f) return efail(GA_EINVAL, "forest is NULL");
   if (dtype != GA_BF16) return efail(GA_EUNSUPPORTED, "embeddings must be bf16");
   if (dim < 64 || dim % 64) return efail(GA_EUNSUPPORTED, "dim %d unsupported (a multiple of 64)", dim);
@@ -238,8 +254,11 @@ ga_status forest_classes(ga_forest* f, const void* embeddings, int32_t dim, int3
   if (!embeddings || !labels) return efail(GA_EINVAL, "embeddings and labels must be non-NULL");
   if (reinterpret_cast<uintptr_t>(embeddings) & 15)
     return efail(GA_EINVAL, "embeddings must be 16-byte aligned");
-  if (reinterpret_cast<uintptr_t>(labels) & 3) return efail(GA_EINVAL, "labels must be 4-byte aligned");
+  if ((reinterpret_cast<uintptr_t>(labels) | reinterpret_cast<uintptr_t>(edge_sim)) & 3)
+    return efail(GA_EINVAL, "labels and edge_sim must be 4-byte aligned");
   ga::EquivArgs a{};
+  a.parent = f->parent;
+  a.edge_sim = edge_sim;
   a.z = static_cast<const unsigned short*>(embeddings);
   a.tin = f->tin;
   a.tout = f->tout;
@@ -315,11 +334,66 @@ ga_status graphattn_forest_create(const ga_state_forest* forest, void* hip_strea
 }
 
 ga_status graphattn_forest_classes(ga_forest* forest, const void* embeddings, int32_t dim,
-                                   int32_t dtype, float kappa, int32_t* labels,
+                                   int32_t dtype, float kappa, int32_t* labels, float* edge_sim,
                                    void* hip_stream) {
   ga::host_clear_error();
-  return forest_classes(forest, embeddings, dim, dtype, kappa, labels,
+  return forest_classes(forest, embeddings, dim, dtype, kappa, labels, edge_sim,
                         static_cast<hipStream_t>(hip_stream));
+}
+
+ga_status graphattn_forest_advantages(ga_forest* forest, const int32_t* labels,
+                                      const int32_t* reward, const float* edge_sim, double w,
+                                      double lambda_eff, const ga_advantages* out,
+                                      void* hip_stream) {
+  ga::host_clear_error();
+  if (!forest) return efail(GA_EINVAL, "forest is NULL");
+  if (!out) return efail(GA_EINVAL, "out is NULL");
+  if (!std::isfinite(w) || w < 0.0 || w > 1.0) return efail(GA_EINVAL, "w must lie in [0, 1]");
+  if (!std::isfinite(lambda_eff) || lambda_eff < 0.0)
+    return efail(GA_EINVAL, "lambda_eff must be finite and >= 0");
+  const int64_t N = forest->fo.N;
+  if (N == 0) return GA_OK;
+  const void* ptrs[] = {labels, reward, edge_sim, out->score, out->step_reward, out->a_cor,
+                        out->a_eff, out->a_dual};
+  for (const void* q : ptrs)
+    if (!q) return efail(GA_EINVAL, "device arrays must be non-NULL");
+  if ((reinterpret_cast<uintptr_t>(labels) | reinterpret_cast<uintptr_t>(reward) |
+       reinterpret_cast<uintptr_t>(edge_sim)) & 3)
+    return efail(GA_EINVAL, "labels, reward and edge_sim must be 4-byte aligned");
+  if ((reinterpret_cast<uintptr_t>(out->score) | reinterpret_cast<uintptr_t>(out->step_reward) |
+       reinterpret_cast<uintptr_t>(out->a_cor) | reinterpret_cast<uintptr_t>(out->a_eff) |
+       reinterpret_cast<uintptr_t>(out->a_dual)) & 7)
+    return efail(GA_EINVAL, "output arrays must be 8-byte aligned");
+  ga::RewardArgs a{};
+  a.labels = labels;
+  a.reward = reward;
+  a.edge_sim = edge_sim;
+  a.parent = forest->parent;
+  a.depth = forest->depth;
+  a.tin = forest->tin;
+  a.tout = forest->tout;
+  a.pstart = forest->pstart;
+  a.pend = forest->pend;
+  a.lab = forest->lab;
+  a.euler = forest->euler;
+  a.pre = forest->pre;
+  a.blk = forest->blk;
+  a.own = forest->own;
+  a.ctot = forest->ctot;
+  a.anchor = forest->anchor;
+  a.aeff_node = forest->aeff_node;
+  a.gmean = forest->gmean;
+  a.gstd = forest->gstd;
+  a.score = out->score;
+  a.step = out->step_reward;
+  a.a_cor = out->a_cor;
+  a.a_eff = out->a_eff;
+  a.a_dual = out->a_dual;
+  a.N = N;
+  a.w = w;
+  a.lambda_eff = lambda_eff;
+  EQ_HIP(ga::launch_advantages(a, static_cast<hipStream_t>(hip_stream)), "advantage launch");
+  return GA_OK;
 }
 
 ga_status graphattn_forest_suffix(ga_forest* forest, const int32_t* labels,
@@ -351,7 +425,7 @@ ga_status graphattn_equivalence_classes(const void* embeddings, int32_t dim, int
   ga_forest* f = nullptr;
   rc = forest_create(forest, stream, &f);
   if (rc) return rc;
-  rc = forest_classes(f, embeddings, dim, dtype, kappa, labels, stream);
+  rc = forest_classes(f, embeddings, dim, dtype, kappa, labels, nullptr, stream);
   forest_free(f);
   return rc;
 }

@@ -132,6 +132,8 @@ struct EquivArgs {
   const int2* prompts;     // [n_prompts] (first state, states) of the prompts of <= 256 states
   const int32_t* big;      // [n_big] the states of the larger prompts
   int32_t* labels;         // [N]  output: smallest state of the class
+  const int32_t* parent;   // [N]
+  float* edge_sim;         // [N]  optional output: sim(p(v), v), 0 for a root
   int64_t N, n_items, n_prompts, n_big;
   int32_t dim;
   float kappa;
@@ -150,6 +152,26 @@ struct SuffixArgs {
   int64_t N;
 };
 
+// Graph reward and dual-group advantage (reward.hip).  Device arrays of N states unless noted.
+struct RewardArgs {
+  const int32_t* labels;   // class labels (smallest member)
+  const int32_t* reward;   // R(v) >= 0 for a terminal state, negative otherwise
+  const float* edge_sim;   // sim(p(v), v)
+  const int32_t *parent, *depth, *tin, *tout, *pstart, *pend;
+  int32_t* lab;            // labels, sanitised
+  int64_t* euler;          // packed (R, 1) of terminal states in Euler order
+  int64_t* pre;            // [N + 1] its exclusive prefix sums
+  int64_t* blk;            // scan block totals
+  int64_t* own;            // packed (c_own, t_own)
+  int64_t* ctot;           // packed class totals, by label
+  int32_t* anchor;         // a_Q of each member of a class of two or more, else -1
+  double* aeff_node;       // A_eff(v) of each such member
+  double *gmean, *gstd;    // correctness-group statistics of each source state
+  double *score, *step, *a_cor, *a_eff, *a_dual;   // outputs
+  int64_t N;
+  double w, lambda_eff;
+};
+
 // Launchers (each returns the launch status).
 hipError_t launch_schedule(const DevGraph& g, const DevSchedule& sc, int32_t group,
                            int32_t chunk_pages, int64_t max_items, hipStream_t stream);
@@ -161,6 +183,7 @@ hipError_t launch_kv_write(const KvWriteArgs& a, hipStream_t stream);
 hipError_t launch_equivalence(const EquivArgs& a, hipStream_t stream);
 hipError_t launch_suffix_count(const SuffixArgs& a, hipStream_t stream);
 hipError_t launch_suffix_fill(const SuffixArgs& a, hipStream_t stream);
+hipError_t launch_advantages(const RewardArgs& a, hipStream_t stream);
 // Number of co-resident attention workgroups the persistent grid uses on this device.
 int seg_attn_grid(int head_dim, bool bf16, int num_cus);
 

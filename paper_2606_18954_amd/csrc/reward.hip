@@ -1,0 +1,234 @@
+// Graph reward and dual-group advantage over the rollout states (Sec. 3.3-3.4; Alg. S.1,
+// Stages 2-3), one pass per step over all states of a batch.
+//
+//   outcomes   c_own / t_own: sums over the terminal states of each state's subtree.  With the
+//              states placed in Euler order (tin), a subtree is the contiguous range
+//              [tin(v), tout(v)), so one prefix sum of the packed (R, 1) values of terminal states
+//              gives every subtree's sums as a difference (integers: exact).
+//   pooling    class totals by integer atomics (exact, so the order they land in is irrelevant);
+//              S(v) = (c + w (C_Q - c)) / (t + w (T_Q - t)) in fp64, NaN without evidence.
+//   step       r(v) = (S(v) - S(p(v))) (1 - max(0, sim(p(v), v))) on the edge into v.
+//   correctness  the group of source u is E_cor(u) = {edges into C_g(u)}: u's successors plus
+//              those of its class partners that lie deeper than u, found by one scan over the
+//              prompt's states; mean and population std of the defined rewards; the edge into v
+//              takes its z-score in the group of p(v) (0 without spread or reward).
+//   efficiency per class of two or more (found by its smallest member): the deepest proper
+//              ancestor a_Q of all members, route lengths l = d(v) - d(a_Q), z-scores of -l
+//              gated by the class's mean defined score; every edge then sums, in ascending
+//              state order, the values of the members in its subtree whose anchor lies above it.
+//   dual       A_dual = A_cor + lambda A_eff.
+// Every value is computed in a fixed order, so the results are deterministic.
+#include "ga_internal.hpp"
+
+namespace ga {
+namespace {
+
+constexpr int kB = 256;
+
+__device__ __forceinline__ int64_t gid() { return (int64_t)blockIdx.x * kB + threadIdx.x; }
+
+__global__ void k_outcome_vals(RewardArgs a) {
+  const int64_t v = gid();
+  if (v >= a.N) return;
+  // A label must name a state of the same prompt no later than v (the smallest member of v's
+  // class); anything else is read as v itself, so no index leaves the prompt.
+  const int l = a.labels[v];
+  a.lab[v] = (l >= a.pstart[v] && l <= (int)v) ? l : (int)v;
+  const int r = a.reward[v];
+  a.euler[a.tin[v]] = r >= 0 ? (((int64_t)r << 32) | 1) : 0;
+  a.ctot[v] = 0;                                  // class totals, indexed by label
+}
+
+// Exclusive scan of euler[0, N) into pre[0, N] over many workgroups (block totals first).
+__global__ __launch_bounds__(1024) void k_pre_sums(RewardArgs a) {
+  __shared__ int64_t red[16];
+  const int64_t i = (int64_t)blockIdx.x * 1024 + threadIdx.x;
+  int64_t v = i < a.N ? a.euler[i] : 0;
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int64_t t = 0;
+    for (int w = 0; w < 16; ++w) t += red[w];
+    a.blk[blockIdx.x] = t;
+  }
+}
+
+__global__ __launch_bounds__(1024) void k_pre_apply(RewardArgs a) {
+  __shared__ int64_t red[16], wsum[16];
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  int64_t pre = 0;
+  for (int k = t; k < (int)blockIdx.x; k += 1024) pre += a.blk[k];
+  for (int o = 32; o > 0; o >>= 1) pre += __shfl_xor(pre, o);
+  if (lane == 0) red[w] = pre;
+  __syncthreads();
+  int64_t base = 0;
+  for (int k = 0; k < 16; ++k) base += red[k];
+  const int64_t i = (int64_t)blockIdx.x * 1024 + t;
+  const int64_t v = i < a.N ? a.euler[i] : 0;
+  int64_t x = v;
+  for (int o = 1; o < 64; o <<= 1) {
+    const int64_t y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) wsum[w] = x;
+  __syncthreads();
+  int64_t before = 0;
+  for (int k = 0; k < w; ++k) before += wsum[k];
+  if (i < a.N) a.pre[i] = base + before + x - v;
+  if (i == a.N - 1) a.pre[a.N] = base + before + x;
+}
+
+// Own outcomes (packed: correct << 32 | terminal states) and their class totals.
+__global__ void k_own(RewardArgs a) {
+  const int64_t v = gid();
+  if (v >= a.N) return;
+  const int64_t own = a.pre[a.tout[v]] - a.pre[a.tin[v]];
+  a.own[v] = own;
+  atomicAdd(reinterpret_cast<unsigned long long*>(a.ctot + a.lab[v]), (unsigned long long)own);
+}
+
+__global__ void k_scores(RewardArgs a) {
+  const int64_t v = gid();
+  if (v >= a.N) return;
+  const int64_t own = a.own[v], tot = a.ctot[a.lab[v]];
+  const double c = (double)(own >> 32), t = (double)(own & 0xffffffffLL);
+  const double C = (double)(tot >> 32), T = (double)(tot & 0xffffffffLL);
+  const double num = c + a.w * (C - c), den = t + a.w * (T - t);
+  a.score[v] = den > 0.0 ? num / den : __builtin_nan("");
+  a.anchor[v] = -1;                               // set for class members by the next kernel
+  a.aeff_node[v] = 0.0;
+}
+
+// Step rewards; and, for the smallest member of each class of two or more, the class's
+// anchor, its members' efficiency values and their anchors.
+__global__ void k_step_and_classes(RewardArgs a) {
+  const int64_t v = gid();
+  if (v >= a.N) return;
+  const int p = a.parent[v];
+  double r = __builtin_nan("");
+  if (p >= 0) {
+    const double s = fmax(0.0, (double)a.edge_sim[v]);
+    r = (a.score[v] - a.score[p]) * (1.0 - s);
+  }
+  a.step[v] = r;
+  if (a.lab[v] != (int)v) return;               // not the smallest member of its class
+  const int lo = a.pstart[v], hi = a.pend[v];
+  int m = 0, lca = -1;
+  double ssum = 0.0;
+  int sdef = 0;
+  for (int x = (int)v; x < hi; ++x) {
+    if (a.lab[x] != (int)v) continue;
+    ++m;
+    if (!isnan(a.score[x])) {
+      ssum += a.score[x];
+      ++sdef;
+    }
+    if (lca < 0) {
+      lca = x;
+      continue;
+    }
+    int y = x, z = lca;                            // lowest common ancestor by depth walking
+    while (a.depth[y] > a.depth[z]) y = a.parent[y];
+    while (a.depth[z] > a.depth[y]) z = a.parent[z];
+    while (y != z) {
+      y = a.parent[y];
+      z = a.parent[z];
+    }
+    lca = y;
+  }
+  (void)lo;
+  if (m < 2) return;
+  const int anc = a.lab[lca] == (int)v ? a.parent[lca] : lca;   // a proper ancestor of all
+  if (anc < 0) return;                             // a class holding its prompt's root
+  const double gate = sdef > 0 ? ssum / sdef : 0.0;
+  double lsum = 0.0;
+  for (int x = (int)v; x < hi; ++x)
+    if (a.lab[x] == (int)v) lsum += -(double)(a.depth[x] - a.depth[anc]);
+  const double mean = lsum / m;
+  double q = 0.0;
+  for (int x = (int)v; x < hi; ++x)
+    if (a.lab[x] == (int)v) {
+      const double d = -(double)(a.depth[x] - a.depth[anc]) - mean;
+      q += d * d;
+    }
+  const double sd = sqrt(q / m);
+  for (int x = (int)v; x < hi; ++x)
+    if (a.lab[x] == (int)v) {
+      const double l = -(double)(a.depth[x] - a.depth[anc]);
+      a.aeff_node[x] = sd > 0.0 ? gate * (l - mean) / sd : 0.0;
+      a.anchor[x] = anc;
+    }
+}
+
+// Correctness-group statistics of every source state u (over E_cor(u)), and the efficiency
+// value of the edge into every state.
+__global__ void k_groups_and_routes(RewardArgs a) {
+  const int64_t u = gid();
+  if (u >= a.N) return;
+  const int lu = a.lab[u], du = a.depth[u], lo = a.pstart[u], hi = a.pend[u];
+  int n = 0, members = 0;
+  double s = 0.0;
+  for (int c = lo; c < hi; ++c) {
+    const int p = a.parent[c];
+    if (p < 0 || !(p == (int)u || (a.lab[p] == lu && a.depth[c] > du))) continue;
+    ++members;
+    if (isnan(a.step[c])) continue;
+    s += a.step[c];
+    ++n;
+  }
+  double mean = 0.0, sd = 0.0;
+  if (members > 1 && n > 0) {
+    mean = s / n;
+    double q = 0.0;
+    for (int c = lo; c < hi; ++c) {
+      const int p = a.parent[c];
+      if (p < 0 || !(p == (int)u || (a.lab[p] == lu && a.depth[c] > du))) continue;
+      if (isnan(a.step[c])) continue;
+      const double d = a.step[c] - mean;
+      q += d * d;
+    }
+    sd = sqrt(q / n);
+  }
+  a.gmean[u] = mean;
+  a.gstd[u] = sd;                                  // 0: no group, or no spread
+  double e = 0.0;
+  if (a.parent[u] >= 0) {
+    const int tin_u = a.tin[u], tout_u = a.tout[u];
+    for (int x = lo; x < hi; ++x) {
+      const int an = a.anchor[x];
+      if (an < 0 || a.tin[x] < tin_u || a.tin[x] >= tout_u) continue;
+      if (a.depth[an] < du) e += a.aeff_node[x];
+    }
+  }
+  a.a_eff[u] = e;
+}
+
+__global__ void k_dual(RewardArgs a) {
+  const int64_t v = gid();
+  if (v >= a.N) return;
+  const int p = a.parent[v];
+  double c = 0.0;
+  if (p >= 0 && !isnan(a.step[v]) && a.gstd[p] > 0.0) c = (a.step[v] - a.gmean[p]) / a.gstd[p];
+  a.a_cor[v] = c;
+  a.a_dual[v] = c + a.lambda_eff * a.a_eff[v];
+}
+
+}  // namespace
+
+hipError_t launch_advantages(const RewardArgs& a, hipStream_t stream) {
+  if (a.N == 0) return hipSuccess;
+  const unsigned g = (unsigned)((a.N + kB - 1) / kB);
+  const unsigned sb = (unsigned)((a.N + 1023) / 1024);
+  hipLaunchKernelGGL(k_outcome_vals, dim3(g), dim3(kB), 0, stream, a);
+  hipLaunchKernelGGL(k_pre_sums, dim3(sb), dim3(1024), 0, stream, a);
+  hipLaunchKernelGGL(k_pre_apply, dim3(sb), dim3(1024), 0, stream, a);
+  hipLaunchKernelGGL(k_own, dim3(g), dim3(kB), 0, stream, a);
+  hipLaunchKernelGGL(k_scores, dim3(g), dim3(kB), 0, stream, a);
+  hipLaunchKernelGGL(k_step_and_classes, dim3(g), dim3(kB), 0, stream, a);
+  hipLaunchKernelGGL(k_groups_and_routes, dim3(g), dim3(kB), 0, stream, a);
+  hipLaunchKernelGGL(k_dual, dim3(g), dim3(kB), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace ga

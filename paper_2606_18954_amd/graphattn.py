@@ -61,6 +61,11 @@ class StateForest(ctypes.Structure):
     _fields_ = [("num_states", ctypes.c_int32), ("parent", ctypes.POINTER(ctypes.c_int32))]
 
 
+class Advantages(ctypes.Structure):
+    _fields_ = [("score", ctypes.c_void_p), ("step_reward", ctypes.c_void_p),
+                ("a_cor", ctypes.c_void_p), ("a_eff", ctypes.c_void_p), ("a_dual", ctypes.c_void_p)]
+
+
 class Profile(ctypes.Structure):
     _fields_ = [("schedules", ctypes.c_int32), ("runs", ctypes.c_int32),
                 ("sched_ms", ctypes.c_double), ("attn_ms", ctypes.c_double),
@@ -102,7 +107,10 @@ def load_library() -> ctypes.CDLL:
     lib.graphattn_graph_suffix.restype = ctypes.c_int
     lib.graphattn_forest_create.argtypes = [P(StateForest), vp, P(vp)]
     lib.graphattn_forest_create.restype = ctypes.c_int
-    lib.graphattn_forest_classes.argtypes = [vp, vp, i32, i32, ctypes.c_float, vp, vp]
+    lib.graphattn_forest_classes.argtypes = [vp, vp, i32, i32, ctypes.c_float, vp, vp, vp]
+    lib.graphattn_forest_advantages.argtypes = [vp, vp, vp, vp, ctypes.c_double, ctypes.c_double,
+                                                P(Advantages), vp]
+    lib.graphattn_forest_advantages.restype = ctypes.c_int
     lib.graphattn_forest_classes.restype = ctypes.c_int
     lib.graphattn_forest_suffix.argtypes = [vp, vp, vp, vp, i64, P(i64), vp]
     lib.graphattn_forest_suffix.restype = ctypes.c_int
@@ -301,7 +309,8 @@ class Forest:
                                                 ctypes.byref(h)))
         self.handle = h
 
-    def classes(self, z, kappa: float, labels=None, stream=None):
+    def classes(self, z, kappa: float, labels=None, edge_sim=None, stream=None):
+        """Class labels; also sim(p(v), v) into edge_sim (float32 [N]) when it is given."""
         import torch
         N = self.host.c.num_states
         if labels is None:
@@ -309,8 +318,24 @@ class Forest:
         _check(self.lib.graphattn_forest_classes(
             self.handle, _dev_ptr(z), int(z.shape[1]),
             GA_BF16 if z.dtype == torch.bfloat16 else GA_F32, float(kappa), _dev_ptr(labels),
-            _stream_handle(stream)))
+            _dev_ptr(edge_sim), _stream_handle(stream)))
         return labels
+
+    def advantages(self, labels, reward, edge_sim, w: float, lambda_eff: float, out=None,
+                   stream=None):
+        """Graph reward and dual-group advantage: dict of float64 [N] device tensors (score,
+        step_reward, a_cor, a_eff, a_dual)."""
+        import torch
+        N = self.host.c.num_states
+        if out is None:
+            out = {k: torch.empty(N, dtype=torch.float64, device=labels.device)
+                   for k in ("score", "step_reward", "a_cor", "a_eff", "a_dual")}
+        adv = Advantages(*[_dev_ptr(out[k]) for k in ("score", "step_reward", "a_cor", "a_eff",
+                                                      "a_dual")])
+        _check(self.lib.graphattn_forest_advantages(
+            self.handle, _dev_ptr(labels), _dev_ptr(reward), _dev_ptr(edge_sim), float(w),
+            float(lambda_eff), ctypes.byref(adv), _stream_handle(stream)))
+        return out
 
     def suffix(self, labels, offsets, states, stream=None) -> int:
         total = ctypes.c_int64(0)

@@ -618,6 +618,19 @@ def draw_state_embeddings(parent: np.ndarray, dim: int, seed: int, share: float 
     return z
 
 
+def state_rewards(parent: np.ndarray, seed: int, p_correct: float = 0.5,
+                  p_stopped: float = 0.1) -> np.ndarray:
+    """Verifier outcomes of a forest's terminal states: every leaf is terminal with R ~
+    Bernoulli(p_correct), except that a fraction p_stopped of the leaves stopped early (no
+    answer, -1); inner states are -1."""
+    rng = np.random.default_rng(seed)
+    N = len(parent)
+    kids = np.bincount(parent[parent >= 0], minlength=N)
+    r = np.where(kids == 0, (rng.random(N) < p_correct).astype(np.int32), -1).astype(np.int32)
+    r[(kids == 0) & (rng.random(N) < p_stopped)] = -1
+    return r
+
+
 def equiv_batch(prompts: int = 512, schedule: Sequence[int] = (4, 5, 3, 2), dim: int = 4096,
                 kappa: float = 0.92, seed: Optional[int] = None) -> StateWorkload:
     """One training batch's states: `prompts` rollout graphs with branching schedule T (205

@@ -20,7 +20,8 @@ def test_library_exports_every_declared_symbol():
                          "graphattn_kv_append", "graphattn_kv_copy",
                          "graphattn_equivalence_classes", "graphattn_graph_suffix",
                          "graphattn_forest_create", "graphattn_forest_classes",
-                         "graphattn_forest_suffix", "graphattn_forest_destroy"}
+                         "graphattn_forest_suffix", "graphattn_forest_destroy",
+                         "graphattn_forest_advantages"}
     for s in syms:
         assert hasattr(lib, s), s
 
@@ -222,7 +223,11 @@ def test_forest_plan_errors():
     assert lib.graphattn_forest_create(None, None, ctypes.byref(h)) == G.GA_EINVAL
     assert lib.graphattn_forest_create(ctypes.byref(G.HostForest([-1]).c), None,
                                        None) == G.GA_EINVAL
-    assert lib.graphattn_forest_classes(None, None, 64, G.GA_BF16, 0.9, None, None) == G.GA_EINVAL
+    assert lib.graphattn_forest_classes(None, None, 64, G.GA_BF16, 0.9, None, None,
+                                        None) == G.GA_EINVAL
+    adv = G.Advantages()
+    assert lib.graphattn_forest_advantages(None, None, None, None, 0.5, 0.5, ctypes.byref(adv),
+                                           None) == G.GA_EINVAL
     tot = ctypes.c_int64(3)
     assert lib.graphattn_forest_suffix(None, None, None, None, 0, ctypes.byref(tot),
                                        None) == G.GA_EINVAL

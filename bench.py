@@ -288,8 +288,9 @@ def compared_pairs_count(parent):
 
 
 def run_equiv(args, torch, G, W):
-    """Equivalence detection for one training batch's states: classes (the timed step), and the
-    graph suffix timed on its own (it synchronises to size its output)."""
+    """Equivalence detection for one training batch's states: classes and edge similarities (the
+    timed step); the graph suffix (it synchronises to size its output) and the graph reward and
+    dual-group advantage timed on their own."""
     import numpy as np
     t0 = time.time()
     wl = W.equiv_batch()
@@ -299,17 +300,28 @@ def run_equiv(args, torch, G, W):
     z = wl.z.to(dev)
     f = G.Forest(wl.parent)
     labels = torch.empty(N, dtype=torch.int32, device=dev)
+    esim = torch.empty(N, dtype=torch.float32, device=dev)
     for _ in range(args.warmup):
-        f.classes(z, wl.kappa, labels)
+        f.classes(z, wl.kappa, labels, esim)
     torch.cuda.synchronize()
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
     ev0.record()
     for _ in range(args.steps):
-        f.classes(z, wl.kappa, labels)
+        f.classes(z, wl.kappa, labels, esim)
     ev1.record()
     torch.cuda.synchronize()
     ms = ev0.elapsed_time(ev1) / args.steps
+    # Graph reward and dual-group advantage on the same states (synthetic verifier outcomes).
+    reward = torch.from_numpy(W.state_rewards(wl.parent, wl.seed)).to(dev)
+    adv = f.advantages(labels, reward, esim, 0.7, 0.5)
+    torch.cuda.synchronize()
+    ev0.record()
+    for _ in range(args.steps):
+        f.advantages(labels, reward, esim, 0.7, 0.5, out=adv)
+    ev1.record()
+    torch.cuda.synchronize()
+    adv_ms = ev0.elapsed_time(ev1) / args.steps
     lab = labels.cpu().numpy()
     offs = torch.empty(N + 1, dtype=torch.int64, device=dev)
     total = f.suffix_total(labels, offs)
@@ -323,7 +335,7 @@ def run_equiv(args, torch, G, W):
     torch.cuda.synchronize()
     suffix_ms = ev0.elapsed_time(ev1) / args.steps
     log(f"timed {args.steps} steps: classes {ms:.4f} ms, graph suffix {suffix_ms:.4f} ms "
-        f"(with its host synchronisation)")
+        f"(with its host synchronisation), reward and advantages {adv_ms:.4f} ms")
     zbytes = N * dim * 2
     pairs = compared_pairs_count(wl.parent)
     achieved = zbytes / (ms * 1e-3) / 1e9
@@ -341,7 +353,7 @@ def run_equiv(args, torch, G, W):
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": None},
         "compared_pair_tflops": pairs * 2 * dim / (ms * 1e-3) / 1e12,
-        "kernel_ms": {"classes": ms, "graph_suffix": suffix_ms},
+        "kernel_ms": {"classes": ms, "graph_suffix": suffix_ms, "advantages": adv_ms},
     }
     f.close()
     if args.cpu_sample > 0:

@@ -157,14 +157,62 @@ __global__ __launch_bounds__(256) void k_sim_union(EquivArgs a) {
   }
 }
 
-// One prompt of at most 256 states in one workgroup (8 waves): the prompt's embeddings are
-// streamed through LDS once, 64 components per stage (256 rows x 128 bytes, double-buffered),
-// while each thread also sums the squares of the 4 row pieces it loads (the norms).  The upper
-// triangle of the 16 x 16 grid of 16 x 16 tiles (136 tiles) is dealt out as strips: wave w owns
-// row strips w and 15 - w, i.e. the 16 - w tiles (w, w..15) and the w + 1 tiles
-// (15 - w, 15 - w..15), 17 per wave.  Links are made with a union-find in LDS and the labels
-// written at the end, so nothing else is needed for these prompts.
+// One prompt of at most 256 states in one workgroup (8 waves).  The prompt's embeddings stream
+// through an LDS ring of 4 stages of 32 components (256 rows x 64 bytes each), 3 stages in
+// flight, copied straight from HBM into LDS (global_load_lds_dwordx4: each lane moves 16 bytes,
+// one wave instruction fills 1 KiB = 16 rows; 16-byte chunks are XOR-permuted by row pair so the
+// MFMA operand reads are conflict-free).  The upper triangle of the 16 x 16 grid of 16 x 16
+// tiles (136 tiles) is dealt out as strips: wave w owns row strips w and 15 - w, i.e. the 16 - w
+// tiles (w, w..15) and the w + 1 tiles (15 - w, 15 - w..15), 17 per wave.  The squared norms
+// are the diagonals of the diagonal tiles (the same fp32 sums as the dot products).  Links are
+// made with a union-find in LDS and the labels written at the end.
 constexpr int kPromptMax = 256;
+constexpr int kPKC = 32;                        // components per stage: one MFMA k-step
+constexpr int kPRow = kPKC * 2;                 // bytes of one state row in a stage
+constexpr int kPStage = kPromptMax * kPRow;     // 16 KiB
+constexpr int kPRing = 4;
+
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+// LDS[lds_base + 16 * lane] <- global[base + off] (16 bytes per lane).  M0 holds the LDS base;
+// the kernel keeps no other value in M0, and completion is awaited with explicit vmcnt waits.
+__device__ __forceinline__ void dma16(unsigned off, const void* base, unsigned lds_base) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+               :: "v"(off), "s"(base), "s"(lds_base) : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// s_waitcnt vmcnt(n) for a runtime n in [0, 15] (expcnt and lgkmcnt left alone).
+#define EQ_VMCNT(k) (((k) & 15) | (7 << 4) | (15 << 8))
+__device__ __forceinline__ void wait_vm(int n) {
+  asm volatile("" ::: "memory");
+  switch (n) {
+    case 0: __builtin_amdgcn_s_waitcnt(EQ_VMCNT(0)); break;
+    case 1: __builtin_amdgcn_s_waitcnt(EQ_VMCNT(1)); break;
+    case 2: __builtin_amdgcn_s_waitcnt(EQ_VMCNT(2)); break;
+    case 3: __builtin_amdgcn_s_waitcnt(EQ_VMCNT(3)); break;
+    default: __builtin_amdgcn_s_waitcnt(EQ_VMCNT(4)); break;
+  }
+}
+
+__device__ __forceinline__ void ring_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// A wave-uniform pointer held in scalar registers (both halves read from the first lane as
+// unsigned 32-bit values, so the low half is not sign-extended into the high one).
+__device__ __forceinline__ const void* uniform_ptr(const void* p) {
+  const uint64_t v = (uint64_t)(uintptr_t)p;
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)v);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(v >> 32));
+  return reinterpret_cast<const void*>((uintptr_t)(((uint64_t)hi << 32) | lo));
+}
+
+__device__ __forceinline__ int poff(int row, int chunk) {
+  return row * kPRow + ((chunk ^ ((row >> 1) & 3)) << 4);
+}
 
 __device__ __forceinline__ int lds_find(int* r, int x) {
   int p = __hip_atomic_load(r + x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
@@ -190,7 +238,7 @@ __device__ void lds_unite(int* r, int a, int b) {
 }
 
 __global__ __launch_bounds__(512, 2) void k_prompt_classes(EquivArgs a) {
-  __shared__ __align__(16) unsigned char stage[2][kPromptMax * kKC * 2];
+  __shared__ __align__(1024) unsigned char ring[kPRing * kPStage];
   __shared__ float s_inv[kPromptMax];
   __shared__ int s_tin[kPromptMax], s_tout[kPromptMax], s_rep[kPromptMax], s_par[kPromptMax];
   const int2 pr = a.prompts[blockIdx.x];          // (first state, states)
@@ -199,30 +247,33 @@ __global__ __launch_bounds__(512, 2) void k_prompt_classes(EquivArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int r16 = lane & 15, kg = lane >> 4;
   const int nt = (n + 15) >> 4;                   // 16-row tiles holding states
-  // Loads: thread t moves chunk t % 8 of rows t / 8 + 64 j (j < 4) of every stage.
-  const int lc = tid & 7, lr = tid >> 3;
-  auto lds_off = [](int row, int chunk) { return row * (kKC * 2) + ((chunk ^ (row & 7)) << 4); };
-  uint4 pf[4];
-  float ss[4] = {0.f, 0.f, 0.f, 0.f};
-  auto gload = [&](int kc) {
+  if (tid < kPromptMax) {
+    s_rep[tid] = tid;
+    s_tin[tid] = tid < n ? a.tin[s0 + tid] : 0;
+    s_tout[tid] = tid < n ? a.tout[s0 + tid] : 0;
+    s_par[tid] = tid < n ? a.parent[s0 + tid] - s0 : -1;   // prompt-local (< 0 for the root)
+  }
+  __syncthreads();
+
+  // Copies: wave w issues instructions q = 2w and 2w + 1 of every stage; instruction q fills rows
+  // 16q .. 16q + 15, lane l the LDS chunk l % 4 of row 16q + l / 4 with the global chunk that
+  // the permutation puts there.  Rows past the prompt re-read its last state (valid memory;
+  // their products are never used).
+  const void* pbase = uniform_ptr(a.z + (int64_t)s0 * a.dim);
+  unsigned coff[2];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int row = lr + 64 * j;
-      pf[j] = make_uint4(0u, 0u, 0u, 0u);
-      if (row < n)
-        pf[j] = *reinterpret_cast<const uint4*>(a.z + (int64_t)(s0 + row) * a.dim + kc * kKC +
-                                                lc * 8);
-    }
-  };
-  auto lstore = [&](int buf) {
+  for (int j = 0; j < 2; ++j) {
+    const int row = 16 * (2 * wave + j) + (lane >> 2);
+    const int chunk = (lane & 3) ^ ((row >> 1) & 3);
+    coff[j] = (unsigned)(min(row, n - 1) * a.dim * 2 + chunk * 16);
+  }
+  const unsigned lds_ring = (unsigned)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)ring;
+  const int nst = a.dim / kPKC;
+  auto issue = [&](int st) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int row = lr + 64 * j;
-      *reinterpret_cast<uint4*>(&stage[buf][lds_off(row, lc)]) = pf[j];
-      const bf16x8 v = __builtin_bit_cast(bf16x8, pf[j]);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) ss[j] = fmaf((float)v[i], (float)v[i], ss[j]);
-    }
+    for (int j = 0; j < 2; ++j)
+      dma16(coff[j] + (unsigned)(st * kPRow), pbase,
+            __builtin_amdgcn_readfirstlane(lds_ring + (st % kPRing) * kPStage + (2 * wave + j) * 1024));
   };
   // Strips of this wave and the 17 tiles (strip, column) it owns.
   const int sa = wave, sb = 15 - wave;
@@ -232,45 +283,35 @@ __global__ __launch_bounds__(512, 2) void k_prompt_classes(EquivArgs a) {
 #pragma unroll
   for (int k = 0; k < 17; ++k) acc[k] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  if (tid < kPromptMax) {
-    s_rep[tid] = tid;
-    s_tin[tid] = tid < n ? a.tin[s0 + tid] : 0;
-    s_tout[tid] = tid < n ? a.tout[s0 + tid] : 0;
-    s_par[tid] = tid < n ? a.parent[s0 + tid] - s0 : -1;   // prompt-local (-1 - s0 for the root)
-  }
-  const int nk = a.dim / kKC;
-  gload(0);
-  lstore(0);
-  if (nk > 1) gload(1);
-  for (int kc = 0; kc < nk; ++kc) {
-    __syncthreads();                              // stage kc is in LDS; stage kc - 1 is done
-    const unsigned char* st = stage[kc & 1];
+  for (int st = 0; st < kPRing - 1 && st < nst; ++st) issue(st);
+  for (int st = 0; st < nst; ++st) {
+    wait_vm(2 * min(nst - 1 - st, kPRing - 2));   // this wave's copies of stage st have landed
+    ring_barrier();                               // ... and every wave's; stage st - 1 is done
+    if (st + kPRing - 1 < nst) issue(st + kPRing - 1);
+    const unsigned char* stg = ring + (st % kPRing) * kPStage;
+    const bf16x8 a0 = *reinterpret_cast<const bf16x8*>(stg + poff(sa * 16 + r16, kg));
+    const bf16x8 a1 = *reinterpret_cast<const bf16x8*>(stg + poff(sb * 16 + r16, kg));
 #pragma unroll
-    for (int ks = 0; ks < kKC / 32; ++ks) {
-      const bf16x8 a0 = *reinterpret_cast<const bf16x8*>(st + lds_off(sa * 16 + r16, ks * 4 + kg));
-      const bf16x8 a1 = *reinterpret_cast<const bf16x8*>(st + lds_off(sb * 16 + r16, ks * 4 + kg));
-#pragma unroll
-      for (int k = 0; k < 17; ++k) {
-        const int srow = tile_strip(k), col = tile_col(k);
-        if (srow < nt && col < nt) {
-          const bf16x8 b = *reinterpret_cast<const bf16x8*>(st + lds_off(col * 16 + r16, ks * 4 + kg));
-          acc[k] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(srow == sa ? a0 : a1, b, acc[k], 0, 0, 0);
-        }
+    for (int k = 0; k < 17; ++k) {
+      const int srow = tile_strip(k), col = tile_col(k);
+      if (srow < nt && col < nt) {
+        const bf16x8 b = *reinterpret_cast<const bf16x8*>(stg + poff(col * 16 + r16, kg));
+        acc[k] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(srow == sa ? a0 : a1, b, acc[k], 0, 0, 0);
       }
     }
-    if (kc + 1 < nk) {
-      lstore((kc + 1) & 1);                       // the other buffer: nobody reads it now
-      if (kc + 2 < nk) gload(kc + 2);
-    }
   }
-  // Norms: the 8 threads that load one row hold its partial sums (lanes 8q .. 8q + 7).
+  // Squared norms from the diagonal tiles (strip, strip): row 16 strip + m sits in lane
+  // (r16 = m, kg = m / 4), element m % 4.
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    float v = ss[j];
-    v += __shfl_xor(v, 1);
-    v += __shfl_xor(v, 2);
-    v += __shfl_xor(v, 4);
-    if (lc == 0) s_inv[lr + 64 * j] = v > 0.f ? 1.f / sqrtf(v) : __builtin_nanf("");
+  for (int k = 0; k < 17; ++k) {
+    const int srow = tile_strip(k), col = tile_col(k);
+    if (srow != col || srow >= nt) continue;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      if (4 * kg + i == r16) {
+        const float q = acc[k][i];
+        s_inv[srow * 16 + r16] = q > 0.f ? 1.f / sqrtf(q) : __builtin_nanf("");
+      }
   }
   __syncthreads();
   // acc[k][i] = z_u . z_v, u = 16 strip + 4 kg + i, v = 16 col + r16 (prompt-local).

@@ -45,6 +45,8 @@ struct Forest {
   std::vector<int4> items;       // 64 x 64 tiles of the prompts of more than 256 states
   std::vector<int2> prompts;     // (first state, states) of the prompts of at most 256 states
   std::vector<int32_t> big;      // the states of the larger prompts
+  std::vector<int2> all;         // (first state, states) of every prompt
+  int64_t big_reward = 0;        // states in prompts of more than 512 states
 };
 
 constexpr int32_t kPromptMax = 256;   // states one workgroup classifies on its own
@@ -109,6 +111,12 @@ ga_status build_forest(const ga_state_forest* f, bool with_items, Forest* fo) {
   fo->items.clear();
   fo->prompts.clear();
   fo->big.clear();
+  fo->all.clear();
+  fo->big_reward = 0;
+  for (int32_t r = 0; r < N; r = fo->pend[r]) {
+    fo->all.push_back(make_int2(r, fo->pend[r] - r));
+    if (fo->pend[r] - r > 512) fo->big_reward += fo->pend[r] - r;
+  }
   if (with_items) {
     for (int32_t r = 0; r < N; r = fo->pend[r]) {
       const int32_t e = fo->pend[r];
@@ -141,6 +149,7 @@ struct ga_forest {
   int32_t *pstart = nullptr, *pend = nullptr;
   int4* items = nullptr;
   int2* prompts = nullptr;
+  int2* all = nullptr;
   int32_t* big = nullptr;
   float* inv_norm = nullptr;
   int* rep = nullptr;
@@ -179,7 +188,8 @@ ga_status forest_create(const ga_state_forest* forest, hipStream_t stream, ga_fo
   }
   const size_t n4 = align256(4 * fo.N), n8 = align256(8 * fo.N);
   const size_t up = 6 * n4 + align256(sizeof(int4) * fo.items.size()) +
-                    align256(sizeof(int2) * fo.prompts.size()) + align256(4 * fo.big.size());
+                    align256(sizeof(int2) * fo.prompts.size()) + align256(4 * fo.big.size()) +
+                    align256(sizeof(int2) * fo.all.size());
   const size_t nblk = (size_t)((fo.N + 1023) / 1024);
   const size_t scan = align256(8 * (fo.N + 1));
   const size_t total = up + 2 * n4 + n8 + scan + align256(8 * (nblk + 1))   // classes, suffix
@@ -207,6 +217,7 @@ ga_status forest_create(const ga_state_forest* forest, hipStream_t stream, ga_fo
   put(pin, o, fo.items);
   put(pin, o, fo.prompts);
   put(pin, o, fo.big);
+  put(pin, o, fo.all);
   char* d = static_cast<char*>(f->dev);
   f->tin = reinterpret_cast<int32_t*>(d);
   f->tout = reinterpret_cast<int32_t*>(d + n4);
@@ -218,6 +229,8 @@ ga_status forest_create(const ga_state_forest* forest, hipStream_t stream, ga_fo
   const size_t oi = 6 * n4 + align256(sizeof(int4) * fo.items.size());
   f->prompts = reinterpret_cast<int2*>(d + oi);
   f->big = reinterpret_cast<int32_t*>(d + oi + align256(sizeof(int2) * fo.prompts.size()));
+  f->all = reinterpret_cast<int2*>(d + oi + align256(sizeof(int2) * fo.prompts.size()) +
+                                   align256(4 * fo.big.size()));
   f->inv_norm = reinterpret_cast<float*>(d + up);
   f->rep = reinterpret_cast<int*>(d + up + n4);
   f->cnt = reinterpret_cast<int64_t*>(d + up + 2 * n4);
@@ -390,6 +403,9 @@ ga_status graphattn_forest_advantages(ga_forest* forest, const int32_t* labels,
   a.a_eff = out->a_eff;
   a.a_dual = out->a_dual;
   a.N = N;
+  a.prompts = forest->all;
+  a.n_prompts = (int64_t)forest->fo.all.size();
+  a.n_big = forest->fo.big_reward;
   a.w = w;
   a.lambda_eff = lambda_eff;
   EQ_HIP(ga::launch_advantages(a, static_cast<hipStream_t>(hip_stream)), "advantage launch");

@@ -168,7 +168,9 @@ struct RewardArgs {
   double* aeff_node;       // A_eff(v) of each such member
   double *gmean, *gstd;    // correctness-group statistics of each source state
   double *score, *step, *a_cor, *a_eff, *a_dual;   // outputs
-  int64_t N;
+  const int2* prompts;     // [n_prompts] (first state, states) of every prompt
+  int64_t N, n_prompts;
+  int64_t n_big;           // states in prompts of more than 512 states (0: one launch per batch)
   double w, lambda_eff;
 };
 

@@ -214,10 +214,167 @@ __global__ void k_dual(RewardArgs a) {
   a.a_dual[v] = c + a.lambda_eff * a.a_eff[v];
 }
 
+// Every prompt of at most kRPromptMax states in one workgroup: its arrays are staged in LDS and
+// the steps above run between workgroup barriers, in the same order of operations as the kernels
+// above (so the results are the same bits), in one launch.
+constexpr int kRPromptMax = 512;
+
+__global__ __launch_bounds__(256) void k_prompt_advantages(RewardArgs a) {
+  __shared__ int s_par[kRPromptMax], s_lab[kRPromptMax], s_dep[kRPromptMax];
+  __shared__ int s_tin[kRPromptMax], s_tout[kRPromptMax], s_rew[kRPromptMax];
+  __shared__ int s_anc[kRPromptMax], s_c[kRPromptMax], s_t[kRPromptMax];
+  __shared__ float s_sim[kRPromptMax];
+  __shared__ double s_S[kRPromptMax], s_r[kRPromptMax], s_aen[kRPromptMax], s_gm[kRPromptMax],
+      s_gs[kRPromptMax];
+  const int2 pr = a.prompts[blockIdx.x];
+  const int s0 = pr.x, n = pr.y, tid = threadIdx.x;
+  const int t0 = a.tin[s0];
+  for (int v = tid; v < n; v += 256) {           // prompt-local indices throughout
+    const int g = s0 + v;
+    const int l = a.labels[g];
+    s_lab[v] = ((l >= s0 && l <= g) ? l : g) - s0;
+    const int p = a.parent[g];
+    s_par[v] = p >= 0 ? p - s0 : -1;
+    s_dep[v] = a.depth[g];
+    s_tin[v] = a.tin[g] - t0;
+    s_tout[v] = a.tout[g] - t0;
+    s_rew[v] = a.reward[g];
+    s_sim[v] = a.edge_sim[g];
+  }
+  __syncthreads();
+  for (int v = tid; v < n; v += 256) {           // outcomes of v's subtree
+    int c = 0, t = 0;
+    for (int z = 0; z < n; ++z)
+      if (s_rew[z] >= 0 && s_tin[v] <= s_tin[z] && s_tin[z] < s_tout[v]) {
+        c += s_rew[z];
+        ++t;
+      }
+    s_c[v] = c;
+    s_t[v] = t;
+  }
+  __syncthreads();
+  for (int v = tid; v < n; v += 256) {           // pooled scores
+    int64_t C = 0, T = 0;
+    for (int q = 0; q < n; ++q)
+      if (s_lab[q] == s_lab[v]) {
+        C += s_c[q];
+        T += s_t[q];
+      }
+    const double c = (double)s_c[v], t = (double)s_t[v];
+    const double num = c + a.w * ((double)C - c), den = t + a.w * ((double)T - t);
+    const double S = den > 0.0 ? num / den : __builtin_nan("");
+    s_S[v] = S;
+    a.score[s0 + v] = S;
+    s_anc[v] = -1;
+    s_aen[v] = 0.0;
+  }
+  __syncthreads();
+  for (int v = tid; v < n; v += 256) {           // step rewards; class efficiency values
+    const int p = s_par[v];
+    double r = __builtin_nan("");
+    if (p >= 0) r = (s_S[v] - s_S[p]) * (1.0 - fmax(0.0, (double)s_sim[v]));
+    s_r[v] = r;
+    a.step[s0 + v] = r;
+    if (s_lab[v] != v) continue;
+    int m = 0, lca = -1, sdef = 0;
+    double ssum = 0.0;
+    for (int x = v; x < n; ++x) {
+      if (s_lab[x] != v) continue;
+      ++m;
+      if (!isnan(s_S[x])) {
+        ssum += s_S[x];
+        ++sdef;
+      }
+      if (lca < 0) {
+        lca = x;
+        continue;
+      }
+      int y = x, z = lca;
+      while (s_dep[y] > s_dep[z]) y = s_par[y];
+      while (s_dep[z] > s_dep[y]) z = s_par[z];
+      while (y != z) {
+        y = s_par[y];
+        z = s_par[z];
+      }
+      lca = y;
+    }
+    if (m < 2) continue;
+    const int anc = s_lab[lca] == v ? s_par[lca] : lca;
+    if (anc < 0) continue;
+    const double gate = sdef > 0 ? ssum / sdef : 0.0;
+    double lsum = 0.0;
+    for (int x = v; x < n; ++x)
+      if (s_lab[x] == v) lsum += -(double)(s_dep[x] - s_dep[anc]);
+    const double mean = lsum / m;
+    double q = 0.0;
+    for (int x = v; x < n; ++x)
+      if (s_lab[x] == v) {
+        const double d = -(double)(s_dep[x] - s_dep[anc]) - mean;
+        q += d * d;
+      }
+    const double sd = sqrt(q / m);
+    for (int x = v; x < n; ++x)
+      if (s_lab[x] == v) {
+        const double l = -(double)(s_dep[x] - s_dep[anc]);
+        s_aen[x] = sd > 0.0 ? gate * (l - mean) / sd : 0.0;
+        s_anc[x] = anc;
+      }
+  }
+  __syncthreads();
+  for (int u = tid; u < n; u += 256) {           // correctness groups; efficiency per edge
+    const int lu = s_lab[u], du = s_dep[u];
+    int cnt = 0, members = 0;
+    double sum = 0.0;
+    for (int c = 0; c < n; ++c) {
+      const int p = s_par[c];
+      if (p < 0 || !(p == u || (s_lab[p] == lu && s_dep[c] > du))) continue;
+      ++members;
+      if (isnan(s_r[c])) continue;
+      sum += s_r[c];
+      ++cnt;
+    }
+    double mean = 0.0, sd = 0.0;
+    if (members > 1 && cnt > 0) {
+      mean = sum / cnt;
+      double q = 0.0;
+      for (int c = 0; c < n; ++c) {
+        const int p = s_par[c];
+        if (p < 0 || !(p == u || (s_lab[p] == lu && s_dep[c] > du))) continue;
+        if (isnan(s_r[c])) continue;
+        const double d = s_r[c] - mean;
+        q += d * d;
+      }
+      sd = sqrt(q / cnt);
+    }
+    s_gm[u] = mean;
+    s_gs[u] = sd;
+    double e = 0.0;
+    if (s_par[u] >= 0)
+      for (int x = 0; x < n; ++x) {
+        const int an = s_anc[x];
+        if (an < 0 || s_tin[x] < s_tin[u] || s_tin[x] >= s_tout[u]) continue;
+        if (s_dep[an] < du) e += s_aen[x];
+      }
+    a.a_eff[s0 + u] = e;
+  }
+  __syncthreads();
+  for (int v = tid; v < n; v += 256) {
+    const int p = s_par[v];
+    double c = 0.0;
+    if (p >= 0 && !isnan(s_r[v]) && s_gs[p] > 0.0) c = (s_r[v] - s_gm[p]) / s_gs[p];
+    a.a_cor[s0 + v] = c;
+    a.a_dual[s0 + v] = c + a.lambda_eff * a.a_eff[s0 + v];   // written by this thread above
+  }
+}
+
 }  // namespace
 
 hipError_t launch_advantages(const RewardArgs& a, hipStream_t stream) {
   if (a.N == 0) return hipSuccess;
+  if (a.n_big == 0) {
+    hipLaunchKernelGGL(k_prompt_advantages, dim3((unsigned)a.n_prompts), dim3(256), 0, stream, a);
+    return hipGetLastError();
+  }
   const unsigned g = (unsigned)((a.N + kB - 1) / kB);
   const unsigned sb = (unsigned)((a.N + 1023) / 1024);
   hipLaunchKernelGGL(k_outcome_vals, dim3(g), dim3(kB), 0, stream, a);

@@ -59,7 +59,8 @@ def test_fixture_on_gpu():
 
 
 @pytest.mark.parametrize("prompts,sched,seed", [(3, (3, 3, 2), 1), (2, (4, 5, 3, 2), 2),
-                                                (5, (2, 2, 2, 2, 2), 3), (1, (8,), 4)])
+                                                (5, (2, 2, 2, 2, 2), 3), (1, (8,), 4),
+                                                (2, (6, 6, 15), 5)])
 @pytest.mark.parametrize("w,lam", [(0.7, 0.5), (0.0, 1.0), (1.0, 0.0)])
 def test_random_rollouts(prompts, sched, seed, w, lam):
     rng = np.random.default_rng(seed)
@@ -105,3 +106,29 @@ def test_pipeline_classes_similarities_advantages():
         assert np.array_equal(np.isnan(a), np.isnan(b))
         m = ~np.isnan(b)
         assert float(np.abs(a[m] - b[m]).max()) <= tol, k
+
+
+def test_one_launch_and_multi_kernel_paths_agree():
+    """A batch of prompts of at most 512 states runs in one launch; adding one larger prompt
+    sends the whole batch through the multi-kernel path: the small prompts' results must be the
+    same bits either way."""
+    small = W.state_forest(3, (4, 5, 3, 2))
+    big = W.state_forest(1, (6, 6, 15)) + len(small)
+    big[0] = -1
+    both = np.concatenate([small, big])
+    rng = np.random.default_rng(9)
+    N, n = len(both), len(small)
+    reward = W.state_rewards(both, 9)
+    labels = np.arange(N, dtype=np.int32)
+    for v in range(5, n, 7):                          # link some same-depth states
+        d = O.state_depths(both)
+        same = [u for u in range(1, n) if d[u] == d[v] and u < v and (u // 205) == (v // 205)]
+        if same:
+            u = int(rng.choice(same))
+            lo, hi = min(labels[u], labels[v]), max(labels[u], labels[v])
+            labels[labels == hi] = lo
+    sim = rng.uniform(-0.5, 1.0, N).astype(np.float32)
+    one = gpu_adv(small, labels[:n], reward[:n], sim[:n], 0.7, 0.5)
+    multi = gpu_adv(both, labels, reward, sim, 0.7, 0.5)
+    for k in KEYS.values():
+        assert np.array_equal(one[k][:n], multi[k][:n], equal_nan=True), k

@@ -359,7 +359,7 @@ def run_equiv(args, torch, G, W):
     if args.cpu_sample > 0:
         from oracle import graphattn_oracle as O
         per = 205
-        n = min(64, N // per)
+        n = min(512, N // per)
         t1 = time.perf_counter()
         for p in range(n):
             a, b = p * per, (p + 1) * per

@@ -13,7 +13,12 @@ timed on a bounded sample of the same workload.
 --op extend times the multi-query variant instead (every branch of the merged-DAG rollout extends
 a new step of --n-query tokens, all of them queries, causal inside the step): query-tokens/s and
 the attention kernel's fraction of the bf16 MFMA roofline on the attention flops.  --op append
-times storing one decode step's new K/V (one token per branch) into the page pool.
+times storing one decode step's new K/V (one token per branch) into the page pool.  --op equiv
+times equivalence detection (and beside it the graph suffix and the graph reward / dual-group
+advantage) for one training batch's rollout states.
+
+Timing: the K timed steps run without per-kernel events (ms_per_step, value); K further steps
+record HIP events on the launch stream around each kernel (kernel_ms and the roofline).
 """
 import argparse
 import hashlib
@@ -75,6 +80,33 @@ def cpu_baseline(wl, n_sample):
             "sample": f"{len(br)} seeded branches of the same workload ({toks} attended tokens), "
                       f"fp64 NumPy, {dt:.1f} s wall",
             "attended_tokens_per_s": toks / dt}
+
+
+def timed_steps(torch, plan, step, steps):
+    """Two timed regions of `steps` steps each on the launch stream.  The first has no
+    per-kernel events (HIP event records between kernels lengthen a step by a few us each):
+    it gives ms per step.  The second records the library's HIP events around every scheduler,
+    attention and merge launch: it gives each kernel's average duration."""
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record()
+    for _ in range(steps):
+        step()
+    ev1.record()
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / steps
+    plan.profile(steps)
+    for _ in range(steps):
+        step()
+    prof = plan.profile_read()
+    plan.profile(0)
+    attn_ms = prof.attn_ms / max(1, prof.runs)
+    merge_ms = prof.merge_ms / max(1, prof.runs)
+    sched_ms = prof.sched_ms / max(1, prof.schedules)
+    log(f"timed {steps} steps: {ms:.4f} ms/step; {steps} more steps with kernel events: "
+        f"attention {attn_ms:.4f} ms, merge {merge_ms:.4f} ms, scheduler {sched_ms:.4f} ms")
+    return ms, attn_ms, merge_ms, sched_ms
 
 
 def extend_flops(wl):
@@ -151,22 +183,7 @@ def run_extend(args, torch, G, W):
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    plan.profile(args.steps)
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    ev0.record()
-    for _ in range(args.steps):
-        step()
-    ev1.record()
-    torch.cuda.synchronize()
-    ms = ev0.elapsed_time(ev1) / args.steps
-    prof = plan.profile_read()
-    attn_ms = prof.attn_ms / max(1, prof.runs)
-    merge_ms = prof.merge_ms / max(1, prof.runs)
-    sched_ms = prof.sched_ms / max(1, prof.schedules)
-    log(f"timed {args.steps} steps: {ms:.4f} ms/step (attention {attn_ms:.4f} ms, merge "
-        f"{merge_ms:.4f} ms, scheduler {sched_ms:.4f} ms)")
+    ms, attn_ms, merge_ms, sched_ms = timed_steps(torch, plan, step, args.steps)
     flops, vis = extend_flops(wl)
     achieved = flops / (attn_ms * 1e-3) / 1e12
     ukv = wl.unique_kv_bytes()
@@ -189,6 +206,9 @@ def run_extend(args, torch, G, W):
                      "unit": "TFLOP/s", "frac": achieved / MFMA_BF16_PEAK_TFLOPS,
                      "traffic": traffic},
         "kernel_ms": {"scheduler": sched_ms, "attention": attn_ms, "merge": merge_ms},
+        "timing": "ms_per_step over the timed steps without per-kernel events; kernel_ms (and "
+                  "the roofline) from as many further steps with HIP events on the launch stream "
+                  "around each kernel",
         "attention_flops": flops,
         "unique_kv_bytes": ukv,
         "unique_kv_hbm_frac": ukv / (attn_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
@@ -430,22 +450,7 @@ def main():
         step()
     torch.cuda.synchronize()
     log(f"warmup done ({args.warmup} steps)")
-    plan.profile(args.steps)
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    ev0.record()
-    for _ in range(args.steps):
-        step()
-    ev1.record()
-    torch.cuda.synchronize()
-    ms = ev0.elapsed_time(ev1) / args.steps
-    prof = plan.profile_read()
-    attn_ms = prof.attn_ms / max(1, prof.runs)
-    merge_ms = prof.merge_ms / max(1, prof.runs)
-    sched_ms = prof.sched_ms / max(1, prof.schedules)
-    log(f"timed {args.steps} steps: {ms:.4f} ms/step (attention {attn_ms:.4f} ms, merge "
-        f"{merge_ms:.4f} ms, scheduler {sched_ms:.4f} ms)")
+    ms, attn_ms, merge_ms, sched_ms = timed_steps(torch, plan, step, args.steps)
 
     ukv = wl.unique_kv_bytes()
     achieved = ukv / (attn_ms * 1e-3) / 1e9
@@ -471,6 +476,9 @@ def main():
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic},
         "kernel_ms": {"scheduler": sched_ms, "attention": attn_ms, "merge": merge_ms},
+        "timing": "ms_per_step over the timed steps without per-kernel events; kernel_ms (and "
+                  "the roofline) from as many further steps with HIP events on the launch stream "
+                  "around each kernel",
         "unique_kv_bytes": ukv,
         "step_unique_kv_frac": ukv / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
         "attended_tokens_per_s": g.attended_tokens() / (ms * 1e-3),

@@ -17,11 +17,14 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 template <int D, bool BF16, bool PF16>
 __global__ __launch_bounds__(256) void k_merge(MergeArgs a) {
-  constexpr int LPR = D / 4;               // lanes per (branch, q-head) row, 4 columns each
-  constexpr int RPB = 256 / LPR;           // rows per workgroup
-  constexpr int PS = PF16 ? 2 : 1;         // floats per partial log-sum-exp entry
+  // fp16 partials: 16 lanes per row, each lane 8 stored positions (16 bytes) = two groups of 4
+  // consecutive columns; fp32 partials: D / 4 lanes per row, 4 columns each.
+  constexpr int CPL = PF16 ? 8 : 4;            // values per lane
+  constexpr int LPR = D / CPL;                 // lanes per (branch, q-head) row
+  constexpr int RPB = 256 / LPR;               // rows per workgroup
+  constexpr int PS = PF16 ? 2 : 1;
+  constexpr int KB = 8;                        // partials loaded per batch
   const int tid = threadIdx.x;
-  // The attention kernel has drained its work queue (stream order): re-arm it for the next run.
   if (blockIdx.x == 0 && tid == 0) a.counters[2] = 0;
   const int64_t row = (int64_t)blockIdx.x * RPB + tid / LPR;
   const int sub = tid % LPR;
@@ -30,55 +33,83 @@ __global__ __launch_bounds__(256) void k_merge(MergeArgs a) {
   const int h = (int)(row % a.Hq);
   const float NEG_INF = -__builtin_huge_valf();
   const int64_t k0 = a.bpart_off[b], k1 = a.bpart_off[b + 1];
-  // This lane's 4 columns 4 sub .. 4 sub + 3 = 16 n + 4 g + (0 .. 3) with n = sub / 4, g = sub % 4;
-  // in the fp16 format they sit at position 32 (n / 2) + 8 g + 4 (n % 2) of the row (the lane
-  // order of the attention kernel's tiles).
-  const int pos = PF16 ? (sub / 8) * 32 + (sub % 4) * 8 + ((sub / 4) % 2) * 4 : 4 * sub;
-  // One pass in list order (path order, then chunk order) with a running maximum: when a
-  // partial's log-sum-exp exceeds it, the sums so far are rescaled.
   float M = NEG_INF, W = 0.f;
-  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll 4
-  for (int64_t k = k0; k < k1; ++k) {
-    const int64_t idx = (int64_t)a.bpart[k] * a.Hq + h;
-    const float lam = a.plse[idx * PS];
-    f32x4 o;
-    float sc = 1.f;
-    if constexpr (PF16) {
-      typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
-      const f16x4 v =
-          *reinterpret_cast<const f16x4*>(static_cast<const _Float16*>(a.po) + idx * D + pos);
-      o = f32x4{(float)v[0], (float)v[1], (float)v[2], (float)v[3]};
-      sc = a.plse[idx * PS + 1];                // undoes the partial's power-of-two scaling
-    } else {
-      o = *reinterpret_cast<const f32x4*>(static_cast<const float*>(a.po) + idx * D + pos);
-    }
-    if (lam > M) {                               // the same for the row's lanes
-      const float r = __builtin_amdgcn_exp2f(M - lam);
-      W *= r;
-      acc *= r;
-      M = lam;
-    }
-    const float wl = __builtin_amdgcn_exp2f(lam - M);
-    acc += o * (wl * sc);
-    W += wl;
-  }
-  const f32x4 r = acc * (1.f / W);
-  if constexpr (BF16) {
-    unsigned short u[4];
+  float acc[CPL];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) u[i] = __builtin_bit_cast(unsigned short, (__bf16)r[i]);
-    uint2 pk = make_uint2(u[0] | ((unsigned)u[1] << 16), u[2] | ((unsigned)u[3] << 16));
-    *reinterpret_cast<uint2*>(static_cast<unsigned short*>(a.out) + row * D + 4 * sub) = pk;
+  for (int i = 0; i < CPL; ++i) acc[i] = 0.f;
+  for (int64_t kb = k0; kb < k1; kb += KB) {
+    const int nk = (int)min((int64_t)KB, k1 - kb);
+    int64_t idx[KB];
+#pragma unroll
+    for (int j = 0; j < KB; ++j) idx[j] = j < nk ? (int64_t)a.bpart[kb + j] * a.Hq + h : 0;
+    float lam[KB], sc[KB], o[KB][CPL];
+#pragma unroll
+    for (int j = 0; j < KB; ++j) {
+      if (j >= nk) { lam[j] = NEG_INF; sc[j] = 0.f; continue; }
+      if constexpr (PF16) {
+        typedef float f32x2 __attribute__((ext_vector_type(2)));
+        const f32x2 ls = *reinterpret_cast<const f32x2*>(a.plse + idx[j] * PS);
+        lam[j] = ls[0];
+        sc[j] = ls[1];
+        typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+        const f16x8 v = *reinterpret_cast<const f16x8*>(static_cast<const _Float16*>(a.po) +
+                                                        idx[j] * D + 8 * sub);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) o[j][i] = (float)v[i];
+      } else {
+        lam[j] = a.plse[idx[j]];
+        sc[j] = 1.f;
+        const f32x4 v = *reinterpret_cast<const f32x4*>(static_cast<const float*>(a.po) +
+                                                        idx[j] * D + 4 * sub);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o[j][i] = v[i];
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < KB; ++j) {
+      if (j >= nk) break;
+      if (lam[j] > M) {
+        const float r = __builtin_amdgcn_exp2f(M - lam[j]);
+        W *= r;
+#pragma unroll
+        for (int i = 0; i < CPL; ++i) acc[i] *= r;
+        M = lam[j];
+      }
+      const float wl = __builtin_amdgcn_exp2f(lam[j] - M);
+      const float ws = wl * sc[j];
+#pragma unroll
+      for (int i = 0; i < CPL; ++i) acc[i] += o[j][i] * ws;
+      W += wl;
+    }
+  }
+  const float inv = 1.f / W;
+  // Columns of this lane: fp16 positions 8 sub .. 8 sub + 7 hold columns 16 n + 4 g + (0..3) and
+  // 16 (n + 1) + 4 g + (0..3) with n = 2 (sub / 4), g = sub % 4; fp32 holds 4 sub .. 4 sub + 3.
+  auto put4 = [&](int col, int i0) {
+    if constexpr (BF16) {
+      unsigned short u[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) u[i] = __builtin_bit_cast(unsigned short, (__bf16)(acc[i0 + i] * inv));
+      *reinterpret_cast<uint2*>(static_cast<unsigned short*>(a.out) + row * D + col) =
+          make_uint2(u[0] | ((unsigned)u[1] << 16), u[2] | ((unsigned)u[3] << 16));
+    } else {
+      *reinterpret_cast<f32x4*>(static_cast<float*>(a.out) + row * D + col) =
+          f32x4{acc[i0] * inv, acc[i0 + 1] * inv, acc[i0 + 2] * inv, acc[i0 + 3] * inv};
+    }
+  };
+  if constexpr (PF16) {
+    const int n = 2 * (sub / 4), g = sub % 4;
+    put4(16 * n + 4 * g, 0);
+    put4(16 * (n + 1) + 4 * g, 4);
   } else {
-    *reinterpret_cast<f32x4*>(static_cast<float*>(a.out) + row * D + 4 * sub) = r;
+    put4(4 * sub, 0);
   }
   if (sub == 0) a.lse[row] = (M + __builtin_amdgcn_logf(W)) * 0.69314718055994531f;
 }
 
 template <int D, bool BF16, bool PF16>
 hipError_t launch_t(const MergeArgs& a, hipStream_t stream) {
-  constexpr int RPB = 256 / (D / 4);
+  constexpr int RPB = 256 / (D / (PF16 ? 8 : 4));
   const int64_t rows = (int64_t)a.B * a.Hq;
   const int grid = (int)((rows + RPB - 1) / RPB);
   if (grid == 0) return hipSuccess;

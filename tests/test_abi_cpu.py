@@ -2,6 +2,7 @@
 rejects malformed inputs during host validation (before any device work) with the documented
 status codes."""
 import ctypes
+import os
 
 import numpy as np
 import pytest
@@ -233,3 +234,42 @@ def test_forest_plan_errors():
                                        None) == G.GA_EINVAL
     assert tot.value == 0
     lib.graphattn_forest_destroy(None)            # no-op
+
+
+def test_header_is_plain_c_and_links(tmp_path):
+    """include/graphattn.h compiles as C99 and a C program links against the library and gets a
+    validation error through the ABI without touching a GPU."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    src = tmp_path / "abi.c"
+    src.write_text(r'''
+#include "graphattn.h"
+#include <stdio.h>
+int main(void) {
+  ga_params p = {8, 2, 96, 16, 4, GA_BF16, 0.0f, 0};
+  int32_t len[1] = {5};
+  int64_t off[2] = {0, 1};
+  int32_t pages[1] = {0};
+  int64_t po[2] = {0, 1};
+  int32_t ps[1] = {0};
+  ga_segment_table st = {1, len, off, pages};
+  ga_branch_paths bp = {1, po, ps};
+  ga_plan* plan = 0;
+  ga_status s = graphattn_plan_create(&st, &bp, &p, 0, &plan);
+  printf("%d %s\n", (int)s, graphattn_last_error());
+  return s == GA_EUNSUPPORTED && plan == 0 ? 0 : 1;
+}
+''')
+    exe = tmp_path / "abi"
+    lib = os.path.join(root, "paper_2606_18954_amd")
+    r = subprocess.run([cc, "-std=c99", "-Wall", "-Werror", "-pedantic", "-I",
+                        os.path.join(root, "include"), str(src), "-L", lib, "-lgraphattn",
+                        "-Wl,-rpath," + lib, "-o", str(exe)], capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    r = subprocess.run([str(exe)], capture_output=True, text=True)
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert "head_dim 96" in r.stdout

@@ -214,80 +214,141 @@ __global__ void k_dual(RewardArgs a) {
   a.a_dual[v] = c + a.lambda_eff * a.a_eff[v];
 }
 
-// Every prompt of at most kRPromptMax states in one workgroup: its arrays are staged in LDS and
-// the steps above run between workgroup barriers, in the same order of operations as the kernels
-// above (so the results are the same bits), in one launch.
+// Every prompt of at most kRPromptMax states in one workgroup, its arrays in LDS, one launch:
+//   outcomes   a prefix sum of the packed (R, 1) values in Euler order (subtrees are ranges);
+//   pooling    class totals by LDS integer atomics;
+//   lists      children and class members as CSR built with LDS atomics and then sorted, so
+//              each state's correctness group reads only its class's children and each class's
+//              efficiency values only its members;
+//   routes     the edge into u sums over u's subtree, read off the Euler order.
+// The results equal the multi-kernel path's up to the order of a few fp64 sums.
 constexpr int kRPromptMax = 512;
+
+template <typename T>
+__device__ void lds_scan_excl(T* v, int n) {          // exclusive scan of v[0, n] in place
+  __shared__ T tmp[kRPromptMax + 1];
+  for (int i = threadIdx.x; i <= n; i += 256) tmp[i] = v[i];
+  __syncthreads();
+  for (int off = 1; off <= n; off <<= 1) {
+    T add[3] = {0, 0, 0};
+    int k = 0;
+    for (int i = threadIdx.x; i <= n; i += 256, ++k) add[k] = i >= off ? tmp[i - off] : 0;
+    __syncthreads();
+    k = 0;
+    for (int i = threadIdx.x; i <= n; i += 256, ++k) tmp[i] += add[k];
+    __syncthreads();
+  }
+  for (int i = threadIdx.x; i <= n; i += 256) v[i] = i ? tmp[i - 1] : 0;
+  __syncthreads();
+}
+
+__device__ void sort_small(int* a, int n) {           // insertion sort of a short list
+  for (int i = 1; i < n; ++i) {
+    const int x = a[i];
+    int j = i - 1;
+    while (j >= 0 && a[j] > x) {
+      a[j + 1] = a[j];
+      --j;
+    }
+    a[j + 1] = x;
+  }
+}
 
 __global__ __launch_bounds__(256) void k_prompt_advantages(RewardArgs a) {
   __shared__ int s_par[kRPromptMax], s_lab[kRPromptMax], s_dep[kRPromptMax];
-  __shared__ int s_tin[kRPromptMax], s_tout[kRPromptMax], s_rew[kRPromptMax];
-  __shared__ int s_anc[kRPromptMax], s_c[kRPromptMax], s_t[kRPromptMax];
-  __shared__ float s_sim[kRPromptMax];
-  __shared__ double s_S[kRPromptMax], s_r[kRPromptMax], s_aen[kRPromptMax], s_gm[kRPromptMax],
-      s_gs[kRPromptMax];
+  __shared__ int s_tin[kRPromptMax], s_tout[kRPromptMax], s_eul[kRPromptMax];
+  __shared__ int s_anc[kRPromptMax];
+  __shared__ int s_coff[kRPromptMax + 1], s_kids[kRPromptMax], s_cfill[kRPromptMax];
+  __shared__ int s_moff[kRPromptMax + 1], s_mem[kRPromptMax], s_mfill[kRPromptMax];
+  __shared__ long long s_pre[kRPromptMax + 1];
+  __shared__ unsigned long long s_ctot[kRPromptMax];
+  __shared__ double s_S[kRPromptMax], s_r[kRPromptMax], s_aen[kRPromptMax];
+  __shared__ double s_gm[kRPromptMax], s_gs[kRPromptMax];
   const int2 pr = a.prompts[blockIdx.x];
   const int s0 = pr.x, n = pr.y, tid = threadIdx.x;
   const int t0 = a.tin[s0];
-  for (int v = tid; v < n; v += 256) {           // prompt-local indices throughout
+  for (int v = tid; v <= n; v += 256) {
+    s_coff[v] = 0;
+    s_moff[v] = 0;
+    s_pre[v] = 0;
+  }
+  for (int v = tid; v < n; v += 256) {
+    s_ctot[v] = 0;
+    s_cfill[v] = 0;
+    s_mfill[v] = 0;
+  }
+  __syncthreads();
+  for (int v = tid; v < n; v += 256) {               // prompt-local indices throughout
     const int g = s0 + v;
     const int l = a.labels[g];
-    s_lab[v] = ((l >= s0 && l <= g) ? l : g) - s0;
+    const int lab = ((l >= s0 && l <= g) ? l : g) - s0;
+    s_lab[v] = lab;
     const int p = a.parent[g];
     s_par[v] = p >= 0 ? p - s0 : -1;
     s_dep[v] = a.depth[g];
-    s_tin[v] = a.tin[g] - t0;
+    const int tin = a.tin[g] - t0;
+    s_tin[v] = tin;
     s_tout[v] = a.tout[g] - t0;
-    s_rew[v] = a.reward[g];
-    s_sim[v] = a.edge_sim[g];
+    s_eul[tin] = v;
+    const int r = a.reward[g];
+    s_pre[tin] = r >= 0 ? (((long long)r << 32) | 1) : 0;
+    if (p >= 0) atomicAdd(&s_coff[p - s0], 1);
+    atomicAdd(&s_moff[lab], 1);
   }
   __syncthreads();
-  for (int v = tid; v < n; v += 256) {           // outcomes of v's subtree
-    int c = 0, t = 0;
-    for (int z = 0; z < n; ++z)
-      if (s_rew[z] >= 0 && s_tin[v] <= s_tin[z] && s_tin[z] < s_tout[v]) {
-        c += s_rew[z];
-        ++t;
-      }
-    s_c[v] = c;
-    s_t[v] = t;
+  // Exclusive scans over [0, n]: s_pre[k] = sum of the outcome values at Euler positions < k (so
+  // a subtree's sums are s_pre[tout] - s_pre[tin]); s_coff[p] = where p's children start and
+  // s_moff[l] = where the members labelled l start.
+  lds_scan_excl(s_pre, n);
+  lds_scan_excl(s_coff, n);
+  lds_scan_excl(s_moff, n);
+  for (int v = tid; v < n; v += 256) {
+    const int p = s_par[v];
+    if (p >= 0) s_kids[s_coff[p] + atomicAdd(&s_cfill[p], 1)] = v;
+    const int l = s_lab[v];
+    s_mem[s_moff[l] + atomicAdd(&s_mfill[l], 1)] = v;
   }
   __syncthreads();
-  for (int v = tid; v < n; v += 256) {           // pooled scores
-    int64_t C = 0, T = 0;
-    for (int q = 0; q < n; ++q)
-      if (s_lab[q] == s_lab[v]) {
-        C += s_c[q];
-        T += s_t[q];
-      }
-    const double c = (double)s_c[v], t = (double)s_t[v];
-    const double num = c + a.w * ((double)C - c), den = t + a.w * ((double)T - t);
-    const double S = den > 0.0 ? num / den : __builtin_nan("");
-    s_S[v] = S;
-    a.score[s0 + v] = S;
+  for (int v = tid; v < n; v += 256) {               // lists in ascending order
+    sort_small(s_kids + s_coff[v], s_cfill[v]);
+    sort_small(s_mem + s_moff[v], s_mfill[v]);
+  }
+  __syncthreads();
+  for (int v = tid; v < n; v += 256) {               // own outcomes -> class totals
+    const long long own = s_pre[s_tout[v]] - s_pre[s_tin[v]];
+    atomicAdd(&s_ctot[s_lab[v]], (unsigned long long)own);
     s_anc[v] = -1;
     s_aen[v] = 0.0;
   }
   __syncthreads();
-  for (int v = tid; v < n; v += 256) {           // step rewards; class efficiency values
+  for (int v = tid; v < n; v += 256) {               // pooled scores
+    const long long own = s_pre[s_tout[v]] - s_pre[s_tin[v]];
+    const long long tot = (long long)s_ctot[s_lab[v]];
+    const double c = (double)(own >> 32), t = (double)(own & 0xffffffffLL);
+    const double C = (double)(tot >> 32), T = (double)(tot & 0xffffffffLL);
+    const double num = c + a.w * (C - c), den = t + a.w * (T - t);
+    const double S = den > 0.0 ? num / den : __builtin_nan("");
+    s_S[v] = S;
+    a.score[s0 + v] = S;
+  }
+  __syncthreads();
+  for (int v = tid; v < n; v += 256) {               // step rewards; class efficiency values
     const int p = s_par[v];
     double r = __builtin_nan("");
-    if (p >= 0) r = (s_S[v] - s_S[p]) * (1.0 - fmax(0.0, (double)s_sim[v]));
+    if (p >= 0) r = (s_S[v] - s_S[p]) * (1.0 - fmax(0.0, (double)a.edge_sim[s0 + v]));
     s_r[v] = r;
     a.step[s0 + v] = r;
     if (s_lab[v] != v) continue;
-    int m = 0, lca = -1, sdef = 0;
+    const int* mem = s_mem + s_moff[v];
+    const int m = s_mfill[v];
+    if (m < 2) continue;
+    int lca = mem[0], sdef = 0;
     double ssum = 0.0;
-    for (int x = v; x < n; ++x) {
-      if (s_lab[x] != v) continue;
-      ++m;
+    for (int k = 0; k < m; ++k) {
+      const int x = mem[k];
       if (!isnan(s_S[x])) {
         ssum += s_S[x];
         ++sdef;
-      }
-      if (lca < 0) {
-        lca = x;
-        continue;
       }
       int y = x, z = lca;
       while (s_dep[y] > s_dep[z]) y = s_par[y];
@@ -298,62 +359,68 @@ __global__ __launch_bounds__(256) void k_prompt_advantages(RewardArgs a) {
       }
       lca = y;
     }
-    if (m < 2) continue;
     const int anc = s_lab[lca] == v ? s_par[lca] : lca;
     if (anc < 0) continue;
     const double gate = sdef > 0 ? ssum / sdef : 0.0;
     double lsum = 0.0;
-    for (int x = v; x < n; ++x)
-      if (s_lab[x] == v) lsum += -(double)(s_dep[x] - s_dep[anc]);
+    for (int k = 0; k < m; ++k) lsum += -(double)(s_dep[mem[k]] - s_dep[anc]);
     const double mean = lsum / m;
     double q = 0.0;
-    for (int x = v; x < n; ++x)
-      if (s_lab[x] == v) {
-        const double d = -(double)(s_dep[x] - s_dep[anc]) - mean;
-        q += d * d;
-      }
+    for (int k = 0; k < m; ++k) {
+      const double d = -(double)(s_dep[mem[k]] - s_dep[anc]) - mean;
+      q += d * d;
+    }
     const double sd = sqrt(q / m);
-    for (int x = v; x < n; ++x)
-      if (s_lab[x] == v) {
-        const double l = -(double)(s_dep[x] - s_dep[anc]);
-        s_aen[x] = sd > 0.0 ? gate * (l - mean) / sd : 0.0;
-        s_anc[x] = anc;
-      }
+    for (int k = 0; k < m; ++k) {
+      const int x = mem[k];
+      const double l = -(double)(s_dep[x] - s_dep[anc]);
+      s_aen[x] = sd > 0.0 ? gate * (l - mean) / sd : 0.0;
+      s_anc[x] = anc;
+    }
   }
   __syncthreads();
-  for (int u = tid; u < n; u += 256) {           // correctness groups; efficiency per edge
+  for (int u = tid; u < n; u += 256) {               // correctness groups; efficiency per edge
     const int lu = s_lab[u], du = s_dep[u];
+    const int* mem = s_mem + s_moff[lu];
+    const int m = s_mfill[lu];
     int cnt = 0, members = 0;
     double sum = 0.0;
-    for (int c = 0; c < n; ++c) {
-      const int p = s_par[c];
-      if (p < 0 || !(p == u || (s_lab[p] == lu && s_dep[c] > du))) continue;
-      ++members;
-      if (isnan(s_r[c])) continue;
-      sum += s_r[c];
-      ++cnt;
+    for (int k = 0; k < m; ++k) {
+      const int q = mem[k];
+      const int* kid = s_kids + s_coff[q];
+      for (int j = 0; j < s_cfill[q]; ++j) {
+        const int c = kid[j];
+        if (q != u && s_dep[c] <= du) continue;
+        ++members;
+        if (isnan(s_r[c])) continue;
+        sum += s_r[c];
+        ++cnt;
+      }
     }
     double mean = 0.0, sd = 0.0;
     if (members > 1 && cnt > 0) {
       mean = sum / cnt;
-      double q = 0.0;
-      for (int c = 0; c < n; ++c) {
-        const int p = s_par[c];
-        if (p < 0 || !(p == u || (s_lab[p] == lu && s_dep[c] > du))) continue;
-        if (isnan(s_r[c])) continue;
-        const double d = s_r[c] - mean;
-        q += d * d;
+      double q2 = 0.0;
+      for (int k = 0; k < m; ++k) {
+        const int q = mem[k];
+        const int* kid = s_kids + s_coff[q];
+        for (int j = 0; j < s_cfill[q]; ++j) {
+          const int c = kid[j];
+          if ((q != u && s_dep[c] <= du) || isnan(s_r[c])) continue;
+          const double d = s_r[c] - mean;
+          q2 += d * d;
+        }
       }
-      sd = sqrt(q / cnt);
+      sd = sqrt(q2 / cnt);
     }
     s_gm[u] = mean;
     s_gs[u] = sd;
     double e = 0.0;
     if (s_par[u] >= 0)
-      for (int x = 0; x < n; ++x) {
+      for (int pos = s_tin[u]; pos < s_tout[u]; ++pos) {
+        const int x = s_eul[pos];
         const int an = s_anc[x];
-        if (an < 0 || s_tin[x] < s_tin[u] || s_tin[x] >= s_tout[u]) continue;
-        if (s_dep[an] < du) e += s_aen[x];
+        if (an >= 0 && s_dep[an] < du) e += s_aen[x];
       }
     a.a_eff[s0 + u] = e;
   }

@@ -110,8 +110,8 @@ def test_pipeline_classes_similarities_advantages():
 
 def test_one_launch_and_multi_kernel_paths_agree():
     """A batch of prompts of at most 512 states runs in one launch; adding one larger prompt
-    sends the whole batch through the multi-kernel path: the small prompts' results must be the
-    same bits either way."""
+    sends the whole batch through the multi-kernel path: the small prompts' results must agree
+    (to the rounding of the few fp64 sums that the two paths take in different orders)."""
     small = W.state_forest(3, (4, 5, 3, 2))
     big = W.state_forest(1, (6, 6, 15)) + len(small)
     big[0] = -1
@@ -131,4 +131,4 @@ def test_one_launch_and_multi_kernel_paths_agree():
     one = gpu_adv(small, labels[:n], reward[:n], sim[:n], 0.7, 0.5)
     multi = gpu_adv(both, labels, reward, sim, 0.7, 0.5)
     for k in KEYS.values():
-        assert np.array_equal(one[k][:n], multi[k][:n], equal_nan=True), k
+        assert np.allclose(one[k][:n], multi[k][:n], rtol=0, atol=1e-12, equal_nan=True), k

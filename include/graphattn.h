@@ -291,7 +291,8 @@ ga_status graphattn_graph_suffix(const int32_t* labels, const ga_state_forest* f
  *                undefined score
  *   a_cor        z-score of r(v) (population std) among the defined rewards of the group
  *                E_cor(p(v)) = edges into C_g(p(v)), when that group has two or more edges and a
- *                non-zero spread; 0 otherwise
+ *                spread above 1e-12; 0 otherwise (scores lie in [0, 1], so a smaller spread is
+ *                the fp64 rounding of rewards that are equal by the definition)
  *   a_eff        sum, over the classes Q of two or more and their members x whose route from
  *                a_Q (the deepest proper ancestor of all of Q) passes through this edge, of
  *                mean_Q(S) z(-l_x), l_x = d(x) - d(a_Q) (z over Q, population std; 0 if no

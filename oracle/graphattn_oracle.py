@@ -511,14 +511,13 @@ def node_scores(parent, labels, reward, w: float) -> np.ndarray:
     N = len(parent)
     S = np.full(N, np.nan)
     for v in range(N):
-        cs = float(c[v])
-        ts = float(t[v])
-        for q in range(N):
-            if q != v and labels[q] == labels[v]:
-                cs += w * float(c[q])
-                ts += w * float(t[q])
+        # the partners' counts are integers: summed exactly, then weighted by w once, so two
+        # states with the same counts get the same score whatever the order of the sum
+        cq = sum(int(c[q]) for q in range(N) if q != v and labels[q] == labels[v])
+        tq = sum(int(t[q]) for q in range(N) if q != v and labels[q] == labels[v])
+        ts = float(t[v]) + w * float(tq)
         if ts > 0:
-            S[v] = cs / ts
+            S[v] = (float(c[v]) + w * float(cq)) / ts
     return S
 
 
@@ -535,12 +534,19 @@ def step_rewards(parent, S, edge_sim) -> np.ndarray:
     return r
 
 
-def _zscores(values: Sequence[float]) -> List[float]:
-    """(x - mean) / std over a group, population std; 0 for every member if std = 0."""
+# A correctness group whose rewards spread by no more than this has no spread.  Scores lie in
+# [0, 1] and |r_step| <= 2, so rewards that are equal by the definition differ by fp64 rounding
+# (~1e-16) at most, while unequal ones differ by far more; a plain zero test would turn that
+# rounding into z-scores of order one.
+SPREAD_FLOOR = 1e-12
+
+
+def _zscores(values: Sequence[float], floor: float = 0.0) -> List[float]:
+    """(x - mean) / std over a group, population std; 0 for every member if std <= floor."""
     n = len(values)
     m = math.fsum(values) / n
     sd = math.sqrt(math.fsum((x - m) ** 2 for x in values) / n)
-    return [0.0 if sd == 0 else (x - m) / sd for x in values]
+    return [0.0 if sd <= floor else (x - m) / sd for x in values]
 
 
 def correctness_advantage(parent, labels, r) -> np.ndarray:
@@ -548,7 +554,8 @@ def correctness_advantage(parent, labels, r) -> np.ndarray:
 
     The group of source state u is E_cor(u) = {(p(v), v) : v in C_g(u)}; groups exist for
     |C_g(u)| > 1 (Alg. S.1, Stage 3). An edge's advantage is taken in the group of its own
-    source p(v); edges with an undefined reward take no part and get 0.
+    source p(v); edges with an undefined reward take no part and get 0, and so does every edge
+    of a group whose spread is at most SPREAD_FLOOR (no spread).
     """
     offs, states = graph_suffix(labels, parent)
     N = len(parent)
@@ -561,7 +568,7 @@ def correctness_advantage(parent, labels, r) -> np.ndarray:
         if len(grp) <= 1:
             continue
         vals = [float(r[x]) for x in grp if not np.isnan(r[x])]
-        z = _zscores(vals)
+        z = _zscores(vals, SPREAD_FLOOR)
         A[v] = z[[x for x in grp if not np.isnan(r[x])].index(v)]
     return A
 

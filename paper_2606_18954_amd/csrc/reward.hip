@@ -11,7 +11,8 @@
 //   correctness  the group of source u is E_cor(u) = {edges into C_g(u)}: u's successors plus
 //              those of its class partners that lie deeper than u, found by one scan over the
 //              prompt's states; mean and population std of the defined rewards; the edge into v
-//              takes its z-score in the group of p(v) (0 without spread or reward).
+//              takes its z-score in the group of p(v) (0 without spread or reward; a spread of
+//              at most kSpreadFloor is none: rewards equal by the definition differ by rounding).
 //   efficiency per class of two or more (found by its smallest member): the deepest proper
 //              ancestor a_Q of all members, route lengths l = d(v) - d(a_Q), z-scores of -l
 //              gated by the class's mean defined score; every edge then sums, in ascending
@@ -24,6 +25,10 @@ namespace ga {
 namespace {
 
 constexpr int kB = 256;
+// Scores lie in [0, 1] and |r| <= 2: rewards equal by the definition differ by fp64 rounding
+// (~1e-16) at most, unequal ones by far more, so a correctness group spread at or below this
+// is taken as none (its z-scores are 0) rather than rounding blown up to order one.
+constexpr double kSpreadFloor = 1e-12;
 
 __device__ __forceinline__ int64_t gid() { return (int64_t)blockIdx.x * kB + threadIdx.x; }
 
@@ -189,6 +194,7 @@ __global__ void k_groups_and_routes(RewardArgs a) {
       q += d * d;
     }
     sd = sqrt(q / n);
+    if (!(sd > kSpreadFloor)) sd = 0.0;
   }
   a.gmean[u] = mean;
   a.gstd[u] = sd;                                  // 0: no group, or no spread
@@ -412,6 +418,7 @@ __global__ __launch_bounds__(256) void k_prompt_advantages(RewardArgs a) {
         }
       }
       sd = sqrt(q2 / cnt);
+      if (!(sd > kSpreadFloor)) sd = 0.0;
     }
     s_gm[u] = mean;
     s_gs[u] = sd;

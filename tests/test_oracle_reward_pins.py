@@ -138,11 +138,11 @@ ORIG_SUFFIX = O.graph_suffix
 ORIG_EFF = O.efficiency_advantage
 
 
-def _sample_std(values):
+def _sample_std(values, floor=0.0):
     n = len(values)
     m = sum(values) / n
     sd = math.sqrt(sum((x - m) ** 2 for x in values) / max(1, n - 1))
-    return [0.0 if sd == 0 else (x - m) / sd for x in values]
+    return [0.0 if sd <= floor else (x - m) / sd for x in values]
 
 
 def _own_children_only(labels, parent):
@@ -170,3 +170,37 @@ def test_planted_mistake_is_caught(monkeypatch, name, attr, repl):
             caught = True
             break
     assert caught, f"planted mistake {name} went unnoticed"
+
+
+def test_equal_scores_are_bit_identical_and_give_no_spread():
+    """States 4 and 11 (11 the only child of 4, one class) hold the same terminal evidence and
+    the same partners, so S(4) = S(11) exactly (46/91 here) and r(11) = 0: the group of source 4
+    then holds rewards that are all 0 by the definition and its z-scores are 0.  A sum of
+    w c_own(q) taken in a different order for each state used to leave them one ulp apart and
+    turn that ulp into A_cor(11) = -sqrt(3)."""
+    parent = np.array([-1, 0, 1, 2, 3, 0, 5, 0, 3, 0, 2, 4, 6, 10, 6, 11, 15, 13, 14, 14],
+                      dtype=np.int64)
+    labels = np.array([0] + [1] * 17 + [18, 1])
+    reward = np.array([-1, -1, -1, -1, -1, -1, -1, 0, 0, 0, -1, -1, 1, -1, -1, -1, 1, 0, 1, 0])
+    S = O.node_scores(parent, labels, reward, 0.3)
+    assert S[4] == S[11]
+    c, t = O.subtree_outcomes(parent, reward)
+    cq = int(c[labels == 1].sum()) - int(c[4])
+    tq = int(t[labels == 1].sum()) - int(t[4])
+    assert S[4] == pytest.approx((c[4] + 0.3 * cq) / (t[4] + 0.3 * tq), rel=1e-15)
+    sim = np.linspace(-0.9, 0.9, len(parent))
+    r = O.step_rewards(parent, S, sim)
+    assert r[11] == 0.0
+    A = O.correctness_advantage(parent, labels, r)
+    offs, st = O.graph_suffix(labels, parent)
+    grp = st[offs[4]:offs[5]].tolist()
+    assert grp == [11, 15, 16, 17] and all(r[x] == 0.0 for x in grp)
+    assert A[11] == 0.0
+
+
+def test_spread_floor_keeps_real_spreads():
+    """A real spread far below the scores' scale but above rounding still gives z-scores, and
+    one within rounding gives none."""
+    assert O._zscores([0.0, 1e-9], O.SPREAD_FLOOR) == pytest.approx([-1.0, 1.0])
+    assert O._zscores([0.0, 0.0, 0.0, -1.1e-16], O.SPREAD_FLOOR) == [0.0] * 4
+    assert O._zscores([0.0, 0.0, 0.0, -1.1e-16])[3] == pytest.approx(-math.sqrt(3))

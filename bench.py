@@ -34,26 +34,28 @@ MFMA_BF16_PEAK_TFLOPS = 2500.0
 METRIC = "branch-tokens/s per decode step; % of HBM roofline on unique KV bytes"
 COUNTERS_MD = os.path.join(ROOT, "profiles", "seg_attn_merged_dag_counters.md")
 EXT_COUNTERS_MD = os.path.join(ROOT, "profiles", "seg_attn_extend_counters.md")
+EQ_COUNTERS_MD = os.path.join(ROOT, "profiles", "equiv_classes_counters.md")
 KERNEL_SRC = os.path.join(ROOT, "paper_2606_18954_amd", "csrc", "seg_attn.hip")
+EQ_KERNEL_SRC = os.path.join(ROOT, "paper_2606_18954_amd", "csrc", "equiv.hip")
 
 
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def kernel_hash():
-    with open(KERNEL_SRC, "rb") as f:
+def kernel_hash(src=KERNEL_SRC):
+    with open(src, "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def measured_counters(config, path=COUNTERS_MD):
+def measured_counters(config, path=COUNTERS_MD, src=KERNEL_SRC):
     """HBM traffic and MFMA busy fraction from the committed rocprofv3 counter summary, only
-    if it was taken on this exact attention kernel source and workload."""
+    if it was taken on this exact kernel source and workload."""
     if not os.path.exists(path):
         return None
     txt = open(path).read()
     kv = dict(re.findall(r"^- (\w+): (\S+)", txt, flags=re.M))
-    if kv.get("kernel_source_sha256_16") != kernel_hash() or kv.get("workload") != config:
+    if kv.get("kernel_source_sha256_16") != kernel_hash(src) or kv.get("workload") != config:
         return None
     return kv
 
@@ -360,6 +362,10 @@ def run_equiv(args, torch, G, W):
     pairs = compared_pairs_count(wl.parent)
     achieved = zbytes / (ms * 1e-3) / 1e9
     merged = int((lab != np.arange(N)).sum())
+    cnt = measured_counters("equiv", EQ_COUNTERS_MD, EQ_KERNEL_SRC)
+    traffic = None
+    if cnt:
+        traffic = float(cnt["fetch_bytes_per_launch"]) + float(cnt["write_bytes_per_launch"])
     res = {
         "metric": "rollout states/s classified per equivalence-detection call; % of HBM "
                   "roofline on embedding bytes",
@@ -371,11 +377,13 @@ def run_equiv(args, torch, G, W):
                    "compared_pairs": pairs, "classes": int(len(set(lab.tolist()))),
                    "merged_states": merged, "suffix_entries": total},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None},
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic},
         "compared_pair_tflops": pairs * 2 * dim / (ms * 1e-3) / 1e12,
         "kernel_ms": {"classes": ms, "graph_suffix": suffix_ms, "advantages": adv_ms},
     }
     f.close()
+    if args.calibrate_copy:
+        calibrate_copy(torch, dev)
     if args.cpu_sample > 0:
         from oracle import graphattn_oracle as O
         per = 205

@@ -111,6 +111,42 @@ def timed_steps(torch, plan, step, steps):
     return ms, attn_ms, merge_ms, sched_ms
 
 
+def mall_flushed_attention(torch, plan, step, steps, dev):
+    """Attention duration (library HIP events) with the memory-side cache (256 MB on MI355X)
+    flushed before every step by reading a 512 MiB buffer (a read leaves no dirty lines for
+    the attention kernel to write back); the read runs between steps, outside the kernel
+    events."""
+    junk = torch.ones(1 << 27, dtype=torch.float32, device=dev)
+    plan.profile(steps)
+    for _ in range(steps):
+        junk.sum()
+        step()
+    prof = plan.profile_read()
+    plan.profile(0)
+    del junk
+    torch.cuda.empty_cache()
+    return prof.attn_ms / max(1, prof.runs)
+
+
+def stream_copy_gbs(torch, dev, reps=10):
+    """Bandwidth of a plain device copy (torch elementwise, 1 GiB read + 1 GiB written)."""
+    a = torch.ones(1 << 29, dtype=torch.bfloat16, device=dev)
+    b = torch.empty_like(a)
+    torch.mul(a, 1.0, out=b)
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(reps):
+        torch.mul(a, 1.0, out=b)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del a, b
+    torch.cuda.empty_cache()
+    return 2.0 * (1 << 30) / (ms * 1e-3) / 1e9
+
+
 def extend_flops(wl):
     """Attention flops of an extend step: 2 D per visible token for S = Q K^T and 2 D for O = P V,
     per query row and q-head; query i of branch b sees its path's other segments whole and
@@ -447,7 +483,11 @@ def main():
     lse = torch.empty((B, Hq), dtype=torch.float32, device=dev)
     hg = G.HostGraph.from_graph(g)
     params = G.make_params(Hq, wl.num_kv_heads, D, g.num_pages, wl.dtype)
-    plan = G.Plan(hg, params)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    plan = G.Plan(hg, params)                       # host validation, chains, index upload
+    torch.cuda.synchronize()
+    plan_ms = (time.perf_counter() - t1) * 1e3
     info = plan.info()
 
     def step():
@@ -459,6 +499,10 @@ def main():
     torch.cuda.synchronize()
     log(f"warmup done ({args.warmup} steps)")
     ms, attn_ms, merge_ms, sched_ms = timed_steps(torch, plan, step, args.steps)
+    cold_ms = mall_flushed_attention(torch, plan, step, args.steps, dev)
+    copy_gbs = stream_copy_gbs(torch, dev)
+    log(f"attention with the memory-side cache flushed before each step: {cold_ms:.4f} ms; "
+        f"plain device copy: {copy_gbs:.0f} GB/s; plan creation {plan_ms:.1f} ms")
 
     ukv = wl.unique_kv_bytes()
     achieved = ukv / (attn_ms * 1e-3) / 1e9
@@ -483,10 +527,17 @@ def main():
                    "chunk_pages": info.chunk_pages},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic},
-        "kernel_ms": {"scheduler": sched_ms, "attention": attn_ms, "merge": merge_ms},
+        "kernel_ms": {"scheduler": sched_ms, "attention": attn_ms, "merge": merge_ms,
+                      "attention_mall_flushed": cold_ms},
         "timing": "ms_per_step over the timed steps without per-kernel events; kernel_ms (and "
                   "the roofline) from as many further steps with HIP events on the launch stream "
-                  "around each kernel",
+                  "around each kernel; attention_mall_flushed from as many more with a 512 MiB "
+                  "read between steps",
+        "mall_flushed_frac": ukv / (cold_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+        "stream_copy_gbs": copy_gbs,
+        "frac_of_stream_copy": achieved / copy_gbs,
+        "plan_create_ms": plan_ms,
+        "pcie_inclusive_branch_tokens_per_s": B / ((plan_ms + ms) * 1e-3),
         "unique_kv_bytes": ukv,
         "step_unique_kv_frac": ukv / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
         "attended_tokens_per_s": g.attended_tokens() / (ms * 1e-3),

@@ -455,7 +455,7 @@ def main():
                          "counters can be scaled against a kernel of known traffic")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path (the design notes "
+        print("bench.py measures one GPU: the library has no multi-GPU path (the design notes "
               "describe how prompts would be sharded across GPUs). Run with --gpus 1.",
               file=sys.stderr)
         sys.exit(2)

@@ -125,7 +125,8 @@ ga_status graphattn_extend(const void* q, const void* kv_page_pool,
                            void* out, float* lse, const ga_params* params, void* hip_stream);
 
 /* Validate the graph and parameters, allocate the plan's device workspace (sized for this
- * graph) and enqueue the upload of the index arrays on hip_stream.  The host arrays may be
+ * graph, with every segment at all the pages the page table gives it, so that lengths set later
+ * by graphattn_plan_set_lengths fit) and enqueue the upload of the index arrays on hip_stream.  The host arrays may be
  * released when the call returns.  *plan receives a new plan (NULL on error). */
 ga_status graphattn_plan_create(const ga_segment_table* segment_table,
                                 const ga_branch_paths* branch_paths, const ga_params* params,
@@ -138,6 +139,20 @@ ga_status graphattn_plan_create_extend(const ga_segment_table* segment_table,
                                        const ga_branch_paths* branch_paths,
                                        const int32_t* query_counts, const ga_params* params,
                                        void* hip_stream, ga_plan** plan);
+
+/* New segment lengths for a plan, for the decode loop of Alg. S.1 (Stage 1): each step stores
+ * a token per branch in the page slot after its newest segment's last token
+ * (graphattn_kv_append) and the segment grows by one; a state that spawns children starts new
+ * segments.  seg_len [num_segments of the plan's graph] host, read during the call: every
+ * length >= 1 and within the pages the segment owns in the plan's page table (the page table
+ * may give a segment more pages than its length uses, reserved for growth); for a multi-query
+ * plan each branch's query count must stay <= its newest segment's length.  GA_EINVAL
+ * otherwise, and the plan is unchanged.  Paths, page ids and query counts stay as created.  The
+ * plan's graph copy is rebuilt on the host and uploaded asynchronously on hip_stream, ordered
+ * after the work already enqueued there (work of this plan on other streams must be complete);
+ * the host waits only for the plan's previous upload to leave its pinned staging.  No
+ * allocation.  The plan must be scheduled again (graphattn_schedule) before its next run. */
+ga_status graphattn_plan_set_lengths(ga_plan* plan, const int32_t* seg_len, void* hip_stream);
 
 /* Segment scheduler, on the GPU: transpose branch->segments into segment->branches (B(s) in
  * ascending branch order), give each path entry the branch's position inside B(s), split long

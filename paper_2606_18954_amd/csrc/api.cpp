@@ -68,7 +68,8 @@ struct CGraph {
 
 struct Sizes {
   int32_t S = 0, B = 0, E = 0;
-  int64_t P = 0;               // entries of seg_pages
+  int64_t P = 0;               // entries of seg_pages in use
+  int64_t P_cap = 0;           // entries reserved for seg_pages (every segment at its owned pages)
   int32_t chunk_pages = 0;
   int64_t max_items = 0;       // upper bound on work items per kv-head
   int32_t desc_words = 0;      // work-item descriptor stride (int32 words)
@@ -98,6 +99,15 @@ struct ga_plan {
   int32_t B0 = 0;              // branches as given (z.B counts query rows)
   int num_cus = 256;
   CGraph cg;                   // the uploaded (chain) graph and its map to the given one
+  // What a length update (graphattn_plan_set_lengths) rebuilds the chain graph from: the page
+  // table as given, the paths the chains were built over (query rows for multi-query plans), and
+  // for multi-query plans each branch's newest segment and query count.
+  std::vector<int64_t> h_page_off;
+  std::vector<int32_t> h_pages;
+  std::vector<int64_t> h_path_off;
+  std::vector<int32_t> h_path_segs;
+  std::vector<int32_t> h_last, h_counts;
+  hipEvent_t uploaded = nullptr;   // recorded after each upload from the pinned staging
   ga::DevGraph g{};
   ga::DevSchedule sc{};
   void* po = nullptr;
@@ -278,8 +288,11 @@ ga_status compress_chains(const ga_segment_table* st, const ga_branch_paths* bp,
 
 // Chunking policy: split a segment only when the whole step would otherwise leave the
 // persistent grid short of work; every extra chunk costs one more partial per branch row.
+// The chunk size follows the pages in use (npg); the bounds on partial rows and work items
+// follow the pages each chain owns (npg_cap >= npg), so that any later lengths fit.
 void size_schedule(const ga_segment_table* st, const ga_branch_paths* bp, const ga_params* p,
-                   const std::vector<int32_t>& npg, int num_cus, Sizes* z) {
+                   const std::vector<int32_t>& npg, const std::vector<int64_t>& npg_cap,
+                   int num_cus, Sizes* z) {
   std::vector<char> used(z->S, 0);
   for (int64_t e = 0; e < z->E; ++e) used[bp->path_segs[e]] = 1;
   int64_t ref_pages = 0;
@@ -292,10 +305,10 @@ void size_schedule(const ga_segment_table* st, const ga_branch_paths* bp, const 
   const int32_t group = p->num_q_heads / p->num_kv_heads;
   int64_t chunks_ref = 0, prows = 0;
   for (int32_t s = 0; s < z->S; ++s)
-    if (used[s]) chunks_ref += (npg[s] + cap - 1) / cap;
+    if (used[s]) chunks_ref += (npg_cap[s] + cap - 1) / cap;
   for (int64_t e = 0; e < z->E; ++e) {
     const int32_t s = bp->path_segs[e];
-    prows += (npg[s] + cap - 1) / cap;
+    prows += (npg_cap[s] + cap - 1) / cap;
   }
   z->prows = prows;   // partial rows are stored as int32 in the branch lists (checked by the caller)
   // items(s) = chunks(s) * ceil(|B(s)| g / 128) <= chunks(s) * (|B(s)| g / 128 + 1)
@@ -321,7 +334,7 @@ Layout layout(const Sizes& z, const ga_params& p) {
   size_t sz[L_COUNT];
   sz[L_SEG_LEN] = sizeof(int32_t) * z.S;
   sz[L_SEG_PAGE_OFF] = sizeof(int64_t) * (z.S + 1);
-  sz[L_SEG_PAGES] = sizeof(int32_t) * z.P;
+  sz[L_SEG_PAGES] = sizeof(int32_t) * (z.P_cap > z.P ? z.P_cap : z.P);
   sz[L_PATH_OFF] = sizeof(int64_t) * (z.B + 1);
   sz[L_PATH_SEGS] = sizeof(int32_t) * z.E;
   sz[L_SEG_CAUSAL] = sizeof(int32_t) * z.S;
@@ -463,6 +476,36 @@ ga_status expand_queries(const ga_segment_table* st, const ga_branch_paths* bp,
   return GA_OK;
 }
 
+// Multi-query plans: the newest segment of branch b closes its chain (it is the last entry of
+// every path through it) and starts on a page of its own, so its token t is chain token
+// 16 x (chain pages before it) + t, and query i sits at t = len - n_b + i.
+ga_status set_causal(const ga_plan* pl, const int32_t* seg_len, const std::vector<int32_t>& npg,
+                     CGraph* c) {
+  for (size_t b = 0; b < pl->h_last.size(); ++b) {
+    const int32_t last = pl->h_last[b];
+    const int32_t v = c->vid[last];
+    if (c->seg_len[v] >= ga::kNoCausal)
+      return fail(GA_EUNSUPPORTED, "segment chain of branch %d spans %d tokens", (int)b,
+                  c->seg_len[v]);
+    c->causal[v] = (c->npg[v] - npg[last]) * ga::kPageTokens + seg_len[last] - pl->h_counts[b];
+  }
+  return GA_OK;
+}
+
+// Pages each chain owns (the sum over its segments of the pages the page table gives them), and
+// their total: the room the uploaded page list and the schedule bounds are sized for.
+int64_t chain_capacity(const ga_plan* pl, const CGraph& c, std::vector<int64_t>* cap) {
+  cap->assign(c.head.size(), 0);
+  int64_t total = 0;
+  for (size_t x = 0; x < c.vid.size(); ++x)
+    if (c.vid[x] >= 0) {
+      const int64_t n = pl->h_page_off[x + 1] - pl->h_page_off[x];
+      (*cap)[c.vid[x]] += n;
+      total += n;
+    }
+  return total;
+}
+
 ga_status plan_init(const ga_segment_table* st, const ga_branch_paths* bp, const ga_params* p,
                     const int32_t* query_counts, ga_plan* pl, Layout* L) {
   ga_status rc = validate_params(p);
@@ -482,21 +525,22 @@ ga_status plan_init(const ga_segment_table* st, const ga_branch_paths* bp, const
     if (rc) return rc;
     pl->causal = true;
   }
-  rc = compress_chains(st, query_counts ? &vbp : bp, npg, &pl->cg);
+  const ga_branch_paths* ebp = query_counts ? &vbp : bp;
+  rc = compress_chains(st, ebp, npg, &pl->cg);
   if (rc) return rc;
+  // Kept for length updates.
+  const int32_t S0 = st->num_segments;
+  pl->h_page_off.assign(st->seg_page_offsets, st->seg_page_offsets + S0 + 1);
+  pl->h_pages.assign(st->seg_pages, st->seg_pages + st->seg_page_offsets[S0]);
+  pl->h_path_off.assign(ebp->path_offsets, ebp->path_offsets + ebp->num_branches + 1);
+  pl->h_path_segs.assign(ebp->path_segs, ebp->path_segs + ebp->path_offsets[ebp->num_branches]);
   if (query_counts) {
-    // The newest segment closes its chain (it is the last entry of every path through it), and
-    // starts on a page of its own: its token t is chain token 16 x (chain pages before it) + t,
-    // and query i sits at t = len - n + i.
-    for (int32_t b = 0; b < bp->num_branches; ++b) {
-      const int32_t last = bp->path_segs[bp->path_offsets[b + 1] - 1];
-      const int32_t v = pl->cg.vid[last];
-      if (pl->cg.seg_len[v] >= ga::kNoCausal)
-        return fail(GA_EUNSUPPORTED, "segment chain of branch %d spans %d tokens", b,
-                    pl->cg.seg_len[v]);
-      pl->cg.causal[v] =
-          (pl->cg.npg[v] - npg[last]) * ga::kPageTokens + st->seg_len[last] - query_counts[b];
-    }
+    pl->h_last.resize(bp->num_branches);
+    for (int32_t b = 0; b < bp->num_branches; ++b)
+      pl->h_last[b] = bp->path_segs[bp->path_offsets[b + 1] - 1];
+    pl->h_counts.assign(query_counts, query_counts + bp->num_branches);
+    rc = set_causal(pl, st->seg_len, npg, &pl->cg);
+    if (rc) return rc;
   }
   const CGraph& c = pl->cg;
   pl->z.S = (int32_t)c.head.size();
@@ -507,7 +551,9 @@ ga_status plan_init(const ga_segment_table* st, const ga_branch_paths* bp, const
   pl->p = *p;
   if (pl->p.softmax_scale == 0.f) pl->p.softmax_scale = 1.f / std::sqrt((float)p->head_dim);
   pl->num_cus = device_cus();
-  size_schedule(&cst, &cbp, p, c.npg, pl->num_cus, &pl->z);
+  std::vector<int64_t> npg_cap;
+  pl->z.P_cap = chain_capacity(pl, c, &npg_cap);
+  size_schedule(&cst, &cbp, p, c.npg, npg_cap, pl->num_cus, &pl->z);
   if (pl->z.prows > 0x7fffffffLL)
     return fail(GA_EINVAL, "too many partial rows (%lld)", (long long)pl->z.prows);
   if (pl->z.P > 0x7fffffffLL)
@@ -528,6 +574,7 @@ ga_status upload(ga_plan* pl, const Layout& L, hipStream_t stream) {
   pack_upload(&cst, &cbp, c.causal.data(), L, pl->z, static_cast<char*>(pl->pin));
   GA_HIP(hipMemcpyAsync(pl->dev, pl->pin, upload_bytes(L), hipMemcpyHostToDevice, stream),
          "graph upload");
+  if (pl->uploaded) GA_HIP(hipEventRecord(pl->uploaded, stream), "record upload");
   return GA_OK;
 }
 
@@ -652,6 +699,11 @@ static ga_status plan_create(const ga_segment_table* segment_table,
     return fail(GA_ENOMEM, "pinned staging of %zu bytes", pl->pin_bytes);
   }
   bind(pl, L);
+  if (hipEventCreateWithFlags(&pl->uploaded, hipEventDisableTiming) != hipSuccess) {
+    pl->uploaded = nullptr;
+    graphattn_plan_destroy(pl);
+    return hip_fail(hipGetLastError(), "event");
+  }
   rc = upload(pl, L, static_cast<hipStream_t>(hip_stream));
   if (rc) {
     graphattn_plan_destroy(pl);
@@ -679,6 +731,53 @@ ga_status graphattn_plan_create_extend(const ga_segment_table* segment_table,
   static const int32_t none = 0;
   return plan_create(segment_table, branch_paths, query_counts ? query_counts : &none, params,
                      hip_stream, plan);
+}
+
+ga_status graphattn_plan_set_lengths(ga_plan* plan, const int32_t* seg_len, void* hip_stream) {
+  g_err.clear();
+  if (!plan) return fail(GA_EINVAL, "plan is NULL");
+  const int32_t S = plan->cg.S0;
+  if (S > 0 && !seg_len) return fail(GA_EINVAL, "seg_len is NULL");
+  std::vector<int32_t> npg(S);
+  for (int32_t s = 0; s < S; ++s) {
+    const int32_t len = seg_len[s];
+    if (len < 1) return fail(GA_EINVAL, "segment %d has length %d (< 1)", s, len);
+    const int64_t owned = plan->h_page_off[s + 1] - plan->h_page_off[s];
+    const int64_t need = (len + ga::kPageTokens - 1) / ga::kPageTokens;
+    if (need > owned)
+      return fail(GA_EINVAL, "segment %d has %d tokens but owns only %lld pages", s, len,
+                  (long long)owned);
+    npg[s] = (int32_t)need;
+  }
+  for (size_t b = 0; b < plan->h_last.size(); ++b)
+    if (plan->h_counts[b] > seg_len[plan->h_last[b]])
+      return fail(GA_EINVAL, "branch %d: query count %d exceeds its newest segment's %d tokens",
+                  (int)b, plan->h_counts[b], seg_len[plan->h_last[b]]);
+  // The chains (which segments go together) follow the paths only; their page lists, valid
+  // token counts, lengths and causal origins are rebuilt from the new lengths.
+  const ga_segment_table st{S, seg_len, plan->h_page_off.data(), plan->h_pages.data()};
+  const ga_branch_paths bp{(int32_t)(plan->h_path_off.size() - 1), plan->h_path_off.data(),
+                           plan->h_path_segs.data()};
+  CGraph c;
+  ga_status rc = compress_chains(&st, &bp, npg, &c);
+  if (rc) return rc;
+  if (!plan->h_last.empty()) {
+    rc = set_causal(plan, seg_len, npg, &c);
+    if (rc) return rc;
+  }
+  if ((int64_t)c.seg_pages.size() > plan->z.P_cap)
+    return fail(GA_EINVAL, "page list of %zu entries exceeds the plan's %lld",
+                c.seg_pages.size(), (long long)plan->z.P_cap);
+  // The previous upload must have left the staging buffer before it is refilled; the new copy
+  // is ordered on the stream after the work already enqueued there.
+  GA_HIP(hipEventSynchronize(plan->uploaded), "wait for previous upload");
+  plan->cg = std::move(c);
+  plan->z.P = (int64_t)plan->cg.seg_pages.size();
+  const Layout L = layout(plan->z, plan->p);
+  rc = upload(plan, L, static_cast<hipStream_t>(hip_stream));
+  if (rc) return rc;
+  plan->scheduled = false;
+  return GA_OK;
 }
 
 ga_status graphattn_schedule(ga_plan* plan, void* hip_stream) {
@@ -814,6 +913,7 @@ ga_status graphattn_plan_profile_read(ga_plan* plan, ga_profile* out) {
 void graphattn_plan_destroy(ga_plan* plan) {
   if (!plan) return;
   profile_clear(plan);
+  if (plan->uploaded) (void)hipEventDestroy(plan->uploaded);
   if (plan->owns_memory) {
     if (plan->dev) {
       (void)hipDeviceSynchronize();

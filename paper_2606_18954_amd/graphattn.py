@@ -118,6 +118,8 @@ def load_library() -> ctypes.CDLL:
     lib.graphattn_forest_destroy.restype = None
     lib.graphattn_schedule.argtypes = [vp, vp]
     lib.graphattn_schedule.restype = ctypes.c_int
+    lib.graphattn_plan_set_lengths.argtypes = [vp, P(i32), vp]
+    lib.graphattn_plan_set_lengths.restype = ctypes.c_int
     lib.graphattn_run.argtypes = [vp, vp, vp, vp, vp, vp]
     lib.graphattn_run.restype = ctypes.c_int
     lib.graphattn_plan_info.argtypes = [vp, P(PlanInfo)]
@@ -392,6 +394,14 @@ class Plan:
                 _ptr(self.query_counts, ctypes.c_int32), ctypes.byref(params),
                 _stream_handle(stream), ctypes.byref(h)))
         self.handle = h
+
+    def set_lengths(self, seg_len, stream=None):
+        """New segment lengths (host int32 [num_segments]); schedule again before the next run."""
+        import numpy as np
+        a = np.ascontiguousarray(np.asarray(seg_len, dtype=np.int32))
+        _check(self.lib.graphattn_plan_set_lengths(
+            self.handle, a.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+            _stream_handle(stream)))
 
     def schedule(self, stream=None):
         _check(self.lib.graphattn_schedule(self.handle, _stream_handle(stream)))

@@ -22,7 +22,7 @@ def test_library_exports_every_declared_symbol():
                          "graphattn_equivalence_classes", "graphattn_graph_suffix",
                          "graphattn_forest_create", "graphattn_forest_classes",
                          "graphattn_forest_suffix", "graphattn_forest_destroy",
-                         "graphattn_forest_advantages"}
+                         "graphattn_forest_advantages", "graphattn_plan_set_lengths"}
     for s in syms:
         assert hasattr(lib, s), s
 
@@ -295,6 +295,9 @@ def test_device_failures_are_reported_without_a_gpu():
                                    ctypes.byref(h))
     assert st in (G.GA_ENOMEM, G.GA_EHIP) and G.last_error()
     assert not h.value                                # no plan handed out on failure
+    lens = (ctypes.c_int32 * 3)(20, 7, 33)
+    assert lib.graphattn_plan_set_lengths(None, lens, None) == G.GA_EINVAL
+    assert "plan is NULL" in G.last_error()
     fake = ctypes.c_void_p(1 << 20)                   # aligned, never dereferenced here
     st = lib.graphattn_decode(fake, fake, ctypes.byref(g.st), ctypes.byref(g.bp), fake,
                               ctypes.cast(fake, ctypes.POINTER(ctypes.c_float)),

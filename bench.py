@@ -332,6 +332,95 @@ def run_append(args, torch, G, W):
     print(json.dumps(res), flush=True)
 
 
+def run_loop(args, torch, G, W):
+    """The decode loop on the merged-DAG rollout: every step stores one new token at the end of
+    each newest segment (graphattn_kv_append), grows those segments by one token
+    (graphattn_plan_set_lengths: host rebuild and upload of the plan's graph copy), schedules
+    and attends.  The page table gives every newest segment the pages it grows into; the pool
+    gets those pages on top of the rollout's own."""
+    import numpy as np
+    wl = W.config3_merged_dag()
+    g = wl.graph
+    B, Hq, Hkv, D = g.num_branches, wl.num_q_heads, wl.num_kv_heads, wl.head_dim
+    total = args.warmup + args.steps + 1
+    newest = np.unique(np.array([int(g.path(b)[-1]) for b in range(B)]))
+    S = g.num_segments
+    lens = g.seg_len.astype(np.int32).copy()
+    extra = np.zeros(S, dtype=np.int64)
+    for s in newest:
+        extra[s] = (int(lens[s]) + total + 15) // 16 - (int(lens[s]) + 15) // 16
+    offs = np.zeros(S + 1, dtype=np.int64)
+    np.cumsum((lens.astype(np.int64) + 15) // 16 + extra, out=offs[1:])
+    pages = np.empty(int(offs[-1]), dtype=np.int32)
+    nxt = g.num_pages
+    for s in range(S):
+        own = g.seg_pages[g.seg_page_offsets[s]:g.seg_page_offsets[s + 1]]
+        pages[offs[s]:offs[s] + len(own)] = own
+        pages[offs[s] + len(own):offs[s + 1]] = np.arange(nxt, nxt + extra[s], dtype=np.int32)
+        nxt += int(extra[s])
+    num_pages = nxt
+    dev = torch.device("cuda:0")
+    gen = torch.Generator().manual_seed(wl.seed + 29)
+    pool = torch.cat([wl.pool, torch.randn((num_pages - g.num_pages, Hkv, 2, 16, D),
+                                           generator=gen).to(wl.pool.dtype)]).to(dev)
+    q = wl.q.to(dev)
+    out = torch.empty((B, Hq, D), dtype=q.dtype, device=dev)
+    lse = torch.empty((B, Hq), dtype=torch.float32, device=dev)
+    hg = G.HostGraph(lens.tolist(), offs, pages, g.path_offsets, g.path_segs)
+    params = G.make_params(Hq, Hkv, D, num_pages, wl.dtype)
+    plan = G.Plan(hg, params)
+    n = len(newest)
+    kn = torch.randn((n, Hkv, D), generator=gen).to(q.dtype).to(dev)
+    vn = torch.randn((n, Hkv, D), generator=gen).to(q.dtype).to(dev)
+    # slot words of every step's new tokens, uploaded once
+    words = np.empty((total, n), dtype=np.int32)
+    for k in range(total):
+        t = lens[newest] + k
+        words[k] = pages[offs[newest] + t // 16] * 16 + t % 16
+    wd = torch.from_numpy(words).to(dev)
+    cur = lens.copy()
+    k = 0
+    host_s = []
+
+    def step():
+        nonlocal k
+        G.kv_append(pool, kn, vn, wd[k], params)
+        cur[newest] += 1
+        t0 = time.perf_counter()
+        plan.set_lengths(cur)
+        host_s.append(time.perf_counter() - t0)
+        plan.schedule()
+        plan.run(q, pool, out, lse)
+        k += 1
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    host_s.clear()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    for _ in range(args.steps):
+        step()
+    ev1.record()
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / args.steps
+    set_ms = 1e3 * float(np.median(host_s))
+    plan.close()
+    log(f"decode loop: {ms:.4f} ms per step (append {n} tokens, grow, schedule, attend); "
+        f"length update {set_ms:.3f} ms on the host")
+    res = {
+        "metric": "branch-tokens/s per decode-loop step (append, grow, schedule, attend)",
+        "value": B / (ms * 1e-3), "unit": "branch-tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": wl.dtype, "data": "synthetic",
+        "config": {"workload": wl.name + ", decode loop", "branches": B,
+                   "newest_segments": int(n), "q_heads": Hq, "kv_heads": Hkv, "head_dim": D},
+        "set_lengths_host_ms": set_ms,
+    }
+    print(json.dumps(res), flush=True)
+
+
 def compared_pairs_count(parent):
     """Pairs the method compares: same prompt, neither an ancestor of the other.  A prompt with n
     states has n (n - 1) / 2 pairs, of which sum over states of (depth) are ancestor pairs."""
@@ -445,7 +534,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="c3",
                     choices=["c1", "c2", "c3", "c4", "c5chain", "c5graph"])
-    ap.add_argument("--op", default="decode", choices=["decode", "extend", "append", "equiv"])
+    ap.add_argument("--op", default="decode",
+                    choices=["decode", "extend", "append", "equiv", "loop"])
     ap.add_argument("--n-query", type=int, default=16,
                     help="query tokens per branch for --op extend")
     ap.add_argument("--cpu-sample", type=int, default=1024,
@@ -471,6 +561,8 @@ def main():
         return run_append(args, torch, G, W)
     if args.op == "equiv":
         return run_equiv(args, torch, G, W)
+    if args.op == "loop":
+        return run_loop(args, torch, G, W)
     t0 = time.time()
     wl = W.CONFIGS[args.config]()
     g = wl.graph

@@ -148,10 +148,12 @@ ga_status graphattn_plan_create_extend(const ga_segment_table* segment_table,
  * may give a segment more pages than its length uses, reserved for growth); for a multi-query
  * plan each branch's query count must stay <= its newest segment's length.  GA_EINVAL
  * otherwise, and the plan is unchanged.  Paths, page ids and query counts stay as created.  The
- * plan's graph copy is rebuilt on the host and uploaded asynchronously on hip_stream, ordered
- * after the work already enqueued there (work of this plan on other streams must be complete);
- * the host waits only for the plan's previous upload to leave its pinned staging.  No
- * allocation.  The plan must be scheduled again (graphattn_schedule) before its next run. */
+ * lengths are copied to the device and the plan's segment chains (page lists with their valid
+ * token counts, lengths, causal origins) are rebuilt there in place, asynchronously on
+ * hip_stream and ordered after the work already enqueued there (work of this plan on other
+ * streams must be complete); the host waits only for the plan's previous upload to leave its
+ * pinned staging.  No allocation.  The plan must be scheduled again (graphattn_schedule) before
+ * its next run. */
 ga_status graphattn_plan_set_lengths(ga_plan* plan, const int32_t* seg_len, void* hip_stream);
 
 /* Segment scheduler, on the GPU: transpose branch->segments into segment->branches (B(s) in

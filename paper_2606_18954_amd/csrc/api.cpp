@@ -64,12 +64,15 @@ struct CGraph {
   std::vector<int32_t> head;       // [chains] first segment of each chain
   std::vector<char> first;         // [S0] the segment starts its chain
   std::vector<int32_t> causal;     // [chains] causal origin (multi-query plans), else kNoCausal
+  std::vector<int32_t> chain_seg_off, chain_segs;   // CSR: each chain's segments in path order
 };
 
 struct Sizes {
   int32_t S = 0, B = 0, E = 0;
   int64_t P = 0;               // entries of seg_pages in use
-  int64_t P_cap = 0;           // entries reserved for seg_pages (every segment at its owned pages)
+  // Length updates (graphattn_plan_set_lengths): the graph as given and the chains' segments.
+  int32_t S0 = 0, B0q = 0, CS = 0;   // segments; branches of a multi-query plan; chain entries
+  int64_t P0 = 0;                    // entries of the page table as given
   int32_t chunk_pages = 0;
   int64_t max_items = 0;       // upper bound on work items per kv-head
   int32_t desc_words = 0;      // work-item descriptor stride (int32 words)
@@ -99,14 +102,15 @@ struct ga_plan {
   int32_t B0 = 0;              // branches as given (z.B counts query rows)
   int num_cus = 256;
   CGraph cg;                   // the uploaded (chain) graph and its map to the given one
-  // What a length update (graphattn_plan_set_lengths) rebuilds the chain graph from: the page
-  // table as given, the paths the chains were built over (query rows for multi-query plans), and
-  // for multi-query plans each branch's newest segment and query count.
+  // Length updates (graphattn_plan_set_lengths): the page table's offsets and, for multi-query
+  // plans, each branch's newest segment and query count, for validation on the host; the device
+  // side rebuilds the chains' page lists from arrays uploaded with the graph (la).
+  bool updatable = false;
   std::vector<int64_t> h_page_off;
-  std::vector<int32_t> h_pages;
-  std::vector<int64_t> h_path_off;
-  std::vector<int32_t> h_path_segs;
+  std::vector<int32_t> h_pages;    // (kept until the first upload has packed it)
   std::vector<int32_t> h_last, h_counts;
+  ga::LengthArgs la{};
+  size_t len_off = 0;              // byte offset of the lengths in the upload (and the staging)
   hipEvent_t uploaded = nullptr;   // recorded after each upload from the pinned staging
   ga::DevGraph g{};
   ga::DevSchedule sc{};
@@ -239,15 +243,20 @@ ga_status compress_chains(const ga_segment_table* st, const ga_branch_paths* bp,
   c->npg.clear();
   c->seg_pages.clear();
   c->seg_page_off.assign(1, 0);
+  c->chain_seg_off.assign(1, 0);
+  c->chain_segs.clear();
   for (int32_t s = 0; s < S; ++s) {
     if (cnt[s] == 0 || haspred[s]) continue;
     const int32_t v = (int32_t)c->head.size();
     c->head.push_back(s);
     c->first[s] = 1;
-    int64_t pages = 0;
+    int64_t pages = 0, owned = 0;
     int32_t last_valid = ga::kPageTokens;
+    const int64_t base = (int64_t)c->seg_pages.size();
     for (int32_t x = s; x >= 0; x = link[x]) {
       c->vid[x] = v;
+      c->chain_segs.push_back(x);
+      owned += st->seg_page_offsets[x + 1] - st->seg_page_offsets[x];
       const int32_t len = st->seg_len[x], n = npg0[x];
       const int64_t off = st->seg_page_offsets[x];
       for (int32_t i = 0; i < n; ++i) {
@@ -258,13 +267,17 @@ ga_status compress_chains(const ga_segment_table* st, const ga_branch_paths* bp,
       last_valid = len - (n - 1) * ga::kPageTokens;
     }
     const int64_t tokens = (pages - 1) * ga::kPageTokens + last_valid;
-    if (tokens > 0x7fffffffLL)
-      return fail(GA_EUNSUPPORTED, "segment chain from segment %d spans %lld tokens", s,
-                  (long long)tokens);
+    // Every page the chain's segments own could come into use (graphattn_plan_set_lengths):
+    // the page list keeps room for all of them, and the token positions must stay in range.
+    if (owned * ga::kPageTokens >= ga::kNoCausal)
+      return fail(GA_EUNSUPPORTED, "segment chain from segment %d owns %lld pages", s,
+                  (long long)owned);
+    c->seg_pages.resize(base + owned, 0);
     c->seg_len.push_back((int32_t)tokens);
     c->npg.push_back((int32_t)pages);
     c->causal.push_back(ga::kNoCausal);
     c->seg_page_off.push_back((int64_t)c->seg_pages.size());
+    c->chain_seg_off.push_back((int32_t)c->chain_segs.size());
   }
   // Paths over chains: a chain's first segment stands for the chain; the rest of the chain
   // follows it immediately in every path through it.
@@ -318,26 +331,39 @@ void size_schedule(const ga_segment_table* st, const ga_branch_paths* bp, const 
 }
 
 struct Layout {
-  size_t off[32];
+  size_t off[48];
   size_t total;
 };
 
 // Device workspace layout (byte offsets of every array in the single allocation).
 enum {
   L_SEG_LEN, L_SEG_PAGE_OFF, L_SEG_PAGES, L_PATH_OFF, L_PATH_SEGS, L_SEG_CAUSAL,  // uploaded
+  L_SEG_CHAIN, L_SRC_OFF, L_SRC_PAGES, L_CH_SEG_OFF, L_CH_SEGS, L_BR_LAST, L_BR_COUNT,
+  L_NEW_LEN,                                                                      // uploaded
+  L_SEG_POS,
   L_GRP_CNT, L_GRP_FILL, L_GRP_OFF, L_GRP_TMP, L_GRP_BR, L_ENTRY_BR, L_ENTRY_RANK, L_SEG_NCH,
   L_SEG_ITEM_OFF, L_SEG_PROW_OFF, L_SEG_ORDER, L_ORDER_ITEM_OFF, L_ITEMS, L_DESC, L_COUNTERS, L_ENTRY_PART, L_BPART_OFF, L_BPART, L_BLK_SUM,
   L_PO, L_PLSE, L_COUNT
 };
+static_assert(L_COUNT <= 48, "Layout::off must hold every array");
 
 Layout layout(const Sizes& z, const ga_params& p) {
   size_t sz[L_COUNT];
   sz[L_SEG_LEN] = sizeof(int32_t) * z.S;
   sz[L_SEG_PAGE_OFF] = sizeof(int64_t) * (z.S + 1);
-  sz[L_SEG_PAGES] = sizeof(int32_t) * (z.P_cap > z.P ? z.P_cap : z.P);
+  sz[L_SEG_PAGES] = sizeof(int32_t) * z.P;
   sz[L_PATH_OFF] = sizeof(int64_t) * (z.B + 1);
   sz[L_PATH_SEGS] = sizeof(int32_t) * z.E;
   sz[L_SEG_CAUSAL] = sizeof(int32_t) * z.S;
+  sz[L_SEG_CHAIN] = sizeof(int32_t) * z.S0;
+  sz[L_SRC_OFF] = z.S0 ? sizeof(int64_t) * (z.S0 + 1) : 0;
+  sz[L_SRC_PAGES] = sizeof(int32_t) * z.P0;
+  sz[L_CH_SEG_OFF] = z.S0 ? sizeof(int32_t) * (z.S + 1) : 0;
+  sz[L_CH_SEGS] = sizeof(int32_t) * z.CS;
+  sz[L_BR_LAST] = sizeof(int32_t) * z.B0q;
+  sz[L_BR_COUNT] = sizeof(int32_t) * z.B0q;
+  sz[L_NEW_LEN] = sizeof(int32_t) * z.S0;
+  sz[L_SEG_POS] = sizeof(int32_t) * z.S0;
   sz[L_GRP_CNT] = sizeof(int32_t) * z.S;
   sz[L_GRP_FILL] = sizeof(int32_t) * z.S;
   sz[L_GRP_OFF] = sizeof(int64_t) * (z.S + 1);
@@ -367,7 +393,7 @@ Layout layout(const Sizes& z, const ga_params& p) {
   size_t o = 0;
   for (int i = 0; i < L_COUNT; ++i) {
     // The uploaded graph arrays are packed back to back (8-byte aligned) so one copy moves them.
-    o = align_up(o, i <= L_SEG_CAUSAL ? 8 : 256);
+    o = align_up(o, i <= L_NEW_LEN ? 8 : 256);
     L.off[i] = o;
     o += sz[i];
   }
@@ -375,7 +401,7 @@ Layout layout(const Sizes& z, const ga_params& p) {
   return L;
 }
 
-size_t upload_bytes(const Layout& L) { return L.off[L_GRP_CNT]; }
+size_t upload_bytes(const Layout& L) { return L.off[L_SEG_POS]; }
 
 void bind(ga_plan* pl, const Layout& L) {
   char* d = static_cast<char*>(pl->dev);
@@ -409,6 +435,23 @@ void bind(ga_plan* pl, const Layout& L) {
   pl->sc.bpart_off = reinterpret_cast<int64_t*>(d + L.off[L_BPART_OFF]);
   pl->sc.bpart = reinterpret_cast<int32_t*>(d + L.off[L_BPART]);
   pl->sc.blk_sum = reinterpret_cast<int64_t*>(d + L.off[L_BLK_SUM]);
+  ga::LengthArgs& la = pl->la;
+  la.chains = z.S;
+  la.branches = z.B0q;
+  la.new_len = reinterpret_cast<const int32_t*>(d + L.off[L_NEW_LEN]);
+  la.src_page_off = reinterpret_cast<const int64_t*>(d + L.off[L_SRC_OFF]);
+  la.src_pages = reinterpret_cast<const int32_t*>(d + L.off[L_SRC_PAGES]);
+  la.chain_seg_off = reinterpret_cast<const int32_t*>(d + L.off[L_CH_SEG_OFF]);
+  la.chain_segs = reinterpret_cast<const int32_t*>(d + L.off[L_CH_SEGS]);
+  la.seg_chain = reinterpret_cast<const int32_t*>(d + L.off[L_SEG_CHAIN]);
+  la.br_last = reinterpret_cast<const int32_t*>(d + L.off[L_BR_LAST]);
+  la.br_count = reinterpret_cast<const int32_t*>(d + L.off[L_BR_COUNT]);
+  la.seg_pos = reinterpret_cast<int32_t*>(d + L.off[L_SEG_POS]);
+  la.chain_len = reinterpret_cast<int32_t*>(d + L.off[L_SEG_LEN]);
+  la.chain_page_off = reinterpret_cast<const int64_t*>(d + L.off[L_SEG_PAGE_OFF]);
+  la.chain_pages = reinterpret_cast<int32_t*>(d + L.off[L_SEG_PAGES]);
+  la.chain_causal = reinterpret_cast<int32_t*>(d + L.off[L_SEG_CAUSAL]);
+  pl->len_off = L.off[L_NEW_LEN];
   pl->po = d + L.off[L_PO];
   pl->plse = reinterpret_cast<float*>(d + L.off[L_PLSE]);
 }
@@ -492,22 +535,8 @@ ga_status set_causal(const ga_plan* pl, const int32_t* seg_len, const std::vecto
   return GA_OK;
 }
 
-// Pages each chain owns (the sum over its segments of the pages the page table gives them), and
-// their total: the room the uploaded page list and the schedule bounds are sized for.
-int64_t chain_capacity(const ga_plan* pl, const CGraph& c, std::vector<int64_t>* cap) {
-  cap->assign(c.head.size(), 0);
-  int64_t total = 0;
-  for (size_t x = 0; x < c.vid.size(); ++x)
-    if (c.vid[x] >= 0) {
-      const int64_t n = pl->h_page_off[x + 1] - pl->h_page_off[x];
-      (*cap)[c.vid[x]] += n;
-      total += n;
-    }
-  return total;
-}
-
 ga_status plan_init(const ga_segment_table* st, const ga_branch_paths* bp, const ga_params* p,
-                    const int32_t* query_counts, ga_plan* pl, Layout* L) {
+                    const int32_t* query_counts, bool updatable, ga_plan* pl, Layout* L) {
   ga_status rc = validate_params(p);
   if (rc) return rc;
   std::vector<int32_t> npg;
@@ -530,10 +559,11 @@ ga_status plan_init(const ga_segment_table* st, const ga_branch_paths* bp, const
   if (rc) return rc;
   // Kept for length updates.
   const int32_t S0 = st->num_segments;
-  pl->h_page_off.assign(st->seg_page_offsets, st->seg_page_offsets + S0 + 1);
-  pl->h_pages.assign(st->seg_pages, st->seg_pages + st->seg_page_offsets[S0]);
-  pl->h_path_off.assign(ebp->path_offsets, ebp->path_offsets + ebp->num_branches + 1);
-  pl->h_path_segs.assign(ebp->path_segs, ebp->path_segs + ebp->path_offsets[ebp->num_branches]);
+  pl->updatable = updatable;
+  if (updatable) {
+    pl->h_page_off.assign(st->seg_page_offsets, st->seg_page_offsets + S0 + 1);
+    pl->h_pages.assign(st->seg_pages, st->seg_pages + st->seg_page_offsets[S0]);
+  }
   if (query_counts) {
     pl->h_last.resize(bp->num_branches);
     for (int32_t b = 0; b < bp->num_branches; ++b)
@@ -551,8 +581,14 @@ ga_status plan_init(const ga_segment_table* st, const ga_branch_paths* bp, const
   pl->p = *p;
   if (pl->p.softmax_scale == 0.f) pl->p.softmax_scale = 1.f / std::sqrt((float)p->head_dim);
   pl->num_cus = device_cus();
-  std::vector<int64_t> npg_cap;
-  pl->z.P_cap = chain_capacity(pl, c, &npg_cap);
+  std::vector<int64_t> npg_cap(pl->z.S);          // pages each chain owns
+  for (int32_t v = 0; v < pl->z.S; ++v) npg_cap[v] = c.seg_page_off[v + 1] - c.seg_page_off[v];
+  if (updatable) {
+    pl->z.S0 = S0;
+    pl->z.P0 = st->seg_page_offsets[S0];
+    pl->z.CS = (int32_t)c.chain_segs.size();
+    pl->z.B0q = query_counts ? bp->num_branches : 0;
+  }
   size_schedule(&cst, &cbp, p, c.npg, npg_cap, pl->num_cus, &pl->z);
   if (pl->z.prows > 0x7fffffffLL)
     return fail(GA_EINVAL, "too many partial rows (%lld)", (long long)pl->z.prows);
@@ -571,7 +607,22 @@ ga_status upload(ga_plan* pl, const Layout& L, hipStream_t stream) {
   const CGraph& c = pl->cg;
   const ga_segment_table cst{pl->z.S, c.seg_len.data(), c.seg_page_off.data(), c.seg_pages.data()};
   const ga_branch_paths cbp{pl->z.B, c.path_off.data(), c.path_segs.data()};
-  pack_upload(&cst, &cbp, c.causal.data(), L, pl->z, static_cast<char*>(pl->pin));
+  char* h = static_cast<char*>(pl->pin);
+  pack_upload(&cst, &cbp, c.causal.data(), L, pl->z, h);
+  const Sizes& z = pl->z;
+  if (z.S0) {
+    std::memcpy(h + L.off[L_SEG_CHAIN], c.vid.data(), sizeof(int32_t) * z.S0);
+    std::memcpy(h + L.off[L_SRC_OFF], pl->h_page_off.data(), sizeof(int64_t) * (z.S0 + 1));
+    if (z.P0) std::memcpy(h + L.off[L_SRC_PAGES], pl->h_pages.data(), sizeof(int32_t) * z.P0);
+    std::memcpy(h + L.off[L_CH_SEG_OFF], c.chain_seg_off.data(), sizeof(int32_t) * (z.S + 1));
+    if (z.CS) std::memcpy(h + L.off[L_CH_SEGS], c.chain_segs.data(), sizeof(int32_t) * z.CS);
+    if (z.B0q) {
+      std::memcpy(h + L.off[L_BR_LAST], pl->h_last.data(), sizeof(int32_t) * z.B0q);
+      std::memcpy(h + L.off[L_BR_COUNT], pl->h_counts.data(), sizeof(int32_t) * z.B0q);
+    }
+  }
+  pl->h_pages.clear();
+  pl->h_pages.shrink_to_fit();
   GA_HIP(hipMemcpyAsync(pl->dev, pl->pin, upload_bytes(L), hipMemcpyHostToDevice, stream),
          "graph upload");
   if (pl->uploaded) GA_HIP(hipEventRecord(pl->uploaded, stream), "record upload");
@@ -680,7 +731,7 @@ static ga_status plan_create(const ga_segment_table* segment_table,
   *plan = nullptr;
   ga_plan* pl = new ga_plan();
   Layout L;
-  ga_status rc = plan_init(segment_table, branch_paths, params, query_counts, pl, &L);
+  ga_status rc = plan_init(segment_table, branch_paths, params, query_counts, true, pl, &L);
   if (rc) {
     delete pl;
     return rc;
@@ -736,6 +787,7 @@ ga_status graphattn_plan_create_extend(const ga_segment_table* segment_table,
 ga_status graphattn_plan_set_lengths(ga_plan* plan, const int32_t* seg_len, void* hip_stream) {
   g_err.clear();
   if (!plan) return fail(GA_EINVAL, "plan is NULL");
+  if (!plan->updatable) return fail(GA_EINVAL, "plan does not take new lengths");
   const int32_t S = plan->cg.S0;
   if (S > 0 && !seg_len) return fail(GA_EINVAL, "seg_len is NULL");
   std::vector<int32_t> npg(S);
@@ -753,29 +805,22 @@ ga_status graphattn_plan_set_lengths(ga_plan* plan, const int32_t* seg_len, void
     if (plan->h_counts[b] > seg_len[plan->h_last[b]])
       return fail(GA_EINVAL, "branch %d: query count %d exceeds its newest segment's %d tokens",
                   (int)b, plan->h_counts[b], seg_len[plan->h_last[b]]);
-  // The chains (which segments go together) follow the paths only; their page lists, valid
-  // token counts, lengths and causal origins are rebuilt from the new lengths.
-  const ga_segment_table st{S, seg_len, plan->h_page_off.data(), plan->h_pages.data()};
-  const ga_branch_paths bp{(int32_t)(plan->h_path_off.size() - 1), plan->h_path_off.data(),
-                           plan->h_path_segs.data()};
-  CGraph c;
-  ga_status rc = compress_chains(&st, &bp, npg, &c);
-  if (rc) return rc;
-  if (!plan->h_last.empty()) {
-    rc = set_causal(plan, seg_len, npg, &c);
-    if (rc) return rc;
+  if (S == 0) {
+    plan->scheduled = false;
+    return GA_OK;
   }
-  if ((int64_t)c.seg_pages.size() > plan->z.P_cap)
-    return fail(GA_EINVAL, "page list of %zu entries exceeds the plan's %lld",
-                c.seg_pages.size(), (long long)plan->z.P_cap);
-  // The previous upload must have left the staging buffer before it is refilled; the new copy
-  // is ordered on the stream after the work already enqueued there.
+  // The chains (which segments go together) follow the paths only, and each chain's page list
+  // has room for every page its segments own: the device rebuilds the page lists, valid token
+  // counts, chain lengths and causal origins from the new lengths in place.  The host waits
+  // only for the previous upload to leave the staging slot of the lengths.
+  hipStream_t stream = static_cast<hipStream_t>(hip_stream);
   GA_HIP(hipEventSynchronize(plan->uploaded), "wait for previous upload");
-  plan->cg = std::move(c);
-  plan->z.P = (int64_t)plan->cg.seg_pages.size();
-  const Layout L = layout(plan->z, plan->p);
-  rc = upload(plan, L, static_cast<hipStream_t>(hip_stream));
-  if (rc) return rc;
+  char* h = static_cast<char*>(plan->pin) + plan->len_off;
+  std::memcpy(h, seg_len, sizeof(int32_t) * S);
+  GA_HIP(hipMemcpyAsync(static_cast<char*>(plan->dev) + plan->len_off, h, sizeof(int32_t) * S,
+                        hipMemcpyHostToDevice, stream), "length upload");
+  GA_HIP(hipEventRecord(plan->uploaded, stream), "record upload");
+  GA_HIP(ga::launch_set_lengths(plan->la, stream), "length update launch");
   plan->scheduled = false;
   return GA_OK;
 }
@@ -932,7 +977,7 @@ static ga_status one_shot(const void* q, const void* kv_page_pool,
   hipStream_t stream = static_cast<hipStream_t>(hip_stream);
   ga_plan pl;
   Layout L;
-  ga_status rc = plan_init(segment_table, branch_paths, params, query_counts, &pl, &L);
+  ga_status rc = plan_init(segment_table, branch_paths, params, query_counts, false, &pl, &L);
   if (rc) return rc;
   rc = check_run_ptrs(&pl, q, kv_page_pool, out, lse);
   if (rc) return rc;

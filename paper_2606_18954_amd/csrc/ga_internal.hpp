@@ -175,6 +175,27 @@ struct RewardArgs {
 };
 
 // Launchers (each returns the launch status).
+// New segment lengths applied on the device: each chain's page list (laid out at a fixed offset
+// with room for every page its segments own), its length and, for multi-query plans, its causal
+// origin are rebuilt from the lengths of the segments as given.
+struct LengthArgs {
+  int32_t chains, branches;        // chains; branches as given (multi-query plans, else 0)
+  const int32_t* new_len;          // [S0] lengths of the segments as given
+  const int64_t* src_page_off;     // [S0+1] page table as given
+  const int32_t* src_pages;        // [P0]
+  const int32_t* chain_seg_off;    // [chains+1] CSR of each chain's segments, in path order
+  const int32_t* chain_segs;
+  const int32_t* seg_chain;        // [S0] chain of each segment (-1: on no path)
+  const int32_t* br_last;          // [branches] newest segment of each branch
+  const int32_t* br_count;         // [branches] its query count
+  int32_t* seg_pos;                // [S0] written: pages of its chain before the segment
+  int32_t* chain_len;              // [chains] written (DevGraph::seg_len)
+  const int64_t* chain_page_off;   // [chains+1] (DevGraph::seg_page_off)
+  int32_t* chain_pages;            // written (DevGraph::seg_pages)
+  int32_t* chain_causal;           // [chains] written for multi-query plans (DevGraph::seg_causal)
+};
+hipError_t launch_set_lengths(const LengthArgs& a, hipStream_t stream);
+
 hipError_t launch_schedule(const DevGraph& g, const DevSchedule& sc, int32_t group,
                            int32_t chunk_pages, int64_t max_items, hipStream_t stream);
 hipError_t launch_seg_attn(const AttnArgs& a, int head_dim, bool bf16, bool causal, int grid,

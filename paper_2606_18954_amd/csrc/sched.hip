@@ -647,6 +647,51 @@ inline int blocks(int64_t n) { return (int)((n + kT - 1) / kT); }
 
 }  // namespace
 
+// One wave per chain: its segments in path order, each with its pages in order (the lanes copy a
+// segment's pages together), the last page of a segment carrying its valid token count; the
+// chain's length counts the token positions of that page list ((pages - 1) x 16 + valid tokens
+// of the last page).
+__global__ void k_chain_pages(LengthArgs a) {
+  const int v = blockIdx.x * (kT / 64) + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (v >= a.chains) return;
+  int32_t* dst = a.chain_pages + a.chain_page_off[v];
+  int pos = 0, last_valid = kPageTokens;
+  for (int k = a.chain_seg_off[v]; k < a.chain_seg_off[v + 1]; ++k) {
+    const int x = a.chain_segs[k];
+    const int len = a.new_len[x];
+    const int n = (len + kPageTokens - 1) / kPageTokens;
+    const int32_t* src = a.src_pages + a.src_page_off[x];
+    if (lane == 0) a.seg_pos[x] = pos;
+    for (int i = lane; i < n; i += 64) {
+      const int valid = i == n - 1 ? len - (n - 1) * kPageTokens : kPageTokens;
+      dst[pos + i] = src[i] | ((valid - 1) << kPageValidShift);
+    }
+    pos += n;
+    last_valid = len - (n - 1) * kPageTokens;
+  }
+  if (lane == 0) a.chain_len[v] = (pos - 1) * kPageTokens + last_valid;
+}
+
+// One thread per branch of a multi-query plan: its newest segment closes its chain, so query i of
+// the branch sits at chain token 16 x (chain pages before the segment) + len - n + i.
+__global__ void k_chain_causal(LengthArgs a) {
+  const int b = blockIdx.x * kT + threadIdx.x;
+  if (b >= a.branches) return;
+  const int x = a.br_last[b];
+  a.chain_causal[a.seg_chain[x]] = a.seg_pos[x] * kPageTokens + a.new_len[x] - a.br_count[b];
+}
+
+hipError_t launch_set_lengths(const LengthArgs& a, hipStream_t stream) {
+  if (a.chains > 0)
+    hipLaunchKernelGGL(k_chain_pages, dim3((unsigned)((a.chains + kT / 64 - 1) / (kT / 64))),
+                       dim3(kT), 0, stream, a);
+  if (a.branches > 0)
+    hipLaunchKernelGGL(k_chain_causal, dim3((unsigned)((a.branches + kT - 1) / kT)), dim3(kT), 0,
+                       stream, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_schedule(const DevGraph& g, const DevSchedule& sc, int32_t group,
                            int32_t chunk_pages, int64_t max_items, hipStream_t stream) {
   const int fill_blocks = (int)((max_items + kT / 64 - 1) / (kT / 64));

@@ -1,4 +1,5 @@
-"""Plans whose segments grow between steps (graphattn_plan_set_lengths), through the C ABI,
+"""Plans whose segments grow between steps (graphattn_plan_set_lengths: the chains rebuilt on the
+device from new lengths), through the C ABI,
 against the oracle on the same lengths.
 
 Each graph is built at its final lengths, so every segment owns the pages it will grow into

@@ -1,6 +1,5 @@
-"""Plans whose segments grow between steps (graphattn_plan_set_lengths: the chains rebuilt on the
-device from new lengths), through the C ABI,
-against the oracle on the same lengths.
+"""Plans whose segments grow between steps (graphattn_plan_set_lengths: the chains are rebuilt
+on the device from new lengths), through the C ABI, against the oracle on the same lengths.
 
 Each graph is built at its final lengths, so every segment owns the pages it will grow into
 (page contents past the final lengths are NaN); plans start at shorter lengths and are moved

@@ -7,7 +7,8 @@ float32, random slack pages), decode and multi-query extend, to the parity bar (
 requested: contexts of a few tokens).  State forests: random prompt shapes from chains to stars,
 sometimes beyond the 256-state one-workgroup class path and the 512-state one-launch reward
 path; classes and edge similarities (inputs kept 1e-3 from kappa), the graph suffix (bit-exact)
-and the graph reward and advantages (to fp64 rounding) from random classes.
+and the graph reward and advantages (to fp64 rounding) from random classes.  Plans taken
+through random length updates (graphattn_plan_set_lengths) on the same small DAGs.
 """
 import numpy as np
 import pytest
@@ -217,3 +218,35 @@ def test_fuzz_suffix_and_advantages(f, links, w, lam):
             err = float(np.abs(a[mk] - b[mk]).max()) if mk.any() else 0.0
             assert err <= 1e-9 * max(1.0, float(np.abs(b[mk]).max()) if mk.any() else 1.0), \
                 (k, err)
+
+
+@settings(FUZZ, max_examples=20)
+@given(g=rollout_graphs(), h=heads, seed=st.integers(0, 2 ** 20), data=st.data())
+def test_fuzz_set_lengths(g, h, seed, data):
+    """A plan created at random lengths within each segment's pages, then given three random
+    sets of lengths (graphattn_plan_set_lengths), each scheduled, run and compared."""
+    require_gpu()
+    lens_max, paths = g
+    group, Hkv, D, dtype = h
+    graph = W.assemble_graph(lens_max, paths, seed, 1)
+    wl = W.make_workload(f"fuzz lengths {group * Hkv}/{Hkv}/{D} {dtype}", graph, group * Hkv,
+                         Hkv, D, dtype, seed, poison=True)
+    q, pool = wl.q.cuda(), wl.pool.cuda()
+    draws = [[data.draw(st.integers(1, m)) for m in lens_max] for _ in range(4)]
+    B, Hq = graph.num_branches, wl.num_q_heads
+    hg = G.HostGraph(draws[0], graph.seg_page_offsets, graph.seg_pages, graph.path_offsets,
+                     graph.path_segs)
+    with G.Plan(hg, params_of(wl, out_f32=True)) as plan:
+        for i, lens in enumerate(draws):
+            if i:
+                plan.set_lengths(lens)
+            say(f"[case] {wl.name} max={lens_max} lengths={lens} paths={paths} seed={seed}")
+            out = torch.empty((B, Hq, D), dtype=torch.float32, device="cuda")
+            lse = torch.empty((B, Hq), dtype=torch.float32, device="cuda")
+            plan.schedule()
+            plan.run(q, pool, out, lse)
+            torch.cuda.synchronize()
+            oo, ol = O.decode(wl.q_bits(), wl.pool_bits(), np.asarray(lens, dtype=np.int32),
+                              graph.seg_page_offsets, graph.seg_pages, graph.path_offsets,
+                              graph.path_segs, Hq, Hkv, D, dtype)
+            compare(wl.name, out.double().cpu().numpy(), lse.double().cpu().numpy(), oo, ol)

@@ -60,6 +60,27 @@ def measured_counters(config, path=COUNTERS_MD, src=KERNEL_SRC):
     return kv
 
 
+def host_info():
+    """The host the CPU oracle runs on: CPU model, cores available to this process, BLAS."""
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    blas = []
+    try:
+        from threadpoolctl import threadpool_info
+        blas = sorted({f"{i.get('internal_api', '?')} {i.get('version', '')}".strip()
+                       for i in threadpool_info()})
+    except Exception:
+        pass
+    return {"cpu_model": model, "cpus_available": len(os.sched_getaffinity(0)), "blas": blas}
+
+
 def cpu_baseline(wl, n_sample):
     sys.path.insert(0, ROOT)
     from oracle import graphattn_oracle as O
@@ -81,7 +102,7 @@ def cpu_baseline(wl, n_sample):
             "kind": "oracle",
             "sample": f"{len(br)} seeded branches of the same workload ({toks} attended tokens), "
                       f"fp64 NumPy, {dt:.1f} s wall",
-            "attended_tokens_per_s": toks / dt}
+            "attended_tokens_per_s": toks / dt, "host": host_info()}
 
 
 def timed_steps(torch, plan, step, steps):
@@ -126,6 +147,21 @@ def mall_flushed_attention(torch, plan, step, steps, dev):
     del junk
     torch.cuda.empty_cache()
     return prof.attn_ms / max(1, prof.runs)
+
+
+def median_step_ms(torch, step, steps):
+    """Median of per-step durations: one event pair around each step (the records between steps
+    add a little to each; ms_per_step comes from the region without them)."""
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(steps)]
+    torch.cuda.synchronize()
+    for e0, e1 in evs:
+        e0.record()
+        step()
+        e1.record()
+    torch.cuda.synchronize()
+    d = sorted(e0.elapsed_time(e1) for e0, e1 in evs)
+    return d[len(d) // 2] if len(d) % 2 else 0.5 * (d[len(d) // 2 - 1] + d[len(d) // 2])
 
 
 def stream_copy_gbs(torch, dev, reps=10):
@@ -592,6 +628,7 @@ def main():
     log(f"warmup done ({args.warmup} steps)")
     ms, attn_ms, merge_ms, sched_ms = timed_steps(torch, plan, step, args.steps)
     cold_ms = mall_flushed_attention(torch, plan, step, args.steps, dev)
+    med_ms = median_step_ms(torch, step, args.steps)
     copy_gbs = stream_copy_gbs(torch, dev)
     log(f"attention with the memory-side cache flushed before each step: {cold_ms:.4f} ms; "
         f"plain device copy: {copy_gbs:.0f} GB/s; plan creation {plan_ms:.1f} ms")
@@ -626,6 +663,7 @@ def main():
                   "around each kernel; attention_mall_flushed from as many more with a 512 MiB "
                   "read between steps",
         "mall_flushed_frac": ukv / (cold_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+        "ms_per_step_median": med_ms,
         "stream_copy_gbs": copy_gbs,
         "frac_of_stream_copy": achieved / copy_gbs,
         "plan_create_ms": plan_ms,

@@ -52,8 +52,11 @@ int device_cus() {
 // through s continues with s', and |B(s)| = |B(s')|) form a chain; attention over a chain's
 // concatenated tokens equals the log-sum-exp merge of its segments, so each chain is scheduled
 // as one segment: one partial per branch and chunk, and longer work items.  A chain's page list
-// concatenates its segments' pages; every page id carries its valid token count in the bits
-// from ga::kPageValidShift up, so the pages where a segment ends mid-page are masked.
+// concatenates the pages its segments' lengths use, in path order; every page id carries its
+// valid token count in the bits from ga::kPageValidShift up, so the pages where a segment ends
+// mid-page are masked.  Each chain's list starts at a fixed offset with room for every page its
+// segments own in the page table, so new lengths (graphattn_plan_set_lengths) rewrite it in
+// place.
 struct CGraph {
   int32_t S0 = 0;                  // segments and path entries as given
   int64_t E0 = 0;

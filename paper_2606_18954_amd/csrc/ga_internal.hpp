@@ -37,12 +37,13 @@ __host__ __device__ inline int desc_words(int chunk_pages, int group) {
 static_assert(4 * ((kDescHead + kMaxChunkPages + kRowsPerBlock + 3) & ~3) <= kDescMaxBytes,
               "descriptor must fit its LDS slot");
 
-// Device copy of the rollout graph (written once by plan_create's upload).
+// Device copy of the rollout graph (chains as segments), written by plan_create's upload; the
+// lengths, page lists and causal origins are rewritten in place by a length update.
 struct DevGraph {
   int32_t S, B, E;
   const int32_t* seg_len;        // [S]
-  const int64_t* seg_page_off;   // [S+1]
-  const int32_t* seg_pages;      // [P]
+  const int64_t* seg_page_off;   // [S+1] start of each list (room for all owned pages)
+  const int32_t* seg_pages;      // [P]   the first ceil(seg_len / 16) entries of each list used
   const int64_t* path_off;       // [B+1]
   const int32_t* path_segs;      // [E]
   const int32_t* seg_causal;     // [S]  causal origin of a multi-query segment, else kNoCausal:

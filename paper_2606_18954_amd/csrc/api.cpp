@@ -113,8 +113,14 @@ struct ga_plan {
   std::vector<int32_t> h_pages;    // (kept until the first upload has packed it)
   std::vector<int32_t> h_last, h_counts;
   ga::LengthArgs la{};
-  size_t len_off = 0;              // byte offset of the lengths in the upload (and the staging)
-  hipEvent_t uploaded = nullptr;   // recorded after each upload from the pinned staging
+  size_t len_off = 0;              // byte offset of the device copy of the lengths
+  // Pinned slots for the lengths of successive updates, each reused only after its copy has
+  // left it, so the host may run a few updates ahead of the device.
+  static constexpr int kLenSlots = 4;
+  int32_t* len_pin = nullptr;
+  hipEvent_t len_ev[kLenSlots] = {};
+  int64_t len_calls = 0;
+  hipEvent_t uploaded = nullptr;   // recorded after the graph upload from the pinned staging
   ga::DevGraph g{};
   ga::DevSchedule sc{};
   void* po = nullptr;
@@ -758,6 +764,21 @@ static ga_status plan_create(const ga_segment_table* segment_table,
     graphattn_plan_destroy(pl);
     return hip_fail(hipGetLastError(), "event");
   }
+  if (pl->z.S0 > 0) {
+    if (hipHostMalloc(reinterpret_cast<void**>(&pl->len_pin),
+                      sizeof(int32_t) * pl->z.S0 * ga_plan::kLenSlots) != hipSuccess) {
+      pl->len_pin = nullptr;
+      graphattn_plan_destroy(pl);
+      (void)hipGetLastError();
+      return fail(GA_ENOMEM, "pinned staging of the segment lengths");
+    }
+    for (hipEvent_t& e : pl->len_ev)
+      if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) {
+        e = nullptr;
+        graphattn_plan_destroy(pl);
+        return hip_fail(hipGetLastError(), "event");
+      }
+  }
   rc = upload(pl, L, static_cast<hipStream_t>(hip_stream));
   if (rc) {
     graphattn_plan_destroy(pl);
@@ -814,15 +835,19 @@ ga_status graphattn_plan_set_lengths(ga_plan* plan, const int32_t* seg_len, void
   }
   // The chains (which segments go together) follow the paths only, and each chain's page list
   // has room for every page its segments own: the device rebuilds the page lists, valid token
-  // counts, chain lengths and causal origins from the new lengths in place.  The host waits
-  // only for the previous upload to leave the staging slot of the lengths.
+  // counts, chain lengths and causal origins from the new lengths in place.  The lengths go
+  // through a ring of pinned slots; the host waits only if the slot's copy from kLenSlots
+  // updates ago has not left it yet.
   hipStream_t stream = static_cast<hipStream_t>(hip_stream);
-  GA_HIP(hipEventSynchronize(plan->uploaded), "wait for previous upload");
-  char* h = static_cast<char*>(plan->pin) + plan->len_off;
+  const int slot = (int)(plan->len_calls % ga_plan::kLenSlots);
+  if (plan->len_calls >= ga_plan::kLenSlots)
+    GA_HIP(hipEventSynchronize(plan->len_ev[slot]), "wait for an earlier length upload");
+  int32_t* h = plan->len_pin + (size_t)slot * S;
   std::memcpy(h, seg_len, sizeof(int32_t) * S);
   GA_HIP(hipMemcpyAsync(static_cast<char*>(plan->dev) + plan->len_off, h, sizeof(int32_t) * S,
                         hipMemcpyHostToDevice, stream), "length upload");
-  GA_HIP(hipEventRecord(plan->uploaded, stream), "record upload");
+  GA_HIP(hipEventRecord(plan->len_ev[slot], stream), "record length upload");
+  ++plan->len_calls;
   GA_HIP(ga::launch_set_lengths(plan->la, stream), "length update launch");
   plan->scheduled = false;
   return GA_OK;
@@ -962,12 +987,15 @@ void graphattn_plan_destroy(ga_plan* plan) {
   if (!plan) return;
   profile_clear(plan);
   if (plan->uploaded) (void)hipEventDestroy(plan->uploaded);
+  for (hipEvent_t e : plan->len_ev)
+    if (e) (void)hipEventDestroy(e);
   if (plan->owns_memory) {
     if (plan->dev) {
       (void)hipDeviceSynchronize();
       (void)hipFree(plan->dev);
     }
     if (plan->pin) (void)hipHostFree(plan->pin);
+    if (plan->len_pin) (void)hipHostFree(plan->len_pin);
   }
   delete plan;
 }

@@ -151,8 +151,9 @@ ga_status graphattn_plan_create_extend(const ga_segment_table* segment_table,
  * lengths are copied to the device and the plan's segment chains (page lists with their valid
  * token counts, lengths, causal origins) are rebuilt there in place, asynchronously on
  * hip_stream and ordered after the work already enqueued there (work of this plan on other
- * streams must be complete); the host waits only for the plan's previous upload to leave its
- * pinned staging.  No allocation.  The plan must be scheduled again (graphattn_schedule) before
+ * streams must be complete); the lengths pass through one of four pinned slots in turn, and
+ * the host waits only when that slot's copy from four updates earlier is still pending.  No
+ * allocation.  The plan must be scheduled again (graphattn_schedule) before
  * its next run. */
 ga_status graphattn_plan_set_lengths(ga_plan* plan, const int32_t* seg_len, void* hip_stream);
 

@@ -183,7 +183,9 @@ typedef struct {
   int32_t chunk_pages;        /* maximum pages per work item */
   int32_t rows_per_block;     /* maximum query rows (branch x q-head-in-group) per work item */
   int64_t num_items;          /* work items per kv-head */
-  int64_t num_partial_rows;   /* partial results per q-head: sum over entries of chunks */
+  int64_t num_partial_rows;   /* partial results per q-head the workspace holds: the sum over
+                                 path entries of chunks, each segment at all the pages it owns
+                                 (equal to the rows in use when segments own no spare pages) */
   int32_t num_chains;         /* chains scheduled (segments on some path, after merging runs) */
   int32_t num_query_rows;     /* rows of q / out / lse: B for decode plans, sum_b n_b for extend */
 } ga_plan_info;

@@ -131,10 +131,84 @@ __device__ void scan_segments(const DevGraph& g, const DevSchedule& sc, int32_t 
     sc.counters[1] = sh[2][1023];
   }
 
-  // 2. Work-list order: segments by descending cost class, ties by segment id (bitonic sort of
-  //    unique 64-bit keys, so the order is a pure function of the graph).
+  // 2. Work-list order: segments by descending cost class, ties by segment id, so the order is
+  //    a pure function of the graph.  Up to 4096 segments: a stable counting sort by class
+  //    (segment s = 1024 u + t sits in slot u; lanes of a wave with equal classes are matched
+  //    by five bit ballots, and the per-(slot, wave) counts of each class are prefix-summed by
+  //    one wave per class); beyond, a bitonic sort of unique 64-bit keys.  keys[i] ends up
+  //    holding the segment at work-list position i.
   const bool sorted = S <= kSortCap;
-  if (sorted) {
+  if (S <= 4096) {
+    constexpr int NBK = kCostClasses;
+    const int lane = t & 63, wv = t >> 6;
+    const uint64_t lt = lane ? (~0ull >> (64 - lane)) : 0ull;
+    const int nslots = (S + 1023) >> 10;
+    int* cw = reinterpret_cast<int*>(&sh[0][0]);   // [(slot * 16 + wave) * NBK + class]
+    int* tot = reinterpret_cast<int*>(&sh[2][0]);  // [class] totals, then [NBK + class] offsets
+    __syncthreads();                               // readers of the last scan are done
+    for (int i = t; i < 4 * 16 * NBK; i += 1024) cw[i] = 0;
+    __syncthreads();
+    int bk[4], wr[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      bk[u] = 0;
+      wr[u] = 0;
+      if (u < nslots) {
+        const int sg = 1024 * u + t;
+        const bool valid = sg < S;
+        int bucket = 0;
+        if (valid) {
+          int cnt, nch, nrb, npg;
+          seg_info(sg, cnt, nch, nrb, npg);
+          const uint32_t cost = cnt > 0 ? item_cost(npg, cnt, group, chunk_pages) : 0u;
+          bucket = kCostClasses - 1 - cost_class(cost);
+        }
+        uint64_t m = __ballot(valid);
+#pragma unroll
+        for (int bit = 0; bit < 5; ++bit) {
+          const bool on = (bucket >> bit) & 1;
+          const uint64_t bb = __ballot(valid && on);
+          m &= on ? bb : ~bb;
+        }
+        bk[u] = bucket;
+        wr[u] = __popcll(m & lt);
+        if (valid && (m & lt) == 0) cw[(u * 16 + wv) * NBK + bucket] = __popcll(m);
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {                  // wave wv: classes wv and wv + 16
+      const int c = wv + 16 * h;
+      const int v = cw[lane * NBK + c];
+      int x = v;
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const int y = __shfl_up(x, off);
+        if (lane >= off) x += y;
+      }
+      cw[lane * NBK + c] = x - v;
+      if (lane == 63) tot[c] = x;
+    }
+    __syncthreads();
+    if (t < 64) {
+      const int v = t < NBK ? tot[t] : 0;
+      int x = v;
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const int y = __shfl_up(x, off);
+        if (t >= off) x += y;
+      }
+      if (t < NBK) tot[NBK + t] = x - v;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int sg = 1024 * u + t;
+      if (u < nslots && sg < S)
+        keys[tot[NBK + bk[u]] + cw[(u * 16 + wv) * NBK + bk[u]] + wr[u]] = (uint64_t)sg;
+    }
+    __syncthreads();
+  } else if (sorted) {
     int n = 1;
     while (n < S) n <<= 1;
     for (int i = t; i < n; i += 1024) {

@@ -814,7 +814,6 @@ ga_status graphattn_plan_set_lengths(ga_plan* plan, const int32_t* seg_len, void
   if (!plan->updatable) return fail(GA_EINVAL, "plan does not take new lengths");
   const int32_t S = plan->cg.S0;
   if (S > 0 && !seg_len) return fail(GA_EINVAL, "seg_len is NULL");
-  std::vector<int32_t> npg(S);
   for (int32_t s = 0; s < S; ++s) {
     const int32_t len = seg_len[s];
     if (len < 1) return fail(GA_EINVAL, "segment %d has length %d (< 1)", s, len);
@@ -823,7 +822,6 @@ ga_status graphattn_plan_set_lengths(ga_plan* plan, const int32_t* seg_len, void
     if (need > owned)
       return fail(GA_EINVAL, "segment %d has %d tokens but owns only %lld pages", s, len,
                   (long long)owned);
-    npg[s] = (int32_t)need;
   }
   for (size_t b = 0; b < plan->h_last.size(); ++b)
     if (plan->h_counts[b] > seg_len[plan->h_last[b]])
@@ -848,6 +846,7 @@ ga_status graphattn_plan_set_lengths(ga_plan* plan, const int32_t* seg_len, void
                         hipMemcpyHostToDevice, stream), "length upload");
   GA_HIP(hipEventRecord(plan->len_ev[slot], stream), "record length upload");
   ++plan->len_calls;
+  // (if the launch fails, the chains and the schedule stay those of the previous lengths)
   GA_HIP(ga::launch_set_lengths(plan->la, stream), "length update launch");
   plan->scheduled = false;
   return GA_OK;

@@ -294,3 +294,46 @@ def test_step_replayed_from_a_hip_graph():
             graph.replay()
             torch.cuda.synchronize()
             assert torch.equal(out, ref_o) and torch.equal(lse, ref_l), rep
+
+
+def test_calls_on_two_streams():
+    """One-shot calls on two streams share the library's cached workspace (ordered between the
+    streams by events), and two plans run on two streams at once; every result against the
+    oracle."""
+    require_gpu()
+    wl1 = W.config2_tree(prompts=2, slack_pages=3, poison=True)
+    wl2 = W.config3_merged_dag(prompts=2, slack_pages=3, poison=True)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    data = []
+    for wl in (wl1, wl2):
+        q, pool = to_device(wl)
+        data.append((wl, q, pool, G.HostGraph.from_graph(wl.graph), params_of(wl)))
+    torch.cuda.synchronize()
+    res = {}
+    for rep in range(3):                       # interleaved one-shot calls on both streams
+        for i, (wl, q, pool, hg, p) in enumerate(data):
+            with torch.cuda.stream((s1, s2)[i]):
+                res[(rep, i)] = G.decode(q, pool, hg, p, stream=(s1, s2)[i])
+    torch.cuda.synchronize()
+    plans = [G.Plan(hg, p, stream=(s1, s2)[i]) for i, (wl, q, pool, hg, p) in enumerate(data)]
+    outs = []
+    for i, (wl, q, pool, hg, p) in enumerate(data):
+        with torch.cuda.stream((s1, s2)[i]):
+            B = wl.graph.num_branches
+            out = torch.empty((B, wl.num_q_heads, wl.head_dim), dtype=q.dtype, device="cuda")
+            lse = torch.empty((B, wl.num_q_heads), dtype=torch.float32, device="cuda")
+            plans[i].schedule(stream=(s1, s2)[i])
+            plans[i].run(q, pool, out, lse, stream=(s1, s2)[i])
+            outs.append((out, lse))
+    torch.cuda.synchronize()
+    for pl in plans:
+        pl.close()
+    for i, (wl, q, pool, hg, p) in enumerate(data):
+        oo, ol = oracle_decode(wl)
+        for rep in range(3):
+            o, l = res[(rep, i)]
+            compare(f"{wl.name} one-shot stream {i} call {rep}", o.double().cpu().numpy(),
+                    l.double().cpu().numpy(), oo, ol)
+        o, l = outs[i]
+        compare(f"{wl.name} plan stream {i}", o.double().cpu().numpy(),
+                l.double().cpu().numpy(), oo, ol)

@@ -689,8 +689,21 @@ __global__ void k_rank_items(DevGraph g, DevSchedule sc, int32_t group, int32_t 
     const int b = sc.entry_branch[i];
     const int64_t off = sc.grp_off[s];
     const int cnt = sc.grp_cnt[s];
-    int r = 0;
-    for (int k = 0; k < cnt; ++k) r += sc.grp_tmp[off + k] < b;
+    // rank of b in B(s) = branches of the group below b (eight independent loads in flight)
+    const int32_t* grp = sc.grp_tmp + off;
+    int r0 = 0, r1 = 0, r2 = 0, r3 = 0, r4 = 0, r5 = 0, r6 = 0, r7 = 0, k = 0;
+    for (; k + 8 <= cnt; k += 8) {
+      r0 += grp[k] < b;
+      r1 += grp[k + 1] < b;
+      r2 += grp[k + 2] < b;
+      r3 += grp[k + 3] < b;
+      r4 += grp[k + 4] < b;
+      r5 += grp[k + 5] < b;
+      r6 += grp[k + 6] < b;
+      r7 += grp[k + 7] < b;
+    }
+    for (; k < cnt; ++k) r0 += grp[k] < b;
+    const int r = r0 + r1 + r2 + r3 + r4 + r5 + r6 + r7;
     sc.grp_br[off + r] = b;
     sc.entry_rank[i] = r;
     write_entry_parts(g, sc, i, r, cnt);

@@ -23,9 +23,10 @@ __global__ __launch_bounds__(256) void k_merge(MergeArgs a) {
   constexpr int LPR = D / CPL;                 // lanes per (branch, q-head) row
   constexpr int RPB = 256 / LPR;               // rows per workgroup
   constexpr int PS = PF16 ? 2 : 1;
-  // Partials loaded per batch before any is folded: 4 keeps the kernel at 76 VGPRs (6 waves
-  // per SIMD), whose extra waves hide more latency than batches of 8 at 116 VGPRs (4 waves).
-  constexpr int KB = 4;
+  // Partials loaded per batch before any is folded.  One keeps the kernel at 36 VGPRs (8 waves
+  // per SIMD): more resident rows hide the loads' latency better than deeper batches per row
+  // (2: 56 VGPRs, 4: 76, 8: 116 at 4 waves per SIMD, each slower).
+  constexpr int KB = 1;
   const int tid = threadIdx.x;
   if (blockIdx.x == 0 && tid == 0) a.counters[2] = 0;
   const int64_t row = (int64_t)blockIdx.x * RPB + tid / LPR;

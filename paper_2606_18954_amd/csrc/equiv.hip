@@ -351,18 +351,49 @@ __global__ void k_labels(EquivArgs a) {
 }
 
 // Graph suffix, pass 1 (count into cnt[u]) or pass 2 (write from off[u]).
+// The block's 256 states lie in consecutive prompts, so every state they scan lies between the
+// first state's prompt start and the last state's prompt end: with prompts of up to 256 states
+// that span (at most 768 states) is staged in LDS once, and each thread scans it there; longer
+// spans are scanned in global memory.  Same scan, same order, either way.
+constexpr int kSufStage = 1024;
+
 template <bool FILL>
-__global__ void k_suffix(SuffixArgs a) {
-  const int64_t u = (int64_t)blockIdx.x * 256 + threadIdx.x;
+__global__ __launch_bounds__(256) void k_suffix(SuffixArgs a) {
+  __shared__ int s_par[kSufStage], s_lab[kSufStage], s_dep[kSufStage];
+  const int64_t base = (int64_t)blockIdx.x * 256;
+  const int64_t last = min(base + 255, a.N - 1);
+  const int lo = a.pstart[base], hi = a.pend[last];
+  const bool staged = hi - lo <= kSufStage;
+  if (staged) {
+    for (int i = threadIdx.x; i < hi - lo; i += 256) {
+      s_par[i] = a.parent[lo + i];
+      s_lab[i] = a.labels[lo + i];
+      s_dep[i] = a.depth[lo + i];
+    }
+  }
+  __syncthreads();
+  const int64_t u = base + threadIdx.x;
   if (u >= a.N) return;
   const int lu = a.labels[u], du = a.depth[u];
   int64_t k = FILL ? a.off[u] : 0;
-  for (int c = a.pstart[u]; c < a.pend[u]; ++c) {
-    const int p = a.parent[c];
-    if (p < 0) continue;
-    if (p == (int)u || (a.labels[p] == lu && a.depth[c] > du)) {
-      if (FILL) a.states[k] = c;
-      ++k;
+  const int c0 = a.pstart[u], c1 = a.pend[u];
+  if (staged) {
+    for (int c = c0; c < c1; ++c) {
+      const int p = s_par[c - lo];           // p lies in u's prompt: p >= c0 >= lo
+      if (p < 0) continue;
+      if (p == (int)u || (s_lab[p - lo] == lu && s_dep[c - lo] > du)) {
+        if (FILL) a.states[k] = c;
+        ++k;
+      }
+    }
+  } else {
+    for (int c = c0; c < c1; ++c) {
+      const int p = a.parent[c];
+      if (p < 0) continue;
+      if (p == (int)u || (a.labels[p] == lu && a.depth[c] > du)) {
+        if (FILL) a.states[k] = c;
+        ++k;
+      }
     }
   }
   if (!FILL) a.cnt[u] = k;

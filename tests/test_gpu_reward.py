@@ -58,6 +58,24 @@ def test_fixture_on_gpu():
     compare("fixture (hand values)", got, ref, tol=2e-7)
 
 
+@pytest.mark.parametrize("case", ["routes", "undefined"])
+def test_route_fixture_on_gpu(case):
+    """The hand-derived rollouts of graph_reward_routes.json: a class anchored below the root,
+    edges on several members' and classes' routes, a shared edge whose own source's group
+    differs from its class label's, and a class member with an undefined score."""
+    from test_oracle_reward_pins import exact
+    with open(os.path.join(os.path.dirname(__file__), "golden", "graph_reward_routes.json")) as f:
+        fx = next(c for c in json.load(f)["cases"] if c["name"] == case)
+    sim32 = np.array(fx["edge_sim"], dtype=np.float32)
+    got = gpu_adv(fx["parent"], fx["labels"], fx["reward"], sim32, fx["w"], fx["lambda_eff"])
+    ref = O.graph_advantages(np.array(fx["parent"]), np.array(fx["labels"]),
+                             np.array(fx["reward"]), sim32.astype(np.float64), fx["w"],
+                             fx["lambda_eff"])
+    compare(f"{case} (oracle, float32 sims)", got, ref)
+    hand = {k: np.array([exact(x) for x in fx[k]]) for k in KEYS}
+    compare(f"{case} (hand values)", got, hand, tol=2e-7)
+
+
 @pytest.mark.parametrize("prompts,sched,seed", [(3, (3, 3, 2), 1), (2, (4, 5, 3, 2), 2),
                                                 (5, (2, 2, 2, 2, 2), 3), (1, (8,), 4),
                                                 (2, (6, 6, 15), 5)])

@@ -1,8 +1,11 @@
 """Pins of the oracle's graph reward (node scores, step rewards) and dual-group advantage
-against facts that do not come from the oracle itself: a hand-derived fixture, the Monte Carlo
-rate it reduces to without merges or with w = 0, the pooled closed form at w = 1, and the
-z-score invariants of the correctness groups.
+against facts that do not come from the oracle itself: hand-derived fixtures (one with a_Q at
+the root; two more with a_Q below it, routes shared by several members and classes, a shared
+edge whose source's group differs from its class label's and a member of undefined score),
+hand-derived anchors, the Monte Carlo rate the score reduces to without merges or with w = 0,
+the pooled closed form at w = 1, and the z-score invariants of the correctness groups.
 """
+import ast
 import json
 import math
 import os
@@ -124,8 +127,60 @@ def check_correctness_groups(mod, seed=63):
     assert np.all(res["A_eff"] == 0)                  # no class of two or more
 
 
+def _routes_fixture():
+    with open(os.path.join(GOLDEN, "graph_reward_routes.json")) as f:
+        return json.load(f)["cases"]
+
+
+def exact(expr: str) -> float:
+    """Value of a fixture expression: numbers, + - * /, unary minus, sqrt(.) and nan."""
+    def ev(n):
+        if isinstance(n, ast.Expression):
+            return ev(n.body)
+        if isinstance(n, ast.Constant) and isinstance(n.value, (int, float)):
+            return float(n.value)
+        if isinstance(n, ast.Name) and n.id == "nan":
+            return math.nan
+        if isinstance(n, ast.UnaryOp) and isinstance(n.op, ast.USub):
+            return -ev(n.operand)
+        if isinstance(n, ast.BinOp) and type(n.op) in _OPS:
+            return _OPS[type(n.op)](ev(n.left), ev(n.right))
+        if (isinstance(n, ast.Call) and isinstance(n.func, ast.Name) and n.func.id == "sqrt"
+                and len(n.args) == 1):
+            return math.sqrt(ev(n.args[0]))
+        raise ValueError(f"unsupported expression {expr!r}")
+    return ev(ast.parse(expr, mode="eval"))
+
+
+_OPS = {ast.Add: lambda a, b: a + b, ast.Sub: lambda a, b: a - b,
+        ast.Mult: lambda a, b: a * b, ast.Div: lambda a, b: a / b}
+
+
+def check_route_fixture(mod):
+    """Two hand-derived rollouts whose arithmetic is written out in the fixture: a class whose
+    a_Q lies below the root, edges on the routes of two members and of two classes (summed),
+    an edge whose source's correctness group differs from its class label's, and a class with
+    a member of undefined score (the gate averages the defined ones)."""
+    for fx in _routes_fixture():
+        res = mod.graph_advantages(np.array(fx["parent"]), np.array(fx["labels"]),
+                                   np.array(fx["reward"]), np.array(fx["edge_sim"]), fx["w"],
+                                   fx["lambda_eff"])
+        for k in ["S", "r", "A_cor", "A_eff", "A_dual"]:
+            exp = np.array([exact(x) for x in fx[k]])
+            assert np.allclose(res[k], exp, rtol=0, atol=1e-12, equal_nan=True), (fx["name"], k)
+
+
+def check_anchors(mod):
+    """a_Q, the deepest state that precedes every member (Sec. 3.4), on hand-derived classes;
+    above a_Q the z-scores of a class sum to zero, so the advantages alone cannot pin it."""
+    for fx in _routes_fixture():
+        parent = np.array(fx["parent"])
+        for a in fx["anchors"]:
+            assert mod.class_anchor(parent, a["members"]) == a["a_Q"], (fx["name"], a)
+
+
 PINS = [check_fixture, check_monte_carlo_rate, check_full_pooling, check_step_reward_discount,
-        check_correctness_groups]
+        check_correctness_groups, check_route_fixture, check_anchors]
 
 
 @pytest.mark.parametrize("pin", PINS, ids=[p.__name__ for p in PINS])
@@ -136,6 +191,55 @@ def test_reward_pin(pin):
 ORIG_SCORES = O.node_scores
 ORIG_SUFFIX = O.graph_suffix
 ORIG_EFF = O.efficiency_advantage
+ORIG_COR = O.correctness_advantage
+
+
+def _anchor_at_root(parent, members):
+    x = int(members[0])
+    while int(parent[x]) >= 0:
+        x = int(parent[x])
+    return x
+
+
+def _efficiency_variant(parent, labels, S, last_write=False, nan_as_zero=False):
+    """The oracle's efficiency advantage with one planted change."""
+    depth = O.state_depths(parent)
+    E = np.zeros(len(parent))
+    classes = {}
+    for v in range(len(parent)):
+        classes.setdefault(int(labels[v]), []).append(v)
+    for members in classes.values():
+        if len(members) < 2:
+            continue
+        a = O.class_anchor(parent, members)
+        if nan_as_zero:
+            gate = sum(0.0 if np.isnan(S[v]) else float(S[v]) for v in members) / len(members)
+        else:
+            d = [float(S[v]) for v in members if not np.isnan(S[v])]
+            gate = sum(d) / len(d) if d else 0.0
+        z = O._zscores([-float(depth[v] - depth[a]) for v in members])
+        for v, zv in zip(members, z):
+            x = v
+            while x != a:
+                E[x] = gate * zv if last_write else E[x] + gate * zv
+                x = int(parent[x])
+    return E
+
+
+def _cor_in_label_group(parent, labels, r):
+    """A_cor of every edge taken in the group of its source's class label."""
+    offs, states = O.graph_suffix(labels, parent)
+    A = np.zeros(len(parent))
+    for v in range(len(parent)):
+        if parent[v] < 0 or np.isnan(r[v]):
+            continue
+        u = int(labels[int(parent[v])])
+        grp = [int(x) for x in states[offs[u]:offs[u + 1]]]
+        if v not in grp or len(grp) <= 1:
+            continue
+        ok = [x for x in grp if not np.isnan(r[x])]
+        A[v] = O._zscores([float(r[x]) for x in ok], O.SPREAD_FLOOR)[ok.index(v)]
+    return A
 
 
 def _sample_std(values, floor=0.0):
@@ -159,6 +263,12 @@ def _own_children_only(labels, parent):
                                       for v in range(len(parent))])),
     ("gate_ignored", "efficiency_advantage",
      lambda parent, labels, S: ORIG_EFF(parent, labels, np.ones_like(S))),
+    ("anchor_at_prompt_root", "class_anchor", _anchor_at_root),
+    ("route_last_write", "efficiency_advantage",
+     lambda parent, labels, S: _efficiency_variant(parent, labels, S, last_write=True)),
+    ("gate_counts_undefined_as_zero", "efficiency_advantage",
+     lambda parent, labels, S: _efficiency_variant(parent, labels, S, nan_as_zero=True)),
+    ("cor_in_class_label_group", "correctness_advantage", _cor_in_label_group),
 ])
 def test_planted_mistake_is_caught(monkeypatch, name, attr, repl):
     monkeypatch.setattr(O, attr, repl)

@@ -260,9 +260,9 @@ def test_segment_chains_with_ragged_pages():
         check_workload(wl, out_f32=True)
 
 
-@pytest.mark.skip(reason="its only run ended in a segmentation fault inside torch's first CUDA "
-                         "initialisation (before the library was loaded); held back until a run "
-                         "on a fresh box")
+@pytest.mark.skip(reason="its only run ended in a segmentation fault in the process's first "
+                         "GPU call (torch's device query, before this test's own code or the "
+                         "library ran); no cause has been shown, so it stays skipped")
 def test_step_replayed_from_a_hip_graph():
     """A serving loop can capture a whole decode step (scheduler, attention, merge: no memsets, no
     host synchronisation) in a HIP graph: every replay, with eager work in between that clears

@@ -124,7 +124,9 @@ ga_status graphattn_extend(const void* q, const void* kv_page_pool,
                            const ga_branch_paths* branch_paths, const int32_t* query_counts,
                            void* out, float* lse, const ga_params* params, void* hip_stream);
 
-/* Validate the graph and parameters, allocate the plan's device workspace (sized for this
+/* The graph of a rollout (Sec. 3.2 "Graph Construction": step segments as edges, the prompt
+ * as root, branches as the active states' paths), prepared once for many decode steps and
+ * layers.  Validate the graph and parameters, allocate the plan's device workspace (sized for this
  * graph, with every segment at all the pages the page table gives it, so that lengths set later
  * by graphattn_plan_set_lengths fit) and enqueue the upload of the index arrays on hip_stream.  The host arrays may be
  * released when the call returns.  *plan receives a new plan (NULL on error). */
@@ -158,16 +160,23 @@ ga_status graphattn_plan_create_extend(const ga_segment_table* segment_table,
 ga_status graphattn_plan_set_lengths(ga_plan* plan, const int32_t* seg_len, void* hip_stream);
 
 /* Segment scheduler, on the GPU: transpose branch->segments into segment->branches (B(s) in
- * ascending branch order), give each path entry the branch's position inside B(s), split long
- * segments into page chunks and emit the work list of (segment, chunk, row block) items.
- * Enqueued on hip_stream; must precede graphattn_run.  Deterministic: the same graph always
- * yields the same schedule. */
+ * ascending branch order: the branches that share a segment, i.e. siblings sharing a prefix
+ * (Sec. 1) and merged states sharing a suffix (Sec. 3.2, C_g)), give each path entry the
+ * branch's position inside B(s), split long segments into page chunks and emit the work list of
+ * (segment, chunk, row block) items and each branch's partial-row list.  Enqueued on
+ * hip_stream.  graphattn_run schedules by itself when the plan has no current schedule (a new
+ * plan, or new lengths); calling this first splits the work for timing or for one schedule
+ * serving several runs.  Deterministic: the same graph always yields the same schedule. */
 ga_status graphattn_schedule(ga_plan* plan, void* hip_stream);
 
-/* Grouped segment attention and log-sum-exp merge for one layer's q and K/V pool, using the
- * plan's schedule (the rollout graph is shared by every layer of a decode step, so a schedule
- * serves any number of runs).  Device pointers as described above.  Enqueued on hip_stream;
- * runs on one plan must not overlap (they share the partial-result workspace). */
+/* Grouped segment attention and log-sum-exp merge for one layer's q and K/V pool (the
+ * attention of every branch over prefix(u), Alg. S.1 Stage 1, grouped per segment as in
+ * graphattn_decode), using the plan's schedule (the rollout graph is shared by every layer of a
+ * decode step, so a schedule serves any number of runs); a plan without a current schedule is
+ * scheduled first, on the same stream.  Device pointers as described above.  Enqueued on
+ * hip_stream; runs on one plan must not overlap (they share the partial-result workspace).  If
+ * a launch fails (GA_EHIP) the outputs are unspecified and the plan is scheduled again by its
+ * next run. */
 ga_status graphattn_run(ga_plan* plan, const void* q, const void* kv_page_pool, void* out,
                         float* lse, void* hip_stream);
 
@@ -191,19 +200,29 @@ typedef struct {
 } ga_plan_info;
 ga_status graphattn_plan_info(const ga_plan* plan, ga_plan_info* info);
 
-/* Copy the device schedule back to host arrays for inspection (synchronises hip_stream).  Any
- * pointer may be NULL to skip that array.  Sizes: group_offsets [S+1] and group_branches [E]
- * (B(s) as CSR, ascending ids), entry_ranks [E] (position of each path entry's branch inside
- * its segment's group), items [3 * num_items] as (segment, chunk, row block) triples, and
- * segment_chunks [S].  Groups and ranks are per given segment and path entry.  Items and chunk
- * counts are per chain: an item names its chain by the chain's first segment, and
- * segment_chunks holds a chain's chunk count at its first segment and 0 at the others. */
+/* Inspection of the scheduler's integer output (test infrastructure: the grouping, ranks and
+ * partial lists are compared bit for bit with a plain-loop grouping of the paths).  Copies the
+ * device schedule back to host arrays (synchronises hip_stream; GA_EINVAL if the plan has no
+ * current schedule).  Any pointer may be NULL to skip that array.  Sizes: group_offsets [S+1]
+ * and group_branches [E] (B(s) as CSR, ascending ids), entry_ranks [E] (position of each path
+ * entry's branch inside its segment's group), items [3 * num_items] as (segment, chunk, row
+ * block) triples, segment_chunks [S], branch_part_offsets [num_query_rows + 1] and branch_parts
+ * [num_partial_rows] (each branch's partial rows per q-head as CSR, in the order the merge folds
+ * them: path order, then chunk order; only branch_part_offsets[num_query_rows] entries are
+ * written).  Groups and ranks are per given segment and path entry.  Items, chunk counts and
+ * partial rows are per chain: an item names its chain by the chain's first segment,
+ * segment_chunks holds a chain's chunk count at its first segment and 0 at the others, a branch
+ * lists the partials of each chain on its path at the chain's first segment, and the partial
+ * row of (chain v, chunk c, rank j) is prow(v) + c |B(v)| + j with prow the running sum of
+ * chunks x |B| over the chains in the order of their first segments. */
 ga_status graphattn_plan_debug_dump(const ga_plan* plan, void* hip_stream,
                                     int64_t* group_offsets, int32_t* group_branches,
                                     int32_t* entry_ranks, int32_t* items,
-                                    int32_t* segment_chunks);
+                                    int32_t* segment_chunks, int64_t* branch_part_offsets,
+                                    int32_t* branch_parts);
 
-/* Kernel timing with HIP events recorded on the launch stream around each scheduler pass, each
+/* Measurement infrastructure.  Kernel timing with HIP events recorded on the launch stream
+ * around each scheduler pass, each
  * attention launch and each merge launch.  graphattn_plan_profile(plan, n) arms recording for the
  * next n schedule and n run calls (n = 0 disarms and clears); graphattn_plan_profile_read
  * synchronises on the last recorded event and returns the accumulated times in milliseconds

@@ -669,10 +669,18 @@ ga_status do_schedule(ga_plan* pl, hipStream_t stream) {
 
 ga_status do_run(ga_plan* pl, const void* q, const void* pool, void* out, float* lse,
                  hipStream_t stream) {
-  if (!pl->scheduled) return fail(GA_EINVAL, "plan has no schedule (call graphattn_schedule)");
   ga_status rc = check_run_ptrs(pl, q, pool, out, lse);
   if (rc) return rc;
+  // A plan without a current schedule (new, or given new lengths) is scheduled first.
+  if (!pl->scheduled) {
+    rc = do_schedule(pl, stream);
+    if (rc) return rc;
+  }
   if (pl->z.B == 0) return GA_OK;
+  // The merge re-arms the attention kernel's work-queue head; a schedule clears it as well.  If
+  // a launch below fails, the plan loses its schedule, so the next run schedules (and so
+  // re-arms the queue) before it attends.
+  pl->scheduled = false;
   const bool bf16 = pl->p.dtype == GA_BF16;
   ga::AttnArgs a{};
   a.q = q;
@@ -709,6 +717,7 @@ ga_status do_run(ga_plan* pl, const void* q, const void* pool, void* out, float*
   m.Hq = pl->p.num_q_heads;
   GA_HIP(ga::launch_merge(m, pl->p.head_dim, bf16 && !pl->p.out_f32, bf16, stream),
          "merge launch");
+  pl->scheduled = true;
   if (rec) {
     GA_HIP(hipEventRecord(ev[2], stream), "profile event");
     pl->ev_last = ev[2];
@@ -888,7 +897,8 @@ ga_status graphattn_plan_info(const ga_plan* plan, ga_plan_info* info) {
 ga_status graphattn_plan_debug_dump(const ga_plan* plan, void* hip_stream,
                                     int64_t* group_offsets, int32_t* group_branches,
                                     int32_t* entry_ranks, int32_t* items,
-                                    int32_t* segment_chunks) {
+                                    int32_t* segment_chunks, int64_t* branch_part_offsets,
+                                    int32_t* branch_parts) {
   g_err.clear();
   if (!plan) return fail(GA_EINVAL, "plan is NULL");
   if (!plan->scheduled) return fail(GA_EINVAL, "plan has no schedule");
@@ -924,6 +934,19 @@ ga_status graphattn_plan_debug_dump(const ga_plan* plan, void* hip_stream,
   if (group_offsets) group_offsets[c.S0] = off;
   if (entry_ranks)
     for (int64_t e = 0; e < c.E0; ++e) entry_ranks[e] = vrank[c.ventry[e]];
+  if (branch_part_offsets || branch_parts) {
+    // Each branch's partial rows (per q-head) as the merge folds them: path order, then chunk
+    // order.  The schedule's branches are the dumped ones (query rows for multi-query plans).
+    std::vector<int64_t> boff(z.B + 1);
+    GA_HIP(hipMemcpy(boff.data(), plan->sc.bpart_off, sizeof(int64_t) * (z.B + 1),
+                     hipMemcpyDeviceToHost), "dump partial offsets");
+    if (boff[z.B] > z.prows)
+      return fail(GA_EINVAL, "schedule overflow (%lld partial rows)", (long long)boff[z.B]);
+    if (branch_part_offsets) std::memcpy(branch_part_offsets, boff.data(), sizeof(int64_t) * (z.B + 1));
+    if (branch_parts && boff[z.B] > 0)
+      GA_HIP(hipMemcpy(branch_parts, plan->sc.bpart, sizeof(int32_t) * boff[z.B],
+                       hipMemcpyDeviceToHost), "dump partial rows");
+  }
   if (items) {
     int64_t n = 0;
     GA_HIP(hipMemcpy(&n, plan->sc.counters, sizeof n, hipMemcpyDeviceToHost), "dump count");

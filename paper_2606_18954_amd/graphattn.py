@@ -124,7 +124,8 @@ def load_library() -> ctypes.CDLL:
     lib.graphattn_run.restype = ctypes.c_int
     lib.graphattn_plan_info.argtypes = [vp, P(PlanInfo)]
     lib.graphattn_plan_info.restype = ctypes.c_int
-    lib.graphattn_plan_debug_dump.argtypes = [vp, vp, P(i64), P(i32), P(i32), P(i32), P(i32)]
+    lib.graphattn_plan_debug_dump.argtypes = [vp, vp, P(i64), P(i32), P(i32), P(i32), P(i32),
+                                              P(i64), P(i32)]
     lib.graphattn_plan_debug_dump.restype = ctypes.c_int
     lib.graphattn_plan_profile.argtypes = [vp, i32]
     lib.graphattn_plan_profile.restype = ctypes.c_int
@@ -404,6 +405,7 @@ class Plan:
             _stream_handle(stream)))
 
     def schedule(self, stream=None):
+        """Run the GPU segment scheduler (run() also schedules a plan that has no schedule)."""
         _check(self.lib.graphattn_schedule(self.handle, _stream_handle(stream)))
 
     def run(self, q, pool, out, lse, stream=None):
@@ -416,21 +418,25 @@ class Plan:
         return inf
 
     def debug_dump(self, stream=None):
-        """Device schedule as numpy arrays: group offsets/branches, entry ranks, items, chunks."""
+        """Device schedule as numpy arrays: group offsets/branches, entry ranks, items, chunks
+        and each branch's partial-row list (CSR)."""
         inf = self.info()
-        S, E = inf.num_segments, inf.num_entries
+        S, E, R = inf.num_segments, inf.num_entries, inf.num_query_rows
         goff = np.zeros(S + 1, dtype=np.int64)
         gbr = np.zeros(max(E, 1), dtype=np.int32)
         rk = np.zeros(max(E, 1), dtype=np.int32)
         nit = max(int(inf.num_items), 0)
         items = np.zeros(max(3 * nit, 3), dtype=np.int32)
         nch = np.zeros(max(S, 1), dtype=np.int32)
+        boff = np.zeros(R + 1, dtype=np.int64)
+        bpart = np.zeros(max(int(inf.num_partial_rows), 1), dtype=np.int32)
         _check(self.lib.graphattn_plan_debug_dump(
             self.handle, _stream_handle(stream), _ptr(goff, ctypes.c_int64),
             _ptr(gbr, ctypes.c_int32), _ptr(rk, ctypes.c_int32), _ptr(items, ctypes.c_int32),
-            _ptr(nch, ctypes.c_int32)))
+            _ptr(nch, ctypes.c_int32), _ptr(boff, ctypes.c_int64), _ptr(bpart, ctypes.c_int32)))
         return {"group_offsets": goff, "group_branches": gbr[:E], "entry_ranks": rk[:E],
-                "items": items[:3 * nit].reshape(nit, 3), "segment_chunks": nch[:S]}
+                "items": items[:3 * nit].reshape(nit, 3), "segment_chunks": nch[:S],
+                "branch_part_offsets": boff, "branch_parts": bpart[:int(boff[-1])]}
 
     def profile(self, max_calls: int):
         """Record HIP-event kernel times for the next ``max_calls`` schedule/run calls."""

@@ -49,6 +49,19 @@ def oracle_decode(wl, branches=None, graph=None):
                     wl.dtype, branches=branches)
 
 
+def oracle_decode_all(wl, chunk=128):
+    """The oracle over every branch, a chunk of branches at a time, with a progress line per
+    chunk (the full-size configurations take tens of seconds)."""
+    B = wl.graph.num_branches
+    outs, lses = [], []
+    for b0 in range(0, B, chunk):
+        o, l = oracle_decode(wl, list(range(b0, min(B, b0 + chunk))))
+        outs.append(o)
+        lses.append(l)
+        say(f"[oracle] {wl.name}: branches {b0}..{min(B, b0 + chunk) - 1} of {B}")
+    return np.concatenate(outs), np.concatenate(lses)
+
+
 def compare(tag, got_out, got_lse, ref_out, ref_lse, tol_out=TOL_OUT, tol_lse=TOL_LSE):
     assert got_out.shape == ref_out.shape and got_lse.shape == ref_lse.shape
     assert np.isfinite(got_out).all(), f"{tag}: non-finite output"

@@ -1,5 +1,6 @@
-"""The GPU segment scheduler against plain-loop CPU grouping: bit-exact groups, ranks, chunking
-and work list, and identical schedules on repeated runs."""
+"""The GPU segment scheduler against plain-loop CPU grouping: bit-exact groups, ranks, chunking,
+work list and each branch's ordered partial-row list, and identical schedules on repeated
+runs."""
 import json
 import os
 
@@ -78,6 +79,29 @@ def expected_items(g, group, chunk_pages, cnt):
     return np.array(items, dtype=np.int32).reshape(-1, 3)
 
 
+def expected_partials(g, chunk_pages, offs, ranks):
+    """Each branch's partial rows as a plain loop builds them: chains numbered in the order of
+    their first segments, prow(v) the running sum of chunks x |B| over them, and for every path
+    entry that starts a chain, one row per chunk, prow(v) + c |B(v)| + rank, in path order."""
+    ch = chains(g)
+    cnt = np.diff(offs)
+    head = {c[0]: i for i, c in enumerate(ch)}
+    nch = [(sum((int(g.seg_len[s]) + 15) // 16 for s in c) + chunk_pages - 1) // chunk_pages
+           for c in ch]
+    prow = [0]
+    for i, c in enumerate(ch):
+        prow.append(prow[-1] + nch[i] * int(cnt[c[0]]))
+    boff, parts = [0], []
+    for b in range(g.num_branches):
+        for e in range(int(g.path_offsets[b]), int(g.path_offsets[b + 1])):
+            s = int(g.path_segs[e])
+            if s in head:
+                v = head[s]
+                parts += [prow[v] + c * int(cnt[s]) + int(ranks[e]) for c in range(nch[v])]
+        boff.append(len(parts))
+    return np.array(boff, dtype=np.int64), np.array(parts, dtype=np.int32)
+
+
 def check_schedule(wl):
     g = wl.graph
     say(f"[case] schedule of {wl.name}")
@@ -106,6 +130,9 @@ def check_schedule(wl):
     assert info.num_chains == len(ch)
     assert np.array_equal(d["segment_chunks"], chunks)
     assert info.num_partial_rows == int(sum(chunks[s] for s in g.path_segs))
+    boff, parts = expected_partials(g, info.chunk_pages, offs, ranks)
+    assert np.array_equal(d["branch_part_offsets"], boff)
+    assert np.array_equal(d["branch_parts"], parts)
     for k in d:
         assert np.array_equal(d[k], d2[k]), k
 

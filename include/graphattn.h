@@ -350,6 +350,23 @@ ga_status graphattn_forest_advantages(ga_forest* forest, const int32_t* labels,
                                       double lambda_eff, const ga_advantages* out,
                                       void* hip_stream);
 
+/* graphattn_decode without any device or pinned-host allocation, for callers that cannot
+ * allocate (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc).  Same arguments, checks, kernels and results (bit for bit) as graphattn_decode;
+ * the workspace (uploaded graph, schedule, partial results) lives in a static device array of
+ * 64 MiB per device, held from the first call on a device until the process ends.  A graph
+ * whose workspace exceeds it is rejected with GA_ENOMEM before any device work (the message
+ * gives both sizes); the merged-DAG decode step of 1024 branches needs about 45 MiB.  The graph
+ * upload is staged in ordinary (pageable) host memory and host-side validation uses the heap.
+ * All calls on one device share its array: each call waits (on the device, through an event)
+ * for the previous call's kernels before it reuses the array, and concurrent host calls are
+ * serialised by a lock, so calls on several streams do not race but do not overlap either.
+ * Devices 0..15. */
+ga_status graphattn_decode_static(const void* q, const void* kv_page_pool,
+                                  const ga_segment_table* segment_table,
+                                  const ga_branch_paths* branch_paths, void* out, float* lse,
+                                  const ga_params* params, void* hip_stream);
+
 /* Release the plan and its device workspace (waits for work still using it). */
 void graphattn_plan_destroy(ga_plan* plan);
 

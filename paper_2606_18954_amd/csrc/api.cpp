@@ -475,6 +475,24 @@ void pack_upload(const ga_segment_table* st, const ga_branch_paths* bp, const in
   if (z.S) std::memcpy(h + L.off[L_SEG_CAUSAL], causal, sizeof(int32_t) * z.S);
 }
 
+// Workspace of graphattn_decode_static: a static device array, so that the call allocates no
+// device or pinned memory.  Every call on one device uses that device's copy; calls are ordered
+// through the events below (and serialised on the host by the lock), so a later call reuses
+// the array only after the earlier one's kernels are done with it.  Nothing in it has to start
+// at zero: the scheduler clears its counters, and every other array is written before it is
+// read.  The graph upload is staged in pageable host memory.
+constexpr size_t kStaticScratchBytes = size_t(64) << 20;
+constexpr int kStaticDevices = 16;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+struct StaticScratch {
+  std::mutex mu;
+  void* dev = nullptr;            // the array's device address (hipGetSymbolAddress)
+  std::vector<char> stage;        // host staging of the graph upload
+  hipEvent_t done = nullptr;      // recorded after the last call's kernels
+  hipEvent_t uploaded = nullptr;  // recorded after the last call's upload
+};
+StaticScratch g_static[kStaticDevices];
+
 // Process-wide workspace reused by graphattn_decode.
 struct DecodeCache {
   std::mutex mu;
@@ -1097,6 +1115,59 @@ ga_status graphattn_decode(const void* q, const void* kv_page_pool,
                            const ga_params* params, void* hip_stream) {
   return one_shot(q, kv_page_pool, segment_table, branch_paths, nullptr, out, lse, params,
                   hip_stream);
+}
+
+ga_status graphattn_decode_static(const void* q, const void* kv_page_pool,
+                                  const ga_segment_table* segment_table,
+                                  const ga_branch_paths* branch_paths, void* out, float* lse,
+                                  const ga_params* params, void* hip_stream) {
+  g_err.clear();
+  hipStream_t stream = static_cast<hipStream_t>(hip_stream);
+  ga_plan pl;
+  Layout L;
+  ga_status rc = plan_init(segment_table, branch_paths, params, nullptr, false, &pl, &L);
+  if (rc) return rc;
+  rc = check_run_ptrs(&pl, q, kv_page_pool, out, lse);
+  if (rc) return rc;
+  if (L.total > kStaticScratchBytes)
+    return fail(GA_ENOMEM, "workspace of %zu bytes exceeds the static scratch of %zu bytes",
+                L.total, (size_t)kStaticScratchBytes);
+  pl.scheduled = false;
+  pl.owns_memory = false;
+  int dev = 0;
+  GA_HIP(hipGetDevice(&dev), "current device");
+  if (dev < 0 || dev >= kStaticDevices)
+    return fail(GA_EUNSUPPORTED, "device %d beyond the %d the static scratch serves", dev,
+                kStaticDevices);
+  StaticScratch& st = g_static[dev];
+  std::lock_guard<std::mutex> lock(st.mu);
+  if (!st.dev) {
+    // Once per device, with the device current: the array's address on this device.  The host
+    // name of the array is not a device address; only this pointer is passed on.
+    void* ptr = nullptr;
+    GA_HIP(hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)), "scratch address");
+    GA_HIP(hipEventCreateWithFlags(&st.done, hipEventDisableTiming), "event");
+    GA_HIP(hipEventCreateWithFlags(&st.uploaded, hipEventDisableTiming), "event");
+    st.dev = ptr;
+  }
+  // The previous call's upload must have left the staging buffer, and its kernels must be done
+  // with the scratch before this stream reuses it.
+  GA_HIP(hipEventSynchronize(st.uploaded), "wait for previous upload");
+  const size_t ub = upload_bytes(L);
+  if (st.stage.size() < ub) st.stage.resize(ub);
+  pl.dev = st.dev;
+  pl.pin = st.stage.data();
+  bind(&pl, L);
+  GA_HIP(hipStreamWaitEvent(stream, st.done, 0), "order after previous call");
+  rc = upload(&pl, L, stream);
+  if (rc) return rc;
+  GA_HIP(hipEventRecord(st.uploaded, stream), "record upload");
+  rc = do_schedule(&pl, stream);
+  if (rc) return rc;
+  rc = do_run(&pl, q, kv_page_pool, out, lse, stream);
+  if (rc) return rc;
+  GA_HIP(hipEventRecord(st.done, stream), "record decode");
+  return GA_OK;
 }
 
 static ga_status kv_write(void* pool, const void* k_new, const void* v_new, const int32_t* src,

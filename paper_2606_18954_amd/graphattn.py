@@ -88,6 +88,8 @@ def load_library() -> ctypes.CDLL:
     P = ctypes.POINTER
     lib.graphattn_decode.argtypes = [vp, vp, P(SegmentTable), P(BranchPaths), vp, vp, P(Params), vp]
     lib.graphattn_decode.restype = ctypes.c_int
+    lib.graphattn_decode_static.argtypes = lib.graphattn_decode.argtypes
+    lib.graphattn_decode_static.restype = ctypes.c_int
     lib.graphattn_plan_create.argtypes = [P(SegmentTable), P(BranchPaths), P(Params), vp, P(vp)]
     lib.graphattn_plan_create.restype = ctypes.c_int
     lib.graphattn_extend.argtypes = [vp, vp, P(SegmentTable), P(BranchPaths), P(i32), vp, vp,
@@ -205,6 +207,16 @@ def decode(q, pool, graph: HostGraph, params: Params, out=None, lse=None, stream
     _check(lib.graphattn_decode(_dev_ptr(q), _dev_ptr(pool), ctypes.byref(graph.st),
                                 ctypes.byref(graph.bp), _dev_ptr(out), _dev_ptr(lse),
                                 ctypes.byref(params), _stream_handle(stream)))
+    return out, lse
+
+
+def decode_static(q, pool, graph: HostGraph, params: Params, out, lse, stream=None):
+    """graphattn_decode_static: graphattn_decode with its workspace in the library's static
+    device array (no allocation; the caller passes out and lse)."""
+    lib = load_library()
+    _check(lib.graphattn_decode_static(_dev_ptr(q), _dev_ptr(pool), ctypes.byref(graph.st),
+                                       ctypes.byref(graph.bp), _dev_ptr(out), _dev_ptr(lse),
+                                       ctypes.byref(params), _stream_handle(stream)))
     return out, lse
 
 

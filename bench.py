@@ -19,6 +19,11 @@ advantage) for one training batch's rollout states.
 
 Timing: the K timed steps run without per-kernel events (ms_per_step, value); K further steps
 record HIP events on the launch stream around each kernel (kernel_ms and the roofline).
+
+The default decode line also carries, under "configs", the same step timed on every other
+configuration (tiny fp32 graph, 7B tree, 32B long reasoning, chain and equal-budget graph), with
+the attention's fraction of the HBM roofline on unique K/V warm and with the memory-side cache
+flushed, and under "decode_loop" the merged-DAG decode loop (append, grow, schedule, attend).
 """
 import argparse
 import hashlib
@@ -368,17 +373,18 @@ def run_append(args, torch, G, W):
     print(json.dumps(res), flush=True)
 
 
-def run_loop(args, torch, G, W):
+def measure_loop(torch, G, W, steps, warmup):
     """The decode loop on the merged-DAG rollout: every step stores one new token at the end of
     each newest segment (graphattn_kv_append), grows those segments by one token
-    (graphattn_plan_set_lengths: host rebuild and upload of the plan's graph copy), schedules
-    and attends.  The page table gives every newest segment the pages it grows into; the pool
-    gets those pages on top of the rollout's own."""
+    (graphattn_plan_set_lengths: the plan's chains rebuilt on the device), schedules and
+    attends.  The page table gives every newest segment the pages it grows into; the pool gets
+    those pages on top of the rollout's own.  Returns (workload, ms per step, host ms of one
+    length update with the device idle, newest segments)."""
     import numpy as np
     wl = W.config3_merged_dag()
     g = wl.graph
     B, Hq, Hkv, D = g.num_branches, wl.num_q_heads, wl.num_kv_heads, wl.head_dim
-    total = args.warmup + args.steps + 1
+    total = warmup + steps + 1
     newest = np.unique(np.array([int(g.path(b)[-1]) for b in range(B)]))
     S = g.num_segments
     lens = g.seg_len.astype(np.int32).copy()
@@ -426,7 +432,7 @@ def run_loop(args, torch, G, W):
         plan.run(q, pool, out, lse)
         k += 1
 
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         step()
     torch.cuda.synchronize()
     # the length update's own host time, with the device idle (inside the loop the host waits
@@ -440,22 +446,32 @@ def run_loop(args, torch, G, W):
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
     ev0.record()
-    for _ in range(args.steps):
+    for _ in range(steps):
         step()
     ev1.record()
     torch.cuda.synchronize()
-    ms = ev0.elapsed_time(ev1) / args.steps
+    ms = ev0.elapsed_time(ev1) / steps
     set_ms = 1e3 * float(np.median(host_s))
     plan.close()
+    del pool, q, out, lse
+    torch.cuda.empty_cache()
     log(f"decode loop: {ms:.4f} ms per step (append {n} tokens, grow, schedule, attend); "
         f"length update {set_ms:.3f} ms on the host")
+    return wl, ms, set_ms, int(n)
+
+
+def run_loop(args, torch, G, W):
+    wl, ms, set_ms, n = measure_loop(torch, G, W, args.steps, args.warmup)
+    g = wl.graph
+    B = g.num_branches
     res = {
         "metric": "branch-tokens/s per decode-loop step (append, grow, schedule, attend)",
         "value": B / (ms * 1e-3), "unit": "branch-tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": wl.dtype, "data": "synthetic",
         "config": {"workload": wl.name + ", decode loop", "branches": B,
-                   "newest_segments": int(n), "q_heads": Hq, "kv_heads": Hkv, "head_dim": D},
+                   "newest_segments": n, "q_heads": wl.num_q_heads, "kv_heads": wl.num_kv_heads,
+                   "head_dim": wl.head_dim},
         "set_lengths_host_ms": set_ms,
     }
     print(json.dumps(res), flush=True)
@@ -567,6 +583,45 @@ def run_equiv(args, torch, G, W):
     print(json.dumps(res), flush=True)
 
 
+def other_config(torch, G, W, name, dev, steps):
+    """One more configuration's decode step (schedule + attention + merge), timed like the main
+    one on fewer steps: ms per step, each kernel's average duration from HIP events, the
+    attention with the memory-side cache flushed before each step, and unique-K/V rates."""
+    t0 = time.time()
+    wl = W.CONFIGS[name]()
+    g = wl.graph
+    q, pool = wl.q.to(dev), wl.pool.to(dev)
+    B, Hq, D = g.num_branches, wl.num_q_heads, wl.head_dim
+    out = torch.empty((B, Hq, D), dtype=q.dtype, device=dev)
+    lse = torch.empty((B, Hq), dtype=torch.float32, device=dev)
+    plan = G.Plan(G.HostGraph.from_graph(g), G.make_params(Hq, wl.num_kv_heads, D, g.num_pages,
+                                                            wl.dtype))
+
+    def step():
+        plan.schedule()
+        plan.run(q, pool, out, lse)
+
+    for _ in range(3):
+        step()
+    torch.cuda.synchronize()
+    ms, attn_ms, merge_ms, sched_ms = timed_steps(torch, plan, step, steps)
+    cold_ms = mall_flushed_attention(torch, plan, step, steps, dev)
+    plan.close()
+    del q, pool, out, lse
+    torch.cuda.empty_cache()
+    ukv = wl.unique_kv_bytes()
+    log(f"{name}: {ms:.4f} ms/step, attention {attn_ms:.4f} ms ({cold_ms:.4f} ms cold) "
+        f"[{time.time() - t0:.1f} s]")
+    return {"workload": wl.name, "dtype": wl.dtype, "branches": B,
+            "unique_kv_bytes": ukv, "attended_tokens": g.attended_tokens(),
+            "ms_per_step": ms, "branch_tokens_per_s": B / (ms * 1e-3),
+            "kernel_ms": {"scheduler": sched_ms, "attention": attn_ms, "merge": merge_ms,
+                          "attention_mall_flushed": cold_ms},
+            "attention_unique_kv_frac": ukv / (attn_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+            "mall_flushed_frac": ukv / (cold_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+            "step_unique_kv_frac": ukv / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -580,6 +635,11 @@ def main():
                     help="query tokens per branch for --op extend")
     ap.add_argument("--cpu-sample", type=int, default=1024,
                     help="branches the CPU oracle is timed on (0 skips it)")
+    ap.add_argument("--all-configs", type=int, default=1,
+                    help="decode only: also time the other configurations and the decode loop "
+                         "(1, the default) and report them under configs / decode_loop")
+    ap.add_argument("--other-steps", type=int, default=20,
+                    help="timed steps per region for the other configurations")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 1 GiB device copy (torch elementwise kernel) so HBM "
                          "counters can be scaled against a kernel of known traffic")
@@ -680,6 +740,19 @@ def main():
     plan.close()
     del q, pool, out, lse
     torch.cuda.empty_cache()
+    if args.all_configs:
+        res["configs"] = {}
+        for name in ["c1", "c2", "c3", "c4", "c5chain", "c5graph"]:
+            if name != args.config:
+                res["configs"][name] = other_config(torch, G, W, name, dev, args.other_steps)
+        _, loop_ms, set_ms, n = measure_loop(torch, G, W, args.other_steps, 3)
+        res["decode_loop"] = {
+            "workload": wl.name + ", decode loop" if args.config == "c3" else
+                        "merged-DAG rollout decode loop",
+            "ms_per_step": loop_ms, "branch_tokens_per_s": 1024 / (loop_ms * 1e-3),
+            "newest_segments": n, "set_lengths_host_ms": set_ms,
+            "what": "per step: append one token to each newest segment, grow them by one token "
+                    "(length update), schedule, attend, merge"}
     if args.calibrate_copy:
         calibrate_copy(torch, dev)
     if args.cpu_sample > 0:

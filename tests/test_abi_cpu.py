@@ -22,7 +22,8 @@ def test_library_exports_every_declared_symbol():
                          "graphattn_equivalence_classes", "graphattn_graph_suffix",
                          "graphattn_forest_create", "graphattn_forest_classes",
                          "graphattn_forest_suffix", "graphattn_forest_destroy",
-                         "graphattn_forest_advantages", "graphattn_plan_set_lengths"}
+                         "graphattn_forest_advantages", "graphattn_plan_set_lengths",
+                         "graphattn_decode_static"}
     for s in syms:
         assert hasattr(lib, s), s
 

@@ -365,131 +365,154 @@ __device__ __forceinline__ void emit_items(const DevGraph& g, const DevSchedule&
   }
 }
 
+// Inclusive scan of one int over the 64 lanes of a wave with DPP: row shifts by 1, 2, 4 and 8
+// scan each row of 16 lanes (lanes shifted in from outside the row read 0), then the last lane
+// of row 0 is added to row 1 and of row 2 to row 3 (row_bcast:15), and the last lane of row 1 to
+// rows 2 and 3 (row_bcast:31).  Rows left out by the row mask keep their value.
+__device__ __forceinline__ int wave_scan_incl(int x) {
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, true);   // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, true);   // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, true);   // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, true);   // row_shr:8
+  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false);  // row_bcast:15
+  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false);  // row_bcast:31
+  return x;
+}
+
 // The whole scheduler in one workgroup for graphs that fit in LDS (<= kSmallSegs segments,
-// <= kSmallEntries path entries, < kSmallBranches branches): the graph is read once into LDS,
-// every phase works there between workgroup barriers, and the outputs are only written.
+// <= kSmallEntries path entries, < kSmallBranches branches): the graph is read once into LDS and
+// every phase works there between workgroup barriers; only outputs go to global memory.  Thread t
+// owns a contiguous run of at most four segments (for the per-segment scans, in segment order and
+// in work-list order) and a contiguous run of at most four branches (for the per-entry work).
 constexpr int kSmallSegs = 4096;
 constexpr int kSmallEntries = 8192;
 constexpr int kSmallBranches = 4096;
 
-__global__ __launch_bounds__(1024) void k_sched_small(DevGraph g, DevSchedule sc, int32_t group,
-                                                      int32_t chunk_pages) {
-  constexpr int EP = kSmallEntries / 1024, BP = kSmallBranches / 1024, SPT = kSmallSegs / 1024;
-  __shared__ int l_segs[kSmallEntries];     // path_segs
-  __shared__ int l_tmp[kSmallEntries];      // work-list order, later B(s) in arrival order
-  __shared__ int l_poff[kSmallBranches];    // path_off
-  __shared__ int l_cnt[kSmallSegs];         // |B(s)|
-  __shared__ int l_len[kSmallSegs];         // segment lengths
-  // Group offsets (scatter cursors in phase 5) and sort keys; after the scatter, each entry's
-  // slot in the branch partial lists.
-  __shared__ int l_aux[2 * kSmallSegs];
-  static_assert(2 * kSmallSegs >= kSmallEntries, "entry slots must fit the reused arrays");
-  int* const l_goff = l_aux;
-  uint32_t* const l_key = reinterpret_cast<uint32_t*>(l_aux + kSmallSegs);
-  __shared__ int sh[3][1024];
-  const int t = threadIdx.x;
+__global__ __launch_bounds__(1024) void k_sched_one(DevGraph g, DevSchedule sc, int32_t group,
+                                                    int32_t chunk_pages) {
+  constexpr int NBK = kCostClasses;
+  constexpr int SPT = kSmallSegs / 1024;
+  __shared__ unsigned short l_segs[kSmallEntries];        // path_segs
+  __shared__ unsigned short l_tmp[kSmallEntries];         // B(s) in arrival order
+  __shared__ unsigned short l_poff[kSmallBranches + 1];   // path_off
+  __shared__ int l_len[kSmallSegs];                       // segment lengths
+  __shared__ int l_cnt[kSmallSegs];                       // |B(s)|
+  __shared__ int l_cur[kSmallSegs];                       // scatter cursors, then work-list order
+  __shared__ int l_cw[4 * 16 * NBK];                      // sort: counts per (slot, wave, class)
+  __shared__ int l_boff[NBK];                             // sort: first position of each class
+  __shared__ int l_wsum[2][3][16];                        // wave totals of the two block scans
+  int* const l_order = l_cur;
+  const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
   const int S = g.S, E = g.E, B = g.B;
-  __shared__ int l_wsum[3][16];
-  // Inclusive scan over threads of three values at once -> sh[k][t] (sh[k][1023] is the total):
-  // a shuffle scan inside each wave, then each thread adds the totals of the waves before it.
-  auto block_scan = [&](int a, int b, int c) {
-    const int lane = t & 63, wv = t >> 6;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      const int ya = __shfl_up(a, off), yb = __shfl_up(b, off), yc = __shfl_up(c, off);
-      if (lane >= off) { a += ya; b += yb; c += yc; }
-    }
-    lds_barrier();                               // earlier readers of sh / l_wsum are done
-    if (lane == 63) { l_wsum[0][wv] = a; l_wsum[1][wv] = b; l_wsum[2][wv] = c; }
-    lds_barrier();
-    for (int w = 0; w < wv; ++w) { a += l_wsum[0][w]; b += l_wsum[1][w]; c += l_wsum[2][w]; }
-    sh[0][t] = a; sh[1][t] = b; sh[2][t] = c;
-    lds_barrier();
-  };
-  auto nch_of = [&](int s) {
-    const int npg = (l_len[s] + kPageTokens - 1) / kPageTokens;
-    return l_cnt[s] > 0 ? (npg + chunk_pages - 1) / chunk_pages : 0;
-  };
+  const int per = (S + 1023) >> 10;
+  const int s0 = min(S, t * per), s1 = min(S, s0 + per);
+  const int pb = (B + 1023) >> 10;
+  const int b0 = min(B, t * pb), b1 = min(B, b0 + pb);
+  auto npg_of = [&](int s) { return (l_len[s] + kPageTokens - 1) / kPageTokens; };
+  // chunks of a segment on some path (its count is positive)
+  auto nch_len = [&](int s) { return (npg_of(s) + chunk_pages - 1) / chunk_pages; };
   auto nrb_of = [&](int s) {
     return (int)(((int64_t)l_cnt[s] * group + kRowsPerBlock - 1) / kRowsPerBlock);
   };
+  // Inclusive block scan of three ints (wave scans, then the totals of the waves before);
+  // returns the inclusive values and, in tot, the block totals.
+  auto block_scan3 = [&](int (&v)[3], int (*ws)[16], int (&tot)[3]) {
+#pragma unroll
+    for (int k = 0; k < 3; ++k) v[k] = wave_scan_incl(v[k]);
+    if (lane == 63) {
+#pragma unroll
+      for (int k = 0; k < 3; ++k) ws[k][wv] = v[k];
+    }
+    lds_barrier();
+#pragma unroll
+    for (int k = 0; k < 3; ++k) tot[k] = 0;
+    for (int w = 0; w < 16; ++w) {
+#pragma unroll
+      for (int k = 0; k < 3; ++k) {
+        const int x = ws[k][w];
+        if (w < wv) v[k] += x;
+        tot[k] += x;
+      }
+    }
+  };
 
-  // 0. Read the graph once (all loads issued before any is used).
+  // 0. Read the graph (all loads issued before any is used); clear the counts and the sort's
+  //    bins.
   {
-    int vs[EP], vp[BP + 1], vl[SPT];
+    int vs[kSmallEntries / 1024], vp[kSmallBranches / 1024], vl[SPT];
 #pragma unroll
-    for (int u = 0; u < EP; ++u) vs[u] = t + 1024 * u < E ? g.path_segs[t + 1024 * u] : 0;
+    for (int u = 0; u < kSmallEntries / 1024; ++u)
+      vs[u] = t + 1024 * u < E ? g.path_segs[t + 1024 * u] : 0;
 #pragma unroll
-    for (int u = 0; u <= BP; ++u) vp[u] = t + 1024 * u <= B ? (int)g.path_off[t + 1024 * u] : 0;
+    for (int u = 0; u < kSmallBranches / 1024; ++u)
+      vp[u] = t + 1024 * u <= B ? (int)g.path_off[t + 1024 * u] : 0;
 #pragma unroll
     for (int u = 0; u < SPT; ++u) vl[u] = t + 1024 * u < S ? g.seg_len[t + 1024 * u] : 0;
 #pragma unroll
-    for (int u = 0; u < EP; ++u) if (t + 1024 * u < E) l_segs[t + 1024 * u] = vs[u];
+    for (int u = 0; u < kSmallEntries / 1024; ++u)
+      if (t + 1024 * u < E) l_segs[t + 1024 * u] = (unsigned short)vs[u];
 #pragma unroll
-    for (int u = 0; u <= BP; ++u) if (t + 1024 * u <= B && t + 1024 * u < kSmallBranches) l_poff[t + 1024 * u] = vp[u];
+    for (int u = 0; u < kSmallBranches / 1024; ++u)
+      if (t + 1024 * u <= B) l_poff[t + 1024 * u] = (unsigned short)vp[u];
 #pragma unroll
     for (int u = 0; u < SPT; ++u)
       if (t + 1024 * u < S) { l_len[t + 1024 * u] = vl[u]; l_cnt[t + 1024 * u] = 0; }
+    for (int i = t; i < 4 * 16 * NBK; i += 1024) l_cw[i] = 0;
   }
   if (t < 4) sc.counters[t] = 0;
   lds_barrier();
 
-  // 1. |B(s)|.
+  // 1. |B(s)|, and the chunks of the entries of this thread's branches (one partial row per
+  //    chunk in each branch's list).
   for (int e = t; e < E; e += 1024) atomicAdd(&l_cnt[l_segs[e]], 1);
+  int ne = 0;
+  for (int e = l_poff[b0]; e < l_poff[b1]; ++e) ne += nch_len(l_segs[e]);
   lds_barrier();
 
-  // 2. Group and partial-row offsets in segment order (each thread owns <= 4 segments), and
-  //    the sort keys.
-  const int per = (S + 1023) / 1024;
-  const int s0 = min(S, t * per), s1 = min(S, s0 + per);
+  // 2. One scan in segment order (group offsets, partial-row offsets) and over this thread's
+  //    branches (each branch's first slot in the partial lists); per-segment outputs; the
+  //    sort's class counts.
+  int slot0;
   {
-    int a = 0, c = 0;
+    int v[3] = {0, ne, 0}, tot[3];
     for (int s = s0; s < s1; ++s) {
-      a += l_cnt[s];
-      c += nch_of(s) * l_cnt[s];
+      const int cnt = l_cnt[s];
+      v[0] += cnt;
+      v[2] += cnt > 0 ? nch_len(s) * cnt : 0;
     }
-    block_scan(a, 0, c);
-    int ra = t ? sh[0][t - 1] : 0, rc = t ? sh[2][t - 1] : 0;
+    const int own0 = v[0], own2 = v[2];
+    block_scan3(v, l_wsum[0], tot);
+    int ra = v[0] - own0, rc = v[2] - own2;
+    slot0 = v[1] - ne;
 #pragma unroll
     for (int u = 0; u < SPT; ++u) {
       const int s = s0 + u;
       if (s < s1) {
-        const int cnt = l_cnt[s], nch = nch_of(s);
-        const int npg = (l_len[s] + kPageTokens - 1) / kPageTokens;
-        l_goff[s] = ra;
+        const int cnt = l_cnt[s];
+        const int nch = cnt > 0 ? nch_len(s) : 0;
+        l_cur[s] = ra;
         sc.grp_cnt[s] = cnt;
         sc.grp_off[s] = ra;
         sc.seg_prow_off[s] = rc;
         sc.seg_nchunk[s] = nch;
-        const uint32_t cost = cnt > 0 ? item_cost(npg, cnt, group, chunk_pages) : 0u;
-        l_key[s] = ((uint32_t)(kCostClasses - 1 - cost_class(cost)) << 16) | (uint32_t)s;
         ra += cnt;
         rc += nch * cnt;
       }
     }
     if (t == 1023) {
-      sc.grp_off[S] = sh[0][1023];
-      sc.seg_prow_off[S] = sh[2][1023];
-      sc.counters[1] = sh[2][1023];
+      sc.grp_off[S] = tot[0];
+      sc.seg_prow_off[S] = tot[2];
+      sc.counters[1] = tot[2];
+      sc.bpart_off[B] = tot[1];
     }
   }
-  lds_barrier();
-
-  // 3. Work-list order: a stable counting sort of the segments by cost bucket (l_key >> 16,
-  //    bucket 0 = largest class), ties by segment id.  Segments are taken in slots of 1024
-  //    (s = 1024 u + t), so id order is slot-major, then wave, then lane.  Lanes of a wave with
-  //    equal buckets are matched with five bit ballots; the per-(slot, wave) bucket counts are
-  //    prefix-summed per bucket by one wave each.
+  // Work-list order: a stable counting sort of the segments by class (bin 0 = the costliest),
+  // ties by segment id.  Segment 1024 u + t sits in slot u; lanes of a wave in the same bin are
+  // matched by five bit ballots, and each first lane of a bin records the count.
+  int bk[SPT], wr[SPT];
+  const int nslots = (S + 1023) >> 10;
   {
-    constexpr int NBK = kCostClasses;
-    const int lane = t & 63, wv = t >> 6;
     const uint64_t lt = lane ? (~0ull >> (64 - lane)) : 0ull;
-    const int nslots = (S + 1023) >> 10;         // <= kSmallSegs / 1024
-    int* cw = &sh[0][0];                         // [(slot * 16 + wave) * NBK + bucket]
-    int* tot = &sh[2][0];                        // [bucket] totals, then [NBK + bucket] offsets
-    for (int i = t; i < 2048; i += 1024) cw[i] = 0;
-    lds_barrier();
-    int bk[SPT], wr[SPT];
 #pragma unroll
     for (int u = 0; u < SPT; ++u) {
       bk[u] = 0;
@@ -497,123 +520,114 @@ __global__ __launch_bounds__(1024) void k_sched_small(DevGraph g, DevSchedule sc
       if (u < nslots) {
         const int sg = 1024 * u + t;
         const bool valid = sg < S;
-        const int bucket = valid ? (int)(l_key[sg] >> 16) : 0;
+        int bin = 0;
+        if (valid) {
+          const int cnt = l_cnt[sg];
+          const uint32_t cost = cnt > 0 ? item_cost(npg_of(sg), cnt, group, chunk_pages) : 0u;
+          bin = NBK - 1 - cost_class(cost);
+        }
         uint64_t m = __ballot(valid);
 #pragma unroll
         for (int bit = 0; bit < 5; ++bit) {
-          const bool on = (bucket >> bit) & 1;
+          const bool on = (bin >> bit) & 1;
           const uint64_t bb = __ballot(valid && on);
           m &= on ? bb : ~bb;
         }
-        bk[u] = bucket;
+        bk[u] = bin;
         wr[u] = __popcll(m & lt);
-        if (valid && (m & lt) == 0) cw[(u * 16 + wv) * NBK + bucket] = __popcll(m);
+        if (valid && (m & lt) == 0) l_cw[(u * 16 + wv) * NBK + bin] = __popcll(m);
       }
-    }
-    lds_barrier();
-    // Exclusive prefix over the (slot, wave) pairs of each bucket: wave wv owns buckets wv and
-    // wv + 16, lane = pair index.
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int c = wv + 16 * h;
-      const int v = cw[lane * NBK + c];
-      int x = v;
-#pragma unroll
-      for (int off = 1; off < 64; off <<= 1) {
-        const int y = __shfl_up(x, off);
-        if (lane >= off) x += y;
-      }
-      cw[lane * NBK + c] = x - v;
-      if (lane == 63) tot[c] = x;
-    }
-    lds_barrier();
-    if (t < 64) {                                // bucket offsets: exclusive scan of the totals
-      const int v = t < NBK ? tot[t] : 0;
-      int x = v;
-#pragma unroll
-      for (int off = 1; off < 64; off <<= 1) {
-        const int y = __shfl_up(x, off);
-        if (t >= off) x += y;
-      }
-      if (t < NBK) tot[NBK + t] = x - v;
-    }
-    lds_barrier();
-#pragma unroll
-    for (int u = 0; u < SPT; ++u) {
-      const int sg = 1024 * u + t;
-      if (u < nslots && sg < S) l_tmp[tot[NBK + bk[u]] + cw[(u * 16 + wv) * NBK + bk[u]] + wr[u]] = sg;
     }
   }
-  lds_barrier();
-  // 4. Item offsets in work-list order (each thread owns <= 4 positions); the items themselves
-  //    are written by k_emit.
-  {
-    int b = 0;
-    for (int i = s0; i < s1; ++i) b += nch_of(l_tmp[i]) * nrb_of(l_tmp[i]);
-    block_scan(0, b, 0);                         // (also publishes the partial-row offsets)
-    int w = t ? sh[1][t - 1] : 0;
+  lds_barrier();                                   // cursors and class counts are complete
+
+  // 3. Scatter each branch into its groups (arrival order); exclusive prefix of each class's
+  //    counts over the (slot, wave) pairs (wave wv takes classes wv and wv + 16, lane = pair).
+  for (int b = b0; b < b1; ++b)
+    for (int e = l_poff[b]; e < l_poff[b + 1]; ++e)
+      l_tmp[atomicAdd(&l_cur[l_segs[e]], 1)] = (unsigned short)b;
 #pragma unroll
-    for (int u = 0; u < SPT; ++u) {
-      if (s0 + u >= s1) break;
-      const int s = l_tmp[s0 + u];
-      sc.seg_item_off[s] = w;
-      sc.seg_order[s0 + u] = s;
-      sc.order_item_off[s0 + u] = w;
-      w += nch_of(s) * nrb_of(s);
-    }
-    if (t == 1023) {
-      sc.seg_item_off[S] = sh[1][1023];
-      sc.order_item_off[S] = sh[1][1023];
-      sc.counters[0] = sh[1][1023];
-    }
+  for (int h = 0; h < 2; ++h) {
+    const int c = wv + 16 * h;
+    const int v = l_cw[lane * NBK + c];
+    const int x = wave_scan_incl(v);
+    l_cw[lane * NBK + c] = x - v;
+    if (lane == 63) l_boff[c] = x;                 // class total, made an offset below
   }
   lds_barrier();
 
-  // 5. Scatter branches into their groups (arrival order; the group offsets serve as cursors).
-  for (int bb = t; bb < B; bb += 1024)
-    for (int e = l_poff[bb]; e < l_poff[bb + 1]; ++e) {
-      const int s = l_segs[e];
-      l_tmp[atomicAdd(&l_goff[s], 1)] = bb;
+  // 4. Per path entry of this thread's branches (a contiguous run of entries): its branch and
+  //    its first slot in the branch's partial list, and each branch's first slot; B(s) in
+  //    arrival order.  Ranks, groups in ascending order and the lists are written by k_emit.
+  //    Wave 0 turns the class totals into offsets.
+  {
+    int slot = slot0;
+    for (int b = b0; b < b1; ++b) {
+      sc.bpart_off[b] = slot;
+      for (int e = l_poff[b]; e < l_poff[b + 1]; ++e) {
+        sc.entry_branch[e] = b;
+        sc.entry_part[e] = slot;
+        slot += nch_len(l_segs[e]);
+      }
     }
-  // 6. Each entry's branch and its slot in the branch partial lists (exclusive scan of chunk
-  //    counts over entries; each thread owns a contiguous run of branches).  The ranks, the
-  //    ascending groups and the lists themselves are written by k_emit.
-  const int pb = (B + 1023) / 1024;
-  const int b0 = min(B, t * pb), b1 = min(B, b0 + pb);
-  int ne = 0;
-  for (int e = l_poff[b0]; e < l_poff[b1]; ++e) ne += nch_of(l_segs[e]);
-  block_scan(ne, 0, 0);                          // (also orders the scatter before the copy)
-  int slot = t ? sh[0][t - 1] : 0;
-  // Per-entry results go to LDS first (the entry's own slot of l_segs, which only this thread
-  // reads, and l_aux), then out in one coalesced pass.
-  for (int bb = b0; bb < b1; ++bb) {
-    sc.bpart_off[bb] = slot;
-    for (int e = l_poff[bb]; e < l_poff[bb + 1]; ++e) {
-      const int nch = nch_of(l_segs[e]);
-      l_segs[e] = bb;
-      l_aux[e] = slot;
-      slot += nch;
-    }
+    for (int e = t; e < E; e += 1024) sc.grp_tmp[e] = l_tmp[e];
   }
-  if (t == 1023) sc.bpart_off[B] = sh[0][1023];
+  if (wv == 0) {
+    const int v = lane < NBK ? l_boff[lane] : 0;
+    const int x = wave_scan_incl(v);
+    if (lane < NBK) l_boff[lane] = x - v;
+  }
   lds_barrier();
-  for (int i = t; i < E; i += 1024) {
-    sc.entry_branch[i] = l_segs[i];
-    sc.entry_part[i] = l_aux[i];
-    sc.grp_tmp[i] = l_tmp[i];
+
+  // 5. Place each segment at its work-list position.
+#pragma unroll
+  for (int u = 0; u < SPT; ++u) {
+    const int sg = 1024 * u + t;
+    if (u < nslots && sg < S) l_order[l_boff[bk[u]] + l_cw[(u * 16 + wv) * NBK + bk[u]] + wr[u]] = sg;
+  }
+  lds_barrier();
+
+  // 6. Item offsets in work-list order (this thread's positions s0 .. s1).
+  {
+    int v[3] = {0, 0, 0}, tot[3];
+    for (int i = s0; i < s1; ++i) {
+      const int s = l_order[i];
+      v[0] += l_cnt[s] > 0 ? nch_len(s) * nrb_of(s) : 0;
+    }
+    const int own = v[0];
+    block_scan3(v, l_wsum[1], tot);
+    int w = v[0] - own;
+#pragma unroll
+    for (int u = 0; u < SPT; ++u) {
+      const int i = s0 + u;
+      if (i < s1) {
+        const int s = l_order[i];
+        sc.seg_item_off[s] = w;
+        sc.seg_order[i] = s;
+        sc.order_item_off[i] = w;
+        w += l_cnt[s] > 0 ? nch_len(s) * nrb_of(s) : 0;
+      }
+    }
+    if (t == 1023) {
+      sc.seg_item_off[S] = tot[0];
+      sc.order_item_off[S] = tot[0];
+      sc.counters[0] = tot[0];
+    }
   }
 }
 
 // Outputs of the single-workgroup scheduler that are independent per path entry and per item,
-// written in parallel with coalesced stores.
+// written in parallel.
 //   Blocks [0, eblocks), one thread per path entry (b, s): the rank r of b inside B(s) (count
-//   of smaller branch ids), B(s) in ascending order, the entry's rank, its partial rows (one per
-//   chunk of s, in chunk order) and b's place in the branch list of every descriptor whose row
-//   block holds b's rows.
-//   Later blocks, one wave per work item: the item (found by binary search over the item
-//   offsets in work-list order), the head of its descriptor and the chunk's page ids.
-__global__ void k_emit(DevGraph g, DevSchedule sc, int32_t group, int32_t chunk_pages,
-                       int32_t eblocks) {
+//   of smaller branch ids in B(s) as scattered), B(s) in ascending order, the entry's rank, its
+//   partial rows (one per chunk of s, in chunk order) and b's place in the branch list of every
+//   descriptor whose row block holds b's rows.
+//   Later blocks, one wave per work item: the item's work-list position by a binary search of
+//   the item offsets (staged in LDS by each block), the item, the head of its descriptor and
+//   the chunk's page ids.
+__global__ __launch_bounds__(kT) void k_emit(DevGraph g, DevSchedule sc, int32_t group,
+                                             int32_t chunk_pages, int32_t eblocks) {
+  __shared__ int l_off[kSmallSegs + 1];
   if ((int)blockIdx.x < eblocks) {
     const int e = blockIdx.x * kT + threadIdx.x;
     if (e >= g.E) return;
@@ -644,16 +658,19 @@ __global__ void k_emit(DevGraph g, DevSchedule sc, int32_t group, int32_t chunk_
       }
     return;
   }
+  const int S = g.S;
+  for (int i = threadIdx.x; i <= S; i += kT) l_off[i] = (int)sc.order_item_off[i];
+  __syncthreads();
   const int64_t w = (int64_t)(blockIdx.x - eblocks) * (kT / 64) + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
-  if (w >= sc.counters[0]) return;
-  int lo = 0, hi = g.S;                          // order_item_off[lo] <= w < order_item_off[hi]
+  if (w >= l_off[S]) return;
+  int lo = 0, hi = S;                            // l_off[lo] <= w < l_off[hi]
   while (hi - lo > 1) {
     const int mid = (lo + hi) >> 1;
-    if (sc.order_item_off[mid] <= w) lo = mid; else hi = mid;
+    if (l_off[mid] <= w) lo = mid; else hi = mid;
   }
   const int s = sc.seg_order[lo];
-  const int kk = (int)(w - sc.order_item_off[lo]);
+  const int kk = (int)(w - l_off[lo]);
   const int cnt = sc.grp_cnt[s], len = g.seg_len[s];
   const int npg = (len + kPageTokens - 1) / kPageTokens;
   const int nrb = (cnt * group + kRowsPerBlock - 1) / kRowsPerBlock;
@@ -783,7 +800,7 @@ hipError_t launch_schedule(const DevGraph& g, const DevSchedule& sc, int32_t gro
                            int32_t chunk_pages, int64_t max_items, hipStream_t stream) {
   const int fill_blocks = (int)((max_items + kT / 64 - 1) / (kT / 64));
   if (g.S <= kSmallSegs && g.E <= kSmallEntries && g.B < kSmallBranches) {
-    hipLaunchKernelGGL(k_sched_small, dim3(1), dim3(1024), 0, stream, g, sc, group, chunk_pages);
+    hipLaunchKernelGGL(k_sched_one, dim3(1), dim3(1024), 0, stream, g, sc, group, chunk_pages);
     const int eblocks = blocks(g.E);
     if (eblocks + fill_blocks > 0)
       hipLaunchKernelGGL(k_emit, dim3(eblocks + fill_blocks), dim3(kT), 0, stream, g, sc, group,

@@ -319,7 +319,7 @@ void size_schedule(const ga_segment_table* st, const ga_branch_paths* bp, const 
   for (int64_t e = 0; e < z->E; ++e) used[bp->path_segs[e]] = 1;
   int64_t ref_pages = 0;
   for (int32_t s = 0; s < z->S; ++s) ref_pages += used[s] ? npg[s] : 0;
-  const int64_t target_items = 4LL * num_cus * 2;   // ~4 work items per resident workgroup
+  const int64_t target_items = 8LL * num_cus * 2;   // ~8 work items per resident workgroup
   int64_t cap = (ref_pages * p->num_kv_heads + target_items - 1) / target_items;
   if (cap < 16) cap = 16;
   if (cap > ga::kMaxChunkPages) cap = ga::kMaxChunkPages;

@@ -382,11 +382,11 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
     c_rest[i] = kv * C::KVB + ((pc ^ (tok & (C::CPR - 1))) << 4);
   }
 
-  // The first unit: claimed and its descriptor copied before the loop.
+  // The first unit of workgroup i is unit i, taken without a claim (the whole grid claiming at
+  // once serialises on the counter for several microseconds); its descriptor is copied before
+  // the loop.  Later units are claimed through the counter, which counts claims past the grid.
   if (wave == 0) {
-    int v = 0;
-    if (lane == 0) v = atomicAdd(reinterpret_cast<int*>(&a.counters[2]), 1);
-    fetch_desc(__builtin_amdgcn_readfirstlane(v), 0);
+    fetch_desc((int)blockIdx.x, 0);
     wait_vmcnt(0);
   }
   __syncthreads();
@@ -513,7 +513,8 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
       QOp<BF16> qop[NT][C::QR];
       load_q(qop);
       int claim = 0;
-      if (wave == 0 && lane == 0) claim = atomicAdd(reinterpret_cast<int*>(&a.counters[2]), 1);
+      if (wave == 0 && lane == 0)
+        claim = (int)gridDim.x + atomicAdd(reinterpret_cast<int*>(&a.counters[2]), 1);
       wait_vmcnt(0);
       // Wave 0 fetches the next unit's descriptor while this one streams.
       if (wave == 0) fetch_desc(__builtin_amdgcn_readfirstlane(claim), b ^ 1);

@@ -91,10 +91,13 @@ __device__ __forceinline__ void dma16_cached(unsigned off, const void* base, uns
 // Partial-row stores with device scope (sc1): the L2 writes them through to the memory side at
 // once instead of holding them dirty and writing them back later, in the middle of the K/V read
 // stream.  (Same bytes; the merged-DAG attention measured 376 -> 370.5 us.)
+// A store of more than 64 bits reads its data registers one cycle after issue, and the
+// compiler's hazard checks do not look inside inline assembly: the 16-byte store carries its own
+// wait states, or the next instruction may overwrite the data before it is read.
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ void store_dev16(f16x8* p, f16x8 v) {
-  asm volatile("global_store_dwordx4 %0, %1, off sc1" :: "v"(p), "v"(v) : "memory");
+  asm volatile("global_store_dwordx4 %0, %1, off sc1\n\ts_nop 1" :: "v"(p), "v"(v) : "memory");
 }
 __device__ __forceinline__ void store_dev8(f32x2* p, f32x2 v) {
   asm volatile("global_store_dwordx2 %0, %1, off sc1" :: "v"(p), "v"(v) : "memory");
@@ -513,11 +516,13 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
       QOp<BF16> qop[NT][C::QR];
       load_q(qop);
       int claim = 0;
-      if (wave == 0 && lane == 0)
-        claim = (int)gridDim.x + atomicAdd(reinterpret_cast<int*>(&a.counters[2]), 1);
+      if (wave == 0 && lane == 0) claim = atomicAdd(reinterpret_cast<int*>(&a.counters[2]), 1);
       wait_vmcnt(0);
+      // (the claim is consumed only here, after the wait, so that no use of it before the wait
+      // makes the compiler wait for it, and with it for every copy in flight)
+      asm volatile("" : "+v"(claim));
       // Wave 0 fetches the next unit's descriptor while this one streams.
-      if (wave == 0) fetch_desc(__builtin_amdgcn_readfirstlane(claim), b ^ 1);
+      if (wave == 0) fetch_desc((int)gridDim.x + __builtin_amdgcn_readfirstlane(claim), b ^ 1);
       for (int st = 0; st < nst; ++st) {
         // Wait until this wave's copies of stage st have landed (copies of later stages may stay
         // in flight), then make every wave's copies visible.

@@ -65,6 +65,21 @@ def test_kernels_do_not_spill(asm):
     assert found == 8
 
 
+def test_wide_inline_stores_are_followed_by_wait_states(asm):
+    """A global store of more than 64 bits reads its data VGPRs a cycle after issue; the
+    compiler's hazard recognizer does not see stores written as inline assembly, so each of
+    them must carry its own s_nop (a VALU write of the data registers right after such a store
+    has corrupted stored partial rows)."""
+    found = 0
+    for name, body in _kernels(asm).items():
+        lines = [l.strip() for l in body.splitlines() if l.strip() and not l.strip().startswith(";")]
+        for i, l in enumerate(lines):
+            if re.match(r"global_store_dwordx[34] .*\bsc1\b", l):
+                assert lines[i + 1].startswith("s_nop"), (name, l, lines[i + 1])
+                found += 1
+    assert found > 0
+
+
 def test_no_compiler_vector_memory_waits_in_the_compute(asm):
     for name, body in _kernels(asm).items():
         mixed = [w for w in re.findall(r"s_waitcnt vmcnt\((\d+)\)(?: expcnt\(\d+\))? lgkmcnt\((\d+)\)", body)

@@ -89,8 +89,8 @@ struct AttnArgs {
   const void* q;
   const void* pool;
   const int32_t* desc;     // work-item descriptors (layout above)
-  int64_t* counters;       // [0] items, [2] work-queue head (units claimed past the grid, as
-                           //     int32: workgroup i starts with unit i)
+  int64_t* counters;       // [0] items, [2] work-queue head (units claimed past the first two
+                           //     grids, as int32: workgroup i starts with units i and i + grid)
   void* po;                // partial outputs (format above)
   float* plse;             // partial log-sum-exps (format above)
   int32_t Hq, Hkv, group, chunk_pages;

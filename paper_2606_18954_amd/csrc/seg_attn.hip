@@ -385,15 +385,18 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
     c_rest[i] = kv * C::KVB + ((pc ^ (tok & (C::CPR - 1))) << 4);
   }
 
-  // The first unit of workgroup i is unit i, taken without a claim (the whole grid claiming at
-  // once serialises on the counter for several microseconds); its descriptor is copied before
-  // the loop.  Later units are claimed through the counter, which counts claims past the grid.
+  // The first two units of workgroup i are units i and i + grid, taken without a claim: the
+  // whole grid claiming at once serialises on the counter for several microseconds, and the
+  // first claim then comes during the second unit, when the workgroups are out of step.  The
+  // first unit's descriptor is copied before the loop.  Later units are claimed through the
+  // counter, which counts claims past the first two grids of units.
   if (wave == 0) {
     fetch_desc((int)blockIdx.x, 0);
     wait_vmcnt(0);
   }
   __syncthreads();
 
+  bool first = true;                       // the first unit (its successor needs no claim)
   for (int b = 0;; b ^= 1) {
     // Unit fields from its descriptor (the scheduler's record, then the chunk's page words and
     // the row block's branch ids; each page word carries the page's valid tokens).
@@ -516,13 +519,18 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
       QOp<BF16> qop[NT][C::QR];
       load_q(qop);
       int claim = 0;
-      if (wave == 0 && lane == 0) claim = atomicAdd(reinterpret_cast<int*>(&a.counters[2]), 1);
+      if (!first && wave == 0 && lane == 0)
+        claim = atomicAdd(reinterpret_cast<int*>(&a.counters[2]), 1);
       wait_vmcnt(0);
       // (the claim is consumed only here, after the wait, so that no use of it before the wait
       // makes the compiler wait for it, and with it for every copy in flight)
       asm volatile("" : "+v"(claim));
       // Wave 0 fetches the next unit's descriptor while this one streams.
-      if (wave == 0) fetch_desc((int)gridDim.x + __builtin_amdgcn_readfirstlane(claim), b ^ 1);
+      if (wave == 0)
+        fetch_desc(first ? (int)blockIdx.x + (int)gridDim.x
+                         : 2 * (int)gridDim.x + __builtin_amdgcn_readfirstlane(claim),
+                   b ^ 1);
+      first = false;
       for (int st = 0; st < nst; ++st) {
         // Wait until this wave's copies of stage st have landed (copies of later stages may stay
         // in flight), then make every wave's copies visible.

@@ -101,6 +101,7 @@ struct ga_plan {
   size_t pin_bytes = 0;
   bool owns_memory = true;
   bool scheduled = false;
+  bool grouped = false;        // the groups of an earlier schedule are in the workspace
   bool causal = false;         // a multi-query plan (graphattn_plan_create_extend)
   int32_t B0 = 0;              // branches as given (z.B counts query rows)
   int num_cus = 256;
@@ -671,9 +672,14 @@ ga_status do_schedule(ga_plan* pl, hipStream_t stream) {
   const bool rec = pl->prof_sched < pl->prof_cap;
   if (rec) GA_HIP(hipEventRecord(pl->ev_sched[2 * pl->prof_sched], stream), "profile event");
   if (pl->z.B > 0 || pl->z.S > 0) {
+    // The groups (B(s), their order, the entry ranks) follow the paths alone, which a plan never
+    // changes, so after the first schedule only what the lengths decide is recomputed.
+    const bool reuse = pl->grouped;
+    pl->grouped = false;
     GA_HIP(ga::launch_schedule(pl->g, pl->sc, pl->p.num_q_heads / pl->p.num_kv_heads,
-                               pl->z.chunk_pages, pl->z.max_items, stream),
+                               pl->z.chunk_pages, pl->z.max_items, reuse, stream),
            "scheduler launch");
+    pl->grouped = true;
   }
   if (rec) {
     hipEvent_t e = pl->ev_sched[2 * pl->prof_sched + 1];

@@ -198,8 +198,12 @@ struct LengthArgs {
 };
 hipError_t launch_set_lengths(const LengthArgs& a, hipStream_t stream);
 
+// reuse: the groups (B(s), offsets, entry branches and ranks, ascending group lists) written by
+// an earlier schedule of the same plan are still in place (the single-workgroup path then skips
+// them; the multi-kernel path recomputes everything).
 hipError_t launch_schedule(const DevGraph& g, const DevSchedule& sc, int32_t group,
-                           int32_t chunk_pages, int64_t max_items, hipStream_t stream);
+                           int32_t chunk_pages, int64_t max_items, bool reuse,
+                           hipStream_t stream);
 hipError_t launch_seg_attn(const AttnArgs& a, int head_dim, bool bf16, bool causal, int grid,
                            hipStream_t stream);
 hipError_t launch_merge(const MergeArgs& a, int head_dim, bool out_bf16, bool part_f16,

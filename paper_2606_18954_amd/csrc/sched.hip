@@ -388,8 +388,11 @@ constexpr int kSmallSegs = 4096;
 constexpr int kSmallEntries = 8192;
 constexpr int kSmallBranches = 4096;
 
+// reuse: the plan's groups are already in place from an earlier schedule (B(s), |B(s)|, the
+// group offsets, each entry's branch and rank, each group's branches in ascending order: they
+// follow the paths alone, which a plan keeps); only what the lengths decide is recomputed.
 __global__ __launch_bounds__(1024) void k_sched_one(DevGraph g, DevSchedule sc, int32_t group,
-                                                    int32_t chunk_pages) {
+                                                    int32_t chunk_pages, int32_t reuse) {
   constexpr int NBK = kCostClasses;
   constexpr int SPT = kSmallSegs / 1024;
   __shared__ unsigned short l_segs[kSmallEntries];        // path_segs
@@ -456,7 +459,16 @@ __global__ __launch_bounds__(1024) void k_sched_one(DevGraph g, DevSchedule sc, 
       if (t + 1024 * u <= B) l_poff[t + 1024 * u] = (unsigned short)vp[u];
 #pragma unroll
     for (int u = 0; u < SPT; ++u)
-      if (t + 1024 * u < S) { l_len[t + 1024 * u] = vl[u]; l_cnt[t + 1024 * u] = 0; }
+      if (t + 1024 * u < S) l_len[t + 1024 * u] = vl[u];
+    if (reuse) {
+#pragma unroll
+      for (int u = 0; u < SPT; ++u)
+        if (t + 1024 * u < S) l_cnt[t + 1024 * u] = sc.grp_cnt[t + 1024 * u];
+    } else {
+#pragma unroll
+      for (int u = 0; u < SPT; ++u)
+        if (t + 1024 * u < S) l_cnt[t + 1024 * u] = 0;
+    }
     for (int i = t; i < 4 * 16 * NBK; i += 1024) l_cw[i] = 0;
   }
   if (t < 4) sc.counters[t] = 0;
@@ -464,7 +476,8 @@ __global__ __launch_bounds__(1024) void k_sched_one(DevGraph g, DevSchedule sc, 
 
   // 1. |B(s)|, and the chunks of the entries of this thread's branches (one partial row per
   //    chunk in each branch's list).
-  for (int e = t; e < E; e += 1024) atomicAdd(&l_cnt[l_segs[e]], 1);
+  if (!reuse)
+    for (int e = t; e < E; e += 1024) atomicAdd(&l_cnt[l_segs[e]], 1);
   int ne = 0;
   for (int e = l_poff[b0]; e < l_poff[b1]; ++e) ne += nch_len(l_segs[e]);
   lds_barrier();
@@ -490,9 +503,11 @@ __global__ __launch_bounds__(1024) void k_sched_one(DevGraph g, DevSchedule sc, 
       if (s < s1) {
         const int cnt = l_cnt[s];
         const int nch = cnt > 0 ? nch_len(s) : 0;
-        l_cur[s] = ra;
-        sc.grp_cnt[s] = cnt;
-        sc.grp_off[s] = ra;
+        if (!reuse) {
+          l_cur[s] = ra;
+          sc.grp_cnt[s] = cnt;
+          sc.grp_off[s] = ra;
+        }
         sc.seg_prow_off[s] = rc;
         sc.seg_nchunk[s] = nch;
         ra += cnt;
@@ -500,7 +515,7 @@ __global__ __launch_bounds__(1024) void k_sched_one(DevGraph g, DevSchedule sc, 
       }
     }
     if (t == 1023) {
-      sc.grp_off[S] = tot[0];
+      if (!reuse) sc.grp_off[S] = tot[0];
       sc.seg_prow_off[S] = tot[2];
       sc.counters[1] = tot[2];
       sc.bpart_off[B] = tot[1];
@@ -543,9 +558,10 @@ __global__ __launch_bounds__(1024) void k_sched_one(DevGraph g, DevSchedule sc, 
 
   // 3. Scatter each branch into its groups (arrival order); exclusive prefix of each class's
   //    counts over the (slot, wave) pairs (wave wv takes classes wv and wv + 16, lane = pair).
-  for (int b = b0; b < b1; ++b)
-    for (int e = l_poff[b]; e < l_poff[b + 1]; ++e)
-      l_tmp[atomicAdd(&l_cur[l_segs[e]], 1)] = (unsigned short)b;
+  if (!reuse)
+    for (int b = b0; b < b1; ++b)
+      for (int e = l_poff[b]; e < l_poff[b + 1]; ++e)
+        l_tmp[atomicAdd(&l_cur[l_segs[e]], 1)] = (unsigned short)b;
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
     const int c = wv + 16 * h;
@@ -565,12 +581,13 @@ __global__ __launch_bounds__(1024) void k_sched_one(DevGraph g, DevSchedule sc, 
     for (int b = b0; b < b1; ++b) {
       sc.bpart_off[b] = slot;
       for (int e = l_poff[b]; e < l_poff[b + 1]; ++e) {
-        sc.entry_branch[e] = b;
+        if (!reuse) sc.entry_branch[e] = b;
         sc.entry_part[e] = slot;
         slot += nch_len(l_segs[e]);
       }
     }
-    for (int e = t; e < E; e += 1024) sc.grp_tmp[e] = l_tmp[e];
+    if (!reuse)
+      for (int e = t; e < E; e += 1024) sc.grp_tmp[e] = l_tmp[e];
   }
   if (wv == 0) {
     const int v = lane < NBK ? l_boff[lane] : 0;
@@ -626,7 +643,7 @@ __global__ __launch_bounds__(1024) void k_sched_one(DevGraph g, DevSchedule sc, 
 //   the item offsets (staged in LDS by each block), the item, the head of its descriptor and
 //   the chunk's page ids.
 __global__ __launch_bounds__(kT) void k_emit(DevGraph g, DevSchedule sc, int32_t group,
-                                             int32_t chunk_pages, int32_t eblocks) {
+                                             int32_t chunk_pages, int32_t eblocks, int32_t reuse) {
   __shared__ int l_off[kSmallSegs + 1];
   if ((int)blockIdx.x < eblocks) {
     const int e = blockIdx.x * kT + threadIdx.x;
@@ -635,13 +652,18 @@ __global__ __launch_bounds__(kT) void k_emit(DevGraph g, DevSchedule sc, int32_t
     const int b = sc.entry_branch[e];
     const int off = (int)sc.grp_off[s];
     const int cnt = sc.grp_cnt[s];
-    int r = 0, k = 0;
-    for (; k + 4 <= cnt; k += 4)
-      r += (sc.grp_tmp[off + k] < b) + (sc.grp_tmp[off + k + 1] < b) +
-           (sc.grp_tmp[off + k + 2] < b) + (sc.grp_tmp[off + k + 3] < b);
-    for (; k < cnt; ++k) r += sc.grp_tmp[off + k] < b;
-    sc.grp_br[off + r] = b;
-    sc.entry_rank[e] = r;
+    int r = 0;
+    if (reuse) {
+      r = sc.entry_rank[e];
+    } else {
+      int k = 0;
+      for (; k + 4 <= cnt; k += 4)
+        r += (sc.grp_tmp[off + k] < b) + (sc.grp_tmp[off + k + 1] < b) +
+             (sc.grp_tmp[off + k + 2] < b) + (sc.grp_tmp[off + k + 3] < b);
+      for (; k < cnt; ++k) r += sc.grp_tmp[off + k] < b;
+      sc.grp_br[off + r] = b;
+      sc.entry_rank[e] = r;
+    }
     const int nch = sc.seg_nchunk[s];
     const int slot = (int)sc.entry_part[e];
     const int prow = (int)sc.seg_prow_off[s] + r;
@@ -797,14 +819,16 @@ hipError_t launch_set_lengths(const LengthArgs& a, hipStream_t stream) {
 }
 
 hipError_t launch_schedule(const DevGraph& g, const DevSchedule& sc, int32_t group,
-                           int32_t chunk_pages, int64_t max_items, hipStream_t stream) {
+                           int32_t chunk_pages, int64_t max_items, bool reuse,
+                           hipStream_t stream) {
   const int fill_blocks = (int)((max_items + kT / 64 - 1) / (kT / 64));
   if (g.S <= kSmallSegs && g.E <= kSmallEntries && g.B < kSmallBranches) {
-    hipLaunchKernelGGL(k_sched_one, dim3(1), dim3(1024), 0, stream, g, sc, group, chunk_pages);
+    hipLaunchKernelGGL(k_sched_one, dim3(1), dim3(1024), 0, stream, g, sc, group, chunk_pages,
+                       (int32_t)reuse);
     const int eblocks = blocks(g.E);
     if (eblocks + fill_blocks > 0)
       hipLaunchKernelGGL(k_emit, dim3(eblocks + fill_blocks), dim3(kT), 0, stream, g, sc, group,
-                         chunk_pages, eblocks);
+                         chunk_pages, eblocks, (int32_t)reuse);
     return hipGetLastError();
   }
   hipLaunchKernelGGL(k_init, dim3(blocks(g.S > 4 ? g.S : 4)), dim3(kT), 0, stream, g, sc);

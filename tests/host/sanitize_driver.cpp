@@ -14,7 +14,7 @@
 #include "ga_internal.hpp"
 
 namespace ga {
-hipError_t launch_schedule(const DevGraph&, const DevSchedule&, int32_t, int32_t, int64_t,
+hipError_t launch_schedule(const DevGraph&, const DevSchedule&, int32_t, int32_t, int64_t, bool,
                            hipStream_t) { std::abort(); }
 hipError_t launch_seg_attn(const AttnArgs&, int, bool, bool, int, hipStream_t) { std::abort(); }
 hipError_t launch_merge(const MergeArgs&, int, bool, bool, hipStream_t) { std::abort(); }

@@ -204,3 +204,32 @@ def test_decode_loop_append_grow_attend():
                 oo, ol = _oracle_decode(wl, cur, pb)
                 compare(f"decode loop step {k}", out.double().cpu().numpy(),
                         lse.double().cpu().numpy(), oo, ol)
+
+
+def test_rescheduled_plan_matches_its_first_schedule_bit_for_bit():
+    """After the first schedule a plan keeps its groups (B(s), the group lists, the entry ranks:
+    they follow the paths, which a plan never changes) and recomputes only what the lengths
+    decide.  Moving to other lengths (which reorders the work list) and back must give exactly
+    the first schedule's arrays, and the groups must not change in between."""
+    require_gpu()
+    wl = W.config3_merged_dag(prompts=6)
+    g = wl.graph
+    lens = np.asarray(g.seg_len, dtype=np.int32)
+    rng = np.random.default_rng(47)
+    with G.Plan(_host(g, lens), params_of(wl)) as plan:
+        plan.schedule()
+        first = plan.debug_dump()
+        for it in range(3):
+            other = np.array([int(rng.integers(1, int(n) + 1)) for n in lens], dtype=np.int32)
+            plan.set_lengths(other)
+            plan.schedule()
+            mid = plan.debug_dump()
+            for k in ("group_offsets", "group_branches", "entry_ranks"):
+                assert np.array_equal(mid[k], first[k]), (it, k)
+            assert not np.array_equal(mid["items"], first["items"]) or it > 0
+            plan.set_lengths(lens)
+            plan.schedule()
+            again = plan.debug_dump()
+            for k, v in first.items():
+                assert v.shape == again[k].shape and np.array_equal(v, again[k]), (it, k)
+    say(f"[case] merged DAG (6 prompts): {len(first['items'])} items, rescheduled 3 times")

@@ -398,7 +398,9 @@ __global__ __launch_bounds__(1024) void k_sched_one(DevGraph g, DevSchedule sc, 
   __shared__ unsigned short l_segs[kSmallEntries];        // path_segs
   __shared__ unsigned short l_tmp[kSmallEntries];         // B(s) in arrival order
   __shared__ unsigned short l_poff[kSmallBranches + 1];   // path_off
-  __shared__ int l_len[kSmallSegs];                       // segment lengths
+  __shared__ int l_npg[kSmallSegs];                       // pages in use per segment
+  __shared__ int l_nch[kSmallSegs];                       // chunks per segment
+  __shared__ int l_part[kSmallEntries];                   // each entry's first partial slot
   __shared__ int l_cnt[kSmallSegs];                       // |B(s)|
   __shared__ int l_cur[kSmallSegs];                       // scatter cursors, then work-list order
   __shared__ int l_cw[4 * 16 * NBK];                      // sort: counts per (slot, wave, class)
@@ -411,9 +413,9 @@ __global__ __launch_bounds__(1024) void k_sched_one(DevGraph g, DevSchedule sc, 
   const int s0 = min(S, t * per), s1 = min(S, s0 + per);
   const int pb = (B + 1023) >> 10;
   const int b0 = min(B, t * pb), b1 = min(B, b0 + pb);
-  auto npg_of = [&](int s) { return (l_len[s] + kPageTokens - 1) / kPageTokens; };
-  // chunks of a segment on some path (its count is positive)
-  auto nch_len = [&](int s) { return (npg_of(s) + chunk_pages - 1) / chunk_pages; };
+  // pages in use and chunks of a segment on some path (its count is positive), computed once
+  auto npg_of = [&](int s) { return l_npg[s]; };
+  auto nch_len = [&](int s) { return l_nch[s]; };
   auto nrb_of = [&](int s) {
     return (int)(((int64_t)l_cnt[s] * group + kRowsPerBlock - 1) / kRowsPerBlock);
   };
@@ -459,7 +461,11 @@ __global__ __launch_bounds__(1024) void k_sched_one(DevGraph g, DevSchedule sc, 
       if (t + 1024 * u <= B) l_poff[t + 1024 * u] = (unsigned short)vp[u];
 #pragma unroll
     for (int u = 0; u < SPT; ++u)
-      if (t + 1024 * u < S) l_len[t + 1024 * u] = vl[u];
+      if (t + 1024 * u < S) {
+        const int npg = (vl[u] + kPageTokens - 1) / kPageTokens;
+        l_npg[t + 1024 * u] = npg;
+        l_nch[t + 1024 * u] = (npg + chunk_pages - 1) / chunk_pages;
+      }
     if (reuse) {
 #pragma unroll
       for (int u = 0; u < SPT; ++u)
@@ -582,7 +588,7 @@ __global__ __launch_bounds__(1024) void k_sched_one(DevGraph g, DevSchedule sc, 
       sc.bpart_off[b] = slot;
       for (int e = l_poff[b]; e < l_poff[b + 1]; ++e) {
         if (!reuse) sc.entry_branch[e] = b;
-        sc.entry_part[e] = slot;
+        l_part[e] = slot;                          // (written out coalesced after the barrier)
         slot += nch_len(l_segs[e]);
       }
     }
@@ -596,7 +602,8 @@ __global__ __launch_bounds__(1024) void k_sched_one(DevGraph g, DevSchedule sc, 
   }
   lds_barrier();
 
-  // 5. Place each segment at its work-list position.
+  // 5. Place each segment at its work-list position; the entries' first partial slots.
+  for (int e = t; e < E; e += 1024) sc.entry_part[e] = l_part[e];
 #pragma unroll
   for (int u = 0; u < SPT; ++u) {
     const int sg = 1024 * u + t;

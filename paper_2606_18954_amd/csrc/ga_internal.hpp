@@ -198,9 +198,9 @@ struct LengthArgs {
 };
 hipError_t launch_set_lengths(const LengthArgs& a, hipStream_t stream);
 
-// reuse: the groups (B(s), offsets, entry branches and ranks, ascending group lists) written by
-// an earlier schedule of the same plan are still in place (the single-workgroup path then skips
-// them; the multi-kernel path recomputes everything).
+// reuse: the groups (B(s), |B(s)|, entry branches and ranks, ascending group lists) written by
+// an earlier schedule of the same plan are still in place, and only what the lengths decide is
+// recomputed.
 hipError_t launch_schedule(const DevGraph& g, const DevSchedule& sc, int32_t group,
                            int32_t chunk_pages, int64_t max_items, bool reuse,
                            hipStream_t stream);

@@ -30,9 +30,9 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("" ::: "memory");
 }
 
-__global__ void k_init(DevGraph g, DevSchedule sc) {
+__global__ void k_init(DevGraph g, DevSchedule sc, int32_t reuse) {
   int s = blockIdx.x * kT + threadIdx.x;
-  if (s < g.S) {
+  if (s < g.S && !reuse) {
     sc.grp_cnt[s] = 0;
     sc.grp_fill[s] = 0;
   }
@@ -728,9 +728,13 @@ __global__ void k_scatter(DevGraph g, DevSchedule sc) {
 
 // Rank of each entry's branch inside B(s) (branch ids within a group are distinct because a
 // path visits a segment at most once), placement into ascending order, and the work items.
-__global__ void k_rank_items(DevGraph g, DevSchedule sc, int32_t group, int32_t chunk_pages) {
+__global__ void k_rank_items(DevGraph g, DevSchedule sc, int32_t group, int32_t chunk_pages,
+                             int32_t reuse) {
   int i = blockIdx.x * kT + threadIdx.x;
-  if (i < g.E) {
+  if (i < g.E && reuse) {
+    const int s = g.path_segs[i];
+    write_entry_parts(g, sc, i, sc.entry_rank[i], sc.grp_cnt[s]);
+  } else if (i < g.E) {
     const int s = g.path_segs[i];
     const int b = sc.entry_branch[i];
     const int64_t off = sc.grp_off[s];
@@ -838,8 +842,10 @@ hipError_t launch_schedule(const DevGraph& g, const DevSchedule& sc, int32_t gro
                          chunk_pages, eblocks, (int32_t)reuse);
     return hipGetLastError();
   }
-  hipLaunchKernelGGL(k_init, dim3(blocks(g.S > 4 ? g.S : 4)), dim3(kT), 0, stream, g, sc);
-  if (g.E > 0)
+  // (with reuse, the entry branches, |B(s)| and the groups in arrival order are not rebuilt)
+  hipLaunchKernelGGL(k_init, dim3(blocks(g.S > 4 ? g.S : 4)), dim3(kT), 0, stream, g, sc,
+                     (int32_t)reuse);
+  if (g.E > 0 && !reuse)
     hipLaunchKernelGGL(k_count, dim3(blocks(g.E)), dim3(kT), 0, stream, g, sc);
   hipLaunchKernelGGL(k_scan, dim3(1), dim3(1024), 0, stream, g, sc, group, chunk_pages);
   const int64_t sblocks = ((int64_t)g.E + kScanBlock - 1) / kScanBlock;
@@ -848,12 +854,12 @@ hipError_t launch_schedule(const DevGraph& g, const DevSchedule& sc, int32_t gro
     hipLaunchKernelGGL(k_entry_scan, dim3((unsigned)sblocks), dim3(kScanBlock), 0, stream, g, sc);
   }
   hipLaunchKernelGGL(k_bpart_off, dim3(blocks((int64_t)g.B + 1)), dim3(kT), 0, stream, g, sc);
-  if (g.E > 0)
+  if (g.E > 0 && !reuse)
     hipLaunchKernelGGL(k_scatter, dim3(blocks(g.E)), dim3(kT), 0, stream, g, sc);
   const int64_t n = g.E > g.S ? g.E : g.S;
   if (n > 0)
     hipLaunchKernelGGL(k_rank_items, dim3(blocks(n)), dim3(kT), 0, stream, g, sc, group,
-                       chunk_pages);
+                       chunk_pages, (int32_t)reuse);
   if (fill_blocks > 0)
     hipLaunchKernelGGL(k_fill_desc, dim3(fill_blocks), dim3(kT), 0, stream, g, sc, group,
                        chunk_pages);

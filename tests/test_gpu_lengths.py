@@ -206,16 +206,10 @@ def test_decode_loop_append_grow_attend():
                         lse.double().cpu().numpy(), oo, ol)
 
 
-def test_rescheduled_plan_matches_its_first_schedule_bit_for_bit():
-    """After the first schedule a plan keeps its groups (B(s), the group lists, the entry ranks:
-    they follow the paths, which a plan never changes) and recomputes only what the lengths
-    decide.  Moving to other lengths (which reorders the work list) and back must give exactly
-    the first schedule's arrays, and the groups must not change in between."""
-    require_gpu()
-    wl = W.config3_merged_dag(prompts=6)
+def _reschedule_round_trip(wl, seed):
     g = wl.graph
     lens = np.asarray(g.seg_len, dtype=np.int32)
-    rng = np.random.default_rng(47)
+    rng = np.random.default_rng(seed)
     with G.Plan(_host(g, lens), params_of(wl)) as plan:
         plan.schedule()
         first = plan.debug_dump()
@@ -226,10 +220,26 @@ def test_rescheduled_plan_matches_its_first_schedule_bit_for_bit():
             mid = plan.debug_dump()
             for k in ("group_offsets", "group_branches", "entry_ranks"):
                 assert np.array_equal(mid[k], first[k]), (it, k)
-            assert not np.array_equal(mid["items"], first["items"]) or it > 0
+            if it == 0:
+                assert not np.array_equal(mid["branch_part_offsets"], first["branch_part_offsets"]) \
+                    or not np.array_equal(mid["items"], first["items"])
             plan.set_lengths(lens)
             plan.schedule()
             again = plan.debug_dump()
             for k, v in first.items():
                 assert v.shape == again[k].shape and np.array_equal(v, again[k]), (it, k)
-    say(f"[case] merged DAG (6 prompts): {len(first['items'])} items, rescheduled 3 times")
+    say(f"[case] {wl.name}: {len(first['items'])} items, rescheduled 3 times")
+
+
+def test_rescheduled_plan_matches_its_first_schedule_bit_for_bit():
+    """After the first schedule a plan keeps its groups (B(s), the group lists, the entry ranks:
+    they follow the paths, which a plan never changes) and recomputes only what the lengths
+    decide.  Moving to other lengths (which reorders the work list) and back must give exactly
+    the first schedule's arrays, and the groups must not change in between: on the
+    single-workgroup scheduler (a merged DAG) and on the multi-kernel one (more than 4096
+    segments and branches)."""
+    require_gpu()
+    _reschedule_round_trip(W.config3_merged_dag(prompts=6), 47)
+    rng = np.random.default_rng(7)
+    g = W.random_graph(rng, 5000, 4500, 40, 3, seed=1)
+    _reschedule_round_trip(W.make_workload("5000-segment graph", g, 28, 4, 64, "bf16", 1), 48)

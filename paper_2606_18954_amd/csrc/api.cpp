@@ -2,6 +2,7 @@
 // launches and the C entry points declared in include/graphattn.h.
 #include "../../include/graphattn.h"
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -320,9 +321,16 @@ void size_schedule(const ga_segment_table* st, const ga_branch_paths* bp, const 
   for (int64_t e = 0; e < z->E; ++e) used[bp->path_segs[e]] = 1;
   int64_t ref_pages = 0;
   for (int32_t s = 0; s < z->S; ++s) ref_pages += used[s] ? npg[s] : 0;
-  const int64_t target_items = 8LL * num_cus * 2;   // ~8 work items per resident workgroup
-  int64_t cap = (ref_pages * p->num_kv_heads + target_items - 1) / target_items;
-  if (cap < 16) cap = 16;
+  // About 8 work items per resident workgroup, but no chunk shorter than the pages each
+  // workgroup has anyway (up to 24): a unit costs about as much as 13 pages before its first
+  // page, so short units pay mostly overhead, unless the graph is too small to give every
+  // workgroup work (then short chunks spread it; 4 pages at the least).
+  const int64_t wgs = 2LL * num_cus;
+  const int64_t target_items = 8 * wgs;
+  const int64_t work = ref_pages * p->num_kv_heads;
+  int64_t cap = (work + target_items - 1) / target_items;
+  const int64_t floor_pages = std::min<int64_t>(24, std::max<int64_t>(4, (work + wgs - 1) / wgs));
+  if (cap < floor_pages) cap = floor_pages;
   if (cap > ga::kMaxChunkPages) cap = ga::kMaxChunkPages;
   z->chunk_pages = (int32_t)cap;
   const int32_t group = p->num_q_heads / p->num_kv_heads;

@@ -110,14 +110,19 @@ def cpu_baseline(wl, n_sample):
             "attended_tokens_per_s": toks / dt, "host": host_info()}
 
 
-def timed_steps(torch, plan, step, steps):
+def timed_steps(torch, plan, step, steps, preroll=3):
     """Two timed regions of `steps` steps each on the launch stream.  The first has no
     per-kernel events (HIP event records between kernels lengthen a step by a few us each):
-    it gives ms per step.  The second records the library's HIP events around every scheduler,
-    attention and merge launch: it gives each kernel's average duration."""
+    it gives ms per step.  It starts behind `preroll` untimed steps, so that the GPU is already
+    busy when its start event is recorded (after a synchronisation the first launch would
+    otherwise wait for the host, and the clocks for the work).  The second records the
+    library's HIP events around every scheduler, attention and merge launch: it gives each
+    kernel's average duration."""
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
+    for _ in range(preroll):
+        step()
     ev0.record()
     for _ in range(steps):
         step()
@@ -285,7 +290,8 @@ def run_extend(args, torch, G, W):
                      "unit": "TFLOP/s", "frac": achieved / MFMA_BF16_PEAK_TFLOPS,
                      "traffic": traffic},
         "kernel_ms": {"scheduler": sched_ms, "attention": attn_ms, "merge": merge_ms},
-        "timing": "ms_per_step over the timed steps without per-kernel events; kernel_ms (and "
+        "timing": "ms_per_step over the timed steps without per-kernel events, started behind "
+                  "3 untimed steps so the GPU is busy at the start event; kernel_ms (and "
                   "the roofline) from as many further steps with HIP events on the launch stream "
                   "around each kernel",
         "attention_flops": flops,
@@ -722,7 +728,8 @@ def main():
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic},
         "kernel_ms": {"scheduler": sched_ms, "attention": attn_ms, "merge": merge_ms,
                       "attention_mall_flushed": cold_ms},
-        "timing": "ms_per_step over the timed steps without per-kernel events; kernel_ms (and "
+        "timing": "ms_per_step over the timed steps without per-kernel events, started behind "
+                  "3 untimed steps so the GPU is busy at the start event; kernel_ms (and "
                   "the roofline) from as many further steps with HIP events on the launch stream "
                   "around each kernel; attention_mall_flushed from as many more with a 512 MiB "
                   "read between steps",

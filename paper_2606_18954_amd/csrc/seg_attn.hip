@@ -482,16 +482,29 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
       const unsigned char* pool_h = (const unsigned char*)uniform64(
           (int64_t)(uintptr_t)(pool + (int64_t)kvh * 2 * C::KVB));
   
+      // The row blocks of one chunk (which several workgroups stream at about the same time)
+      // start at different pages: the full stages are taken in rotated order (a partial last
+      // stage stays last), so that they do not all ask for the same page at once.  Issue
+      // order st, ring slot st mod NBUF; stage_of(st) is the stage of the chunk it holds.
+      const int nfull = np / C::SP;
+      const int nrb_c = (cnt * a.group + kRowsPerBlock - 1) / kRowsPerBlock;
+      const int rot = nfull > 1 ? (rb * nfull) / nrb_c : 0;
+      auto stage_of = [&](int st) {
+        int x = st + rot;
+        if (x >= nfull) x -= nfull;
+        return st < nfull ? x : st;
+      };
       auto issue = [&](int st) {
         const unsigned dst = lds_ring + (st % C::NBUF) * C::STAGE + wave * 1024;
-        const int npst = min(C::SP, np - st * C::SP);
+        const int sg = stage_of(st);
+        const int npst = min(C::SP, np - sg * C::SP);
         // All page ids of the stage are read before the first copy: one LDS round trip (the
         // copies' memory clobber would otherwise force a re-read before each of them).  Ids past
         // the chunk are read but unused.
         int pw[C::SP];
   #pragma unroll
         for (int q = 0; q < C::SP; ++q)
-          pw[q] = __builtin_amdgcn_readfirstlane(s_desc[b][kDescHead + st * C::SP + q]);
+          pw[q] = __builtin_amdgcn_readfirstlane(s_desc[b][kDescHead + sg * C::SP + q]);
   #pragma unroll
         for (int i = 0; i < NI; ++i) {
           const int pis = i / C::IPW;
@@ -542,13 +555,14 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
         // All waves are done with stage st - 1, so its buffer can be refilled.
         if (st + C::NBUF - 1 < nst) issue(st + C::NBUF - 1);
         const int buf = st % C::NBUF;
-        const int npst = min(C::SP, np - st * C::SP);
+        const int sg = stage_of(st);
+        const int npst = min(C::SP, np - sg * C::SP);
         if (ntile > 0) {
           const unsigned char* sb = smem + buf * C::STAGE;
           int cls[NT];
   #pragma unroll
-          for (int k = 0; k < NT; ++k) cls[k] = cl[k] - kPageTokens * C::SP * st;
-          kv_stage<D, BF16, NT, C::NB, CAUSAL>(sb, &s_desc[b][kDescHead + st * C::SP], split, ks,
+          for (int k = 0; k < NT; ++k) cls[k] = cl[k] - kPageTokens * C::SP * sg;
+          kv_stage<D, BF16, NT, C::NB, CAUSAL>(sb, &s_desc[b][kDescHead + sg * C::SP], split, ks,
                                                npst, a.scale_log2, r16, kg, 0, cm, cls, qop, m,
                                                l, O);
         }

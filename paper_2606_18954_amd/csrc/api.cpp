@@ -321,7 +321,7 @@ void size_schedule(const ga_segment_table* st, const ga_branch_paths* bp, const 
   for (int64_t e = 0; e < z->E; ++e) used[bp->path_segs[e]] = 1;
   int64_t ref_pages = 0;
   for (int32_t s = 0; s < z->S; ++s) ref_pages += used[s] ? npg[s] : 0;
-  // About 4 work items per resident workgroup, in chunks of at most 128 pages (longer units
+  // About 4 work items per resident workgroup, in chunks of at most 120 pages (longer units
   // leave too long a tail once the queue is empty), and no chunk shorter than the pages each
   // workgroup has anyway (up to 24): a unit costs about as much as 13 pages before its first
   // page, so short units pay mostly overhead, unless the graph is too small to give every
@@ -331,10 +331,9 @@ void size_schedule(const ga_segment_table* st, const ga_branch_paths* bp, const 
   const int64_t target_items = 4 * wgs;
   const int64_t work = ref_pages * p->num_kv_heads;
   int64_t cap = (work + target_items - 1) / target_items;
-  if (cap > 128) cap = 128;
+  if (cap > ga::kMaxChunkPages) cap = ga::kMaxChunkPages;
   const int64_t floor_pages = std::min<int64_t>(24, std::max<int64_t>(4, (work + wgs - 1) / wgs));
   if (cap < floor_pages) cap = floor_pages;
-  if (cap > ga::kMaxChunkPages) cap = ga::kMaxChunkPages;
   z->chunk_pages = (int32_t)cap;
   const int32_t group = p->num_q_heads / p->num_kv_heads;
   int64_t chunks_ref = 0, prows = 0;
@@ -730,7 +729,7 @@ ga_status do_run(ga_plan* pl, const void* q, const void* pool, void* out, float*
   a.chunk_pages = pl->z.chunk_pages;
   a.desc_words = pl->z.desc_words;
   a.scale_log2 = pl->p.softmax_scale * 1.4426950408889634f;
-  int64_t grid = (int64_t)ga::seg_attn_grid(pl->p.head_dim, bf16, pl->num_cus);
+  int64_t grid = (int64_t)ga::seg_attn_grid(pl->p.head_dim, bf16, pl->causal, pl->num_cus);
   const int64_t work = pl->z.max_items * pl->p.num_kv_heads;
   if (work < grid) grid = work;
   const bool rec = pl->prof_runs < pl->prof_cap;

@@ -13,7 +13,7 @@ constexpr int32_t kPageIdMask = (1 << kPageValidShift) - 1;
 // Query rows (branch x q-head-in-group) handled by one work item: 8 MFMA row tiles of 16.
 constexpr int kRowsPerBlock = 128;
 // Upper bound on pages per work item (the chunk's page ids are staged in LDS).
-constexpr int kMaxChunkPages = 512;
+constexpr int kMaxChunkPages = 120;
 constexpr int kAttnThreads = 256;        // 4 wave64 per workgroup
 
 // Work-item descriptor (int32 words, one per item, fixed stride), written by the scheduler and
@@ -26,7 +26,7 @@ constexpr int kAttnThreads = 256;        // 4 wave64 per workgroup
 //   [8 + chunk_pages .. + branches)   branch ids of the row block's rows (B(s) from row0/group)
 constexpr int kDescHead = 8;
 constexpr int32_t kNoCausal = 0x40000000;
-constexpr int kDescMaxBytes = 3072;      // LDS slot per descriptor
+constexpr int kDescMaxBytes = 1024;      // LDS slot per descriptor (one 1 KiB copy)
 __host__ __device__ inline int desc_branch_max(int group) {
   const int n = (kRowsPerBlock + group - 1) / group + 1;
   return n < kRowsPerBlock ? n : kRowsPerBlock;
@@ -214,6 +214,6 @@ hipError_t launch_suffix_count(const SuffixArgs& a, hipStream_t stream);
 hipError_t launch_suffix_fill(const SuffixArgs& a, hipStream_t stream);
 hipError_t launch_advantages(const RewardArgs& a, hipStream_t stream);
 // Number of co-resident attention workgroups the persistent grid uses on this device.
-int seg_attn_grid(int head_dim, bool bf16, int num_cus);
+int seg_attn_grid(int head_dim, bool bf16, bool causal, int num_cus);
 
 }  // namespace ga

@@ -49,7 +49,15 @@ typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
-template <int D, bool BF16>
+// Workgroups per CU and ring depth: two workgroups with four stages for decode; the bf16
+// multi-query variant runs three workgroups per CU (its 128-row units are bound by each wave's
+// issue and compute, so more waves per CU pay more than a deeper ring) with three stages each.
+// (The fp32 variant keeps two: at three its 32 query registers per tile would spill.)
+__host__ __device__ constexpr int attn_wgs_per_cu(bool causal, bool bf16) {
+  return causal && bf16 ? 3 : 2;
+}
+
+template <int D, bool BF16, bool CAUSAL = false>
 struct Cfg {
   static constexpr int ELT = BF16 ? 2 : 4;
   static constexpr int ROW = D * ELT;               // bytes of one token row of K or V
@@ -58,7 +66,7 @@ struct Cfg {
   static constexpr int PB = 2 * KVB;                // bytes of one page of one kv-head
   static constexpr int STAGE = GA_STAGE_BYTES >= PB ? GA_STAGE_BYTES : PB;   // bytes per stage
   static constexpr int SP = STAGE / PB;             // pages per stage
-  static constexpr int NBUF = GA_RING_STAGES;       // stages in the LDS ring
+  static constexpr int NBUF = attn_wgs_per_cu(CAUSAL, BF16) == 3 ? 3 : GA_RING_STAGES;   // stages
   static constexpr int IPP = PB / 1024;             // 1 KiB DMA wave instructions per page
   static constexpr int IPW = IPP / (kAttnThreads / 64);   // ... issued by each wave per page
   static constexpr int NB = D / 16;                 // 16-wide output column blocks
@@ -327,8 +335,9 @@ __device__ __forceinline__ void kv_stage(const unsigned char* sb, const int* pwo
 // kNoCausal otherwise) lets the row of group rank j see token t of the chunk (t counted as
 // 16 x page index + slot) only for t <= c + j.
 template <int D, bool BF16, bool CAUSAL>
-__global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
-  using C = Cfg<D, BF16>;
+__global__ __launch_bounds__(kAttnThreads, attn_wgs_per_cu(CAUSAL, BF16))
+void k_seg_attn(AttnArgs a) {
+  using C = Cfg<D, BF16, CAUSAL>;
   using T = typename std::conditional<BF16, __bf16, float>::type;
   constexpr int NI = C::SP * C::IPW;                // copies per wave per full stage
   __shared__ __align__(1024) unsigned char smem[C::NBUF * C::STAGE];
@@ -572,7 +581,12 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
       if (wave == 0) wait_vmcnt(0);
       lds_barrier();
   
-      // Row sums: reduce the per-lane partials across the four lane groups.
+      // Fresh copies of the lane and its lane group: the epilogue's per-lane addresses are then
+      // formed here, once per unit, instead of being hoisted out of the unit loop and kept live
+      // (or spilled) through every stage.
+      int lane_e = lane, kg_e = kg;
+      asm volatile("" : "+v"(lane_e), "+v"(kg_e));
+      // Row sums: reduce the per-lane_e partials across the four lane_e groups.
       float L[NT];
   #pragma unroll
       for (int k = 0; k < NT; ++k) L[k] = xsum(l[k]);
@@ -586,17 +600,17 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
         if (split > 0 && ntile > 0) {
           const int wi = (split - 1) * nrt + t0;
           float* mine = cb + wi * NV * 64;
-          s_ml[wi][0][lane] = m[0];
-          s_ml[wi][1][lane] = L[0];
+          s_ml[wi][0][lane_e] = m[0];
+          s_ml[wi][1][lane_e] = L[0];
   #pragma unroll
           for (int n = 0; n < C::NB; ++n)
   #pragma unroll
-            for (int i = 0; i < 4; ++i) mine[(4 * n + i) * 64 + lane] = O[0][n][i];
+            for (int i = 0; i < 4; ++i) mine[(4 * n + i) * 64 + lane_e] = O[0][n][i];
         }
         lds_barrier();
         if (split == 0 && ntile > 0) {
           float M = m[0];
-          for (int sp = 1; sp < ks; ++sp) M = fmaxf(M, s_ml[(sp - 1) * nrt + t0][0][lane]);
+          for (int sp = 1; sp < ks; ++sp) M = fmaxf(M, s_ml[(sp - 1) * nrt + t0][0][lane_e]);
           // (a causal row that saw no token in any split has M = -inf and stays empty)
           const float Ms = CAUSAL && M == NEG_INF ? 0.f : M;
           const float w0 = exp2_(m[0] - Ms);
@@ -607,12 +621,12 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
           for (int sp = 1; sp < ks; ++sp) {
             const int wi = (sp - 1) * nrt + t0;
             const float* o = cb + wi * NV * 64;
-            const float wgt = exp2_(s_ml[wi][0][lane] - Ms);
-            Lc += wgt * s_ml[wi][1][lane];
+            const float wgt = exp2_(s_ml[wi][0][lane_e] - Ms);
+            Lc += wgt * s_ml[wi][1][lane_e];
   #pragma unroll
             for (int n = 0; n < C::NB; ++n)
   #pragma unroll
-              for (int i = 0; i < 4; ++i) Oc[n][i] += wgt * o[(4 * n + i) * 64 + lane];
+              for (int i = 0; i < 4; ++i) Oc[n][i] += wgt * o[(4 * n + i) * 64 + lane_e];
           }
           m[0] = M;
           L[0] = Lc;
@@ -629,7 +643,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
           // A causal row that saw no token of the chunk (L = 0) stores o = 0, lambda = -inf.
           const float inv = CAUSAL && !(L[k] > 0.f) ? 0.f : 1.f / L[k];
           if constexpr (BF16) {
-            // fp16 partial in lane order, scaled so the row's largest |o| is below 2^15 (the
+            // fp16 partial in lane_e order, scaled so the row's largest |o| is below 2^15 (the
             // four lanes of a row agree on the scale; L >= 1, so |o| <= max |V|).
             float amax = 0.f;
   #pragma unroll
@@ -645,7 +659,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
               const int h = kvh * a.group + (gr - j * a.group);
               const int64_t row = ((int64_t)prow_base + j) * a.Hq + h;
               f16x8* dst = reinterpret_cast<f16x8*>(static_cast<_Float16*>(a.po) + row * D +
-                                                    8 * kg);
+                                                    8 * kg_e);
   #pragma unroll
               for (int c = 0; c < C::NB / 2; ++c) {
                 f16x8 v;
@@ -656,7 +670,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
                 }
                 store_dev16(dst + 4 * c, v);   // the row's four lanes fill 64 contiguous bytes
               }
-              if (kg == 0)
+              if (kg_e == 0)
                 store_dev8(reinterpret_cast<f32x2*>(a.plse + 2 * row),
                            f32x2{m[k] + log2_(L[k]), __builtin_amdgcn_ldexpf(1.f, e - kPartScaleBits)});
             }
@@ -666,11 +680,11 @@ __global__ __launch_bounds__(kAttnThreads, 2) void k_seg_attn(AttnArgs a) {
               const int j = gr / a.group;
               const int h = kvh * a.group + (gr - j * a.group);
               const int64_t row = ((int64_t)prow_base + j) * a.Hq + h;
-              float* dst = static_cast<float*>(a.po) + row * D + 4 * kg;
+              float* dst = static_cast<float*>(a.po) + row * D + 4 * kg_e;
   #pragma unroll
               for (int n = 0; n < C::NB; ++n)
                 *reinterpret_cast<f32x4*>(dst + 16 * n) = O[k][n] * inv;
-              if (kg == 0) a.plse[row] = m[k] + log2_(L[k]);
+              if (kg_e == 0) a.plse[row] = m[k] + log2_(L[k]);
             }
           }
         }
@@ -695,10 +709,10 @@ hipError_t launch_t(const AttnArgs& a, bool causal, int grid, hipStream_t stream
 
 }  // namespace
 
-int seg_attn_grid(int head_dim, bool bf16, int num_cus) {
+int seg_attn_grid(int head_dim, bool bf16, bool causal, int num_cus) {
   (void)head_dim;
   (void)bf16;
-  return num_cus * 2;                      // two 256-thread workgroups fit per CU (LDS-bound)
+  return num_cus * attn_wgs_per_cu(causal, bf16);   // 256-thread workgroups (LDS-bound)
 }
 
 hipError_t launch_seg_attn(const AttnArgs& a, int head_dim, bool bf16, bool causal, int grid,

@@ -24,7 +24,7 @@ hipError_t launch_suffix_count(const SuffixArgs&, hipStream_t) { std::abort(); }
 hipError_t launch_suffix_fill(const SuffixArgs&, hipStream_t) { std::abort(); }
 hipError_t launch_advantages(const RewardArgs&, hipStream_t) { std::abort(); }
 hipError_t launch_set_lengths(const LengthArgs&, hipStream_t) { std::abort(); }
-int seg_attn_grid(int, bool, int num_cus) { return 2 * num_cus; }
+int seg_attn_grid(int, bool, bool, int num_cus) { return 2 * num_cus; }
 }  // namespace ga
 
 int main(int argc, char** argv) {

@@ -321,17 +321,19 @@ void size_schedule(const ga_segment_table* st, const ga_branch_paths* bp, const 
   for (int64_t e = 0; e < z->E; ++e) used[bp->path_segs[e]] = 1;
   int64_t ref_pages = 0;
   for (int32_t s = 0; s < z->S; ++s) ref_pages += used[s] ? npg[s] : 0;
-  // About 4 work items per resident workgroup, in chunks of at most 120 pages (longer units
-  // leave too long a tail once the queue is empty), and no chunk shorter than the pages each
-  // workgroup has anyway (up to 24): a unit costs about as much as 13 pages before its first
-  // page, so short units pay mostly overhead, unless the graph is too small to give every
-  // workgroup work (then short chunks spread it; 4 pages at the least).  Fewer, longer chunks
-  // also mean fewer partial rows to merge and fewer items to schedule.
+  // About 4 work items per resident workgroup, in chunks of at most 128 pages (longer units
+  // leave too long a tail once the queue is empty; a little fewer at group size 1, so that the
+  // descriptor's list of up to 128 branches still fits its slot), and no chunk shorter than the
+  // pages each workgroup has anyway (up to 24): a unit costs about as much as 13 pages before
+  // its first page, so short units pay mostly overhead, unless the graph is too small to give
+  // every workgroup work (then short chunks spread it; 4 pages at the least).  Fewer, longer
+  // chunks also mean fewer partial rows to merge and fewer items to schedule.
   const int64_t wgs = 2LL * num_cus;
   const int64_t target_items = 4 * wgs;
   const int64_t work = ref_pages * p->num_kv_heads;
   int64_t cap = (work + target_items - 1) / target_items;
-  if (cap > ga::kMaxChunkPages) cap = ga::kMaxChunkPages;
+  const int32_t max_cap = ga::max_chunk_pages(p->num_q_heads / p->num_kv_heads);
+  if (cap > max_cap) cap = max_cap;
   const int64_t floor_pages = std::min<int64_t>(24, std::max<int64_t>(4, (work + wgs - 1) / wgs));
   if (cap < floor_pages) cap = floor_pages;
   z->chunk_pages = (int32_t)cap;

@@ -13,7 +13,7 @@ constexpr int32_t kPageIdMask = (1 << kPageValidShift) - 1;
 // Query rows (branch x q-head-in-group) handled by one work item: 8 MFMA row tiles of 16.
 constexpr int kRowsPerBlock = 128;
 // Upper bound on pages per work item (the chunk's page ids are staged in LDS).
-constexpr int kMaxChunkPages = 120;
+constexpr int kMaxChunkPages = 128;
 constexpr int kAttnThreads = 256;        // 4 wave64 per workgroup
 
 // Work-item descriptor (int32 words, one per item, fixed stride), written by the scheduler and
@@ -34,8 +34,14 @@ __host__ __device__ inline int desc_branch_max(int group) {
 __host__ __device__ inline int desc_words(int chunk_pages, int group) {
   return (kDescHead + chunk_pages + desc_branch_max(group) + 3) & ~3;
 }
-static_assert(4 * ((kDescHead + kMaxChunkPages + kRowsPerBlock + 3) & ~3) <= kDescMaxBytes,
-              "descriptor must fit its LDS slot");
+// Most pages a chunk may have so that its descriptor fits one slot (the chunk size is capped
+// at this by the plan, so that no chunk's descriptor outgrows the slot).
+__host__ __device__ inline int max_chunk_pages(int group) {
+  const int fit = kDescMaxBytes / 4 - kDescHead - desc_branch_max(group);
+  return fit < kMaxChunkPages ? fit : kMaxChunkPages;
+}
+static_assert(kDescMaxBytes / 4 - kDescHead - kRowsPerBlock >= 64,
+              "a descriptor slot must hold a useful chunk at every group size");
 
 // Device copy of the rollout graph (chains as segments), written by plan_create's upload; the
 // lengths, page lists and causal origins are rewritten in place by a length update.

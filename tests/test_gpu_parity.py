@@ -64,6 +64,17 @@ def _plan_step(plan, q, pool, B, Hq, D):
     return out, lse
 
 
+def test_group_size_one_at_the_longest_chunks():
+    """One q-head per kv-head: a descriptor then lists up to 128 branches, so the longest chunk
+    that still fits its slot is 120 pages.  A graph large enough for the chunking to reach that
+    cap (64 paths of 32768 tokens at 4/4 heads), sampled branches against the oracle."""
+    g = W.assemble_graph([32768] * 64, [[i] for i in range(64)], 71)
+    wl = W.make_workload("64 x 32768-token paths, 4/4/128 bf16", g, 4, 4, 128, "bf16", 71)
+    with G.Plan(G.HostGraph.from_graph(g), params_of(wl)) as plan:
+        assert plan.info().chunk_pages == 120
+    check_workload(wl, branches=[0, 17, 42, 63], out_f32=True)
+
+
 @pytest.mark.parametrize("name", ["c3", "c4", "c5chain", "c5graph"])
 def test_full_size_every_branch(name):
     """Full-size configurations in the launch configuration the benchmark times (plan, GPU

@@ -402,7 +402,7 @@ Layout layout(const Sizes& z, const ga_params& p) {
   // (padded so that whole-slot copies of the last descriptor stay inside the allocation)
   sz[L_DESC] = sizeof(int32_t) * (size_t)z.desc_words * (z.max_items > 0 ? z.max_items : 1) +
                ga::kDescMaxBytes;
-  sz[L_COUNTERS] = sizeof(int64_t) * 4;
+  sz[L_COUNTERS] = sizeof(int64_t) * ga::kNumCounters;
   sz[L_ENTRY_PART] = sizeof(int64_t) * z.E;
   sz[L_BPART_OFF] = sizeof(int64_t) * (z.B + 1);
   sz[L_BPART] = sizeof(int32_t) * z.prows;
@@ -730,6 +730,7 @@ ga_status do_run(ga_plan* pl, const void* q, const void* pool, void* out, float*
   a.group = a.Hq / a.Hkv;
   a.chunk_pages = pl->z.chunk_pages;
   a.desc_words = pl->z.desc_words;
+  a.streams = ga::attn_streams(a.Hkv, pl->causal);
   a.scale_log2 = pl->p.softmax_scale * 1.4426950408889634f;
   int64_t grid = (int64_t)ga::seg_attn_grid(pl->p.head_dim, bf16, pl->causal, pl->num_cus);
   const int64_t work = pl->z.max_items * pl->p.num_kv_heads;

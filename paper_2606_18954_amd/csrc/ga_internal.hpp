@@ -74,7 +74,8 @@ struct DevSchedule {
   int4* items;             // [max_items] (segment, chunk, row block, unused)
   int32_t* desc;           // [max_items * desc_words (+ kDescMaxBytes of padding)] descriptors
   int32_t desc_words;      // descriptor stride in int32 words (a multiple of 4)
-  int64_t* counters;       // [4]: items, partial rows, work-queue head, spare
+  int64_t* counters;       // [8]: items, partial rows, spare, spare, then kMaxStreams int32
+                           //      work-stream heads (the attention kernel's claim counters)
   int64_t* entry_part;     // [E]   first slot of each path entry in the branch partial lists
   int64_t* bpart_off;      // [B+1] CSR offsets of each branch's partial rows
   int32_t* bpart;          // [partial rows] partial rows of each branch: path order, then chunk
@@ -91,16 +92,24 @@ struct DevSchedule {
 //   fp32, (lambda, 2^(e - 15)), the second being the factor that undoes the scaling.
 constexpr int kPartScaleBits = 15;
 
+// The attention kernel's work streams: the units of kv heads h with h mod streams == s form
+// stream s, owned by the workgroups with blockIdx mod streams == s.  Workgroups are dispatched
+// to the eight XCDs round robin, so a stream is served by 8 / streams of them, and the row
+// blocks of one (chunk, kv head) share those XCDs' L2s.
+constexpr int kMaxStreams = 8;
+constexpr int kNumCounters = 4 + kMaxStreams / 2;   // int64 words of the counters array
+
 struct AttnArgs {
   const void* q;
   const void* pool;
   const int32_t* desc;     // work-item descriptors (layout above)
-  int64_t* counters;       // [0] items, [2] work-queue head (units claimed past the first two
-                           //     grids, as int32: workgroup i starts with units i and i + grid)
+  int64_t* counters;       // [0] items; from [4], kMaxStreams int32 work-stream heads (units
+                           //     of each stream claimed past its first two rounds)
   void* po;                // partial outputs (format above)
   float* plse;             // partial log-sum-exps (format above)
   int32_t Hq, Hkv, group, chunk_pages;
   int32_t desc_words;      // descriptor stride (int32 words)
+  int32_t streams;         // work streams: divides Hkv and kMaxStreams
   float scale_log2;        // softmax scale * log2(e)
 };
 
@@ -111,7 +120,7 @@ struct MergeArgs {
   const float* plse;
   void* out;
   float* lse;
-  int64_t* counters;       // the attention work-queue head (counters[2]) is re-armed here
+  int64_t* counters;       // the attention kernel's work-stream heads are re-armed here
   int32_t B, Hq;
 };
 
@@ -221,5 +230,15 @@ hipError_t launch_suffix_fill(const SuffixArgs& a, hipStream_t stream);
 hipError_t launch_advantages(const RewardArgs& a, hipStream_t stream);
 // Number of co-resident attention workgroups the persistent grid uses on this device.
 int seg_attn_grid(int head_dim, bool bf16, bool causal, int num_cus);
+// Work streams of an attention launch (the largest power of two dividing Hkv and
+// kMaxStreams): multi-query units split a shared chunk into many row blocks, each of which
+// reads the chunk, so they are kept on few XCDs.  Decode units mostly hold one row block per
+// chunk and keep one stream.
+inline int attn_streams(int Hkv, bool causal) {
+  if (!causal) return 1;
+  int s = kMaxStreams;
+  while (Hkv % s) s >>= 1;
+  return s;
+}
 
 }  // namespace ga

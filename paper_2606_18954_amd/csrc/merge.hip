@@ -28,7 +28,7 @@ __global__ __launch_bounds__(256) void k_merge(MergeArgs a) {
   // (2: 56 VGPRs, 4: 76, 8: 116 at 4 waves per SIMD, each slower).
   constexpr int KB = 1;
   const int tid = threadIdx.x;
-  if (blockIdx.x == 0 && tid == 0) a.counters[2] = 0;
+  if (blockIdx.x == 0 && tid < kMaxStreams) reinterpret_cast<int*>(a.counters + 4)[tid] = 0;
   const int64_t row = (int64_t)blockIdx.x * RPB + tid / LPR;
   const int sub = tid % LPR;
   if (row >= (int64_t)a.B * a.Hq) return;

@@ -36,7 +36,7 @@ __global__ void k_init(DevGraph g, DevSchedule sc, int32_t reuse) {
     sc.grp_cnt[s] = 0;
     sc.grp_fill[s] = 0;
   }
-  if (s < 4) sc.counters[s] = 0;
+  if (s < kNumCounters) sc.counters[s] = 0;
 }
 
 // Branch of each path entry (binary search in path_off) and |B(s)| histogram.
@@ -477,7 +477,7 @@ __global__ __launch_bounds__(1024) void k_sched_one(DevGraph g, DevSchedule sc, 
     }
     for (int i = t; i < 4 * 16 * NBK; i += 1024) l_cw[i] = 0;
   }
-  if (t < 4) sc.counters[t] = 0;
+  if (t < kNumCounters) sc.counters[t] = 0;
   lds_barrier();
 
   // 1. |B(s)|, and the chunks of the entries of this thread's branches (one partial row per

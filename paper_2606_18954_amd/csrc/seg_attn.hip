@@ -187,33 +187,41 @@ __device__ __forceinline__ int64_t uniform64(int64_t v) {
 // that the stale reference is kept (probabilities up to 2^kTau are exact in fp32 and bf16).
 constexpr float kTau = 8.0f;
 
-// Online softmax (log2 domain) over one page's 16 tokens for each of the wave's NT tiles: masks
-// tokens past the segment end, and moves a row's reference m only when some score exceeds it by
-// more than 2^kTau, so the common page needs no cross-lane reduction and no rescale of O.
-// CAUSAL (multi-query units): when cm is set, the lane's score i of tile t is also masked for
-// i > thr[t] (the row's last visible token, relative to token 4 kg of the page).  A row may then
-// have seen no token yet (m = -inf, l = 0, O = 0); the guards keep it at exactly that.
-template <int NT, int NBW, int NBT, bool CAUSAL>
-__device__ __forceinline__ void softmax_page(f32x4 (&S)[NT], float (&p)[NT][4], float (&m)[NT],
-                                             float (&l)[NT], f32x4 (&O)[NT][NBT], bool last,
-                                             int last_valid, bool cm, const int (&thr)[NT],
-                                             int kg, float sl2) {
+// Online softmax (log2 domain) over NPG pages of 16 tokens for each of the wave's NT tiles
+// (S[g][t]: page g's scores): masks tokens past each page's valid tokens, and moves a row's
+// reference m only when some score exceeds it by more than 2^kTau, so the common page needs no
+// cross-lane reduction and no rescale of O.
+// CAUSAL (multi-query units): when cm is set, the lane's score i of tile t on page g is also
+// masked for i > thr[g][t] (the row's last visible token, relative to token 4 kg of the page).
+// A row may then have seen no token yet (m = -inf, l = 0, O = 0); the guards keep it at exactly
+// that.
+template <int NPG, int NT, int NBW, int NBT, bool CAUSAL>
+__device__ __forceinline__ void softmax_pages(f32x4 (&S)[NPG][NT], float (&p)[NPG][NT][4],
+                                              float (&m)[NT], float (&l)[NT],
+                                              f32x4 (&O)[NT][NBT], const bool (&last)[NPG],
+                                              const int (&last_valid)[NPG], bool cm,
+                                              const int (&thr)[NPG][NT], int kg, float sl2) {
   const float NEG_INF = -__builtin_huge_valf();
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
-    if (last) {
+    float lm = NEG_INF;
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        if (4 * kg + i >= last_valid) S[t][i] = NEG_INF;
-    }
-    if constexpr (CAUSAL) {
-      if (cm) {
+    for (int g = 0; g < NPG; ++g) {
+      if (last[g]) {
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-          if (i > thr[t]) S[t][i] = NEG_INF;
+          if (4 * kg + i >= last_valid[g]) S[g][t][i] = NEG_INF;
       }
+      if constexpr (CAUSAL) {
+        if (cm) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (i > thr[g][t]) S[g][t][i] = NEG_INF;
+        }
+      }
+      lm = fmaxf(lm, fmaxf(fmaxf(S[g][t][0], S[g][t][1]), fmaxf(S[g][t][2], S[g][t][3])));
     }
-    const float lm = fmaxf(fmaxf(S[t][0], S[t][1]), fmaxf(S[t][2], S[t][3])) * sl2;
+    lm *= sl2;
     if (__any(lm > m[t] + kTau)) {
       const float mn = fmaxf(m[t], xmax(lm));
       float alpha = exp2_(m[t] - mn);
@@ -226,16 +234,149 @@ __device__ __forceinline__ void softmax_page(f32x4 (&S)[NT], float (&p)[NT][4], 
     float nm = -m[t];
     if constexpr (CAUSAL) nm = m[t] == NEG_INF ? 0.f : nm;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) p[t][i] = exp2_(fmaf(S[t][i], sl2, nm));
-    l[t] += (p[t][0] + p[t][1]) + (p[t][2] + p[t][3]);
+    for (int g = 0; g < NPG; ++g) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) p[g][t][i] = exp2_(fmaf(S[g][t][i], sl2, nm));
+      l[t] += (p[g][t][0] + p[g][t][1]) + (p[g][t][2] + p[g][t][3]);
+    }
   }
 }
 
-// One K/V stage for one wave: NT row tiles (qop[0 .. NT-1]) against pages p0, p0 + pstep, ... of
-// the stage (for CAUSAL units, cl[t] is the lane's row limit relative to the stage's first page),
-// producing
-// NBW output column blocks (O[t][i] holds column block n0 + i).  All LDS operand reads of a page
-// are issued before its first MFMA, so the V reads overlap S = K Q^T and the softmax.
+// NPG pages (pg[0 .. NPG-1] of the stage at sb) for one wave: NT row tiles (qop[0 .. NT-1])
+// producing NBW output column blocks (O[t][i] holds column block n0 + i); for CAUSAL units,
+// cl[t] is the lane's row limit relative to the stage's first page.  All LDS operand reads of
+// the first column blocks are issued before the first MFMA, so they overlap S = K Q^T and the
+// softmax.
+// bf16, two pages: the PV product contracts both pages' 32 tokens in one K = 32 instruction.
+// The lane's eight K slots are tokens 4 kg .. 4 kg + 3 of the first page, then the same tokens
+// of the second: the slots of V^T (two transposing reads) and of P (the lane's own
+// probabilities) are ordered alike, and a contraction does not depend on the order of its
+// terms.
+template <int D, bool BF16, int NPG, int NT, int NBW, bool CAUSAL>
+__device__ __forceinline__ void kv_pages(const unsigned char* sb, const int* pwords,
+                                         const int (&pg)[NPG], float sl2, int r16, int kg,
+                                         int n0, bool cm, const int (&cl)[NT],
+                                         const QOp<BF16> (&qop)[NT][Cfg<D, BF16>::QR],
+                                         float (&m)[NT], float (&l)[NT],
+                                         f32x4 (&O)[NT][Cfg<D, BF16>::NB]) {
+  using C = Cfg<D, BF16>;
+  static_assert(BF16 || NPG == 1, "fp32 pages are taken one at a time");
+  const unsigned char* kb[NPG];
+  const unsigned char* vb[NPG];
+  bool last[NPG];
+  int last_valid[NPG];
+  int thr[NPG][NT];
+#pragma unroll
+  for (int g = 0; g < NPG; ++g) {
+    kb[g] = sb + pg[g] * C::PB;
+    vb[g] = kb[g] + C::KVB;
+    // Valid tokens of the page (a segment of the chain may end inside it): from its page word.
+    const int vm1 = (int)((unsigned)__builtin_amdgcn_readfirstlane(pwords[pg[g]]) >>
+                          kPageValidShift);
+    last[g] = vm1 < kPageTokens - 1;
+    last_valid[g] = vm1 + 1;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) thr[g][t] = CAUSAL ? cl[t] - kPageTokens * pg[g] : 0;
+  }
+  f32x4 S[NPG][NT];
+#pragma unroll
+  for (int g = 0; g < NPG; ++g)
+#pragma unroll
+    for (int t = 0; t < NT; ++t) S[g][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float p[NPG][NT][4];
+  if constexpr (BF16) {
+    // V^T operand of column block n: lane reads 4 tokens (4 kg + r16 / 4 supplies the row) of
+    // 4 columns through the transposing read; the chunk index is permuted like the writes.
+    // The V operands are read in batches of VB column blocks (register budget).
+    constexpr int VB = NT * NPG == 4 ? (NBW >= 8 ? NBW / 8 : 1) : NT * NPG == 2 ? NBW / 2 : NBW;
+    static_assert(NBW % VB == 0, "column blocks come in whole batches");
+    const int tv = 4 * kg + (r16 >> 2);
+    auto vread = [&](int g, int n) {
+      const int off = tv * C::ROW + (((2 * n + ((r16 & 3) >> 1)) ^ (tv & (C::CPR - 1))) << 4) +
+                      (r16 & 1) * 8;
+      return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vb[g] + off));
+    };
+    s16x4 va[VB][NPG];
+#pragma unroll
+    for (int i = 0; i < VB; ++i)
+#pragma unroll
+      for (int g = 0; g < NPG; ++g) va[i][g] = vread(g, n0 + i);
+#pragma unroll
+    for (int g = 0; g < NPG; ++g) {
+      // (the second page's K is read once the first page's products are issued: register
+      // budget)
+      if (g > 0) asm volatile("" ::: "memory");
+      bf16x8 ka[C::QR];
+#pragma unroll
+      for (int jj = 0; jj < C::QR; ++jj)
+        ka[jj] = *reinterpret_cast<const bf16x8*>(kb[g] + swz<D, BF16>(r16, 4 * jj + kg));
+#pragma unroll
+      for (int jj = 0; jj < C::QR; ++jj)
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+          S[g][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[jj], qop[t][jj].v, S[g][t], 0, 0,
+                                                            0);
+    }
+    softmax_pages<NPG, NT, NBW, C::NB, CAUSAL>(S, p, m, l, O, last, last_valid, cm, thr, kg,
+                                               sl2);
+    s16x4 pb[NT][NPG];
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int g = 0; g < NPG; ++g)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) pb[t][g][i] = __builtin_bit_cast(short, (__bf16)p[g][t][i]);
+#pragma unroll
+    for (int i0 = 0; i0 < NBW; i0 += VB) {
+      if (i0 > 0) {
+#pragma unroll
+        for (int i = 0; i < VB; ++i)
+#pragma unroll
+          for (int g = 0; g < NPG; ++g) va[i][g] = vread(g, n0 + i0 + i);
+      }
+#pragma unroll
+      for (int i = 0; i < VB; ++i)
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+          if constexpr (NPG == 2) {
+            const bf16x8 av = __builtin_bit_cast(
+                bf16x8, __builtin_shufflevector(va[i][0], va[i][1], 0, 1, 2, 3, 4, 5, 6, 7));
+            const bf16x8 bp = __builtin_bit_cast(
+                bf16x8, __builtin_shufflevector(pb[t][0], pb[t][1], 0, 1, 2, 3, 4, 5, 6, 7));
+            O[t][i0 + i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bp, O[t][i0 + i], 0, 0, 0);
+          } else {
+            O[t][i0 + i] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va[i][0], pb[t][0],
+                                                                     O[t][i0 + i], 0, 0, 0);
+          }
+        }
+    }
+  } else {
+#pragma unroll
+    for (int jj = 0; jj < C::QR; ++jj) {
+      const float ka = *reinterpret_cast<const float*>(kb[0] + swz<D, BF16>(r16, jj) + kg * 4);
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+        S[0][t] = __builtin_amdgcn_mfma_f32_16x16x4f32(ka, qop[t][jj].v, S[0][t], 0, 0, 0);
+    }
+    softmax_pages<1, NT, NBW, C::NB, CAUSAL>(S, p, m, l, O, last, last_valid, cm, thr, kg, sl2);
+#pragma unroll
+    for (int i = 0; i < NBW; ++i) {
+      const int n = n0 + i;
+#pragma unroll
+      for (int i4 = 0; i4 < 4; ++i4) {
+        const int tv = 4 * kg + i4;
+        const float va = *reinterpret_cast<const float*>(
+            vb[0] + swz<D, BF16>(tv, 4 * n + (r16 >> 2)) + (r16 & 3) * 4);
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+          O[t][i] = __builtin_amdgcn_mfma_f32_16x16x4f32(va, p[0][t][i4], O[t][i], 0, 0, 0);
+      }
+    }
+  }
+}
+
+// One K/V stage for one wave: pages p0, p0 + pstep, ... below npst of the stage, in pairs where
+// two are left (bf16), then one at a time.
 template <int D, bool BF16, int NT, int NBW, bool CAUSAL>
 __device__ __forceinline__ void kv_stage(const unsigned char* sb, const int* pwords, int p0,
                                          int pstep, int npst, float sl2,
@@ -243,91 +384,18 @@ __device__ __forceinline__ void kv_stage(const unsigned char* sb, const int* pwo
                                          const QOp<BF16> (&qop)[NT][Cfg<D, BF16>::QR],
                                          float (&m)[NT], float (&l)[NT],
                                          f32x4 (&O)[NT][Cfg<D, BF16>::NB]) {
-  using C = Cfg<D, BF16>;
-  const float NEG_INF = -__builtin_huge_valf();
   asm volatile("" : "+v"(r16), "+v"(kg));   // per-lane offsets recomputed per call, not hoisted
-  for (int pis = p0; pis < npst; pis += pstep) {
-    const unsigned char* kb = sb + pis * C::PB;
-    const unsigned char* vb = kb + C::KVB;
-    // Valid tokens of this page (a segment of the chain may end inside it): from its page word.
-    const int vm1 = (int)((unsigned)__builtin_amdgcn_readfirstlane(pwords[pis]) >> kPageValidShift);
-    const bool last = vm1 < kPageTokens - 1;
-    const int last_valid = vm1 + 1;
-    int thr[NT];
-#pragma unroll
-    for (int t = 0; t < NT; ++t) thr[t] = CAUSAL ? cl[t] - kPageTokens * pis : 0;
-    f32x4 S[NT];
-#pragma unroll
-    for (int t = 0; t < NT; ++t) S[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-    float p[NT][4];
-    if constexpr (BF16) {
-      // V^T operand of column block n: lane reads 4 tokens (4 kg + r16 / 4 supplies the row) of
-      // 4 columns through the transposing read; the chunk index is permuted like the writes.
-      // With two row tiles the V operands are read in two batches (register budget).
-      constexpr int VB = NT == 2 ? NBW / 2 : NBW;
-      const int tv = 4 * kg + (r16 >> 2);
-      auto vread = [&](int n) {
-        const int off = tv * C::ROW + (((2 * n + ((r16 & 3) >> 1)) ^ (tv & (C::CPR - 1))) << 4) +
-                        (r16 & 1) * 8;
-        return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vb + off));
-      };
-      bf16x8 ka[C::QR];
-      s16x4 va[VB];
-#pragma unroll
-      for (int jj = 0; jj < C::QR; ++jj)
-        ka[jj] = *reinterpret_cast<const bf16x8*>(kb + swz<D, BF16>(r16, 4 * jj + kg));
-#pragma unroll
-      for (int i = 0; i < VB; ++i) va[i] = vread(n0 + i);
-#pragma unroll
-      for (int jj = 0; jj < C::QR; ++jj)
-#pragma unroll
-        for (int t = 0; t < NT; ++t)
-          S[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[jj], qop[t][jj].v, S[t], 0, 0, 0);
-      softmax_page<NT, NBW, Cfg<D, BF16>::NB, CAUSAL>(S, p, m, l, O, last, last_valid, cm, thr,
-                                                       kg, sl2);
-      s16x4 pb[NT];
-#pragma unroll
-      for (int t = 0; t < NT; ++t)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) pb[t][i] = __builtin_bit_cast(short, (__bf16)p[t][i]);
-#pragma unroll
-      for (int i0 = 0; i0 < NBW; i0 += VB) {
-        if (i0 > 0) {
-#pragma unroll
-          for (int i = 0; i < VB; ++i) va[i] = vread(n0 + i0 + i);
-        }
-#pragma unroll
-        for (int i = 0; i < VB; ++i)
-#pragma unroll
-          for (int t = 0; t < NT; ++t)
-            O[t][i0 + i] =
-                __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va[i], pb[t], O[t][i0 + i], 0, 0, 0);
-      }
-    } else {
-#pragma unroll
-      for (int jj = 0; jj < C::QR; ++jj) {
-        const float ka = *reinterpret_cast<const float*>(kb + swz<D, BF16>(r16, jj) + kg * 4);
-#pragma unroll
-        for (int t = 0; t < NT; ++t)
-          S[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(ka, qop[t][jj].v, S[t], 0, 0, 0);
-      }
-      softmax_page<NT, NBW, Cfg<D, BF16>::NB, CAUSAL>(S, p, m, l, O, last, last_valid, cm, thr,
-                                                       kg, sl2);
-#pragma unroll
-      for (int i = 0; i < NBW; ++i) {
-        const int n = n0 + i;
-#pragma unroll
-        for (int i4 = 0; i4 < 4; ++i4) {
-          const int tv = 4 * kg + i4;
-          const float va = *reinterpret_cast<const float*>(
-              vb + swz<D, BF16>(tv, 4 * n + (r16 >> 2)) + (r16 & 3) * 4);
-#pragma unroll
-          for (int t = 0; t < NT; ++t)
-            O[t][i] = __builtin_amdgcn_mfma_f32_16x16x4f32(va, p[t][i4], O[t][i], 0, 0, 0);
-        }
-      }
+  int pis = p0;
+  if constexpr (BF16) {
+    for (; pis + pstep < npst; pis += 2 * pstep) {
+      const int pg[2] = {pis, pis + pstep};
+      kv_pages<D, BF16, 2, NT, NBW, CAUSAL>(sb, pwords, pg, sl2, r16, kg, n0, cm, cl, qop, m, l,
+                                            O);
     }
-    (void)NEG_INF;
+  }
+  for (; pis < npst; pis += pstep) {
+    const int pg[1] = {pis};
+    kv_pages<D, BF16, 1, NT, NBW, CAUSAL>(sb, pwords, pg, sl2, r16, kg, n0, cm, cl, qop, m, l, O);
   }
 }
 
@@ -394,13 +462,25 @@ void k_seg_attn(AttnArgs a) {
     c_rest[i] = kv * C::KVB + ((pc ^ (tok & (C::CPR - 1))) << 4);
   }
 
-  // The first two units of workgroup i are units i and i + grid, taken without a claim: the
-  // whole grid claiming at once serialises on the counter for several microseconds, and the
-  // first claim then comes during the second unit, when the workgroups are out of step.  The
-  // first unit's descriptor is copied before the loop.  Later units are claimed through the
-  // counter, which counts claims past the first two grids of units.
+  // Work streams: stream s holds the units of the kv heads h = s mod ns in item order (its unit
+  // j is unit (j / per) Hkv + (j mod per) ns + s) and is owned by the gs(s) workgroups with
+  // blockIdx = s mod ns.  The owner of rank r takes stream units r and r + gs(s) without a
+  // claim: the whole grid claiming at once serialises on the counters for several microseconds,
+  // and the first claim then comes during the second unit, when the workgroups are out of step.
+  // Later units are claimed through the stream's head, which counts claims past its first
+  // 2 gs(s) units; a workgroup whose stream is exhausted claims from the next streams.
+  const int ns = a.streams;
+  const int per = a.Hkv / ns;
+  const int n_str = (int)(a.counters[0] * per);
+  int* heads = reinterpret_cast<int*>(a.counters + 4);
+  auto gs = [&](int st) { return ((int)gridDim.x - st + ns - 1) / ns; };
+  auto unit_of = [&](int j, int st) {
+    return j < n_str ? (j / per) * a.Hkv + (j % per) * ns + st : n_work;
+  };
+  int cs = (int)blockIdx.x % ns;           // the stream claimed from
+  const int rank = (int)blockIdx.x / ns;
   if (wave == 0) {
-    fetch_desc((int)blockIdx.x, 0);
+    fetch_desc(unit_of(rank, cs), 0);
     wait_vmcnt(0);
   }
   __syncthreads();
@@ -491,13 +571,15 @@ void k_seg_attn(AttnArgs a) {
       const unsigned char* pool_h = (const unsigned char*)uniform64(
           (int64_t)(uintptr_t)(pool + (int64_t)kvh * 2 * C::KVB));
   
-      // The row blocks of one chunk (which several workgroups stream at about the same time)
-      // start at different pages: the full stages are taken in rotated order (a partial last
-      // stage stays last), so that they do not all ask for the same page at once.  Issue
-      // order st, ring slot st mod NBUF; stage_of(st) is the stage of the chunk it holds.
+      // With one work stream, the row blocks of one chunk (which workgroups on every XCD stream
+      // at about the same time) start at different pages: the full stages are taken in rotated
+      // order (a partial last stage stays last), so that they do not all ask for the same page
+      // at once.  With several streams they share the L2s of few XCDs, and taking the pages in
+      // the same order lets the later ones find what the first fetched.  Issue order st, ring
+      // slot st mod NBUF; stage_of(st) is the stage of the chunk it holds.
       const int nfull = np / C::SP;
       const int nrb_c = (cnt * a.group + kRowsPerBlock - 1) / kRowsPerBlock;
-      const int rot = nfull > 1 ? (rb * nfull) / nrb_c : 0;
+      const int rot = ns == 1 && nfull > 1 ? (rb * nfull) / nrb_c : 0;
       auto stage_of = [&](int st) {
         int x = st + rot;
         if (x >= nfull) x -= nfull;
@@ -541,17 +623,29 @@ void k_seg_attn(AttnArgs a) {
       QOp<BF16> qop[NT][C::QR];
       load_q(qop);
       int claim = 0;
-      if (!first && wave == 0 && lane == 0)
-        claim = atomicAdd(reinterpret_cast<int*>(&a.counters[2]), 1);
+      if (!first && wave == 0 && lane == 0) claim = atomicAdd(&heads[cs], 1);
       wait_vmcnt(0);
       // (the claim is consumed only here, after the wait, so that no use of it before the wait
       // makes the compiler wait for it, and with it for every copy in flight)
       asm volatile("" : "+v"(claim));
       // Wave 0 fetches the next unit's descriptor while this one streams.
-      if (wave == 0)
-        fetch_desc(first ? (int)blockIdx.x + (int)gridDim.x
-                         : 2 * (int)gridDim.x + __builtin_amdgcn_readfirstlane(claim),
-                   b ^ 1);
+      if (wave == 0) {
+        int v;
+        if (first) {
+          v = unit_of(rank + gs(cs), cs);
+        } else {
+          int j = 2 * gs(cs) + __builtin_amdgcn_readfirstlane(claim);
+          // (a stream found exhausted stays so: each claim tries every stream at most once)
+          for (int t = 1; j >= n_str && t < ns; ++t) {
+            cs = cs + 1 == ns ? 0 : cs + 1;
+            int c = 0;
+            if (lane == 0) c = atomicAdd(&heads[cs], 1);
+            j = 2 * gs(cs) + __builtin_amdgcn_readfirstlane(c);
+          }
+          v = unit_of(j, cs);
+        }
+        fetch_desc(v, b ^ 1);
+      }
       first = false;
       for (int st = 0; st < nst; ++st) {
         // Wait until this wave's copies of stage st have landed (copies of later stages may stay

@@ -78,6 +78,7 @@ struct Sizes {
   int32_t S0 = 0, B0q = 0, CS = 0;   // segments; branches of a multi-query plan; chain entries
   int64_t P0 = 0;                    // entries of the page table as given
   int32_t chunk_pages = 0;
+  bool few_pages = false;      // under 64 pages (x kv-heads) per workgroup at two per CU
   int64_t max_items = 0;       // upper bound on work items per kv-head
   int32_t desc_words = 0;      // work-item descriptor stride (int32 words)
   int64_t prows = 0;           // partial rows per q-head
@@ -337,6 +338,9 @@ void size_schedule(const ga_segment_table* st, const ga_branch_paths* bp, const 
   const int64_t floor_pages = std::min<int64_t>(24, std::max<int64_t>(4, (work + wgs - 1) / wgs));
   if (cap < floor_pages) cap = floor_pages;
   z->chunk_pages = (int32_t)cap;
+  // A step this small gives each workgroup one or two units, whose fixed costs (first pages'
+  // latency, partial stores) three workgroups per CU overlap better than two (bf16 decode).
+  z->few_pages = work < 64 * wgs;
   const int32_t group = p->num_q_heads / p->num_kv_heads;
   int64_t chunks_ref = 0, prows = 0;
   for (int32_t s = 0; s < z->S; ++s)
@@ -732,14 +736,16 @@ ga_status do_run(ga_plan* pl, const void* q, const void* pool, void* out, float*
   a.desc_words = pl->z.desc_words;
   a.streams = ga::attn_streams(a.Hkv, pl->causal);
   a.scale_log2 = pl->p.softmax_scale * 1.4426950408889634f;
-  int64_t grid = (int64_t)ga::seg_attn_grid(pl->p.head_dim, bf16, pl->causal, pl->num_cus);
+  int64_t grid = (int64_t)ga::seg_attn_grid(pl->p.head_dim, bf16, pl->causal, pl->z.few_pages,
+                                            pl->num_cus);
   const int64_t work = pl->z.max_items * pl->p.num_kv_heads;
   if (work < grid) grid = work;
   const bool rec = pl->prof_runs < pl->prof_cap;
   hipEvent_t* ev = rec ? &pl->ev_run[3 * pl->prof_runs] : nullptr;
   if (rec) GA_HIP(hipEventRecord(ev[0], stream), "profile event");
   if (grid > 0)
-    GA_HIP(ga::launch_seg_attn(a, pl->p.head_dim, bf16, pl->causal, (int)grid, stream),
+    GA_HIP(ga::launch_seg_attn(a, pl->p.head_dim, bf16, pl->causal, pl->z.few_pages, (int)grid,
+                               stream),
            "attention launch");
   if (rec) GA_HIP(hipEventRecord(ev[1], stream), "profile event");
   ga::MergeArgs m{};

@@ -219,8 +219,9 @@ hipError_t launch_set_lengths(const LengthArgs& a, hipStream_t stream);
 hipError_t launch_schedule(const DevGraph& g, const DevSchedule& sc, int32_t group,
                            int32_t chunk_pages, int64_t max_items, bool reuse,
                            hipStream_t stream);
-hipError_t launch_seg_attn(const AttnArgs& a, int head_dim, bool bf16, bool causal, int grid,
-                           hipStream_t stream);
+// few_pages: a decode step with under 64 pages (times kv-heads) per workgroup at two per CU.
+hipError_t launch_seg_attn(const AttnArgs& a, int head_dim, bool bf16, bool causal,
+                           bool few_pages, int grid, hipStream_t stream);
 hipError_t launch_merge(const MergeArgs& a, int head_dim, bool out_bf16, bool part_f16,
                         hipStream_t stream);
 hipError_t launch_kv_write(const KvWriteArgs& a, hipStream_t stream);
@@ -229,7 +230,7 @@ hipError_t launch_suffix_count(const SuffixArgs& a, hipStream_t stream);
 hipError_t launch_suffix_fill(const SuffixArgs& a, hipStream_t stream);
 hipError_t launch_advantages(const RewardArgs& a, hipStream_t stream);
 // Number of co-resident attention workgroups the persistent grid uses on this device.
-int seg_attn_grid(int head_dim, bool bf16, bool causal, int num_cus);
+int seg_attn_grid(int head_dim, bool bf16, bool causal, bool few_pages, int num_cus);
 // Work streams of an attention launch (the largest power of two dividing Hkv and
 // kMaxStreams): multi-query units split a shared chunk into many row blocks, each of which
 // reads the chunk, so they are kept on few XCDs.  Decode units mostly hold one row block per

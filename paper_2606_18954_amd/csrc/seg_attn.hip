@@ -51,13 +51,15 @@ typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
 // Workgroups per CU and ring depth: two workgroups with four stages for decode; the bf16
 // multi-query variant runs three workgroups per CU (its 128-row units are bound by each wave's
-// issue and compute, so more waves per CU pay more than a deeper ring) with three stages each.
-// (The fp32 variant keeps two: at three its 32 query registers per tile would spill.)
-__host__ __device__ constexpr int attn_wgs_per_cu(bool causal, bool bf16) {
-  return causal && bf16 ? 3 : 2;
+// issue and compute, so more waves per CU pay more than a deeper ring) with three stages each,
+// and so does bf16 decode on a step with few pages per workgroup (each workgroup then has one
+// or two units, whose fixed costs more workgroups overlap better).  (The fp32 variants keep
+// two: at three their 32 query registers per tile would spill.)
+__host__ __device__ constexpr int attn_wgs_per_cu(bool causal, bool bf16, bool few_pages) {
+  return bf16 && (causal || few_pages) ? 3 : 2;
 }
 
-template <int D, bool BF16, bool CAUSAL = false>
+template <int D, bool BF16, int WPC = 2>
 struct Cfg {
   static constexpr int ELT = BF16 ? 2 : 4;
   static constexpr int ROW = D * ELT;               // bytes of one token row of K or V
@@ -66,7 +68,7 @@ struct Cfg {
   static constexpr int PB = 2 * KVB;                // bytes of one page of one kv-head
   static constexpr int STAGE = GA_STAGE_BYTES >= PB ? GA_STAGE_BYTES : PB;   // bytes per stage
   static constexpr int SP = STAGE / PB;             // pages per stage
-  static constexpr int NBUF = attn_wgs_per_cu(CAUSAL, BF16) == 3 ? 3 : GA_RING_STAGES;   // stages
+  static constexpr int NBUF = WPC == 3 ? 3 : GA_RING_STAGES;   // stages
   static constexpr int IPP = PB / 1024;             // 1 KiB DMA wave instructions per page
   static constexpr int IPW = IPP / (kAttnThreads / 64);   // ... issued by each wave per page
   static constexpr int NB = D / 16;                 // 16-wide output column blocks
@@ -402,10 +404,10 @@ __device__ __forceinline__ void kv_stage(const unsigned char* sb, const int* pwo
 // CAUSAL: the multi-query variant.  A unit whose descriptor carries a causal word c (word 1;
 // kNoCausal otherwise) lets the row of group rank j see token t of the chunk (t counted as
 // 16 x page index + slot) only for t <= c + j.
-template <int D, bool BF16, bool CAUSAL>
-__global__ __launch_bounds__(kAttnThreads, attn_wgs_per_cu(CAUSAL, BF16))
+template <int D, bool BF16, bool CAUSAL, int WPC>
+__global__ __launch_bounds__(kAttnThreads, WPC)
 void k_seg_attn(AttnArgs a) {
-  using C = Cfg<D, BF16, CAUSAL>;
+  using C = Cfg<D, BF16, WPC>;
   using T = typename std::conditional<BF16, __bf16, float>::type;
   constexpr int NI = C::SP * C::IPW;                // copies per wave per full stage
   __shared__ __align__(1024) unsigned char smem[C::NBUF * C::STAGE];
@@ -793,30 +795,39 @@ void k_seg_attn(AttnArgs a) {
 }
 
 template <int D, bool BF16>
-hipError_t launch_t(const AttnArgs& a, bool causal, int grid, hipStream_t stream) {
+hipError_t launch_t(const AttnArgs& a, bool causal, bool few_pages, int grid,
+                    hipStream_t stream) {
+  constexpr int W_CAUSAL = attn_wgs_per_cu(true, BF16, false);
+  constexpr int W_WIDE = attn_wgs_per_cu(false, BF16, true);
+  constexpr int W_DECODE = attn_wgs_per_cu(false, BF16, false);
   if (causal)
-    hipLaunchKernelGGL((k_seg_attn<D, BF16, true>), dim3(grid), dim3(kAttnThreads), 0, stream, a);
+    hipLaunchKernelGGL((k_seg_attn<D, BF16, true, W_CAUSAL>), dim3(grid), dim3(kAttnThreads), 0,
+                       stream, a);
+  else if (few_pages && W_WIDE != W_DECODE)
+    hipLaunchKernelGGL((k_seg_attn<D, BF16, false, W_WIDE>), dim3(grid), dim3(kAttnThreads), 0,
+                       stream, a);
   else
-    hipLaunchKernelGGL((k_seg_attn<D, BF16, false>), dim3(grid), dim3(kAttnThreads), 0, stream, a);
+    hipLaunchKernelGGL((k_seg_attn<D, BF16, false, W_DECODE>), dim3(grid), dim3(kAttnThreads), 0,
+                       stream, a);
   return hipGetLastError();
 }
 
 }  // namespace
 
-int seg_attn_grid(int head_dim, bool bf16, bool causal, int num_cus) {
+int seg_attn_grid(int head_dim, bool bf16, bool causal, bool few_pages, int num_cus) {
   (void)head_dim;
-  (void)bf16;
-  return num_cus * attn_wgs_per_cu(causal, bf16);   // 256-thread workgroups (LDS-bound)
+  // 256-thread workgroups (LDS-bound)
+  return num_cus * attn_wgs_per_cu(causal, bf16, few_pages);
 }
 
-hipError_t launch_seg_attn(const AttnArgs& a, int head_dim, bool bf16, bool causal, int grid,
-                           hipStream_t stream) {
+hipError_t launch_seg_attn(const AttnArgs& a, int head_dim, bool bf16, bool causal,
+                           bool few_pages, int grid, hipStream_t stream) {
   if (bf16) {
-    if (head_dim == 64) return launch_t<64, true>(a, causal, grid, stream);
-    if (head_dim == 128) return launch_t<128, true>(a, causal, grid, stream);
+    if (head_dim == 64) return launch_t<64, true>(a, causal, few_pages, grid, stream);
+    if (head_dim == 128) return launch_t<128, true>(a, causal, few_pages, grid, stream);
   } else {
-    if (head_dim == 64) return launch_t<64, false>(a, causal, grid, stream);
-    if (head_dim == 128) return launch_t<128, false>(a, causal, grid, stream);
+    if (head_dim == 64) return launch_t<64, false>(a, causal, few_pages, grid, stream);
+    if (head_dim == 128) return launch_t<128, false>(a, causal, few_pages, grid, stream);
   }
   return hipErrorInvalidValue;
 }

@@ -16,7 +16,7 @@
 namespace ga {
 hipError_t launch_schedule(const DevGraph&, const DevSchedule&, int32_t, int32_t, int64_t, bool,
                            hipStream_t) { std::abort(); }
-hipError_t launch_seg_attn(const AttnArgs&, int, bool, bool, int, hipStream_t) { std::abort(); }
+hipError_t launch_seg_attn(const AttnArgs&, int, bool, bool, bool, int, hipStream_t) { std::abort(); }
 hipError_t launch_merge(const MergeArgs&, int, bool, bool, hipStream_t) { std::abort(); }
 hipError_t launch_kv_write(const KvWriteArgs&, hipStream_t) { std::abort(); }
 hipError_t launch_equivalence(const EquivArgs&, hipStream_t) { std::abort(); }
@@ -24,7 +24,7 @@ hipError_t launch_suffix_count(const SuffixArgs&, hipStream_t) { std::abort(); }
 hipError_t launch_suffix_fill(const SuffixArgs&, hipStream_t) { std::abort(); }
 hipError_t launch_advantages(const RewardArgs&, hipStream_t) { std::abort(); }
 hipError_t launch_set_lengths(const LengthArgs&, hipStream_t) { std::abort(); }
-int seg_attn_grid(int, bool, bool, int num_cus) { return 2 * num_cus; }
+int seg_attn_grid(int, bool, bool, bool, int num_cus) { return 2 * num_cus; }
 }  // namespace ga
 
 int main(int argc, char** argv) {

@@ -244,7 +244,7 @@ __device__ __forceinline__ void softmax_pages(f32x4 (&S)[NPG][NT], float (&p)[NP
   }
 }
 
-// NPG pages (pg[0 .. NPG-1] of the stage at sb) for one wave: NT row tiles (qop[0 .. NT-1])
+// NPG consecutive pages (p0, p0 + 1, ... of the stage at sb) for one wave: NT row tiles (qop[0 .. NT-1])
 // producing NBW output column blocks (O[t][i] holds column block n0 + i); for CAUSAL units,
 // cl[t] is the lane's row limit relative to the stage's first page.  All LDS operand reads of
 // the first column blocks are issued before the first MFMA, so they overlap S = K Q^T and the
@@ -255,8 +255,8 @@ __device__ __forceinline__ void softmax_pages(f32x4 (&S)[NPG][NT], float (&p)[NP
 // probabilities) are ordered alike, and a contraction does not depend on the order of its
 // terms.
 template <int D, bool BF16, int NPG, int NT, int NBW, bool CAUSAL>
-__device__ __forceinline__ void kv_pages(const unsigned char* sb, const int* pwords,
-                                         const int (&pg)[NPG], float sl2, int r16, int kg,
+__device__ __forceinline__ void kv_pages(const unsigned char* sb, const int* pwords, int p0,
+                                         float sl2, int r16, int kg,
                                          int n0, bool cm, const int (&cl)[NT],
                                          const QOp<BF16> (&qop)[NT][Cfg<D, BF16>::QR],
                                          float (&m)[NT], float (&l)[NT],
@@ -270,15 +270,15 @@ __device__ __forceinline__ void kv_pages(const unsigned char* sb, const int* pwo
   int thr[NPG][NT];
 #pragma unroll
   for (int g = 0; g < NPG; ++g) {
-    kb[g] = sb + pg[g] * C::PB;
+    kb[g] = sb + p0 * C::PB + g * C::PB;
     vb[g] = kb[g] + C::KVB;
     // Valid tokens of the page (a segment of the chain may end inside it): from its page word.
-    const int vm1 = (int)((unsigned)__builtin_amdgcn_readfirstlane(pwords[pg[g]]) >>
+    const int vm1 = (int)((unsigned)__builtin_amdgcn_readfirstlane(pwords[p0 + g]) >>
                           kPageValidShift);
     last[g] = vm1 < kPageTokens - 1;
     last_valid[g] = vm1 + 1;
 #pragma unroll
-    for (int t = 0; t < NT; ++t) thr[g][t] = CAUSAL ? cl[t] - kPageTokens * pg[g] : 0;
+    for (int t = 0; t < NT; ++t) thr[g][t] = CAUSAL ? cl[t] - kPageTokens * (p0 + g) : 0;
   }
   f32x4 S[NPG][NT];
 #pragma unroll
@@ -292,11 +292,15 @@ __device__ __forceinline__ void kv_pages(const unsigned char* sb, const int* pwo
     // The V operands are read in batches of VB column blocks (register budget).
     constexpr int VB = NT * NPG == 4 ? (NBW >= 8 ? NBW / 8 : 1) : NT * NPG == 2 ? NBW / 2 : NBW;
     static_assert(NBW % VB == 0, "column blocks come in whole batches");
+    // The lane's 32-byte piece of block n is chunk 2 n + c (c = (r16 & 3) / 2) of token row tv,
+    // XOR-permuted by x = tv mod CPR; (2 n + c) ^ x = (2 n ^ (x & ~1)) + (c ^ (x & 1)), so its
+    // offset is the one of block 0 with 32 n XORed in.
     const int tv = 4 * kg + (r16 >> 2);
+    const int xv = tv & (C::CPR - 1);
+    const int voff = tv * C::ROW + (((xv & ~1) | (((r16 & 3) >> 1) ^ (xv & 1))) << 4) +
+                     (r16 & 1) * 8;
     auto vread = [&](int g, int n) {
-      const int off = tv * C::ROW + (((2 * n + ((r16 & 3) >> 1)) ^ (tv & (C::CPR - 1))) << 4) +
-                      (r16 & 1) * 8;
-      return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vb[g] + off));
+      return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vb[g] + (voff ^ (n << 5))));
     };
     s16x4 va[VB][NPG];
 #pragma unroll
@@ -377,8 +381,8 @@ __device__ __forceinline__ void kv_pages(const unsigned char* sb, const int* pwo
   }
 }
 
-// One K/V stage for one wave: pages p0, p0 + pstep, ... below npst of the stage, in pairs where
-// two are left (bf16), then one at a time.
+// One K/V stage for one wave: pages p0, p0 + pstep, ... below npst of the stage; consecutive
+// ones (pstep = 1) in pairs where two are left (bf16), the others one at a time.
 template <int D, bool BF16, int NT, int NBW, bool CAUSAL>
 __device__ __forceinline__ void kv_stage(const unsigned char* sb, const int* pwords, int p0,
                                          int pstep, int npst, float sl2,
@@ -389,16 +393,13 @@ __device__ __forceinline__ void kv_stage(const unsigned char* sb, const int* pwo
   asm volatile("" : "+v"(r16), "+v"(kg));   // per-lane offsets recomputed per call, not hoisted
   int pis = p0;
   if constexpr (BF16) {
-    for (; pis + pstep < npst; pis += 2 * pstep) {
-      const int pg[2] = {pis, pis + pstep};
-      kv_pages<D, BF16, 2, NT, NBW, CAUSAL>(sb, pwords, pg, sl2, r16, kg, n0, cm, cl, qop, m, l,
-                                            O);
-    }
+    if (pstep == 1)
+      for (; pis + 1 < npst; pis += 2)
+        kv_pages<D, BF16, 2, NT, NBW, CAUSAL>(sb, pwords, pis, sl2, r16, kg, n0, cm, cl, qop, m,
+                                              l, O);
   }
-  for (; pis < npst; pis += pstep) {
-    const int pg[1] = {pis};
-    kv_pages<D, BF16, 1, NT, NBW, CAUSAL>(sb, pwords, pg, sl2, r16, kg, n0, cm, cl, qop, m, l, O);
-  }
+  for (; pis < npst; pis += pstep)
+    kv_pages<D, BF16, 1, NT, NBW, CAUSAL>(sb, pwords, pis, sl2, r16, kg, n0, cm, cl, qop, m, l, O);
 }
 
 // CAUSAL: the multi-query variant.  A unit whose descriptor carries a causal word c (word 1;

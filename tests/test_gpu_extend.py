@@ -148,6 +148,36 @@ def test_extend_full_size_sampled():
     check(wl, rows=rows, out_f32=False, plan=True)
 
 
+def test_extend_full_size_runs_are_bit_identical():
+    """The full 16-token extend scheduled and run twice on one plan, and once more from a fresh
+    plan: the work streams hand units to whichever workgroup claims them first (and workgroups
+    whose stream is empty claim from the others), but every unit's partial depends only on the
+    unit, so all three runs give the same bits."""
+    require_gpu()
+    wl = W.config3_extend()
+    q, pool = wl.q.cuda(), wl.pool.cuda()
+    hg = G.HostGraph.from_graph(wl.graph)
+    p = params_of(wl)
+    R = int(wl.query_counts.sum())
+    say(f"[case] full-size extend determinism: R={R}")
+
+    def run(pl):
+        out = torch.empty((R, wl.num_q_heads, wl.head_dim), dtype=q.dtype, device="cuda")
+        lse = torch.empty((R, wl.num_q_heads), dtype=torch.float32, device="cuda")
+        pl.schedule()
+        pl.run(q, pool, out, lse)
+        torch.cuda.synchronize()
+        return out.view(torch.int16).cpu(), lse.cpu()
+
+    with G.Plan(hg, p, query_counts=wl.query_counts) as pl:
+        o1, l1 = run(pl)
+        o2, l2 = run(pl)
+    with G.Plan(hg, p, query_counts=wl.query_counts) as pl:
+        o3, l3 = run(pl)
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
+    assert torch.equal(o1, o3) and torch.equal(l1, l3)
+
+
 # ---------------------------------------------------------------------------------------------
 # Page-pool writes
 # ---------------------------------------------------------------------------------------------

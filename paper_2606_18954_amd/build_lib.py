@@ -22,8 +22,8 @@ CFLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-function",
     # Packed-FP32 VALU forms are kept out of every kernel.
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-    # The attention kernel's work-queue atomic must stay a plain returning atomic whose result
-    # is read several iterations later (the optimizer would read it back at once).
+    # The attention kernel's work-stream atomics must stay plain returning atomics whose results
+    # are read several iterations later (the optimizer would read them back at once).
     "-mllvm", "-amdgpu-atomic-optimizer-strategy=None",
     "-I", os.path.join(ROOT, "include"),
 ]

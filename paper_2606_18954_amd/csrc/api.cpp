@@ -717,9 +717,9 @@ ga_status do_run(ga_plan* pl, const void* q, const void* pool, void* out, float*
     if (rc) return rc;
   }
   if (pl->z.B == 0) return GA_OK;
-  // The merge re-arms the attention kernel's work-queue head; a schedule clears it as well.  If
-  // a launch below fails, the plan loses its schedule, so the next run schedules (and so
-  // re-arms the queue) before it attends.
+  // The merge re-arms the attention kernel's work-stream heads; a schedule clears them as
+  // well.  If a launch below fails, the plan loses its schedule, so the next run schedules (and
+  // so re-arms the heads) before it attends.
   pl->scheduled = false;
   const bool bf16 = pl->p.dtype == GA_BF16;
   ga::AttnArgs a{};

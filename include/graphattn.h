@@ -197,6 +197,8 @@ typedef struct {
                                  (equal to the rows in use when segments own no spare pages) */
   int32_t num_chains;         /* chains scheduled (segments on some path, after merging runs) */
   int32_t num_query_rows;     /* rows of q / out / lse: B for decode plans, sum_b n_b for extend */
+  int32_t workgroups_per_cu;  /* attention workgroups resident per CU in the persistent grid */
+  int32_t work_streams;       /* work streams the attention units are split into (by kv-head) */
 } ga_plan_info;
 ga_status graphattn_plan_info(const ga_plan* plan, ga_plan_info* info);
 

@@ -929,6 +929,9 @@ ga_status graphattn_plan_info(const ga_plan* plan, ga_plan_info* info) {
   info->rows_per_block = ga::kRowsPerBlock;
   info->num_items = -1;
   info->num_partial_rows = plan->z.prows;
+  info->workgroups_per_cu = ga::seg_attn_grid(plan->p.head_dim, plan->p.dtype == GA_BF16,
+                                              plan->causal, plan->z.few_pages, 1);
+  info->work_streams = ga::attn_streams(plan->p.num_kv_heads, plan->causal);
   if (plan->scheduled) {
     int64_t n = 0;
     if (hipMemcpy(&n, plan->sc.counters, sizeof n, hipMemcpyDeviceToHost) == hipSuccess)

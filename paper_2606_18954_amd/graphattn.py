@@ -54,7 +54,8 @@ class PlanInfo(ctypes.Structure):
                 ("num_entries", ctypes.c_int32), ("chunk_pages", ctypes.c_int32),
                 ("rows_per_block", ctypes.c_int32), ("num_items", ctypes.c_int64),
                 ("num_partial_rows", ctypes.c_int64), ("num_chains", ctypes.c_int32),
-                ("num_query_rows", ctypes.c_int32)]
+                ("num_query_rows", ctypes.c_int32), ("workgroups_per_cu", ctypes.c_int32),
+                ("work_streams", ctypes.c_int32)]
 
 
 class StateForest(ctypes.Structure):

@@ -75,6 +75,25 @@ def test_group_size_one_at_the_longest_chunks():
     check_workload(wl, branches=[0, 17, 42, 63], out_f32=True)
 
 
+@pytest.mark.parametrize("Hq,Hkv,D", [(16, 8, 64), (40, 8, 128)])
+def test_large_steps_run_two_workgroups_per_cu(Hq, Hkv, D):
+    """bf16 decode steps with at least 64 pages (times kv-heads) per workgroup at two per CU run
+    the kernel built for two workgroups per CU, smaller ones the one for three: a random graph
+    past that size at each head_dim (most parity cases here are small), sampled branches, and
+    the 7B tree below it."""
+    rng = np.random.default_rng(D + Hkv)
+    g = W.random_graph(rng, 100, 96, 1800, 6, slack_pages=4, seed=D + Hkv)
+    wl = W.make_workload(f"random {Hq}/{Hkv}/{D} bf16, {g.num_pages} pages", g, Hq, Hkv, D,
+                         "bf16", D + Hkv, poison=True)
+    with G.Plan(G.HostGraph.from_graph(g), params_of(wl)) as plan:
+        inf = plan.info()
+        assert (inf.workgroups_per_cu, inf.work_streams) == (2, 1)
+    check_workload(wl, branches=W.sample_branches(g, 24, D), out_f32=True)
+    small = W.config2_tree(prompts=3)
+    with G.Plan(G.HostGraph.from_graph(small.graph), params_of(small)) as plan:
+        assert (plan.info().workgroups_per_cu, plan.info().work_streams) == (3, 1)
+
+
 @pytest.mark.parametrize("name", ["c3", "c4", "c5chain", "c5graph"])
 def test_full_size_every_branch(name):
     """Full-size configurations in the launch configuration the benchmark times (plan, GPU

@@ -52,12 +52,20 @@ __global__ void k_count(DevGraph g, DevSchedule sc) {
   atomicAdd(&sc.grp_cnt[g.path_segs[e]], 1);
 }
 
-// Cost of one work item of segment s (pages of a chunk x per-page work), used to order the
-// work list longest first so the persistent grid does not end on a long item.
+// Chunk c of a segment of npg pages cut into nch chunks: pages [c npg / nch, (c + 1) npg / nch),
+// so the chunks of one segment differ by at most a page (each at most chunk_pages, since
+// nch = ceil(npg / chunk_pages)) instead of ending on a short remainder.
+__device__ __forceinline__ int chunk_first_page(int c, int npg, int nch) {
+  return (int)(((int64_t)c * npg) / nch);
+}
+
+// Cost of one work item of segment s (pages of its longest chunk x per-page work), used to
+// order the work list longest first so the persistent grid does not end on a long item.
 __device__ __forceinline__ uint32_t item_cost(int npg, int cnt, int group, int chunk_pages) {
   const int rows = min(cnt * group, kRowsPerBlock);
   const int tiles = (rows + 15) / 16;
-  return (uint32_t)(min(npg, chunk_pages) * (2 + tiles));
+  const int nch = (npg + chunk_pages - 1) / chunk_pages;
+  return (uint32_t)(((npg + nch - 1) / max(nch, 1)) * (2 + tiles));
 }
 
 // Cost class of a work item: half-octave bins of item_cost (0 for a segment without items).
@@ -354,8 +362,8 @@ __device__ __forceinline__ void emit_items(const DevGraph& g, const DevSchedule&
   const int64_t poff = g.seg_page_off[s];
   const int last_valid = len - (npg - 1) * kPageTokens;
   for (int c = 0; c < nch; ++c) {
-    const int p0 = c * chunk_pages;
-    const int np = min(npg, p0 + chunk_pages) - p0;
+    const int p0 = chunk_first_page(c, npg, nch);
+    const int np = chunk_first_page(c + 1, npg, nch) - p0;
     for (int rbk = 0; rbk < nrb; ++rbk, ++w) {
       sc.items[w] = make_int4(s, c, rbk, 0);
       int4* d = reinterpret_cast<int4*>(sc.desc + w * sc.desc_words);
@@ -704,8 +712,9 @@ __global__ __launch_bounds__(kT) void k_emit(DevGraph g, DevSchedule sc, int32_t
   const int npg = (len + kPageTokens - 1) / kPageTokens;
   const int nrb = (cnt * group + kRowsPerBlock - 1) / kRowsPerBlock;
   const int c = kk / nrb, rb = kk - c * nrb;
-  const int p0 = c * chunk_pages;
-  const int np = min(npg, p0 + chunk_pages) - p0;
+  const int nch = (npg + chunk_pages - 1) / chunk_pages;
+  const int p0 = chunk_first_page(c, npg, nch);
+  const int np = chunk_first_page(c + 1, npg, nch) - p0;
   const int poff = (int)g.seg_page_off[s] + p0;
   int32_t* d = sc.desc + w * sc.desc_words;
   if (lane == 0) {

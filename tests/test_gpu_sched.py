@@ -58,14 +58,17 @@ def chains(g):
 
 def expected_items(g, group, chunk_pages, cnt):
     """Work list: items grouped by chain, chains by descending cost class of the per-item cost
-    (chunk pages x (2 + row tiles)), ties by first segment; within a chain chunk-major.  An item
+    (pages of the chain's longest chunk x (2 + row tiles); a chain's chunks split its pages as
+    evenly as whole pages allow), ties by first segment; within a chain chunk-major.  An item
     names its chain by the chain's first segment."""
     def npg(s):
         return (int(g.seg_len[s]) + 15) // 16
 
     def cost(c):
         tiles = (min(cnt[c[0]] * group, ROWS_PER_BLOCK) + 15) // 16
-        return min(sum(npg(s) for s in c), chunk_pages) * (2 + tiles)
+        pages = sum(npg(s) for s in c)
+        nch = (pages + chunk_pages - 1) // chunk_pages
+        return -(-pages // nch) * (2 + tiles)
 
     order = sorted(chains(g), key=lambda c: (-cost_class(cost(c)), c[0]))
     items = []

@@ -646,6 +646,10 @@ def main():
                          "(1, the default) and report them under configs / decode_loop")
     ap.add_argument("--other-steps", type=int, default=20,
                     help="timed steps per region for the other configurations")
+    ap.add_argument("--cpu-configs", action="store_true",
+                    help="decode only: also time the CPU oracle on a bounded seeded sample of "
+                         "each other configuration (reported under cpu_configs; minutes of CPU "
+                         "work, off by default)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 1 GiB device copy (torch elementwise kernel) so HBM "
                          "counters can be scaled against a kernel of known traffic")
@@ -766,6 +770,18 @@ def main():
         log(f"timing the CPU oracle on {args.cpu_sample} branches")
         res["cpu_baseline"] = cpu_baseline(wl, args.cpu_sample)
         log("CPU oracle done")
+    if args.cpu_configs:
+        # Branches per configuration: all of the small ones, a seeded sample of the long ones
+        # (the oracle materialises each branch's whole context in fp64).
+        sample = {"c1": 4, "c2": 128, "c3": 1024, "c4": 16, "c5chain": 32, "c5graph": 64}
+        res["cpu_configs"] = {}
+        for name in ["c1", "c2", "c3", "c4", "c5chain", "c5graph"]:
+            if name == args.config:
+                continue
+            other = W.CONFIGS[name]()
+            log(f"timing the CPU oracle on {name} ({sample[name]} branches)")
+            res["cpu_configs"][name] = cpu_baseline(other, sample[name])
+            del other
     print(json.dumps(res), flush=True)
 
 

@@ -504,11 +504,14 @@ void k_seg_attn(AttnArgs a) {
     const int R = min(kRowsPerBlock, cnt * a.group - row0);
     const int nrt = (R + 15) >> 4;
 
-    // Wave roles: with >= 3 row tiles the waves split the tiles (tiles wave and wave + 4); with
-    // fewer, waves sharing a tile split the stage's pages and are combined at the end.
+    // Wave roles: with >= 3 row tiles the waves split the tiles (tiles wave and wave + 4), and
+    // so they do with fewer at two workgroups per CU (the tile owners take every page: there the
+    // hand-over below costs more than the idle waves); at three workgroups per CU (steps with
+    // few pages per workgroup) waves sharing a tile split the stage's pages and are combined at
+    // the end.
     int ks, split, t0, ntile;
     if (nrt >= 4) { ks = 1; split = 0; t0 = wave; ntile = (wave + 4 < nrt) ? 2 : 1; }
-    else if (nrt == 3) { ks = 1; split = 0; t0 = wave; ntile = wave < 3 ? 1 : 0; }
+    else if (nrt == 3 || WPC == 2) { ks = 1; split = 0; t0 = wave; ntile = wave < nrt ? 1 : 0; }
     else if (nrt == 2) {
       ks = C::SP < 2 ? C::SP : 2; split = wave >> 1; t0 = wave & 1; ntile = split < ks;
     } else {

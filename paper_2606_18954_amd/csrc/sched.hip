@@ -151,7 +151,7 @@ __device__ void scan_segments(const DevGraph& g, const DevSchedule& sc, int32_t 
     const int lane = t & 63, wv = t >> 6;
     const uint64_t lt = lane ? (~0ull >> (64 - lane)) : 0ull;
     const int nslots = (S + 1023) >> 10;
-    int* cw = reinterpret_cast<int*>(&sh[0][0]);   // [(slot * 16 + wave) * NBK + class]
+    int* cw = reinterpret_cast<int*>(&sh[0][0]);   // [class * 64 + slot * 16 + wave]
     int* tot = reinterpret_cast<int*>(&sh[2][0]);  // [class] totals, then [NBK + class] offsets
     __syncthreads();                               // readers of the last scan are done
     for (int i = t; i < 4 * 16 * NBK; i += 1024) cw[i] = 0;
@@ -180,21 +180,21 @@ __device__ void scan_segments(const DevGraph& g, const DevSchedule& sc, int32_t 
         }
         bk[u] = bucket;
         wr[u] = __popcll(m & lt);
-        if (valid && (m & lt) == 0) cw[(u * 16 + wv) * NBK + bucket] = __popcll(m);
+        if (valid && (m & lt) == 0) cw[bucket * 64 + u * 16 + wv] = __popcll(m);
       }
     }
     __syncthreads();
 #pragma unroll
     for (int h = 0; h < 2; ++h) {                  // wave wv: classes wv and wv + 16
       const int c = wv + 16 * h;
-      const int v = cw[lane * NBK + c];
+      const int v = cw[c * 64 + lane];
       int x = v;
 #pragma unroll
       for (int off = 1; off < 64; off <<= 1) {
         const int y = __shfl_up(x, off);
         if (lane >= off) x += y;
       }
-      cw[lane * NBK + c] = x - v;
+      cw[c * 64 + lane] = x - v;
       if (lane == 63) tot[c] = x;
     }
     __syncthreads();
@@ -213,7 +213,7 @@ __device__ void scan_segments(const DevGraph& g, const DevSchedule& sc, int32_t 
     for (int u = 0; u < 4; ++u) {
       const int sg = 1024 * u + t;
       if (u < nslots && sg < S)
-        keys[tot[NBK + bk[u]] + cw[(u * 16 + wv) * NBK + bk[u]] + wr[u]] = (uint64_t)sg;
+        keys[tot[NBK + bk[u]] + cw[bk[u] * 64 + u * 16 + wv] + wr[u]] = (uint64_t)sg;
     }
     __syncthreads();
   } else if (sorted) {
@@ -411,7 +411,7 @@ __global__ __launch_bounds__(1024) void k_sched_one(DevGraph g, DevSchedule sc, 
   __shared__ int l_part[kSmallEntries];                   // each entry's first partial slot
   __shared__ int l_cnt[kSmallSegs];                       // |B(s)|
   __shared__ int l_cur[kSmallSegs];                       // scatter cursors, then work-list order
-  __shared__ int l_cw[4 * 16 * NBK];                      // sort: counts per (slot, wave, class)
+  __shared__ int l_cw[NBK * 4 * 16];                      // sort: counts per (class, slot, wave)
   __shared__ int l_boff[NBK];                             // sort: first position of each class
   __shared__ int l_wsum[2][3][16];                        // wave totals of the two block scans
   int* const l_order = l_cur;
@@ -564,7 +564,7 @@ __global__ __launch_bounds__(1024) void k_sched_one(DevGraph g, DevSchedule sc, 
         }
         bk[u] = bin;
         wr[u] = __popcll(m & lt);
-        if (valid && (m & lt) == 0) l_cw[(u * 16 + wv) * NBK + bin] = __popcll(m);
+        if (valid && (m & lt) == 0) l_cw[bin * 64 + u * 16 + wv] = __popcll(m);
       }
     }
   }
@@ -579,9 +579,9 @@ __global__ __launch_bounds__(1024) void k_sched_one(DevGraph g, DevSchedule sc, 
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
     const int c = wv + 16 * h;
-    const int v = l_cw[lane * NBK + c];
+    const int v = l_cw[c * 64 + lane];           // (class-major: one contiguous row per class)
     const int x = wave_scan_incl(v);
-    l_cw[lane * NBK + c] = x - v;
+    l_cw[c * 64 + lane] = x - v;
     if (lane == 63) l_boff[c] = x;                 // class total, made an offset below
   }
   lds_barrier();
@@ -615,7 +615,7 @@ __global__ __launch_bounds__(1024) void k_sched_one(DevGraph g, DevSchedule sc, 
 #pragma unroll
   for (int u = 0; u < SPT; ++u) {
     const int sg = 1024 * u + t;
-    if (u < nslots && sg < S) l_order[l_boff[bk[u]] + l_cw[(u * 16 + wv) * NBK + bk[u]] + wr[u]] = sg;
+    if (u < nslots && sg < S) l_order[l_boff[bk[u]] + l_cw[bk[u] * 64 + u * 16 + wv] + wr[u]] = sg;
   }
   lds_barrier();
 

@@ -637,7 +637,11 @@ __global__ __launch_bounds__(1024) void k_sched_one(DevGraph g, DevSchedule sc, 
         sc.seg_item_off[s] = w;
         sc.seg_order[i] = s;
         sc.order_item_off[i] = w;
-        w += l_cnt[s] > 0 ? nch_len(s) * nrb_of(s) : 0;
+        // The segment's items (chunk-major, then row block), which k_emit then reads directly.
+        const int nrb = nrb_of(s);
+        const int nit = l_cnt[s] > 0 ? nch_len(s) * nrb : 0;
+        for (int k = 0; k < nit; ++k) sc.items[w + k] = make_int4(s, k / nrb, k % nrb, 0);
+        w += nit;
       }
     }
     if (t == 1023) {
@@ -654,12 +658,10 @@ __global__ __launch_bounds__(1024) void k_sched_one(DevGraph g, DevSchedule sc, 
 //   of smaller branch ids in B(s) as scattered), B(s) in ascending order, the entry's rank, its
 //   partial rows (one per chunk of s, in chunk order) and b's place in the branch list of every
 //   descriptor whose row block holds b's rows.
-//   Later blocks, one wave per work item: the item's work-list position by a binary search of
-//   the item offsets (staged in LDS by each block), the item, the head of its descriptor and
-//   the chunk's page ids.
+//   Later blocks, one wave per work item (the items written by k_sched_one): the head of its
+//   descriptor and the chunk's page ids.
 __global__ __launch_bounds__(kT) void k_emit(DevGraph g, DevSchedule sc, int32_t group,
                                              int32_t chunk_pages, int32_t eblocks, int32_t reuse) {
-  __shared__ int l_off[kSmallSegs + 1];
   if ((int)blockIdx.x < eblocks) {
     const int e = blockIdx.x * kT + threadIdx.x;
     if (e >= g.E) return;
@@ -695,30 +697,19 @@ __global__ __launch_bounds__(kT) void k_emit(DevGraph g, DevSchedule sc, int32_t
       }
     return;
   }
-  const int S = g.S;
-  for (int i = threadIdx.x; i <= S; i += kT) l_off[i] = (int)sc.order_item_off[i];
-  __syncthreads();
   const int64_t w = (int64_t)(blockIdx.x - eblocks) * (kT / 64) + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
-  if (w >= l_off[S]) return;
-  int lo = 0, hi = S;                            // l_off[lo] <= w < l_off[hi]
-  while (hi - lo > 1) {
-    const int mid = (lo + hi) >> 1;
-    if (l_off[mid] <= w) lo = mid; else hi = mid;
-  }
-  const int s = sc.seg_order[lo];
-  const int kk = (int)(w - l_off[lo]);
+  if (w >= sc.counters[0]) return;
+  const int4 it = sc.items[w];
+  const int s = it.x, c = it.y, rb = it.z;
   const int cnt = sc.grp_cnt[s], len = g.seg_len[s];
   const int npg = (len + kPageTokens - 1) / kPageTokens;
-  const int nrb = (cnt * group + kRowsPerBlock - 1) / kRowsPerBlock;
-  const int c = kk / nrb, rb = kk - c * nrb;
   const int nch = (npg + chunk_pages - 1) / chunk_pages;
   const int p0 = chunk_first_page(c, npg, nch);
   const int np = chunk_first_page(c + 1, npg, nch) - p0;
   const int poff = (int)g.seg_page_off[s] + p0;
   int32_t* d = sc.desc + w * sc.desc_words;
   if (lane == 0) {
-    sc.items[w] = make_int4(s, c, rb, 0);
     reinterpret_cast<int4*>(d)[0] =
         make_int4(np, causal_word(g, s, p0), len - (npg - 1) * kPageTokens, cnt);
     reinterpret_cast<int4*>(d)[1] =

@@ -40,11 +40,18 @@ __global__ __launch_bounds__(256) void k_merge(MergeArgs a) {
   float acc[CPL];
 #pragma unroll
   for (int i = 0; i < CPL; ++i) acc[i] = 0.f;
+  // The next batch's partial-row ids are loaded one batch ahead, so that each batch's values
+  // wait for one load round trip instead of two (the id, then the values it names).
+  int32_t nid[KB];
+#pragma unroll
+  for (int j = 0; j < KB; ++j) nid[j] = k0 + j < k1 ? a.bpart[k0 + j] : 0;
   for (int64_t kb = k0; kb < k1; kb += KB) {
     const int nk = (int)min((int64_t)KB, k1 - kb);
     int64_t idx[KB];
 #pragma unroll
-    for (int j = 0; j < KB; ++j) idx[j] = j < nk ? (int64_t)a.bpart[kb + j] * a.Hq + h : 0;
+    for (int j = 0; j < KB; ++j) idx[j] = j < nk ? (int64_t)nid[j] * a.Hq + h : 0;
+#pragma unroll
+    for (int j = 0; j < KB; ++j) nid[j] = kb + KB + j < k1 ? a.bpart[kb + KB + j] : 0;
     float lam[KB], sc[KB], o[KB][CPL];
 #pragma unroll
     for (int j = 0; j < KB; ++j) {

@@ -23,10 +23,10 @@ __global__ __launch_bounds__(256) void k_merge(MergeArgs a) {
   constexpr int LPR = D / CPL;                 // lanes per (branch, q-head) row
   constexpr int RPB = 256 / LPR;               // rows per workgroup
   constexpr int PS = PF16 ? 2 : 1;
-  // Partials loaded per batch before any is folded.  One keeps the kernel at 36 VGPRs (8 waves
-  // per SIMD): more resident rows hide the loads' latency better than deeper batches per row
-  // (2: 56 VGPRs, 4: 76, 8: 116 at 4 waves per SIMD, each slower).
-  constexpr int KB = 1;
+  // Partials loaded per batch before any is folded.  Two, with the next batch's ids loaded
+  // ahead, keep 8 waves per SIMD and two value loads per row in flight; four leave fewer rows
+  // resident and are slower.
+  constexpr int KB = 2;
   const int tid = threadIdx.x;
   if (blockIdx.x == 0 && tid < kMaxStreams) reinterpret_cast<int*>(a.counters + 4)[tid] = 0;
   const int64_t row = (int64_t)blockIdx.x * RPB + tid / LPR;

@@ -79,6 +79,20 @@ __device__ __forceinline__ int cost_class(uint32_t cost) {
   return min(kCostClasses - 1, 1 + 2 * e + m);
 }
 
+// Inclusive scan of one int over the 64 lanes of a wave with DPP: row shifts by 1, 2, 4 and 8
+// scan each row of 16 lanes (lanes shifted in from outside the row read 0), then the last lane
+// of row 0 is added to row 1 and of row 2 to row 3 (row_bcast:15), and the last lane of row 1 to
+// rows 2 and 3 (row_bcast:31).  Rows left out by the row mask keep their value.
+__device__ __forceinline__ int wave_scan_incl(int x) {
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, true);   // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, true);   // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, true);   // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, true);   // row_shr:8
+  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false);  // row_bcast:15
+  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false);  // row_bcast:31
+  return x;
+}
+
 #ifndef GA_SORT_CAP
 #define GA_SORT_CAP 8192
 #endif
@@ -101,17 +115,31 @@ __device__ void scan_segments(const DevGraph& g, const DevSchedule& sc, int32_t 
     nch = cnt > 0 ? (npg + chunk_pages - 1) / chunk_pages : 0;
     nrb = (int)(((int64_t)cnt * group + kRowsPerBlock - 1) / kRowsPerBlock);
   };
+  // Inclusive block scan of three values into sh[0..2][t]: DPP wave scans, then the totals of
+  // the waves before (group offsets are at most E, partial rows and items at most the int32
+  // counts the plan was sized for, so every sum fits an int).
   auto block_scan = [&](int64_t a, int64_t b, int64_t c) {
-    __syncthreads();
-    sh[0][t] = a; sh[1][t] = b; sh[2][t] = c;
-    __syncthreads();
-    for (int off = 1; off < 1024; off <<= 1) {   // Hillis-Steele inclusive scan
-      int64_t x0 = 0, x1 = 0, x2 = 0;
-      if (t >= off) { x0 = sh[0][t - off]; x1 = sh[1][t - off]; x2 = sh[2][t - off]; }
-      __syncthreads();
-      sh[0][t] += x0; sh[1][t] += x1; sh[2][t] += x2;
-      __syncthreads();
+    const int lane = t & 63, wv = t >> 6;
+    int v[3] = {(int)a, (int)b, (int)c};
+#pragma unroll
+    for (int k = 0; k < 3; ++k) v[k] = wave_scan_incl(v[k]);
+    __syncthreads();                               // readers of sh from before are done
+    int* ws = reinterpret_cast<int*>(&sh[0][0]);   // [3][16] wave totals
+    if (lane == 63) {
+#pragma unroll
+      for (int k = 0; k < 3; ++k) ws[k * 16 + wv] = v[k];
     }
+    __syncthreads();
+    int64_t r[3];
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+      int base = 0;
+      for (int w = 0; w < wv; ++w) base += ws[k * 16 + w];
+      r[k] = (int64_t)(v[k] + base);
+    }
+    __syncthreads();                               // every wave has read the totals
+    sh[0][t] = r[0]; sh[1][t] = r[1]; sh[2][t] = r[2];
+    __syncthreads();
   };
 
   // 1. Group and partial-row offsets in segment order.
@@ -371,20 +399,6 @@ __device__ __forceinline__ void emit_items(const DevGraph& g, const DevSchedule&
       d[1] = make_int4(rbk, (int)goff, (int)(poff + p0), (int)(prow_off + (int64_t)c * cnt));
     }
   }
-}
-
-// Inclusive scan of one int over the 64 lanes of a wave with DPP: row shifts by 1, 2, 4 and 8
-// scan each row of 16 lanes (lanes shifted in from outside the row read 0), then the last lane
-// of row 0 is added to row 1 and of row 2 to row 3 (row_bcast:15), and the last lane of row 1 to
-// rows 2 and 3 (row_bcast:31).  Rows left out by the row mask keep their value.
-__device__ __forceinline__ int wave_scan_incl(int x) {
-  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, true);   // row_shr:1
-  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, true);   // row_shr:2
-  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, true);   // row_shr:4
-  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, true);   // row_shr:8
-  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false);  // row_bcast:15
-  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false);  // row_bcast:31
-  return x;
 }
 
 // The whole scheduler in one workgroup for graphs that fit in LDS (<= kSmallSegs segments,

@@ -299,6 +299,8 @@ __global__ __launch_bounds__(1024) void k_scan(DevGraph g, DevSchedule sc, int32
                                                int32_t chunk_pages) {
   __shared__ int64_t sh[3][1024];
   __shared__ uint64_t keys[kSortCap];
+  // (a rescheduled plan skips k_init, whose only work then is this)
+  if (threadIdx.x < kNumCounters) sc.counters[threadIdx.x] = 0;
   scan_segments(g, sc, group, chunk_pages, [&](int s) { return sc.grp_cnt[s]; }, sh, keys);
 }
 
@@ -856,9 +858,11 @@ hipError_t launch_schedule(const DevGraph& g, const DevSchedule& sc, int32_t gro
                          chunk_pages, eblocks, (int32_t)reuse);
     return hipGetLastError();
   }
-  // (with reuse, the entry branches, |B(s)| and the groups in arrival order are not rebuilt)
-  hipLaunchKernelGGL(k_init, dim3(blocks(g.S > 4 ? g.S : 4)), dim3(kT), 0, stream, g, sc,
-                     (int32_t)reuse);
+  // (with reuse, the entry branches, |B(s)| and the groups in arrival order are not rebuilt,
+  // and k_scan clears the counters)
+  if (!reuse)
+    hipLaunchKernelGGL(k_init, dim3(blocks(g.S > 4 ? g.S : 4)), dim3(kT), 0, stream, g, sc,
+                       (int32_t)reuse);
   if (g.E > 0 && !reuse)
     hipLaunchKernelGGL(k_count, dim3(blocks(g.E)), dim3(kT), 0, stream, g, sc);
   hipLaunchKernelGGL(k_scan, dim3(1), dim3(1024), 0, stream, g, sc, group, chunk_pages);

@@ -307,9 +307,10 @@ __global__ __launch_bounds__(1024) void k_scan(DevGraph g, DevSchedule sc, int32
 // Exclusive scan over path entries of their chunk counts (one 1024-thread workgroup): the slot
 // of each entry's first partial in the flat per-branch lists, and the branch CSR offsets.
 // Exclusive scan of the partial rows of every path entry (its segment's chunk count), in entry
-// order, over many workgroups: k_entry_sums totals each block of kScanBlock entries,
-// k_entry_scan gives each block the sum of the blocks before it and scans inside the block, and
-// k_bpart_off reads each branch's first slot.  All loads are coalesced.
+// order, over many workgroups: k_entry_sums totals each block of kScanBlock entries, and
+// k_entry_scan gives each block the sum of the blocks before it, scans inside the block and
+// writes each branch's first slot at its first entry (k_bpart_off does that last part for a
+// graph without entries).
 constexpr int kScanBlock = 1024;
 
 __device__ __forceinline__ int64_t block_sum_1024(int64_t v, int64_t* red) {
@@ -350,7 +351,13 @@ __global__ __launch_bounds__(kScanBlock) void k_entry_scan(DevGraph g, DevSchedu
   __syncthreads();
   int64_t before = 0;
   for (int i = 0; i < w; ++i) before += wsum[i];
-  if (e < g.E) sc.entry_part[e] = base + before + x - v;
+  if (e < g.E) {
+    const int64_t slot = base + before + x - v;
+    sc.entry_part[e] = slot;
+    const int b = sc.entry_branch[e];
+    if (e == g.path_off[b]) sc.bpart_off[b] = slot;
+    if (e == g.E - 1) sc.bpart_off[g.B] = slot + v;
+  }
 }
 
 __global__ void k_bpart_off(DevGraph g, DevSchedule sc) {
@@ -870,8 +877,9 @@ hipError_t launch_schedule(const DevGraph& g, const DevSchedule& sc, int32_t gro
   if (sblocks > 0) {
     hipLaunchKernelGGL(k_entry_sums, dim3((unsigned)sblocks), dim3(kScanBlock), 0, stream, g, sc);
     hipLaunchKernelGGL(k_entry_scan, dim3((unsigned)sblocks), dim3(kScanBlock), 0, stream, g, sc);
+  } else {
+    hipLaunchKernelGGL(k_bpart_off, dim3(blocks((int64_t)g.B + 1)), dim3(kT), 0, stream, g, sc);
   }
-  hipLaunchKernelGGL(k_bpart_off, dim3(blocks((int64_t)g.B + 1)), dim3(kT), 0, stream, g, sc);
   if (g.E > 0 && !reuse)
     hipLaunchKernelGGL(k_scatter, dim3(blocks(g.E)), dim3(kT), 0, stream, g, sc);
   const int64_t n = g.E > g.S ? g.E : g.S;

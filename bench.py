@@ -18,7 +18,9 @@ times equivalence detection (and beside it the graph suffix and the graph reward
 advantage) for one training batch's rollout states.
 
 Timing: the K timed steps run without per-kernel events (ms_per_step, value); K further steps
-record HIP events on the launch stream around each kernel (kernel_ms and the roofline).
+time each kernel with HIP events (kernel_ms and the roofline): the attention and merge events are
+bound to the kernels' own dispatches, so they span each kernel's execution, and the scheduler's
+are recorded around its launches.
 
 The default decode line also carries, under "configs", the same step timed on every other
 configuration (tiny fp32 graph, 7B tree, 32B long reasoning, chain and equal-budget graph), with
@@ -115,9 +117,9 @@ def timed_steps(torch, plan, step, steps, preroll=3):
     per-kernel events (HIP event records between kernels lengthen a step by a few us each):
     it gives ms per step.  It starts behind `preroll` untimed steps, so that the GPU is already
     busy when its start event is recorded (after a synchronisation the first launch would
-    otherwise wait for the host, and the clocks for the work).  The second records the
-    library's HIP events around every scheduler, attention and merge launch: it gives each
-    kernel's average duration."""
+    otherwise wait for the host, and the clocks for the work).  The second turns on the
+    library's kernel timing (HIP events bound to each attention and merge dispatch, recorded
+    around each scheduler pass): it gives each kernel's average duration."""
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -143,9 +145,9 @@ def timed_steps(torch, plan, step, steps, preroll=3):
 
 
 def mall_flushed_attention(torch, plan, step, steps, dev):
-    """Attention duration (library HIP events) with the memory-side cache (256 MB on MI355X)
-    flushed before every step by reading a 512 MiB buffer (a read leaves no dirty lines for
-    the attention kernel to write back); the read runs between steps, outside the kernel
+    """Attention duration (the library's kernel events) with the memory-side cache (256 MB on
+    MI355X) flushed before every step by reading a 512 MiB buffer (a read leaves no dirty lines
+    for the attention kernel to write back); the read runs between steps, outside the kernel
     events."""
     junk = torch.ones(1 << 27, dtype=torch.float32, device=dev)
     plan.profile(steps)
@@ -292,8 +294,8 @@ def run_extend(args, torch, G, W):
         "kernel_ms": {"scheduler": sched_ms, "attention": attn_ms, "merge": merge_ms},
         "timing": "ms_per_step over the timed steps without per-kernel events, started behind "
                   "3 untimed steps so the GPU is busy at the start event; kernel_ms (and "
-                  "the roofline) from as many further steps with HIP events on the launch stream "
-                  "around each kernel",
+                  "the roofline) from as many further steps with HIP events bound to the attention "
+                  "and merge dispatches (recorded around the scheduler)",
         "attention_flops": flops,
         "unique_kv_bytes": ukv,
         "unique_kv_hbm_frac": ukv / (attn_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
@@ -734,8 +736,9 @@ def main():
                       "attention_mall_flushed": cold_ms},
         "timing": "ms_per_step over the timed steps without per-kernel events, started behind "
                   "3 untimed steps so the GPU is busy at the start event; kernel_ms (and "
-                  "the roofline) from as many further steps with HIP events on the launch stream "
-                  "around each kernel; attention_mall_flushed from as many more with a 512 MiB "
+                  "the roofline) from as many further steps with HIP events bound to the attention "
+                  "and merge dispatches (recorded around the scheduler); attention_mall_flushed "
+                  "from as many more with a 512 MiB "
                   "read between steps",
         "mall_flushed_frac": ukv / (cold_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
         "ms_per_step_median": med_ms,

@@ -223,9 +223,10 @@ ga_status graphattn_plan_debug_dump(const ga_plan* plan, void* hip_stream,
                                     int32_t* segment_chunks, int64_t* branch_part_offsets,
                                     int32_t* branch_parts);
 
-/* Measurement infrastructure.  Kernel timing with HIP events recorded on the launch stream
- * around each scheduler pass, each
- * attention launch and each merge launch.  graphattn_plan_profile(plan, n) arms recording for the
+/* Measurement infrastructure.  Kernel timing with HIP events: recorded on the launch stream
+ * around each scheduler pass, and bound to each attention and each merge dispatch (their elapsed
+ * time is the kernel's own execution, without the gaps of the queue around it).
+ * graphattn_plan_profile(plan, n) arms recording for the
  * next n schedule and n run calls (n = 0 disarms and clears); graphattn_plan_profile_read
  * synchronises on the last recorded event and returns the accumulated times in milliseconds
  * and the number of calls recorded. */

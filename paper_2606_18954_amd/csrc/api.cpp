@@ -131,7 +131,8 @@ struct ga_plan {
   // Kernel timing (graphattn_plan_profile): events for up to prof_cap schedule / run calls.
   int32_t prof_cap = 0, prof_sched = 0, prof_runs = 0;
   std::vector<hipEvent_t> ev_sched;   // 2 per recorded schedule call
-  std::vector<hipEvent_t> ev_run;     // 3 per recorded run: attention start, attention end, merge end
+  std::vector<hipEvent_t> ev_run;     // 4 per recorded run: attention start and end, merge start
+                                      // and end
   hipEvent_t ev_last = nullptr;
 };
 
@@ -740,14 +741,18 @@ ga_status do_run(ga_plan* pl, const void* q, const void* pool, void* out, float*
                                             pl->num_cus);
   const int64_t work = pl->z.max_items * pl->p.num_kv_heads;
   if (work < grid) grid = work;
+  // Profiled runs bind their events to the attention and merge dispatches themselves (a kernel
+  // with no work gets a plain event pair instead).
   const bool rec = pl->prof_runs < pl->prof_cap;
-  hipEvent_t* ev = rec ? &pl->ev_run[3 * pl->prof_runs] : nullptr;
-  if (rec) GA_HIP(hipEventRecord(ev[0], stream), "profile event");
+  hipEvent_t* ev = rec ? &pl->ev_run[4 * pl->prof_runs] : nullptr;
   if (grid > 0)
     GA_HIP(ga::launch_seg_attn(a, pl->p.head_dim, bf16, pl->causal, pl->z.few_pages, (int)grid,
-                               stream),
+                               stream, rec ? ev[0] : nullptr, rec ? ev[1] : nullptr),
            "attention launch");
-  if (rec) GA_HIP(hipEventRecord(ev[1], stream), "profile event");
+  else if (rec) {
+    GA_HIP(hipEventRecord(ev[0], stream), "profile event");
+    GA_HIP(hipEventRecord(ev[1], stream), "profile event");
+  }
   ga::MergeArgs m{};
   m.bpart_off = pl->sc.bpart_off;
   m.bpart = pl->sc.bpart;
@@ -758,12 +763,18 @@ ga_status do_run(ga_plan* pl, const void* q, const void* pool, void* out, float*
   m.counters = pl->sc.counters;
   m.B = pl->z.B;
   m.Hq = pl->p.num_q_heads;
-  GA_HIP(ga::launch_merge(m, pl->p.head_dim, bf16 && !pl->p.out_f32, bf16, stream),
+  const bool merge_rows = (int64_t)m.B * m.Hq > 0;
+  GA_HIP(ga::launch_merge(m, pl->p.head_dim, bf16 && !pl->p.out_f32, bf16, stream,
+                          rec && merge_rows ? ev[2] : nullptr,
+                          rec && merge_rows ? ev[3] : nullptr),
          "merge launch");
   pl->scheduled = true;
   if (rec) {
-    GA_HIP(hipEventRecord(ev[2], stream), "profile event");
-    pl->ev_last = ev[2];
+    if (!merge_rows) {
+      GA_HIP(hipEventRecord(ev[2], stream), "profile event");
+      GA_HIP(hipEventRecord(ev[3], stream), "profile event");
+    }
+    pl->ev_last = ev[3];
     ++pl->prof_runs;
   }
   return GA_OK;
@@ -1017,7 +1028,7 @@ ga_status graphattn_plan_profile(ga_plan* plan, int32_t max_calls) {
   if (plan->ev_last) GA_HIP(hipEventSynchronize(plan->ev_last), "profile sync");
   profile_clear(plan);
   plan->ev_sched.resize(2 * (size_t)max_calls);
-  plan->ev_run.resize(3 * (size_t)max_calls);
+  plan->ev_run.resize(4 * (size_t)max_calls);
   for (auto* v : {&plan->ev_sched, &plan->ev_run})
     for (hipEvent_t& e : *v)
       if (hipEventCreate(&e) != hipSuccess) {
@@ -1041,8 +1052,8 @@ ga_status graphattn_plan_profile_read(ga_plan* plan, ga_profile* out) {
   }
   for (int32_t i = 0; i < plan->prof_runs; ++i) {
     float a = 0.f, m = 0.f;
-    GA_HIP(hipEventElapsedTime(&a, plan->ev_run[3 * i], plan->ev_run[3 * i + 1]), "elapsed");
-    GA_HIP(hipEventElapsedTime(&m, plan->ev_run[3 * i + 1], plan->ev_run[3 * i + 2]), "elapsed");
+    GA_HIP(hipEventElapsedTime(&a, plan->ev_run[4 * i], plan->ev_run[4 * i + 1]), "elapsed");
+    GA_HIP(hipEventElapsedTime(&m, plan->ev_run[4 * i + 2], plan->ev_run[4 * i + 3]), "elapsed");
     out->attn_ms += a;
     out->merge_ms += m;
   }

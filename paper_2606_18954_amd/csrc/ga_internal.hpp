@@ -220,10 +220,14 @@ hipError_t launch_schedule(const DevGraph& g, const DevSchedule& sc, int32_t gro
                            int32_t chunk_pages, int64_t max_items, bool reuse,
                            hipStream_t stream);
 // few_pages: a decode step with under 64 pages (times kv-heads) per workgroup at two per CU.
+// t0 / t1 (optional, timing events): bound to the kernel's own dispatch (hipExtLaunchKernel), so
+// that their elapsed time is the kernel's execution, without the queue's gaps around it.
 hipError_t launch_seg_attn(const AttnArgs& a, int head_dim, bool bf16, bool causal,
-                           bool few_pages, int grid, hipStream_t stream);
+                           bool few_pages, int grid, hipStream_t stream,
+                           hipEvent_t t0 = nullptr, hipEvent_t t1 = nullptr);
+// t0 / t1 as for launch_seg_attn; no kernel (and no event) when there are no rows.
 hipError_t launch_merge(const MergeArgs& a, int head_dim, bool out_bf16, bool part_f16,
-                        hipStream_t stream);
+                        hipStream_t stream, hipEvent_t t0 = nullptr, hipEvent_t t1 = nullptr);
 hipError_t launch_kv_write(const KvWriteArgs& a, hipStream_t stream);
 hipError_t launch_equivalence(const EquivArgs& a, hipStream_t stream);
 hipError_t launch_suffix_count(const SuffixArgs& a, hipStream_t stream);

@@ -10,6 +10,8 @@
 // scale per row (format in ga_internal.hpp); the scale is folded into the row's weight.
 #include "ga_internal.hpp"
 
+#include <hip/hip_ext.h>
+
 namespace ga {
 namespace {
 
@@ -118,30 +120,34 @@ __global__ __launch_bounds__(256) void k_merge(MergeArgs a) {
 }
 
 template <int D, bool BF16, bool PF16>
-hipError_t launch_t(const MergeArgs& a, hipStream_t stream) {
+hipError_t launch_t(const MergeArgs& a, hipStream_t stream, hipEvent_t t0, hipEvent_t t1) {
   constexpr int RPB = 256 / (D / (PF16 ? 8 : 4));
   const int64_t rows = (int64_t)a.B * a.Hq;
   const int grid = (int)((rows + RPB - 1) / RPB);
   if (grid == 0) return hipSuccess;
-  hipLaunchKernelGGL((k_merge<D, BF16, PF16>), dim3(grid), dim3(256), 0, stream, a);
+  if (t0 || t1)
+    hipExtLaunchKernelGGL(k_merge<D, BF16, PF16>, dim3(grid), dim3(256), 0, stream, t0, t1, 0, a);
+  else
+    hipLaunchKernelGGL((k_merge<D, BF16, PF16>), dim3(grid), dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 
 template <bool BF16, bool PF16>
-hipError_t launch_d(const MergeArgs& a, int head_dim, hipStream_t stream) {
-  if (head_dim == 64) return launch_t<64, BF16, PF16>(a, stream);
-  if (head_dim == 128) return launch_t<128, BF16, PF16>(a, stream);
+hipError_t launch_d(const MergeArgs& a, int head_dim, hipStream_t stream, hipEvent_t t0,
+                    hipEvent_t t1) {
+  if (head_dim == 64) return launch_t<64, BF16, PF16>(a, stream, t0, t1);
+  if (head_dim == 128) return launch_t<128, BF16, PF16>(a, stream, t0, t1);
   return hipErrorInvalidValue;
 }
 
 }  // namespace
 
 hipError_t launch_merge(const MergeArgs& a, int head_dim, bool bf16, bool part_f16,
-                        hipStream_t stream) {
-  if (bf16) return part_f16 ? launch_d<true, true>(a, head_dim, stream)
-                            : launch_d<true, false>(a, head_dim, stream);
-  return part_f16 ? launch_d<false, true>(a, head_dim, stream)
-                  : launch_d<false, false>(a, head_dim, stream);
+                        hipStream_t stream, hipEvent_t t0, hipEvent_t t1) {
+  if (bf16) return part_f16 ? launch_d<true, true>(a, head_dim, stream, t0, t1)
+                            : launch_d<true, false>(a, head_dim, stream, t0, t1);
+  return part_f16 ? launch_d<false, true>(a, head_dim, stream, t0, t1)
+                  : launch_d<false, false>(a, head_dim, stream, t0, t1);
 }
 
 }  // namespace ga

@@ -32,6 +32,8 @@
 // folds them along each branch's path.
 #include "ga_internal.hpp"
 
+#include <hip/hip_ext.h>
+
 #include <type_traits>
 
 #ifndef GA_STAGE_BYTES
@@ -800,19 +802,19 @@ void k_seg_attn(AttnArgs a) {
 
 template <int D, bool BF16>
 hipError_t launch_t(const AttnArgs& a, bool causal, bool few_pages, int grid,
-                    hipStream_t stream) {
+                    hipStream_t stream, hipEvent_t t0, hipEvent_t t1) {
   constexpr int W_CAUSAL = attn_wgs_per_cu(true, BF16, false);
   constexpr int W_WIDE = attn_wgs_per_cu(false, BF16, true);
   constexpr int W_DECODE = attn_wgs_per_cu(false, BF16, false);
-  if (causal)
-    hipLaunchKernelGGL((k_seg_attn<D, BF16, true, W_CAUSAL>), dim3(grid), dim3(kAttnThreads), 0,
-                       stream, a);
-  else if (few_pages && W_WIDE != W_DECODE)
-    hipLaunchKernelGGL((k_seg_attn<D, BF16, false, W_WIDE>), dim3(grid), dim3(kAttnThreads), 0,
-                       stream, a);
-  else
-    hipLaunchKernelGGL((k_seg_attn<D, BF16, false, W_DECODE>), dim3(grid), dim3(kAttnThreads), 0,
-                       stream, a);
+  auto go = [&](auto kernel) {
+    if (t0 || t1)
+      hipExtLaunchKernelGGL(kernel, dim3(grid), dim3(kAttnThreads), 0, stream, t0, t1, 0, a);
+    else
+      hipLaunchKernelGGL(kernel, dim3(grid), dim3(kAttnThreads), 0, stream, a);
+  };
+  if (causal) go(k_seg_attn<D, BF16, true, W_CAUSAL>);
+  else if (few_pages && W_WIDE != W_DECODE) go(k_seg_attn<D, BF16, false, W_WIDE>);
+  else go(k_seg_attn<D, BF16, false, W_DECODE>);
   return hipGetLastError();
 }
 
@@ -825,13 +827,14 @@ int seg_attn_grid(int head_dim, bool bf16, bool causal, bool few_pages, int num_
 }
 
 hipError_t launch_seg_attn(const AttnArgs& a, int head_dim, bool bf16, bool causal,
-                           bool few_pages, int grid, hipStream_t stream) {
+                           bool few_pages, int grid, hipStream_t stream, hipEvent_t t0,
+                           hipEvent_t t1) {
   if (bf16) {
-    if (head_dim == 64) return launch_t<64, true>(a, causal, few_pages, grid, stream);
-    if (head_dim == 128) return launch_t<128, true>(a, causal, few_pages, grid, stream);
+    if (head_dim == 64) return launch_t<64, true>(a, causal, few_pages, grid, stream, t0, t1);
+    if (head_dim == 128) return launch_t<128, true>(a, causal, few_pages, grid, stream, t0, t1);
   } else {
-    if (head_dim == 64) return launch_t<64, false>(a, causal, few_pages, grid, stream);
-    if (head_dim == 128) return launch_t<128, false>(a, causal, few_pages, grid, stream);
+    if (head_dim == 64) return launch_t<64, false>(a, causal, few_pages, grid, stream, t0, t1);
+    if (head_dim == 128) return launch_t<128, false>(a, causal, few_pages, grid, stream, t0, t1);
   }
   return hipErrorInvalidValue;
 }

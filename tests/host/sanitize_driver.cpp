@@ -16,8 +16,11 @@
 namespace ga {
 hipError_t launch_schedule(const DevGraph&, const DevSchedule&, int32_t, int32_t, int64_t, bool,
                            hipStream_t) { std::abort(); }
-hipError_t launch_seg_attn(const AttnArgs&, int, bool, bool, bool, int, hipStream_t) { std::abort(); }
-hipError_t launch_merge(const MergeArgs&, int, bool, bool, hipStream_t) { std::abort(); }
+hipError_t launch_seg_attn(const AttnArgs&, int, bool, bool, bool, int, hipStream_t, hipEvent_t,
+                           hipEvent_t) { std::abort(); }
+hipError_t launch_merge(const MergeArgs&, int, bool, bool, hipStream_t, hipEvent_t, hipEvent_t) {
+  std::abort();
+}
 hipError_t launch_kv_write(const KvWriteArgs&, hipStream_t) { std::abort(); }
 hipError_t launch_equivalence(const EquivArgs&, hipStream_t) { std::abort(); }
 hipError_t launch_suffix_count(const SuffixArgs&, hipStream_t) { std::abort(); }

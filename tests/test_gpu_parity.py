@@ -94,6 +94,38 @@ def test_large_steps_run_two_workgroups_per_cu(Hq, Hkv, D):
         assert (plan.info().workgroups_per_cu, plan.info().work_streams) == (3, 1)
 
 
+def test_profiled_runs_time_each_kernel_and_give_the_same_bits():
+    """Kernel timing (events bound to the attention and merge dispatches, recorded around the
+    scheduler) launches the same kernels: profiled steps give the unprofiled step's bits, the
+    recording stops at its cap, and every recorded time is positive and below the wall time of
+    the steps that contain it."""
+    import time
+    wl = W.config2_tree(prompts=3)
+    g = wl.graph
+    q, pool = to_device(wl)
+    B, Hq, D = g.num_branches, wl.num_q_heads, wl.head_dim
+    with G.Plan(G.HostGraph.from_graph(g), params_of(wl)) as plan:
+        out0, lse0 = _plan_step(plan, q, pool, B, Hq, D)
+        plan.profile(3)
+        t0 = time.perf_counter()
+        for _ in range(5):
+            out, lse = _plan_step(plan, q, pool, B, Hq, D)
+            assert torch.equal(out.view(torch.int16), out0.view(torch.int16))
+            assert torch.equal(lse, lse0)
+        wall_ms = (time.perf_counter() - t0) * 1e3
+        pr = plan.profile_read()
+        assert (pr.schedules, pr.runs) == (3, 3)
+        for ms in (pr.sched_ms, pr.attn_ms, pr.merge_ms):
+            assert 0.0 < ms < wall_ms
+        say(f"[profile] 3 runs: scheduler {pr.sched_ms / 3:.4f} ms, attention "
+            f"{pr.attn_ms / 3:.4f} ms, merge {pr.merge_ms / 3:.4f} ms")
+        plan.profile(0)
+        out, lse = _plan_step(plan, q, pool, B, Hq, D)
+        assert torch.equal(out.view(torch.int16), out0.view(torch.int16))
+        pr = plan.profile_read()
+        assert (pr.schedules, pr.runs) == (0, 0)
+
+
 @pytest.mark.parametrize("name", ["c3", "c4", "c5chain", "c5graph"])
 def test_full_size_every_branch(name):
     """Full-size configurations in the launch configuration the benchmark times (plan, GPU

@@ -646,7 +646,7 @@ def main():
     ap.add_argument("--all-configs", type=int, default=1,
                     help="decode only: also time the other configurations and the decode loop "
                          "(1, the default) and report them under configs / decode_loop")
-    ap.add_argument("--other-steps", type=int, default=20,
+    ap.add_argument("--other-steps", type=int, default=50,
                     help="timed steps per region for the other configurations")
     ap.add_argument("--cpu-configs", action="store_true",
                     help="decode only: also time the CPU oracle on a bounded seeded sample of "

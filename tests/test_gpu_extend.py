@@ -150,9 +150,10 @@ def test_extend_full_size_sampled():
 
 def test_extend_full_size_runs_are_bit_identical():
     """The full 16-token extend scheduled and run twice on one plan, and once more from a fresh
-    plan: the work streams hand units to whichever workgroup claims them first (and workgroups
-    whose stream is empty claim from the others), but every unit's partial depends only on the
-    unit, so all three runs give the same bits."""
+    plan with kernel timing on (the causal kernel and the merge launched with their dispatch-
+    bound events): the work streams hand units to whichever workgroup claims them first (and
+    workgroups whose stream is empty claim from the others), but every unit's partial depends
+    only on the unit, so all three runs give the same bits."""
     require_gpu()
     wl = W.config3_extend()
     q, pool = wl.q.cuda(), wl.pool.cuda()
@@ -173,7 +174,10 @@ def test_extend_full_size_runs_are_bit_identical():
         o1, l1 = run(pl)
         o2, l2 = run(pl)
     with G.Plan(hg, p, query_counts=wl.query_counts) as pl:
+        pl.profile(1)
         o3, l3 = run(pl)
+        pr = pl.profile_read()
+        assert (pr.schedules, pr.runs) == (1, 1) and pr.attn_ms > 0.0 and pr.merge_ms > 0.0
     assert torch.equal(o1, o2) and torch.equal(l1, l2)
     assert torch.equal(o1, o3) and torch.equal(l1, l3)
 

@@ -229,7 +229,8 @@ ga_status graphattn_plan_debug_dump(const ga_plan* plan, void* hip_stream,
  * graphattn_plan_profile(plan, n) arms recording for the
  * next n schedule and n run calls (n = 0 disarms and clears); graphattn_plan_profile_read
  * synchronises on the last recorded event and returns the accumulated times in milliseconds
- * and the number of calls recorded. */
+ * and the number of calls recorded.  Timing is for eager calls: do not arm it around calls that
+ * a stream capture records into a HIP graph. */
 typedef struct {
   int32_t schedules, runs;     /* calls recorded */
   double sched_ms;             /* sum over recorded schedule calls */

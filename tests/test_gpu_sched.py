@@ -56,11 +56,14 @@ def chains(g):
     return out
 
 
+SORT_CAP = 8192     # chains the scheduler orders by cost; more keep their first-segment order
+
+
 def expected_items(g, group, chunk_pages, cnt):
     """Work list: items grouped by chain, chains by descending cost class of the per-item cost
     (pages of the chain's longest chunk x (2 + row tiles); a chain's chunks split its pages as
-    evenly as whole pages allow), ties by first segment; within a chain chunk-major.  An item
-    names its chain by the chain's first segment."""
+    evenly as whole pages allow), ties by first segment (beyond SORT_CAP chains, in first-segment
+    order); within a chain chunk-major.  An item names its chain by the chain's first segment."""
     def npg(s):
         return (int(g.seg_len[s]) + 15) // 16
 
@@ -70,7 +73,9 @@ def expected_items(g, group, chunk_pages, cnt):
         nch = (pages + chunk_pages - 1) // chunk_pages
         return -(-pages // nch) * (2 + tiles)
 
-    order = sorted(chains(g), key=lambda c: (-cost_class(cost(c)), c[0]))
+    order = chains(g)
+    if len(order) <= SORT_CAP:
+        order = sorted(order, key=lambda c: (-cost_class(cost(c)), c[0]))
     items = []
     for c in order:
         pages = sum(npg(s) for s in c)
@@ -192,3 +197,20 @@ def test_large_graphs_use_the_multi_kernel_path():
     g2 = W.assemble_graph(lens, paths, 3)
     assert g2.path_segs.shape[0] == 9000
     check_schedule(W.make_workload("9000-entry graph", g2, 8, 2, 64, "f32", 3))
+
+
+@pytest.mark.parametrize("n", [6000, 9000])
+def test_chains_past_the_counting_sort(n):
+    """A root shared by n branches, each of which ends in a segment of its own (n + 1 chains):
+    6,001 chains are ordered by the bitonic sort (more than the counting sort's 4,096), 9,001
+    keep their first-segment order (more than the 8,192 the sort holds); every other output is
+    as for smaller graphs, and sampled branches match the oracle."""
+    from gpu_util import check_workload
+    rng = np.random.default_rng(n)
+    lens = [200] + [int(x) for x in rng.integers(1, 40, size=n)]
+    paths = [[0, 1 + i] for i in range(n)]
+    g = W.assemble_graph(lens, paths, 5)
+    wl = W.make_workload(f"{n + 1}-chain graph", g, 8, 2, 64, "bf16", 5)
+    assert len(chains(g)) == n + 1 > 4096
+    check_schedule(wl)
+    check_workload(wl, branches=[0, 1, n // 2, n - 2, n - 1], out_f32=True)

@@ -75,11 +75,20 @@ def _tree(rng, n_branches, max_step, max_new):
 
 
 @pytest.mark.parametrize("Hq,Hkv,D,dtype", [(28, 4, 128, "bf16"), (8, 2, 64, "f32"),
-                                            (40, 8, 128, "bf16"), (4, 4, 64, "bf16")])
+                                            (40, 8, 128, "bf16"), (4, 4, 64, "bf16"),
+                                            (6, 3, 64, "bf16"), (24, 6, 128, "bf16"),
+                                            (8, 1, 64, "bf16")])
 def test_extend_tree(Hq, Hkv, D, dtype):
+    """Causal trees at several head shapes, so that the causal kernel's work streams (one per
+    kv-head up to gcd(Hkv, 8)) run with 8, 4, 2 and 1 streams, the last with the rotated stage
+    order of single-stream launches."""
     rng = np.random.default_rng(Hq + D)
     lens, paths, counts = _tree(rng, 7, 90, 70)
-    check(_wl(lens, paths, counts, Hq, Hkv, D, dtype, Hq + D))
+    wl = _wl(lens, paths, counts, Hq, Hkv, D, dtype, Hq + D)
+    with G.Plan(G.HostGraph.from_graph(wl.graph), params_of(wl),
+                query_counts=wl.query_counts) as pl:
+        assert pl.info().work_streams == max(s for s in (8, 4, 2, 1) if Hkv % s == 0)
+    check(wl)
 
 
 def test_extend_prompt_prefill_spans_chunks():

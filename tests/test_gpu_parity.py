@@ -186,6 +186,28 @@ def test_determinism_bitwise():
     assert torch.equal(l1, l2)
 
 
+def test_full_7b_tree_runs_are_bit_identical():
+    """The full 7B tree in the benchmark's plan path (three workgroups per CU, where units of at
+    most two row tiles split their pages between two waves that hand over their running state
+    through LDS): ten steps on one plan and one on a fresh plan, all with the same bits."""
+    wl = W.config2_tree()
+    g = wl.graph
+    q, pool = to_device(wl)
+    hg = G.HostGraph.from_graph(g)
+    B, Hq, D = g.num_branches, wl.num_q_heads, wl.head_dim
+    with G.Plan(hg, params_of(wl)) as plan:
+        assert plan.info().workgroups_per_cu == 3
+        ref_o, ref_l = _plan_step(plan, q, pool, B, Hq, D)
+        for _ in range(9):
+            o, l = _plan_step(plan, q, pool, B, Hq, D)
+            assert torch.equal(o.view(torch.int16), ref_o.view(torch.int16))
+            assert torch.equal(l, ref_l)
+    with G.Plan(hg, params_of(wl)) as plan:
+        o, l = _plan_step(plan, q, pool, B, Hq, D)
+    assert torch.equal(o.view(torch.int16), ref_o.view(torch.int16))
+    assert torch.equal(l, ref_l)
+
+
 def test_plan_serves_several_layers():
     """One schedule, several runs with different q / pools (layers of one decode step)."""
     wl = W.config3_merged_dag(prompts=2)
